@@ -1,0 +1,202 @@
+"""Benchmark of the per-chunk stream step on one MI355X: score -> select -> compact -> attend.
+
+Workload: the 80K-token history (81,920-slot bf16 pool, 30% of units already evicted, 32 query /
+8 KV heads, d = 128, budget 16,384, a 665-token chunk).  Inputs are seeded synthetic streams
+resident in HBM; ``--copies`` distinct copies of the inputs are rotated so that no step finds its
+inputs in the 256 MB last-level (Infinity) cache.  Each of the K timed steps runs the whole path.
+
+Prints one JSON line.  ``value`` is attention TFLOP/s over the whole step (attention work of a
+step / step time); per-kernel rates and roofline fractions are in ``kernels`` and ``roofline``.
+``cpu_baseline`` times the CPU oracle on one step of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import streamgen as sg  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6
+WORKLOAD = "history_80k"
+
+
+def attn_flops(L, kept, Hq, d):
+    return 4.0 * Hq * d * (L * kept + L * (L + 1) / 2)
+
+
+def score_bytes(lay, H, d, elt, U):
+    live = int((lay.unit_id >= 0).sum())
+    return live * H * d * elt + lay.n_slots * 5 + U * 24
+
+
+def compact_bytes(kept, L, H, d, elt, cap, U):
+    row = H * d * elt
+    return 2 * row * (2 * kept + 2 * L) + kept * 9 + L * 5 + cap * 13 + U * 13
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--copies", type=int, default=4)
+    ap.add_argument("--config", default=WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
+              "multi-GPU path; see DESIGN.md for how it would shard.", file=sys.stderr)
+        sys.exit(2)
+
+    from paper_2609_34653_amd import omnitide as ot
+    from paper_2609_34653_amd.step import StreamStep
+    ot.lib()
+    dev = torch.device("cuda:0")
+    cfg = sg.CONFIG_BY_NAME[args.config]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    H, d, Hq, L = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads, lay.chunk_len
+    elt = 2 if cfg.dtype == "bf16" else 4
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    copies = []
+    for _ in range(args.copies):
+        copies.append(dict(
+            k=seg.k_hist.to(dev)[None].contiguous(), v=seg.v_hist.to(dev)[None].contiguous(),
+            uid=t(lay.unit_id), mod=t(lay.modality), pos=t(lay.pos),
+            kc=seg.k_chunk.to(dev)[None].contiguous(), vc=seg.v_chunk.to(dev)[None].contiguous(),
+            cm=t(lay.chunk_modality), cu=t(lay.chunk_unit), q=seg.q.to(dev)[None].contiguous()))
+    st = StreamStep(n_seg=1, n_slots=lay.n_slots, n_units=lay.n_units, n_q_heads=Hq,
+                    n_kv_heads=H, head_dim=d, chunk_len=L, budget=cfg.budget, recent=cfg.recent,
+                    page_size=cfg.page_size, weights=cfg.weights, device=dev)
+    s = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        c = copies[i % len(copies)]
+        if ev is not None:
+            ev[0].record(s)
+        st.score(c["k"], c["uid"], c["mod"])
+        if ev is not None:
+            ev[1].record(s)
+        st.select()
+        if ev is not None:
+            ev[2].record(s)
+        st.compact(c["k"], c["v"], c["uid"], c["mod"], c["pos"], c["kc"], c["vc"], c["cm"],
+                   c["cu"])
+        if ev is not None:
+            ev[3].record(s)
+        st.attend(c["q"], cfg.scale)
+        if ev is not None:
+            ev[4].record(s)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    status = int(st.d_status.item())
+    if status != 0:
+        raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
+    kept = int(st.kept_tokens.item())
+    n_ctx = int(st.n_ctx.item())
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(s)
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    end.record(s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    per = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in evs])  # ms
+    avg = per.mean(axis=0)
+    names = ["score", "select", "compact", "attend"]
+
+    flops = attn_flops(L, kept, Hq, d)
+    sbytes = score_bytes(lay, H, d, elt, lay.n_units)
+    cbytes = compact_bytes(kept, L, H, d, elt, st.cap_dst, lay.n_units)
+    sel_bytes = lay.n_units * (8 + 4 * 4) + lay.n_units * 9 + 4
+    attn_tflops = flops / (avg[3] * 1e-3) / 1e12
+    kernels = {
+        "score": {"us": avg[0] * 1e3, "bytes": sbytes, "GBps": sbytes / (avg[0] * 1e-3) / 1e9},
+        "select": {"us": avg[1] * 1e3, "bytes": sel_bytes,
+                   "GBps": sel_bytes / (avg[1] * 1e-3) / 1e9},
+        "compact": {"us": avg[2] * 1e3, "bytes": cbytes, "GBps": cbytes / (avg[2] * 1e-3) / 1e9},
+        "attend": {"us": avg[3] * 1e3, "flops": flops, "TFLOPs": attn_tflops},
+    }
+    for k in ("score", "compact"):
+        kernels[k]["frac_hbm"] = kernels[k]["GBps"] / HBM_PEAK_GBPS
+    kernels["attend"]["frac_mfma"] = attn_tflops / BF16_PEAK_TFLOPS
+    for k in kernels:
+        kernels[k] = {a: (round(b, 4) if isinstance(b, float) else b) for a, b in kernels[k].items()}
+
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    result = {
+        "metric": "chunk-attn TFLOP/s + score/compact GB/s (% roofline), 80K-token history, 1 GPU",
+        "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "history_slots": lay.n_slots,
+                   "live_tokens": int((lay.unit_id >= 0).sum()), "units": lay.n_units,
+                   "budget": cfg.budget, "chunk_len": L, "n_q_heads": Hq, "n_kv_heads": H,
+                   "head_dim": d, "page_size": cfg.page_size, "kept_tokens": kept,
+                   "n_ctx": n_ctx, "input_copies": args.copies},
+        "kernels": kernels,
+        "roofline": {"bound": "mfma", "kernel": "attend (chunk attention call)",
+                     "achieved": round(attn_tflops, 3), "peak": BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
+                     "traffic": None},
+        "wall_s_timed_region": round(wall, 4),
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, stream, seg, flops)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(cfg, stream, seg, flops):
+    """The CPU oracle (exact integers + float64 attention) on one step of the same workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    lay = stream.layout
+    bits = lambda x: x.contiguous().view(torch.int16).numpy().view(np.uint16)  # noqa: E731
+    k, v = bits(seg.k_hist), bits(seg.v_hist)
+    t0 = time.perf_counter()
+    sc = oracle.score_units(k, cfg.dtype, lay.unit_id, lay.modality, cfg.weights, lay.n_units)
+    t1 = time.perf_counter()
+    _, keep, kept = oracle.select_units(sc["wsum"], sc["len"], sc["first"], sc["last"],
+                                        sc["flags"], cfg.budget, cfg.recent)
+    t2 = time.perf_counter()
+    cp = oracle.compact_kv(k, v, lay.unit_id, lay.modality, lay.pos, keep, lay.n_units,
+                           bits(seg.k_chunk), bits(seg.v_chunk), lay.chunk_modality,
+                           lay.chunk_unit, cfg.budget + lay.chunk_len, cfg.page_size)
+    t3 = time.perf_counter()
+    oracle.chunk_attention(oracle.to_f64(bits(seg.q), "bf16"), oracle.to_f64(cp["k"], "bf16"),
+                           oracle.to_f64(cp["v"], "bf16"), cfg.scale)
+    t4 = time.perf_counter()
+    step_s = t4 - t0
+    return {"value": round(flops / step_s / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": "one full step of the same workload (score, select, compact, float64 "
+                      "attention of all 665 queries x 32 heads)",
+            "stage_s": {"score": round(t1 - t0, 3), "select": round(t2 - t1, 3),
+                        "compact": round(t3 - t2, 3), "attend": round(t4 - t3, 3)},
+            "step_s": round(step_s, 3)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,203 @@
+/*
+ * omnitide.h -- C ABI of the per-chunk stream step of OmniTide on AMD Instinct MI355X (gfx950).
+ *
+ * One step over a KV pool whose slots are tagged with a unit id and a modality:
+ *   1. omnitide_score_units   per-unit modality-weighted key magnitude (OmniPick importance)
+ *   2. omnitide_select_units  budgeted whole-unit retention plan (OmniPick planning)
+ *   3. omnitide_compact_kv    order-preserving packing of the kept rows + chunk (OmniPage)
+ *   4. omnitide_chunk_attn    GQA prefill attention of the chunk over [history || chunk]
+ *
+ * Conventions shared by every entry point
+ *   - Array arguments are DEVICE pointers into memory the caller allocated (hipMalloc or a
+ *     framework allocator), 16-byte aligned, unless the argument is documented as host.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Every call is asynchronous: it
+ *     validates its arguments on the host, enqueues kernels on `stream` and returns.  Inputs must
+ *     stay alive and unmodified until the stream has executed the call.
+ *   - No call allocates or frees memory, and the library keeps no mutable global state; calls on
+ *     distinct streams with distinct buffers may run from several host threads.
+ *   - A segment is one independent pool (one layer, or one stream): every per-segment array is
+ *     laid out segment-major, segments back to back.
+ *   - Return value: OMNITIDE_OK, or a negative code for host-detected misuse, in which case
+ *     nothing was enqueued.  OMNITIDE_E_HIP reports a failed kernel launch.
+ *   - Data-dependent errors are detected on the device and written to *d_status (an int32 device
+ *     word, may be NULL) with "first error wins" semantics (atomic compare-and-swap from 0).  The
+ *     caller zeroes it and reads it after synchronising.  When it is non-zero the outputs of the
+ *     failing call are unspecified but every write stays inside the caller's buffers.
+ *
+ * KV layout: K and V pools are [n_seg][n_slots][n_kv_heads][head_dim] (token-major: one slot's
+ * keys for all KV heads form one contiguous row).  Tags are int32 unit id (-1 = empty slot),
+ * uint8 modality (0 system, 1 video, 2 audio, 3 text) and int32 logical position per slot.
+ * Units are numbered 0..n_units-1 in temporal order; each live unit occupies one contiguous run
+ * of slots, and runs appear in unit order.
+ */
+#ifndef OMNITIDE_H
+#define OMNITIDE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  OMNITIDE_OK = 0,
+  OMNITIDE_E_NULL = -1,       /* a required pointer is NULL */
+  OMNITIDE_E_SHAPE = -2,      /* a size is out of range or inconsistent */
+  OMNITIDE_E_DTYPE = -3,      /* unsupported element type */
+  OMNITIDE_E_WEIGHT = -4,     /* a modality weight is not an exact multiple of 1/256 in (0, 4] */
+  OMNITIDE_E_CAPACITY = -5,   /* destination pool too small (host: static check; device: actual) */
+  OMNITIDE_E_WORKSPACE = -6,  /* workspace pointer NULL or smaller than required */
+  OMNITIDE_E_ALIAS = -7,      /* an output overlaps an input it must not overlap */
+  OMNITIDE_E_HIP = -8,        /* a HIP launch failed */
+  OMNITIDE_E_BUDGET = -16,    /* device: protected (system) tokens exceed the budget */
+  OMNITIDE_E_TAGS = -17       /* device: malformed tags (id or modality out of range, a unit
+                                 not one contiguous run, runs out of unit order) */
+};
+
+enum { OMNITIDE_BF16 = 0, OMNITIDE_F32 = 1 };
+enum { OMNITIDE_MOD_SYS = 0, OMNITIDE_MOD_VIDEO = 1, OMNITIDE_MOD_AUDIO = 2, OMNITIDE_MOD_TEXT = 3 };
+
+/* Limits checked on the host. */
+#define OMNITIDE_MAX_UNITS 8192       /* units per segment */
+#define OMNITIDE_MAX_ROW_ELEMS 4096   /* n_kv_heads * head_dim */
+
+/*
+ * omnitide_score_units -- unit importance (paper: OmniPick; Introduction, OmniPick paragraph:
+ * the budget beyond the protected prefix and recent window goes by modality importance;
+ * Modality-asymmetric attention).  The paper's planner reads only metadata and prints no score;
+ * this entry point computes this library's importance statistic:
+ *   q(x)  = floor(min(|x|, 32) * 2^16)        (NaN and +-Inf count as 32)
+ *   a_s   = sum of q over the n_kv_heads*head_dim key elements of slot s
+ *   W_u   = sum over live slots s of unit u of w[modality(s)] * a_s, w in units of 1/256
+ * Exact integer arithmetic: the result does not depend on the order of summation.
+ *
+ *   k          [n_seg][n_slots][n_kv_heads][head_dim], dtype OMNITIDE_BF16 or OMNITIDE_F32
+ *   unit_id    int32 [n_seg][n_slots]; -1 marks an empty slot
+ *   modality   uint8 [n_seg][n_slots]
+ *   weights    HOST float[4], weight per modality tag; each an exact multiple of 1/256 in (0, 4]
+ *   outputs, [n_seg][n_units] each, fully overwritten:
+ *     unit_wsum        uint64  W_u
+ *     unit_len         int32   live slots of u
+ *     unit_first_slot  int32   first slot of u (n_slots if u has none)
+ *     unit_last_slot   int32   last slot of u (-1 if u has none)
+ *     unit_flags       uint32  bit 0: u holds a system-modality token
+ *   d_status   device: OMNITIDE_E_TAGS for a unit id outside [-1, n_units) or a modality > 3
+ *              (such a slot is then ignored).
+ * Limits: n_seg >= 1, n_slots >= 0, 1 <= n_units <= 8192, head_dim in {64, 128},
+ * n_kv_heads >= 1, n_kv_heads * head_dim <= 4096.
+ */
+int omnitide_score_units(const void* k, int dtype, int n_seg, int n_slots, int n_kv_heads,
+                         int head_dim, const int32_t* unit_id, const uint8_t* modality,
+                         const float* weights, int n_units, uint64_t* unit_wsum,
+                         int32_t* unit_len, int32_t* unit_first_slot, int32_t* unit_last_slot,
+                         uint32_t* unit_flags, int32_t* d_status, void* stream);
+
+/*
+ * omnitide_select_units -- whole-unit retention plan (paper: Structure-aware retention
+ * planning: system prefix protected, most recent units kept whole, older history kept until a
+ * budget is used up; Overview: must-keep / recent-context / selected-history groups).
+ * Per segment, with len_u > 0 marking live units:
+ *   T_sys  = tokens of units with flag bit 0 (protected); T_sys > budget -> OMNITIDE_E_BUDGET
+ *   recent = newest live non-system units, walked newest to oldest, added while their total
+ *            stays <= min(recent_tokens, budget - T_sys); the walk stops at the first misfit
+ *   score_u = floor(W_u / len_u); the remaining live units are ranked by (score desc, unit id
+ *            desc: ties go to the newer unit) and kept in rank order while they fit into
+ *            budget - T_sys - T_recent; the walk stops at the first that does not fit.
+ *   Inputs are omnitide_score_units' outputs ([n_seg][n_units] each).
+ *   unit_score   uint64 [n_seg][n_units]   floor(W_u / len_u), 0 for units without slots
+ *   keep         uint8  [n_seg][n_units]   1 = unit retained whole
+ *   kept_tokens  int32  [n_seg]            retained history tokens (<= budget)
+ *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run or runs are out
+ *                of unit order; OMNITIDE_E_BUDGET as above.  On either error the segment's
+ *                keep is all 0 and kept_tokens 0.
+ * Limits: 1 <= n_units <= 8192, budget_tokens >= 0, recent_tokens >= 0.  One workgroup per
+ * segment; latency-bound.
+ */
+int omnitide_select_units(const uint64_t* unit_wsum, const int32_t* unit_len,
+                          const int32_t* unit_first_slot, const int32_t* unit_last_slot,
+                          const uint32_t* unit_flags, int n_seg, int n_units, int budget_tokens,
+                          int recent_tokens, uint64_t* unit_score, uint8_t* keep,
+                          int32_t* kept_tokens, int32_t* d_status, void* stream);
+
+/*
+ * omnitide_compact_kv -- eager, order-preserving, out-of-place packing (paper: OmniPage;
+ * Compaction-movement trade-off: eager compaction packs every retained entry into a contiguous
+ * prefix; Selective migration, ordered-suffix mode with the cut at slot 0; Executing accepted
+ * moves: one source-to-destination map; Applying the retention plan: each retained token's
+ * position drops by the number of deleted tokens before it).
+ * Per segment: destination row r < kept holds the r-th slot, in slot order, of the units with
+ * keep != 0; rows [kept, kept + chunk_len) hold the chunk.  K and V rows are copied verbatim.
+ *   k_src, v_src      [n_seg][n_slots_src][n_kv_heads][head_dim], dtype
+ *   unit_id_src, modality_src, pos_src   per-slot tags [n_seg][n_slots_src]
+ *   keep, unit_len, unit_first_slot      [n_seg][n_units] (select's and score's outputs)
+ *   k_chunk, v_chunk  [n_seg][chunk_len][n_kv_heads][head_dim] (may be NULL iff chunk_len == 0)
+ *   chunk_modality    uint8 [chunk_len], chunk_unit int32 [chunk_len]: the chunk's modality
+ *                     and unit index (0.. in order), shared by all segments
+ *   k_dst, v_dst      [n_seg][cap_dst][n_kv_heads][head_dim]; rows >= n_ctx untouched
+ *   unit_id_dst       int32 [n_seg][cap_dst]: kept units renumbered 0.. in order, chunk units
+ *                     after them; rows >= n_ctx are set to -1 (empty), so the destination is a
+ *                     complete pool that can be the source of the next step (n_slots = cap_dst)
+ *   modality_dst      uint8 [n_seg][cap_dst] (0 for rows >= n_ctx)
+ *   pos_dst           int32 [n_seg][cap_dst]: pos_src - (deleted live slots before the source
+ *                     slot); chunk row i gets kept + i; -1 for rows >= n_ctx
+ *   src_of_dst        int32 [n_seg][cap_dst]: source slot of each row, -1 for chunk rows and
+ *                     rows >= n_ctx
+ *   unit_remap        int32 [n_seg][n_units]: new id of each unit, -1 if dropped
+ *   n_ctx, n_pages    int32 [n_seg]: kept + chunk_len, ceil(n_ctx / page_size)
+ *   workspace         device scratch of omnitide_compact_workspace_bytes() bytes
+ *   d_status          OMNITIDE_E_CAPACITY if kept + chunk_len > cap_dst (n_ctx and n_pages
+ *                     are then 0, no K/V row is written and every tag row is empty)
+ * The source and destination pools (and tag arrays) must not overlap (OMNITIDE_E_ALIAS).
+ * Limits: page_size in {32, 64, 128, 256}; cap_dst >= chunk_len; others as for score.
+ */
+int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_seg,
+                        int n_slots_src, int n_kv_heads, int head_dim, int page_size,
+                        const int32_t* unit_id_src, const uint8_t* modality_src,
+                        const int32_t* pos_src, const uint8_t* keep, const int32_t* unit_len,
+                        const int32_t* unit_first_slot, int n_units, const void* k_chunk,
+                        const void* v_chunk, const uint8_t* chunk_modality,
+                        const int32_t* chunk_unit, int chunk_len, void* k_dst, void* v_dst,
+                        int cap_dst, int32_t* unit_id_dst, uint8_t* modality_dst,
+                        int32_t* pos_dst, int32_t* src_of_dst, int32_t* unit_remap,
+                        int32_t* n_ctx, int32_t* n_pages, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream);
+
+size_t omnitide_compact_workspace_bytes(int n_seg, int n_units, int cap_dst);
+
+/*
+ * omnitide_chunk_attn -- grouped-query prefill attention of the new chunk over the compacted
+ * history plus the chunk (paper: Background, prefill appends the new input's KV and attends over
+ * the cache; Retention-aware paging: after packing, attention traverses the contiguous rows
+ * [0, n_ctx)).  For query position i in [0, chunk_len) and query head h:
+ *   out[i][h] = sum_j softmax_j(scale * <q[i][h], k[j][g]>) v[j][g],  g = h / (n_q_heads/n_kv_heads)
+ *   over keys j <= n_ctx - chunk_len + i (causal, anchored bottom-right).
+ *   q      bf16 [n_seg][chunk_len][n_q_heads][head_dim]
+ *   k, v   bf16 [n_seg][cap][n_kv_heads][head_dim]: the pools written by omnitide_compact_kv
+ *          (the chunk's own keys are the last chunk_len rows before n_ctx)
+ *   n_ctx  int32 [n_seg], device: rows in use; chunk_len <= n_ctx <= cap is required (device
+ *          check: OMNITIDE_E_CAPACITY, the segment's output is then not written)
+ *   out    float32 [n_seg][chunk_len][n_q_heads][head_dim]
+ *   workspace  device scratch of omnitide_attn_workspace_bytes() bytes (split-KV partials)
+ * Numerics: bf16 inputs, bf16 matrix-core products with fp32 accumulation, fp32 softmax.
+ * Limits: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0; chunk_len >= 1; cap >= chunk_len.
+ */
+int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                        int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                        int head_dim, float scale, float* out, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream);
+
+size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
+                                     int n_kv_heads, int head_dim);
+
+/* Static description of a status code. */
+const char* omnitide_status_string(int code);
+
+/* Library version string. */
+const char* omnitide_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OMNITIDE_H */

@@ -1,0 +1,265 @@
+// C ABI of the OmniTide stream step: host-side validation, then kernel launches.
+//
+// Validation runs before any HIP runtime call, so a misuse error is returned without touching
+// the device (and can be exercised on a machine with no GPU).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <initializer_list>
+
+#include "kernels.h"
+#include "omnitide.h"
+
+namespace {
+
+using omnitide::AttnArgs;
+using omnitide::CompactArgs;
+
+struct Range {
+  const void* p;
+  size_t bytes;
+};
+
+bool overlaps(Range a, Range b) {
+  if (a.p == nullptr || b.p == nullptr || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// Every output range must be disjoint from every input range and from every other output.
+bool any_alias(std::initializer_list<Range> outs, std::initializer_list<Range> ins) {
+  for (auto o = outs.begin(); o != outs.end(); ++o) {
+    for (const Range& i : ins)
+      if (overlaps(*o, i)) return true;
+    for (auto o2 = o + 1; o2 != outs.end(); ++o2)
+      if (overlaps(*o, *o2)) return true;
+  }
+  return false;
+}
+
+bool all_set(std::initializer_list<const void*> ptrs) {
+  for (const void* p : ptrs)
+    if (p == nullptr) return false;
+  return true;
+}
+
+int elt_bytes(int dtype) { return dtype == OMNITIDE_BF16 ? 2 : dtype == OMNITIDE_F32 ? 4 : 0; }
+
+bool row_ok(int n_kv_heads, int head_dim) {
+  return (head_dim == 64 || head_dim == 128) && n_kv_heads >= 1 &&
+         static_cast<long>(n_kv_heads) * head_dim <= OMNITIDE_MAX_ROW_ELEMS;
+}
+
+constexpr int kMaxGridY = 65535;
+
+int hip_status(hipError_t e) { return e == hipSuccess ? OMNITIDE_OK : OMNITIDE_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int omnitide_score_units(const void* k, int dtype, int n_seg, int n_slots, int n_kv_heads,
+                         int head_dim, const int32_t* unit_id, const uint8_t* modality,
+                         const float* weights, int n_units, uint64_t* unit_wsum,
+                         int32_t* unit_len, int32_t* unit_first_slot, int32_t* unit_last_slot,
+                         uint32_t* unit_flags, int32_t* d_status, void* stream) {
+  if (!all_set({unit_wsum, unit_len, unit_first_slot, unit_last_slot, unit_flags, weights}))
+    return OMNITIDE_E_NULL;
+  if (n_slots > 0 && !all_set({k, unit_id, modality})) return OMNITIDE_E_NULL;
+  const int eb = elt_bytes(dtype);
+  if (eb == 0) return OMNITIDE_E_DTYPE;
+  if (n_seg < 1 || n_seg > kMaxGridY || n_slots < 0 || n_units < 1 ||
+      n_units > OMNITIDE_MAX_UNITS || !row_ok(n_kv_heads, head_dim) ||
+      static_cast<long>(n_seg) * n_units > INT32_MAX)
+    return OMNITIDE_E_SHAPE;
+  uint32_t wq[4];
+  for (int i = 0; i < 4; ++i) {
+    const double w = static_cast<double>(weights[i]) * 256.0;
+    if (!(w >= 1.0 && w <= 1024.0) || std::floor(w) != w) return OMNITIDE_E_WEIGHT;
+    wq[i] = static_cast<uint32_t>(w);
+  }
+  const size_t slots = static_cast<size_t>(n_seg) * n_slots;
+  const size_t units = static_cast<size_t>(n_seg) * n_units;
+  const int row_elems = n_kv_heads * head_dim;
+  if (any_alias({{unit_wsum, units * 8}, {unit_len, units * 4}, {unit_first_slot, units * 4},
+                 {unit_last_slot, units * 4}, {unit_flags, units * 4}, {d_status, 4}},
+                {{k, slots * row_elems * eb}, {unit_id, slots * 4}, {modality, slots}}))
+    return OMNITIDE_E_ALIAS;
+  return hip_status(omnitide::launch_score(
+      k, dtype, n_seg, n_slots, row_elems, unit_id, modality, wq, n_units, unit_wsum, unit_len,
+      unit_first_slot, unit_last_slot, unit_flags, d_status, static_cast<hipStream_t>(stream)));
+}
+
+int omnitide_select_units(const uint64_t* unit_wsum, const int32_t* unit_len,
+                          const int32_t* unit_first_slot, const int32_t* unit_last_slot,
+                          const uint32_t* unit_flags, int n_seg, int n_units, int budget_tokens,
+                          int recent_tokens, uint64_t* unit_score, uint8_t* keep,
+                          int32_t* kept_tokens, int32_t* d_status, void* stream) {
+  if (!all_set({unit_wsum, unit_len, unit_first_slot, unit_last_slot, unit_flags, unit_score,
+                keep, kept_tokens}))
+    return OMNITIDE_E_NULL;
+  if (n_seg < 1 || n_units < 1 || n_units > OMNITIDE_MAX_UNITS || budget_tokens < 0 ||
+      recent_tokens < 0 || static_cast<long>(n_seg) * n_units > INT32_MAX)
+    return OMNITIDE_E_SHAPE;
+  const size_t units = static_cast<size_t>(n_seg) * n_units;
+  if (any_alias({{unit_score, units * 8}, {keep, units}, {kept_tokens, n_seg * 4ull},
+                 {d_status, 4}},
+                {{unit_wsum, units * 8}, {unit_len, units * 4}, {unit_first_slot, units * 4},
+                 {unit_last_slot, units * 4}, {unit_flags, units * 4}}))
+    return OMNITIDE_E_ALIAS;
+  return hip_status(omnitide::launch_select(unit_wsum, unit_len, unit_first_slot,
+                                            unit_last_slot, unit_flags, n_seg, n_units,
+                                            budget_tokens, recent_tokens, unit_score, keep,
+                                            kept_tokens, d_status,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+size_t omnitide_compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
+  if (n_seg < 1 || n_units < 1 || cap_dst < 0) return 0;
+  return omnitide::compact_workspace_bytes(n_seg, n_units, cap_dst);
+}
+
+int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_seg,
+                        int n_slots_src, int n_kv_heads, int head_dim, int page_size,
+                        const int32_t* unit_id_src, const uint8_t* modality_src,
+                        const int32_t* pos_src, const uint8_t* keep, const int32_t* unit_len,
+                        const int32_t* unit_first_slot, int n_units, const void* k_chunk,
+                        const void* v_chunk, const uint8_t* chunk_modality,
+                        const int32_t* chunk_unit, int chunk_len, void* k_dst, void* v_dst,
+                        int cap_dst, int32_t* unit_id_dst, uint8_t* modality_dst,
+                        int32_t* pos_dst, int32_t* src_of_dst, int32_t* unit_remap,
+                        int32_t* n_ctx, int32_t* n_pages, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream) {
+  if (!all_set({keep, unit_len, unit_first_slot, k_dst, v_dst, unit_id_dst, modality_dst,
+                pos_dst, src_of_dst, unit_remap, n_ctx, n_pages}))
+    return OMNITIDE_E_NULL;
+  if (n_slots_src > 0 && !all_set({k_src, v_src, unit_id_src, modality_src, pos_src}))
+    return OMNITIDE_E_NULL;
+  if (chunk_len > 0 && !all_set({k_chunk, v_chunk, chunk_modality, chunk_unit}))
+    return OMNITIDE_E_NULL;
+  const int eb = elt_bytes(dtype);
+  if (eb == 0) return OMNITIDE_E_DTYPE;
+  if (n_seg < 1 || n_seg > kMaxGridY || n_slots_src < 0 || n_units < 1 ||
+      n_units > OMNITIDE_MAX_UNITS || !row_ok(n_kv_heads, head_dim) || chunk_len < 0 ||
+      !(page_size == 32 || page_size == 64 || page_size == 128 || page_size == 256) ||
+      static_cast<long>(n_seg) * n_units > INT32_MAX)
+    return OMNITIDE_E_SHAPE;
+  if (cap_dst < chunk_len || cap_dst < 1) return OMNITIDE_E_CAPACITY;
+  const size_t need = omnitide::compact_workspace_bytes(n_seg, n_units, cap_dst);
+  if (workspace == nullptr || workspace_bytes < need) return OMNITIDE_E_WORKSPACE;
+  const size_t row = static_cast<size_t>(n_kv_heads) * head_dim * eb;
+  const size_t src_slots = static_cast<size_t>(n_seg) * n_slots_src;
+  const size_t dst_slots = static_cast<size_t>(n_seg) * cap_dst;
+  const size_t units = static_cast<size_t>(n_seg) * n_units;
+  const size_t chunk_rows = static_cast<size_t>(n_seg) * chunk_len;
+  if (any_alias({{k_dst, dst_slots * row}, {v_dst, dst_slots * row}, {unit_id_dst, dst_slots * 4},
+                 {modality_dst, dst_slots}, {pos_dst, dst_slots * 4}, {src_of_dst, dst_slots * 4},
+                 {unit_remap, units * 4}, {n_ctx, n_seg * 4ull}, {n_pages, n_seg * 4ull},
+                 {workspace, need}, {d_status, 4}},
+                {{k_src, src_slots * row}, {v_src, src_slots * row}, {unit_id_src, src_slots * 4},
+                 {modality_src, src_slots}, {pos_src, src_slots * 4}, {keep, units},
+                 {unit_len, units * 4}, {unit_first_slot, units * 4},
+                 {k_chunk, chunk_rows * row}, {v_chunk, chunk_rows * row},
+                 {chunk_modality, static_cast<size_t>(chunk_len)},
+                 {chunk_unit, static_cast<size_t>(chunk_len) * 4}}))
+    return OMNITIDE_E_ALIAS;
+  CompactArgs a;
+  a.k_src = k_src;
+  a.v_src = v_src;
+  a.n_seg = n_seg;
+  a.n_slots_src = n_slots_src;
+  a.row_bytes = static_cast<int>(row);
+  a.page_size = page_size;
+  a.unit_id_src = unit_id_src;
+  a.modality_src = modality_src;
+  a.pos_src = pos_src;
+  a.keep = keep;
+  a.unit_len = unit_len;
+  a.unit_first = unit_first_slot;
+  a.n_units = n_units;
+  a.k_chunk = k_chunk;
+  a.v_chunk = v_chunk;
+  a.chunk_modality = chunk_modality;
+  a.chunk_unit = chunk_unit;
+  a.chunk_len = chunk_len;
+  a.k_dst = k_dst;
+  a.v_dst = v_dst;
+  a.cap_dst = cap_dst;
+  a.unit_id_dst = unit_id_dst;
+  a.modality_dst = modality_dst;
+  a.pos_dst = pos_dst;
+  a.src_of_dst = src_of_dst;
+  a.unit_remap = unit_remap;
+  a.n_ctx = n_ctx;
+  a.n_pages = n_pages;
+  a.workspace = workspace;
+  a.d_status = d_status;
+  return hip_status(omnitide::launch_compact(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
+                                     int n_kv_heads, int head_dim) {
+  if (n_seg < 1 || cap < 1 || chunk_len < 1 || n_kv_heads < 1 || n_q_heads < n_kv_heads ||
+      n_q_heads % n_kv_heads != 0 || !(head_dim == 64 || head_dim == 128))
+    return 0;
+  return omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
+}
+
+int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                        int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                        int head_dim, float scale, float* out, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream) {
+  if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
+  if (n_seg < 1 || n_seg > kMaxGridY || chunk_len < 1 || n_kv_heads < 1 ||
+      n_q_heads < n_kv_heads || n_q_heads % n_kv_heads != 0 ||
+      !(head_dim == 64 || head_dim == 128) || !std::isfinite(scale) ||
+      static_cast<long>(chunk_len) * (n_q_heads / n_kv_heads) > (1L << 30))
+    return OMNITIDE_E_SHAPE;
+  if (cap < chunk_len) return OMNITIDE_E_CAPACITY;
+  const size_t need =
+      omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return OMNITIDE_E_WORKSPACE;
+  const size_t qrows = static_cast<size_t>(n_seg) * chunk_len * n_q_heads;
+  const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * 2;
+  if (any_alias({{out, qrows * head_dim * 4}, {workspace, need}, {d_status, 4}},
+                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull}}))
+    return OMNITIDE_E_ALIAS;
+  AttnArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.n_ctx = n_ctx;
+  a.n_seg = n_seg;
+  a.cap = cap;
+  a.chunk_len = chunk_len;
+  a.n_q_heads = n_q_heads;
+  a.n_kv_heads = n_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  a.out = out;
+  a.workspace = need > 0 ? workspace : nullptr;
+  a.d_status = d_status;
+  return hip_status(omnitide::launch_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+const char* omnitide_status_string(int code) {
+  switch (code) {
+    case OMNITIDE_OK: return "ok";
+    case OMNITIDE_E_NULL: return "a required pointer is NULL";
+    case OMNITIDE_E_SHAPE: return "a size is out of range or inconsistent";
+    case OMNITIDE_E_DTYPE: return "unsupported element type";
+    case OMNITIDE_E_WEIGHT: return "modality weight is not an exact multiple of 1/256 in (0, 4]";
+    case OMNITIDE_E_CAPACITY: return "destination pool too small";
+    case OMNITIDE_E_WORKSPACE: return "workspace missing or too small";
+    case OMNITIDE_E_ALIAS: return "an output overlaps an input or another output";
+    case OMNITIDE_E_HIP: return "HIP kernel launch failed";
+    case OMNITIDE_E_BUDGET: return "protected tokens exceed the retention budget";
+    case OMNITIDE_E_TAGS: return "malformed unit/modality tags";
+    default: return "unknown status";
+  }
+}
+
+const char* omnitide_version(void) { return "omnitide-mi355x 0.1.0 (gfx950)"; }
+
+}  // extern "C"

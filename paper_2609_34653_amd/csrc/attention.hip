@@ -1,0 +1,364 @@
+// Chunk prefill attention over [compacted history || chunk]: flash-style, bf16 MFMA on gfx950.
+//
+// Decomposition
+//   rows     for KV head g the L*G query rows (position p, head g*G + r) are flattened as
+//            m = p*G + r and tiled 128 per workgroup (4 waves x 32): GQA packing, so one K/V
+//            tile staged in LDS serves G query heads.
+//   keys     64-key tiles; a workgroup's key range ends at its last row's causal limit; with
+//            n_split > 1 the tile range is cut into equal parts and a combine kernel merges the
+//            partial (O, max, sum) in fixed split order.
+//   products S^T = K Q^T and O^T = V^T P^T with v_mfma_f32_32x32x16_bf16.  Computing the
+//            transposed scores puts one query column in each lane, so the softmax row statistics
+//            are lane-local (plus one exchange between the two 32-lane halves).
+//   layout   the keys of an S^T tile are permuted when K rows are read from LDS so that lane half
+//            h holds keys 16h..16h+15 of the tile in register order; its probabilities then form
+//            the B operand of the P*V product directly (8 consecutive keys per operand).  V is
+//            stored transposed in LDS (V^T, keys contiguous) by an in-register 4x8 transpose
+//            while staging, so each V^T operand is one 16-byte LDS read.
+//   softmax  fp32, base-2 exponent with scale*log2(e) folded into the scores; the causal mask is
+//            applied only to tiles that reach past the workgroup's first row's limit.
+//   order    workgroups that share a (KV head, split) are mapped onto one XCD (workgroups are
+//            dealt round-robin over 8 XCDs), so their K/V re-reads hit that XCD's L2.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace omnitide {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kAttnWaves = 4;
+constexpr int kAttnThreads = kAttnWaves * kWave;
+constexpr int kKT = 64;                  // keys per tile
+constexpr int kRowsWG = kAttnWaves * 32; // query rows per workgroup
+constexpr int kNumXcd = 8;
+constexpr int kTargetWGs = 512;          // two resident workgroups on each of 256 CUs
+
+template <int D>
+struct Smem {
+  static constexpr int KS = D + 8;       // K row stride (bf16 elements), 16-byte multiple
+  static constexpr int VS = kKT + 8;     // V^T row stride (bf16 elements)
+  static constexpr int K_ELEMS = kKT * KS;
+  static constexpr int V_ELEMS = D * VS;
+  static constexpr int K_VECS = kKT * D / 8 / kAttnThreads;   // 16-byte K loads per thread
+  static constexpr int V_BLOCKS = 2 * D;                      // 4-key x 8-dim V blocks per tile
+};
+
+__device__ inline floatx16 mfma(bf16x8 a, bf16x8 b, floatx16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// S^T row r of a 32x32 MFMA tile holds key perm_key(r): lane half h, accumulator i <-> key 16h+i.
+__device__ inline int perm_key(int r) { return 16 * ((r & 7) >> 2) + 4 * (r >> 3) + (r & 3); }
+
+__device__ inline u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+template <int D>
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int L, int Hq,
+    int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
+    float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status) {
+  using S = Smem<D>;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[S::K_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[S::V_ELEMS];
+
+  const int seg = blockIdx.y;
+  const int nctx = n_ctx_g[seg];
+  if (nctx < L || nctx > cap) {
+    if (threadIdx.x == 0) set_status(status, OMNITIDE_E_CAPACITY);
+    return;
+  }
+  // XCD-aware order: blocks b with equal b % 8 run on one XCD; give them consecutive work ids.
+  const int nb = gridDim.x, b = blockIdx.x;
+  const int xcd = b % kNumXcd, q8 = nb / kNumXcd, r8 = nb % kNumXcd;
+  const int lin = (xcd < r8 ? xcd * (q8 + 1) : r8 * (q8 + 1) + (xcd - r8) * q8) + b / kNumXcd;
+  const int mt = lin % n_mt;
+  const int split = (lin / n_mt) % n_split;
+  const int g = lin / (n_mt * n_split);
+
+  const int G = Hq / Hkv;
+  const int rows = L * G;
+  const int kept = nctx - L;
+  const int m0 = mt * kRowsWG;
+  const int p_lo = m0 / G;
+  const int p_hi = min(L - 1, (m0 + kRowsWG - 1) / G);
+  const int kmax = kept + p_hi + 1;               // keys [0, kmax) are needed by this workgroup
+  const int n_tiles = (kmax + kKT - 1) / kKT;
+  const int t_begin = static_cast<int>(static_cast<long>(n_tiles) * split / n_split);
+  const int t_end = static_cast<int>(static_cast<long>(n_tiles) * (split + 1) / n_split);
+  const int full_lim = kept + p_lo;               // keys <= full_lim are visible to every row
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int col = lane & 31;
+  const int h = lane >> 5;
+  const int m = m0 + wave * 32 + col;
+  const bool row_ok = m < rows;
+  const int p = row_ok ? m / G : L - 1;
+  const int head = g * G + (row_ok ? m % G : 0);
+  const int lim = kept + p;
+
+  // Q^T operand: lane holds q[p][head][16c + 8h .. +8] for every 16-wide chunk c of d.
+  bf16x8 qf[D / 16];
+  {
+    const uint16_t* qrow = q + ((static_cast<size_t>(seg) * L + p) * Hq + head) * D;
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) {
+      u32x4 t = row_ok ? ld16(qrow + 16 * c + 8 * h) : u32x4{0, 0, 0, 0};
+      qf[c] = __builtin_bit_cast(bf16x8, t);
+    }
+  }
+
+  const size_t kv_seg = static_cast<size_t>(seg) * cap;
+  auto kv_row = [&](const uint16_t* base, int key) {
+    return base + ((kv_seg + key) * Hkv + g) * D;
+  };
+
+  constexpr int VB = S::V_BLOCKS > kAttnThreads ? S::V_BLOCKS / kAttnThreads : 1;
+  u32x4 kreg[S::K_VECS];
+  u32x4 vreg[VB][4];
+  auto load_tile = [&](int t) {
+    const int j0 = t * kKT;
+#pragma unroll
+    for (int i = 0; i < S::K_VECS; ++i) {
+      const int idx = tid + kAttnThreads * i;
+      const int key = idx / (D / 8), c8 = idx % (D / 8);
+      kreg[i] = (j0 + key < nctx) ? ld16(kv_row(k, j0 + key) + 8 * c8) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int blk = tid + kAttnThreads * i;
+      const int kg = blk / (D / 8), dc = blk % (D / 8);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = j0 + 4 * kg + r;
+        vreg[i][r] = (blk < S::V_BLOCKS && key < nctx) ? ld16(kv_row(v, key) + 8 * dc)
+                                                       : u32x4{0, 0, 0, 0};
+      }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < S::K_VECS; ++i) {
+      const int idx = tid + kAttnThreads * i;
+      const int key = idx / (D / 8), c8 = idx % (D / 8);
+      *reinterpret_cast<u32x4*>(Ks + key * S::KS + 8 * c8) = kreg[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VB; ++i) {
+      const int blk = tid + kAttnThreads * i;
+      if (blk < S::V_BLOCKS) {
+        const int kg = blk / (D / 8), dc = blk % (D / 8);
+        const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
+        const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
+        const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
+        const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const uint32_t sel = e ? 0x07060302u : 0x05040100u;
+            uint2 o;
+            o.x = __builtin_amdgcn_perm(w1[a], w0[a], sel);
+            o.y = __builtin_amdgcn_perm(w3[a], w2[a], sel);
+            *reinterpret_cast<uint2*>(Vt + (8 * dc + 2 * a + e) * S::VS + 4 * kg) = o;
+          }
+        }
+      }
+    }
+  };
+
+  floatx16 o[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt) o[dt] = floatx16{};
+  float m_run = -INFINITY, l_run = 0.f;
+  const int krow = perm_key(col);
+
+  if (t_begin < t_end) load_tile(t_begin);
+  for (int t = t_begin; t < t_end; ++t) {
+    const int j0 = t * kKT;
+    __syncthreads();
+    store_tile();
+    __syncthreads();
+    if (t + 1 < t_end) load_tile(t + 1);
+
+    floatx16 s[2] = {floatx16{}, floatx16{}};
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const bf16x8 a =
+            __builtin_bit_cast(bf16x8, ld16(Ks + (32 * st + krow) * S::KS + 16 * c + 8 * h));
+        s[st] = mfma(a, qf[c], s[st]);
+      }
+    }
+    float mx = -INFINITY;
+    const bool need_mask = j0 + kKT - 1 > full_lim;
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float x = s[st][i] * scale_log2;
+        if (need_mask && j0 + 32 * st + 16 * h + i > lim) x = -INFINITY;
+        s[st][i] = x;
+        mx = fmaxf(mx, x);
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(m_run - m_use);
+    m_run = m_new;
+    float lsum = 0.f;
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float e = exp2f(s[st][i] - m_use);
+        lsum += e;
+        pf[st][i / 8][i % 8] = static_cast<__bf16>(e);
+      }
+    }
+    l_run = l_run * alpha + lsum;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+          const bf16x8 a = __builtin_bit_cast(
+              bf16x8, ld16(Vt + (32 * dt + col) * S::VS + 32 * st + 16 * h + 8 * cc));
+          o[dt] = mfma(a, pf[st][cc], o[dt]);
+        }
+      }
+    }
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  if (!row_ok) return;
+  const size_t orow = (static_cast<size_t>(seg) * L + p) * Hq + head;
+  if (n_split == 1) {
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    float* dst = out + orow * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        float4 val = make_float4(o[dt][4 * qd] * inv, o[dt][4 * qd + 1] * inv,
+                                 o[dt][4 * qd + 2] * inv, o[dt][4 * qd + 3] * inv);
+        *reinterpret_cast<float4*>(dst + 32 * dt + 8 * qd + 4 * h) = val;
+      }
+    }
+  } else {
+    const size_t n_rows_all = static_cast<size_t>(gridDim.y) * L * Hq;
+    const size_t prow = static_cast<size_t>(split) * n_rows_all + orow;
+    float* dst = part_o + prow * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        float4 val = make_float4(o[dt][4 * qd], o[dt][4 * qd + 1], o[dt][4 * qd + 2],
+                                 o[dt][4 * qd + 3]);
+        *reinterpret_cast<float4*>(dst + 32 * dt + 8 * qd + 4 * h) = val;
+      }
+    }
+    if (h == 0) *reinterpret_cast<float2*>(part_ml + 2 * prow) = make_float2(m_run, l_tot);
+  }
+}
+
+// Merge split partials: out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, splits in order.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
+                                                           const float* __restrict__ part_ml,
+                                                           int n_split, size_t n_rows,
+                                                           const int32_t* __restrict__ n_ctx_g,
+                                                           int L, int Hq, int cap,
+                                                           float* __restrict__ out) {
+  constexpr int TPR = D / 4;                       // threads per row, 4 floats each
+  const size_t row = static_cast<size_t>(blockIdx.x) * (256 / TPR) + threadIdx.x / TPR;
+  if (row >= n_rows) return;
+  const int seg = static_cast<int>(row / (static_cast<size_t>(L) * Hq));
+  const int nctx = n_ctx_g[seg];
+  if (nctx < L || nctx > cap) return;
+  const int d4 = threadIdx.x % TPR;
+  float M = -INFINITY;
+  for (int s = 0; s < n_split; ++s) M = fmaxf(M, part_ml[2 * (s * n_rows + row)]);
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
+  for (int s = 0; s < n_split; ++s) {
+    const float ms = part_ml[2 * (s * n_rows + row)];
+    const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
+    den += w * part_ml[2 * (s * n_rows + row) + 1];
+    const float4 ov = *reinterpret_cast<const float4*>(part_o + (s * n_rows + row) * D + 4 * d4);
+    num.x += w * ov.x;
+    num.y += w * ov.y;
+    num.z += w * ov.z;
+    num.w += w * ov.w;
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  *reinterpret_cast<float4*>(out + row * D + 4 * d4) =
+      make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
+}
+
+template <int D>
+hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int n_mt = (a.chunk_len * G + kRowsWG - 1) / kRowsWG;
+  const dim3 grid(n_mt * a.n_kv_heads * n_split, a.n_seg);
+  const size_t n_rows = static_cast<size_t>(a.n_seg) * a.chunk_len * a.n_q_heads;
+  float* part_o = static_cast<float*>(a.workspace);
+  float* part_ml = part_o ? part_o + static_cast<size_t>(n_split) * n_rows * D : nullptr;
+  const float scale_log2 = a.scale * 1.4426950408889634f;
+  hipLaunchKernelGGL((attn_kernel<D>), grid, dim3(kAttnThreads), 0, stream,
+                     static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                     static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
+                     a.n_q_heads, a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_mt,
+                     n_split, a.d_status);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || n_split == 1) return e;
+  constexpr int rows_per_block = 256 / (D / 4);
+  const unsigned blocks = static_cast<unsigned>((n_rows + rows_per_block - 1) / rows_per_block);
+  hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(blocks), dim3(256), 0, stream, part_o,
+                     part_ml, n_split, n_rows, a.n_ctx, a.chunk_len, a.n_q_heads, a.cap, a.out);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                    int head_dim) {
+  (void)head_dim;
+  const int G = n_q_heads / n_kv_heads;
+  const long n_mt = (static_cast<long>(chunk_len) * G + kRowsWG - 1) / kRowsWG;
+  const long base = n_mt * n_kv_heads * n_seg;
+  const long tiles = (cap + kKT - 1) / kKT;
+  long s = kTargetWGs / base;
+  s = std::min(s, tiles / 4);
+  return static_cast<int>(std::max(1L, std::min(s, 16L)));
+}
+
+size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                            int head_dim) {
+  const int s = attn_num_splits(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
+  if (s == 1) return 0;
+  const size_t rows = static_cast<size_t>(n_seg) * chunk_len * n_q_heads;
+  return static_cast<size_t>(s) * rows * (static_cast<size_t>(head_dim) + 2) * sizeof(float);
+}
+
+hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
+  const int s = attn_num_splits(a.n_seg, a.cap, a.chunk_len, a.n_q_heads, a.n_kv_heads,
+                                a.head_dim);
+  if (a.head_dim == 128) return launch_attn_t<128>(a, s, stream);
+  if (a.head_dim == 64) return launch_attn_t<64>(a, s, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace omnitide

@@ -1,0 +1,259 @@
+// Eager, order-preserving, out-of-place compaction of the retained rows plus the chunk append.
+//
+// Two kernels on the caller's stream:
+//   plan  one workgroup per segment.  Exclusive scans over units give each kept unit its
+//         destination offset, its rank (= new unit id) and the number of deleted live tokens
+//         before it; a rank table {offset, first slot, deleted-before} with a sentinel, and for
+//         every destination tile the rank of the unit holding its first row, go to the workspace.
+//   copy  one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
+//         source slots from the rank table (short forward walk from the tile's hint), tags are
+//         written, then every thread moves 16-byte vectors of the K and V rows.  Rows are whole
+//         2 KB (bf16, 8 heads x 128) runs, so reads and writes are fully coalesced; source and
+//         destination never alias, so a single pass is safe (no scratch round trip).
+#include "common.h"
+#include "kernels.h"
+
+namespace omnitide {
+namespace {
+
+constexpr int kPlanThreads = 1024;
+constexpr int kPer = OMNITIDE_MAX_UNITS / kPlanThreads;
+constexpr int kTile = 32;           // destination rows per copy workgroup
+constexpr int kCopyThreads = 256;
+
+struct RankRec {
+  int32_t off;     // destination row of the unit's first token
+  int32_t first;   // source slot of the unit's first token
+  int32_t del;     // deleted live tokens before the unit
+  int32_t pad;
+};
+
+struct WsLayout {
+  size_t rank_off, tile_off, meta_off, seg_bytes;
+};
+
+__host__ __device__ inline WsLayout ws_layout(int n_units, int cap_dst) {
+  WsLayout w;
+  const size_t n_tiles = (static_cast<size_t>(cap_dst) + kTile - 1) / kTile;
+  w.rank_off = 0;
+  w.tile_off = (static_cast<size_t>(n_units) + 1) * sizeof(RankRec);
+  w.meta_off = w.tile_off + ((n_tiles * 4 + 15) / 16) * 16;
+  w.seg_bytes = ((w.meta_off + 16 + 255) / 256) * 256;
+  return w;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
+    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, int n_units, int chunk_len, int cap_dst, int page_size,
+    int32_t* __restrict__ remap_g, int32_t* __restrict__ n_ctx_g,
+    int32_t* __restrict__ n_pages_g, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
+  __shared__ int32_t scr[kPlanThreads / kWave + 1];
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int U = n_units;
+  const int per = (U + kPlanThreads - 1) / kPlanThreads;
+  const int u0 = tid * per;
+  const size_t base = static_cast<size_t>(seg) * U;
+  const WsLayout L = ws_layout(U, cap_dst);
+  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+  RankRec* rank = reinterpret_cast<RankRec*>(wseg + L.rank_off);
+  int32_t* tile_hint = reinterpret_cast<int32_t*>(wseg + L.tile_off);
+  int32_t* meta = reinterpret_cast<int32_t*>(wseg + L.meta_off);
+
+  int kl[kPer], dl[kPer], fs[kPer];
+  int my_k = 0, my_d = 0, my_n = 0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = u0 + i;
+    kl[i] = dl[i] = fs[i] = 0;
+    if (i < per && u < U) {
+      const int n = max(len_g[base + u], 0);
+      const bool kp = keep_g[base + u] != 0;
+      kl[i] = kp ? n : 0;
+      dl[i] = kp ? 0 : n;
+      fs[i] = first_g[base + u];
+    }
+    my_k += kl[i];
+    my_d += dl[i];
+    my_n += kl[i] > 0 ? 1 : 0;
+  }
+  int kept, dropped, n_kept;
+  int off = block_exclusive_scan(my_k, scr, &kept);
+  int del = block_exclusive_scan(my_d, scr, &dropped);
+  int rk = block_exclusive_scan(my_n, scr, &n_kept);
+  (void)dropped;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = u0 + i;
+    if (i < per && u < U) {
+      if (kl[i] > 0) {
+        rank[rk] = RankRec{off, fs[i], del, 0};
+        remap_g[base + u] = rk;
+        for (int t = (off + kTile - 1) / kTile; t * kTile < off + kl[i]; ++t) tile_hint[t] = rk;
+        ++rk;
+      } else {
+        remap_g[base + u] = -1;
+      }
+    }
+    off += kl[i];
+    del += dl[i];
+  }
+  if (tid == 0) {
+    rank[n_kept] = RankRec{kept, 0, 0, 0};
+    const int nctx = kept + chunk_len;
+    meta[0] = kept;
+    meta[1] = n_kept;
+    if (nctx > cap_dst) {
+      set_status(status, OMNITIDE_E_CAPACITY);
+      n_ctx_g[seg] = 0;
+      n_pages_g[seg] = 0;
+    } else {
+      n_ctx_g[seg] = nctx;
+      n_pages_g[seg] = (nctx + page_size - 1) / page_size;
+    }
+  }
+}
+
+template <int VPT>
+__global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
+    const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
+    int row_bytes, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, const uint8_t* __restrict__ k_chunk,
+    const uint8_t* __restrict__ v_chunk, const uint8_t* __restrict__ chunk_mod,
+    const int32_t* __restrict__ chunk_unit, int chunk_len, uint8_t* __restrict__ k_dst,
+    uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
+    uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
+    const uint8_t* __restrict__ ws) {
+  constexpr int RB = VPT >= 16 ? 1 : 16 / VPT;
+  __shared__ int32_t src_row[kTile];
+  const int seg = blockIdx.y;
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int nctx = n_ctx_g[seg];
+  const int r0 = t * kTile;
+  const size_t dst_tag = static_cast<size_t>(seg) * cap_dst;
+  // Rows [n_ctx, cap_dst) become empty slots, so the destination is a complete pool.
+  {
+    const int r = r0 + tid;
+    if (tid < kTile && r >= nctx && r < cap_dst) {
+      uid_dst[dst_tag + r] = -1;
+      mod_dst[dst_tag + r] = 0;
+      pos_dst[dst_tag + r] = -1;
+      src_of_dst[dst_tag + r] = -1;
+    }
+  }
+  if (r0 >= nctx) return;
+  const int nrows = min(kTile, nctx - r0);
+  const int kept = nctx - chunk_len;
+  const WsLayout L = ws_layout(n_units, cap_dst);
+  const uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+  const RankRec* rank = reinterpret_cast<const RankRec*>(wseg + L.rank_off);
+  const int32_t* tile_hint = reinterpret_cast<const int32_t*>(wseg + L.tile_off);
+  const int32_t* meta = reinterpret_cast<const int32_t*>(wseg + L.meta_off);
+  const size_t src_tag = static_cast<size_t>(seg) * n_slots;
+
+  if (tid < nrows) {
+    const int r = r0 + tid;
+    if (r < kept) {
+      int k = tile_hint[t];
+      while (rank[k + 1].off <= r) ++k;
+      const RankRec rec = rank[k];
+      const int s = rec.first + (r - rec.off);
+      uid_dst[dst_tag + r] = k;
+      mod_dst[dst_tag + r] = mod_src[src_tag + s];
+      pos_dst[dst_tag + r] = pos_src[src_tag + s] - rec.del;
+      src_of_dst[dst_tag + r] = s;
+      src_row[tid] = s;
+    } else {
+      const int i = r - kept;
+      uid_dst[dst_tag + r] = meta[1] + chunk_unit[i];
+      mod_dst[dst_tag + r] = chunk_mod[i];
+      pos_dst[dst_tag + r] = kept + i;
+      src_of_dst[dst_tag + r] = -1;
+      src_row[tid] = -1 - i;
+    }
+  }
+  __syncthreads();
+
+  const int row_vecs = row_bytes / 16;
+  const int vecs2 = 2 * row_vecs;       // K row then V row
+  const size_t src_base = static_cast<size_t>(seg) * n_slots;
+  const size_t chunk_base = static_cast<size_t>(seg) * chunk_len;
+  const size_t dst_base = static_cast<size_t>(seg) * cap_dst;
+  for (int rb = 0; rb < nrows; rb += RB) {
+    u32x4 buf[RB][VPT];
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+      const int row = rb + j;
+#pragma unroll
+      for (int v = 0; v < VPT; ++v) {
+        const int f = tid + kCopyThreads * v;
+        buf[j][v] = u32x4{0, 0, 0, 0};
+        if (row < nrows && f < vecs2) {
+          const int s = src_row[row];
+          const bool is_v = f >= row_vecs;
+          const int vec = is_v ? f - row_vecs : f;
+          const uint8_t* src;
+          if (s >= 0)
+            src = (is_v ? v_src : k_src) + (src_base + s) * row_bytes;
+          else
+            src = (is_v ? v_chunk : k_chunk) + (chunk_base + (-1 - s)) * row_bytes;
+          buf[j][v] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + vec);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RB; ++j) {
+      const int row = rb + j;
+#pragma unroll
+      for (int v = 0; v < VPT; ++v) {
+        const int f = tid + kCopyThreads * v;
+        if (row < nrows && f < vecs2) {
+          const bool is_v = f >= row_vecs;
+          const int vec = is_v ? f - row_vecs : f;
+          uint8_t* dst = (is_v ? v_dst : k_dst) + (dst_base + r0 + row) * row_bytes;
+          __builtin_nontemporal_store(buf[j][v], reinterpret_cast<u32x4*>(dst) + vec);
+        }
+      }
+    }
+  }
+}
+
+template <int VPT>
+hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
+  const dim3 grid((a.cap_dst + kTile - 1) / kTile, a.n_seg);
+  hipLaunchKernelGGL((compact_copy_kernel<VPT>), grid, dim3(kCopyThreads), 0, stream,
+                     static_cast<const uint8_t*>(a.k_src), static_cast<const uint8_t*>(a.v_src),
+                     a.n_slots_src, a.row_bytes, a.modality_src, a.pos_src,
+                     static_cast<const uint8_t*>(a.k_chunk), static_cast<const uint8_t*>(a.v_chunk),
+                     a.chunk_modality, a.chunk_unit, a.chunk_len, static_cast<uint8_t*>(a.k_dst),
+                     static_cast<uint8_t*>(a.v_dst), a.cap_dst, a.n_units, a.unit_id_dst,
+                     a.modality_dst, a.pos_dst, a.src_of_dst, a.n_ctx,
+                     static_cast<const uint8_t*>(a.workspace));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
+  return ws_layout(n_units, cap_dst).seg_bytes * static_cast<size_t>(n_seg);
+}
+
+hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream, a.keep,
+                     a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst, a.page_size,
+                     a.unit_remap, a.n_ctx, a.n_pages, static_cast<uint8_t*>(a.workspace),
+                     a.d_status);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int vecs2 = 2 * a.row_bytes / 16;
+  const int vpt = (vecs2 + kCopyThreads - 1) / kCopyThreads;
+  if (vpt <= 1) return launch_copy<1>(a, stream);
+  if (vpt <= 2) return launch_copy<2>(a, stream);
+  if (vpt <= 4) return launch_copy<4>(a, stream);
+  if (vpt <= 8) return launch_copy<8>(a, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace omnitide

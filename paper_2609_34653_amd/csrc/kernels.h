@@ -1,0 +1,73 @@
+// Internal launchers of the OmniTide kernels (called by abi.cpp after host validation).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace omnitide {
+
+hipError_t launch_score(const void* k, int dtype, int n_seg, int n_slots, int row_elems,
+                        const int32_t* unit_id, const uint8_t* modality, const uint32_t wq[4],
+                        int n_units, uint64_t* unit_wsum, int32_t* unit_len, int32_t* unit_first,
+                        int32_t* unit_last, uint32_t* unit_flags, int32_t* d_status,
+                        hipStream_t stream);
+
+hipError_t launch_select(const uint64_t* unit_wsum, const int32_t* unit_len,
+                         const int32_t* unit_first, const int32_t* unit_last,
+                         const uint32_t* unit_flags, int n_seg, int n_units, int budget,
+                         int recent, uint64_t* unit_score, uint8_t* keep, int32_t* kept_tokens,
+                         int32_t* d_status, hipStream_t stream);
+
+struct CompactArgs {
+  const void* k_src;
+  const void* v_src;
+  int n_seg, n_slots_src, row_bytes, page_size;
+  const int32_t* unit_id_src;
+  const uint8_t* modality_src;
+  const int32_t* pos_src;
+  const uint8_t* keep;
+  const int32_t* unit_len;
+  const int32_t* unit_first;
+  int n_units;
+  const void* k_chunk;
+  const void* v_chunk;
+  const uint8_t* chunk_modality;
+  const int32_t* chunk_unit;
+  int chunk_len;
+  void* k_dst;
+  void* v_dst;
+  int cap_dst;
+  int32_t* unit_id_dst;
+  uint8_t* modality_dst;
+  int32_t* pos_dst;
+  int32_t* src_of_dst;
+  int32_t* unit_remap;
+  int32_t* n_ctx;
+  int32_t* n_pages;
+  void* workspace;
+  int32_t* d_status;
+};
+
+size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst);
+hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
+
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* n_ctx;
+  int n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim;
+  float scale;
+  float* out;
+  void* workspace;
+  int32_t* d_status;
+};
+
+int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                    int head_dim);
+size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                            int head_dim);
+hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace omnitide

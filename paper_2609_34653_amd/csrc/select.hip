@@ -1,0 +1,192 @@
+// Budgeted whole-unit selection: one workgroup of 1024 threads per segment, all state in LDS.
+//
+// Groups (paper: must-keep, recent-context, selected-history):
+//   protected  units holding a system token (all kept; over budget -> OMNITIDE_E_BUDGET)
+//   recent     newest live non-system units whose suffix total fits min(R, B - T_sys); because
+//              lengths are positive the suffix total grows monotonically, so "walk newest to
+//              oldest and stop at the first misfit" is the set {u : suffix(u) <= cap}
+//   selected   remaining live units sorted by the 64-bit key (score << 13 | id) descending
+//              (bitonic sort in LDS), kept while the inclusive prefix of their lengths fits;
+//              the prefix sum grows monotonically, so "stop at the first misfit" is again a
+//              threshold on the prefix.
+// Thread t owns the consecutive units [t*per, (t+1)*per), per = ceil(U / 1024) <= 8.
+#include "common.h"
+#include "kernels.h"
+
+namespace omnitide {
+namespace {
+
+constexpr int kSelThreads = 1024;
+constexpr int kMaxUnits = OMNITIDE_MAX_UNITS;
+constexpr int kPer = kMaxUnits / kSelThreads;
+constexpr int kIdBits = 13;   // 2^13 = kMaxUnits
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
+    const uint64_t* __restrict__ wsum_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, const int32_t* __restrict__ last_g,
+    const uint32_t* __restrict__ flags_g, int n_units, int budget, int recent,
+    uint64_t* __restrict__ score_g, uint8_t* __restrict__ keep_g,
+    int32_t* __restrict__ kept_tokens_g, int32_t* __restrict__ status) {
+  __shared__ uint64_t keys[kMaxUnits];
+  __shared__ int32_t lens[kMaxUnits];
+  __shared__ uint8_t chosen[kMaxUnits];
+  __shared__ int32_t scr_i[kSelThreads / kWave + 1];
+
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int U = n_units;
+  const int per = (U + kSelThreads - 1) / kSelThreads;
+  const int u0 = tid * per;
+  const size_t base = static_cast<size_t>(seg) * U;
+
+  int ln[kPer], fs[kPer], ls[kPer];
+  bool sys[kPer];
+  uint64_t sc[kPer];
+  bool bad = false;
+  int my_max_first = -1;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = u0 + i;
+    ln[i] = 0;
+    fs[i] = 0;
+    ls[i] = -1;
+    sys[i] = false;
+    sc[i] = 0;
+    if (i < per && u < U) {
+      ln[i] = len_g[base + u];
+      fs[i] = first_g[base + u];
+      ls[i] = last_g[base + u];
+      if (ln[i] > 0) {
+        sys[i] = (flags_g[base + u] & 1u) != 0;
+        sc[i] = wsum_g[base + u] / static_cast<uint64_t>(ln[i]);
+        bad |= (ls[i] - fs[i] + 1) != ln[i];
+        my_max_first = max(my_max_first, fs[i]);
+      } else {
+        ln[i] = 0;
+      }
+      score_g[base + u] = sc[i];
+      chosen[u] = 0;
+      lens[u] = ln[i];
+    }
+  }
+  // live units must appear in unit order: each first slot exceeds every earlier live unit's
+  int ignored;
+  int run = block_exclusive_max(my_max_first, -1, scr_i, &ignored);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    if (ln[i] > 0) {
+      bad |= fs[i] <= run;
+      run = max(run, fs[i]);
+    }
+  }
+  const int n_bad = block_sum(bad ? 1 : 0, scr_i);
+
+  int my_sys = 0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) my_sys += sys[i] ? ln[i] : 0;
+  const int t_sys = block_sum(my_sys, scr_i);
+
+  if (n_bad > 0 || t_sys > budget) {
+    for (int u = tid; u < U; u += kSelThreads) keep_g[base + u] = 0;
+    if (tid == 0) {
+      kept_tokens_g[seg] = 0;
+      set_status(status, n_bad > 0 ? OMNITIDE_E_TAGS : OMNITIDE_E_BUDGET);
+    }
+    return;
+  }
+
+  // recent window: suffix sums of eligible (live, non-system) lengths
+  const int cap_rec = min(recent, budget - t_sys);
+  int my_elig = 0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) my_elig += (ln[i] > 0 && !sys[i]) ? ln[i] : 0;
+  int elig_total;
+  const int elig_before = block_exclusive_scan(my_elig, scr_i, &elig_total);
+  int suffix = elig_total - elig_before - my_elig;   // eligible tokens in later threads
+  bool rec[kPer];
+  int my_rec = 0;
+#pragma unroll
+  for (int i = kPer - 1; i >= 0; --i) {
+    rec[i] = false;
+    if (ln[i] > 0 && !sys[i]) {
+      suffix += ln[i];
+      rec[i] = suffix <= cap_rec;
+      my_rec += rec[i] ? ln[i] : 0;
+    }
+  }
+  const int t_rec = block_sum(my_rec, scr_i);
+  const int cap_sel = budget - t_sys - t_rec;
+
+  // candidates sorted by (score desc, id desc); key 0 = not a candidate (sorts last)
+  int P = 1;
+  while (P < U) P <<= 1;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = u0 + i;
+    if (i < per && u < U) {
+      const bool cand = ln[i] > 0 && !sys[i] && !rec[i];
+      keys[u] = cand ? ((sc[i] << kIdBits) | static_cast<uint64_t>(u)) + 1 : 0;
+    }
+  }
+  for (int u = U + tid; u < P; u += kSelThreads) keys[u] = 0;
+  __syncthreads();
+  for (int kk = 2; kk <= P; kk <<= 1) {
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < P; i += kSelThreads) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const uint64_t a = keys[i], b = keys[ixj];
+          const bool desc = (i & kk) == 0;
+          if (desc ? (a < b) : (a > b)) {
+            keys[i] = b;
+            keys[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // prefix of candidate lengths in rank order; thread t owns ranks [t*per2, (t+1)*per2)
+  const int per2 = (P + kSelThreads - 1) / kSelThreads;
+  const int r0 = tid * per2;
+  int my_cand = 0;
+  for (int i = 0; i < per2; ++i) {
+    const int r = r0 + i;
+    if (r < P && keys[r] != 0) my_cand += lens[(keys[r] - 1) & (kMaxUnits - 1)];
+  }
+  int ignored2;
+  int pre = block_exclusive_scan(my_cand, scr_i, &ignored2);
+  int my_sel = 0;
+  for (int i = 0; i < per2; ++i) {
+    const int r = r0 + i;
+    if (r < P && keys[r] != 0) {
+      const int u = static_cast<int>((keys[r] - 1) & (kMaxUnits - 1));
+      pre += lens[u];
+      if (pre <= cap_sel) {
+        chosen[u] = 1;
+        my_sel += lens[u];
+      }
+    }
+  }
+  const int t_sel = block_sum(my_sel, scr_i);   // contains a barrier: chosen[] is complete
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = u0 + i;
+    if (i < per && u < U) keep_g[base + u] = (sys[i] || rec[i] || chosen[u]) ? 1 : 0;
+  }
+  if (tid == 0) kept_tokens_g[seg] = t_sys + t_rec + t_sel;
+}
+
+}  // namespace
+
+hipError_t launch_select(const uint64_t* wsum, const int32_t* len, const int32_t* first,
+                         const int32_t* last, const uint32_t* flags, int n_seg, int n_units,
+                         int budget, int recent, uint64_t* score, uint8_t* keep,
+                         int32_t* kept_tokens, int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(select_kernel, dim3(n_seg), dim3(kSelThreads), 0, stream, wsum, len, first,
+                     last, flags, n_units, budget, recent, score, keep, kept_tokens, status);
+  return hipGetLastError();
+}
+
+}  // namespace omnitide

@@ -1,0 +1,154 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every entry point
+the header declares, and rejects misuse with the documented status code before touching the
+device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_34653_amd import omnitide as ot
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "omnitide.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return ot.lib()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|size_t|const char\*)\s+(omnitide_\w+)\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = header_functions()
+    assert len(names) == 8
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(ot.EXPORTS)
+
+
+def test_header_codes_match_binding():
+    text = open(HEADER).read()
+    codes = dict((k, int(v)) for k, v in re.findall(r"OMNITIDE_(E_\w+|OK)\s*=\s*(-?\d+)", text))
+    assert codes["OK"] == ot.OK and codes["E_TAGS"] == ot.E_TAGS
+    assert codes["E_BUDGET"] == ot.E_BUDGET and codes["E_CAPACITY"] == ot.E_CAPACITY
+    assert codes["E_ALIAS"] == ot.E_ALIAS and codes["E_WORKSPACE"] == ot.E_WORKSPACE
+
+
+def test_status_strings_and_version():
+    assert ot.status_string(0) == "ok"
+    assert "budget" in ot.status_string(-16)
+    assert "tags" in ot.status_string(-17)
+    assert ot.status_string(12345) == "unknown status"
+    assert "gfx950" in ot.version()
+
+
+P = ctypes.c_void_p
+W_OK = (ctypes.c_float * 4)(2.0, 1.0, 1.5, 2.0)
+
+
+def fake(i):
+    """A distinct, never-dereferenced device address."""
+    return P(0x10_0000_0000 + i * 0x1_0000_0000)
+
+
+def score(L, **kw):
+    a = dict(k=fake(0), dtype=0, n_seg=1, n_slots=1000, H=8, d=128, uid=fake(1), mod=fake(2),
+             w=ctypes.cast(W_OK, P), U=10, wsum=fake(3), ln=fake(4), fs=fake(5), ls=fake(6),
+             fl=fake(7), st=fake(8))
+    a.update(kw)
+    return L.omnitide_score_units(a["k"], a["dtype"], a["n_seg"], a["n_slots"], a["H"], a["d"],
+                                  a["uid"], a["mod"], a["w"], a["U"], a["wsum"], a["ln"],
+                                  a["fs"], a["ls"], a["fl"], a["st"], None)
+
+
+def test_score_validation(L):
+    assert score(L, k=None) == ot.E_NULL
+    assert score(L, wsum=None) == ot.E_NULL
+    assert score(L, w=None) == ot.E_NULL
+    assert score(L, dtype=7) == ot.E_DTYPE
+    assert score(L, d=96) == ot.E_SHAPE
+    assert score(L, H=64) == ot.E_SHAPE            # 64 x 128 > 4096 elements per row
+    assert score(L, U=0) == ot.E_SHAPE
+    assert score(L, U=8193) == ot.E_SHAPE
+    assert score(L, n_seg=0) == ot.E_SHAPE
+    assert score(L, n_slots=-1) == ot.E_SHAPE
+    for bad in ((2.0, 1.0, 1.0 / 3.0, 2.0), (0.0, 1.0, 1.0, 1.0), (5.0, 1, 1, 1),
+                (float("nan"), 1, 1, 1)):
+        w = (ctypes.c_float * 4)(*bad)
+        assert score(L, w=ctypes.cast(w, P)) == ot.E_WEIGHT
+    # an output overlapping the key pool
+    assert score(L, wsum=P(fake(0).value + 64)) == ot.E_ALIAS
+    assert score(L, ln=fake(3)) == ot.E_ALIAS      # two outputs at one address
+
+
+def select(L, **kw):
+    a = dict(ws=fake(0), ln=fake(1), fs=fake(2), ls=fake(3), fl=fake(4), n_seg=1, U=10, B=100,
+             R=10, sc=fake(5), keep=fake(6), kt=fake(7), st=fake(8))
+    a.update(kw)
+    return L.omnitide_select_units(a["ws"], a["ln"], a["fs"], a["ls"], a["fl"], a["n_seg"],
+                                   a["U"], a["B"], a["R"], a["sc"], a["keep"], a["kt"], a["st"],
+                                   None)
+
+
+def test_select_validation(L):
+    assert select(L, keep=None) == ot.E_NULL
+    assert select(L, U=9000) == ot.E_SHAPE
+    assert select(L, B=-1) == ot.E_SHAPE
+    assert select(L, R=-5) == ot.E_SHAPE
+    assert select(L, keep=fake(1)) == ot.E_ALIAS
+
+
+def compact(L, **kw):
+    a = dict(ks=fake(0), vs=fake(1), dtype=0, n_seg=1, n=1000, H=8, d=128, P=64, uid=fake(2),
+             mod=fake(3), pos=fake(4), keep=fake(5), ln=fake(6), fs=fake(7), U=10, kc=fake(8),
+             vc=fake(9), cm=fake(10), cu=fake(11), Lc=16, kd=fake(12), vd=fake(13), cap=600,
+             uidd=fake(14), modd=fake(15), posd=fake(16), src=fake(17), rm=fake(18), nctx=fake(19),
+             npg=fake(20), ws=fake(21), wsb=1 << 20, st=fake(22))
+    a.update(kw)
+    return L.omnitide_compact_kv(a["ks"], a["vs"], a["dtype"], a["n_seg"], a["n"], a["H"], a["d"],
+                                 a["P"], a["uid"], a["mod"], a["pos"], a["keep"], a["ln"],
+                                 a["fs"], a["U"], a["kc"], a["vc"], a["cm"], a["cu"], a["Lc"],
+                                 a["kd"], a["vd"], a["cap"], a["uidd"], a["modd"], a["posd"],
+                                 a["src"], a["rm"], a["nctx"], a["npg"], a["ws"], a["wsb"],
+                                 a["st"], None)
+
+
+def test_compact_validation(L):
+    assert compact(L, kd=None) == ot.E_NULL
+    assert compact(L, kc=None) == ot.E_NULL                  # chunk_len > 0 needs the chunk
+    assert compact(L, P=48) == ot.E_SHAPE
+    assert compact(L, dtype=3) == ot.E_DTYPE
+    assert compact(L, cap=15) == ot.E_CAPACITY              # smaller than the chunk
+    assert compact(L, ws=None) == ot.E_WORKSPACE
+    assert compact(L, wsb=16) == ot.E_WORKSPACE
+    assert compact(L, kd=P(fake(0).value + 4096)) == ot.E_ALIAS   # destination inside source
+    assert ot.omnitide_compact_workspace_bytes(1, 10, 600) > 0
+
+
+def attn(L, **kw):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), nctx=fake(3), n_seg=1, cap=17049, Lc=665, Hq=32,
+             Hkv=8, d=128, scale=0.0884, out=fake(4), ws=fake(5), wsb=1 << 30, st=fake(6))
+    a.update(kw)
+    return L.omnitide_chunk_attn(a["q"], a["k"], a["v"], a["nctx"], a["n_seg"], a["cap"], a["Lc"],
+                                 a["Hq"], a["Hkv"], a["d"], a["scale"], a["out"], a["ws"],
+                                 a["wsb"], a["st"], None)
+
+
+def test_attention_validation(L):
+    assert attn(L, q=None) == ot.E_NULL
+    assert attn(L, Hq=30) == ot.E_SHAPE
+    assert attn(L, d=80) == ot.E_SHAPE
+    assert attn(L, Lc=0) == ot.E_SHAPE
+    assert attn(L, scale=float("inf")) == ot.E_SHAPE
+    assert attn(L, cap=100) == ot.E_CAPACITY
+    assert attn(L, ws=None) == ot.E_WORKSPACE
+    assert attn(L, out=fake(1)) == ot.E_ALIAS
+    need = ot.omnitide_attn_workspace_bytes(1, 17049, 665, 32, 8, 128)
+    assert need > 0 and attn(L, wsb=need - 1) == ot.E_WORKSPACE
+    # split count: 21 row tiles x 8 KV heads -> 3 splits on the 80K-history shape
+    assert need == 3 * 665 * 32 * 130 * 4
