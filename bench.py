@@ -52,6 +52,9 @@ def main():
     ap.add_argument("--copies", type=int, default=4)
     ap.add_argument("--config", default=WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="run one plain device-to-device copy of this many MiB before the timed "
+                         "region (a known-size reference for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
@@ -98,6 +101,13 @@ def main():
         if ev is not None:
             ev[4].record(s)
 
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty(n, dtype=torch.uint8, device=dev)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
