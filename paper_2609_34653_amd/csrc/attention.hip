@@ -37,15 +37,25 @@ constexpr int kRowsWG = kAttnWaves * 32; // query rows per workgroup
 constexpr int kNumXcd = 8;
 constexpr int kTargetWGs = 512;          // two resident workgroups on each of 256 CUs
 
+// LDS layout (per buffer; two buffers alternate between tiles):
+//   K    [64 keys][D] bf16, 16-byte chunks XOR-swizzled by kswz(key): the 8 (and 16) lanes that
+//        one LDS cycle serves read 8 (16) distinct bank groups, and so do the staging writes.
+//   V^T  [D][64 keys] bf16, 16-byte key chunks XOR-swizzled by vswz(row): conflict-free both
+//        for the transposing 8-byte staging writes and for the 16-byte operand reads.
 template <int D>
 struct Smem {
-  static constexpr int KS = D + 8;       // K row stride (bf16 elements), 16-byte multiple
-  static constexpr int VS = kKT + 8;     // V^T row stride (bf16 elements)
-  static constexpr int K_ELEMS = kKT * KS;
-  static constexpr int V_ELEMS = D * VS;
+  static constexpr int K_ELEMS = kKT * D;
+  static constexpr int V_ELEMS = D * kKT;
+  static constexpr int BUF_ELEMS = K_ELEMS + V_ELEMS;
   static constexpr int K_VECS = kKT * D / 8 / kAttnThreads;   // 16-byte K loads per thread
   static constexpr int V_BLOCKS = 2 * D;                      // 4-key x 8-dim V blocks per tile
+  static constexpr int CHUNKS = D / 8;                        // 16-byte chunks per K row
 };
+
+__device__ inline int kswz(int key) {
+  return (key & 3) | ((key >> 2) & 4) | ((key << 1) & 8);
+}
+__device__ inline int vswz(int row) { return (row & 7) ^ ((row >> 3) & 7); }
 
 __device__ inline floatx16 mfma(bf16x8 a, bf16x8 b, floatx16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -63,8 +73,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status) {
   using S = Smem<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[S::K_ELEMS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[S::V_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * S::BUF_ELEMS];
 
   const int seg = blockIdx.y;
   const int nctx = n_ctx_g[seg];
@@ -120,54 +129,61 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   };
 
   constexpr int VB = S::V_BLOCKS > kAttnThreads ? S::V_BLOCKS / kAttnThreads : 1;
+  // V staging block of this thread: 4 keys x 8 dims.  Within each 16-lane group, lanes 0-7
+  // take 8 consecutive dim-chunks of one 4-key group and lanes 8-15 the next key group, so the
+  // global reads are whole 128-byte lines and the transposed LDS writes hit 16 distinct slots.
+  const int v_kg = ((tid >> 3) & 1) + 2 * (tid >> (D == 128 ? 5 : 4));
+  const int v_dc = (tid & 7) + (D == 128 ? 8 * ((tid >> 4) & 1) : 0);
+  const bool v_act = tid < S::V_BLOCKS;
   u32x4 kreg[S::K_VECS];
-  u32x4 vreg[VB][4];
+  u32x4 vreg[4];
+  static_assert(VB == 1, "one V block per thread");
   auto load_tile = [&](int t) {
     const int j0 = t * kKT;
+    if (j0 + kKT <= nctx) {   // interior tile: every row exists
+#pragma unroll
+      for (int i = 0; i < S::K_VECS; ++i) {
+        const int idx = tid + kAttnThreads * i;
+        kreg[i] = ld16(kv_row(k, j0 + idx / S::CHUNKS) + 8 * (idx % S::CHUNKS));
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        vreg[r] = v_act ? ld16(kv_row(v, j0 + 4 * v_kg + r) + 8 * v_dc) : u32x4{0, 0, 0, 0};
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < S::K_VECS; ++i) {
       const int idx = tid + kAttnThreads * i;
-      const int key = idx / (D / 8), c8 = idx % (D / 8);
+      const int key = idx / S::CHUNKS, c8 = idx % S::CHUNKS;
       kreg[i] = (j0 + key < nctx) ? ld16(kv_row(k, j0 + key) + 8 * c8) : u32x4{0, 0, 0, 0};
     }
 #pragma unroll
-    for (int i = 0; i < VB; ++i) {
-      const int blk = tid + kAttnThreads * i;
-      const int kg = blk / (D / 8), dc = blk % (D / 8);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = j0 + 4 * kg + r;
-        vreg[i][r] = (blk < S::V_BLOCKS && key < nctx) ? ld16(kv_row(v, key) + 8 * dc)
-                                                       : u32x4{0, 0, 0, 0};
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int key = j0 + 4 * v_kg + r;
+      vreg[r] = (v_act && key < nctx) ? ld16(kv_row(v, key) + 8 * v_dc) : u32x4{0, 0, 0, 0};
     }
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](uint16_t* buf) {
+    uint16_t* Ks = buf;
+    uint16_t* Vt = buf + S::K_ELEMS;
 #pragma unroll
     for (int i = 0; i < S::K_VECS; ++i) {
       const int idx = tid + kAttnThreads * i;
-      const int key = idx / (D / 8), c8 = idx % (D / 8);
-      *reinterpret_cast<u32x4*>(Ks + key * S::KS + 8 * c8) = kreg[i];
+      const int key = idx / S::CHUNKS, c8 = idx % S::CHUNKS;
+      *reinterpret_cast<u32x4*>(Ks + key * D + 8 * (c8 ^ (kswz(key) & (S::CHUNKS - 1)))) =
+          kreg[i];
     }
+    if (v_act) {
 #pragma unroll
-    for (int i = 0; i < VB; ++i) {
-      const int blk = tid + kAttnThreads * i;
-      if (blk < S::V_BLOCKS) {
-        const int kg = blk / (D / 8), dc = blk % (D / 8);
-        const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
-        const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
-        const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
-        const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
+      for (int a = 0; a < 4; ++a) {
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const uint32_t sel = e ? 0x07060302u : 0x05040100u;
-            uint2 o;
-            o.x = __builtin_amdgcn_perm(w1[a], w0[a], sel);
-            o.y = __builtin_amdgcn_perm(w3[a], w2[a], sel);
-            *reinterpret_cast<uint2*>(Vt + (8 * dc + 2 * a + e) * S::VS + 4 * kg) = o;
-          }
+        for (int e = 0; e < 2; ++e) {
+          const uint32_t sel = e ? 0x07060302u : 0x05040100u;
+          uint32_t lo = __builtin_amdgcn_perm(vreg[1][a], vreg[0][a], sel);
+          uint32_t hi = __builtin_amdgcn_perm(vreg[3][a], vreg[2][a], sel);
+          const int row = 8 * v_dc + 2 * a + e;
+          const int c16 = (v_kg >> 1) ^ vswz(row);
+          *reinterpret_cast<uint2*>(Vt + row * kKT + 8 * c16 + 4 * (v_kg & 1)) = make_uint2(lo, hi);
         }
       }
     }
@@ -179,40 +195,57 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   float m_run = -INFINITY, l_run = 0.f;
   const int krow = perm_key(col);
 
-  if (t_begin < t_end) load_tile(t_begin);
+  const int fk = kswz(krow) & (S::CHUNKS - 1);
+  if (t_begin < t_end) {
+    load_tile(t_begin);
+    store_tile(lds);
+    if (t_begin + 1 < t_end) load_tile(t_begin + 1);
+  }
+  __syncthreads();
   for (int t = t_begin; t < t_end; ++t) {
     const int j0 = t * kKT;
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (t + 1 < t_end) load_tile(t + 1);
+    const uint16_t* Ks = lds + ((t - t_begin) & 1) * S::BUF_ELEMS;
+    const uint16_t* Vt = Ks + S::K_ELEMS;
 
     floatx16 s[2] = {floatx16{}, floatx16{}};
 #pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
+    for (int st = 0; st < 2; ++st) {
+      bf16x8 ka[D / 16];
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c)
+        ka[c] = __builtin_bit_cast(bf16x8,
+                                   ld16(Ks + (32 * st + krow) * D + 8 * ((2 * c + h) ^ fk)));
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) s[st] = mfma(ka[c], qf[c], s[st]);
+    }
+    // Row maximum of the raw scores (scale > 0 commutes with max); mask only boundary tiles.
+    float mx = -INFINITY;
+    if (j0 + kKT - 1 > full_lim) {
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
-        const bf16x8 a =
-            __builtin_bit_cast(bf16x8, ld16(Ks + (32 * st + krow) * S::KS + 16 * c + 8 * h));
-        s[st] = mfma(a, qf[c], s[st]);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          if (j0 + 32 * st + 16 * h + i > lim) s[st][i] = -INFINITY;
+          mx = fmaxf(mx, s[st][i]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
       }
     }
-    float mx = -INFINITY;
-    const bool need_mask = j0 + kKT - 1 > full_lim;
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float x = s[st][i] * scale_log2;
-        if (need_mask && j0 + 32 * st + 16 * h + i > lim) x = -INFINITY;
-        s[st][i] = x;
-        mx = fmaxf(mx, x);
-      }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
     const float m_new = fmaxf(m_run, mx);
     const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    // Rescale the running output only when some row's maximum moved.
+    if (__any(m_new > m_run)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
+    }
     m_run = m_new;
     float lsum = 0.f;
     bf16x8 pf[2][2];
@@ -220,26 +253,32 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     for (int st = 0; st < 2; ++st) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float e = exp2f(s[st][i] - m_use);
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[st][i], scale_log2, -m_use));
         lsum += e;
         pf[st][i / 8][i % 8] = static_cast<__bf16>(e);
       }
     }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
+    l_run += lsum;
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
+      const int row = 32 * dt + col;
+      const int sw = vswz(row);
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
-          const bf16x8 a = __builtin_bit_cast(
-              bf16x8, ld16(Vt + (32 * dt + col) * S::VS + 32 * st + 16 * h + 8 * cc));
+          const int c16 = (4 * st + 2 * h + cc) ^ sw;
+          const bf16x8 a = __builtin_bit_cast(bf16x8, ld16(Vt + row * kKT + 8 * c16));
           o[dt] = mfma(a, pf[st][cc], o[dt]);
         }
       }
     }
+    // Stage the prefetched tile into the other buffer, then prefetch the one after it.
+    if (t + 1 < t_end) {
+      store_tile(lds + ((t + 1 - t_begin) & 1) * S::BUF_ELEMS);
+      if (t + 2 < t_end) load_tile(t + 2);
+    }
+    __syncthreads();
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
