@@ -37,25 +37,32 @@ constexpr int kRowsWG = kAttnWaves * 32; // query rows per workgroup
 constexpr int kNumXcd = 8;
 constexpr int kTargetWGs = 512;          // two resident workgroups on each of 256 CUs
 
-// LDS layout (per buffer; two buffers alternate between tiles):
-//   K    [64 keys][D] bf16, 16-byte chunks XOR-swizzled by kswz(key): the 8 (and 16) lanes that
-//        one LDS cycle serves read 8 (16) distinct bank groups, and so do the staging writes.
-//   V^T  [D][64 keys] bf16, 16-byte key chunks XOR-swizzled by vswz(row): conflict-free both
-//        for the transposing 8-byte staging writes and for the 16-byte operand reads.
+// LDS layout (per buffer; two buffers alternate between tiles), both row-major [64 keys][D]:
+//   K  16-byte chunks XOR-swizzled by kswz(key), so the 8 (and 16) lanes one LDS cycle serves
+//      read distinct bank groups when they fetch rows perm_key(0..31) of the S^T tile.
+//   V  32-byte units XOR-swizzled by vswz(key); the V^T operand of O^T = V^T P^T is gathered
+//      with the transposing 64-bit LDS read (ds_read_b64_tr_b16): within a 16-lane group, lane i
+//      receives element i%4 of the 8-byte rows read by lanes i/4, 4+i/4, 8+i/4, 12+i/4, i.e.
+//      one dimension of four consecutive keys.  Each group reads four rows x 32 bytes; the
+//      swizzle puts them (and the neighbouring group's) in distinct banks.
+// Tiles are copied global -> LDS by the 16-byte direct loads (no register staging); a lane's LDS
+// destination is fixed (lane-contiguous), so the swizzles are realised by choosing which global
+// chunk each lane fetches.
 template <int D>
 struct Smem {
-  static constexpr int K_ELEMS = kKT * D;
-  static constexpr int V_ELEMS = D * kKT;
-  static constexpr int BUF_ELEMS = K_ELEMS + V_ELEMS;
-  static constexpr int K_VECS = kKT * D / 8 / kAttnThreads;   // 16-byte K loads per thread
-  static constexpr int V_BLOCKS = 2 * D;                      // 4-key x 8-dim V blocks per tile
-  static constexpr int CHUNKS = D / 8;                        // 16-byte chunks per K row
+  static constexpr int TILE_ELEMS = kKT * D;
+  static constexpr int BUF_ELEMS = 2 * TILE_ELEMS;             // K then V
+  static constexpr int CHUNKS = D / 8;                         // 16-byte chunks per row
+  static constexpr int CALLS = TILE_ELEMS / 8 / kWave / kAttnWaves;  // 1 KB loads per wave
 };
 
 __device__ inline int kswz(int key) {
   return (key & 3) | ((key >> 2) & 4) | ((key << 1) & 8);
 }
-__device__ inline int vswz(int row) { return (row & 7) ^ ((row >> 3) & 7); }
+template <int D>
+__device__ inline int vswz(int key) {
+  return D == 128 ? ((key & 3) ^ ((key & 1) << 2)) : (key & 3);
+}
 
 __device__ inline floatx16 mfma(bf16x8 a, bf16x8 b, floatx16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -66,6 +73,14 @@ __device__ inline int perm_key(int r) { return 16 * ((r & 7) >> 2) + 4 * (r >> 3
 
 __device__ inline u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ inline shortx4 ld_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) shortx4*)(p));
+}
+
 template <int D>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -73,7 +88,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status) {
   using S = Smem<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * S::BUF_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * S::BUF_ELEMS];
 
   const int seg = blockIdx.y;
   const int nctx = n_ctx_g[seg];
@@ -124,68 +139,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   }
 
   const size_t kv_seg = static_cast<size_t>(seg) * cap;
-  auto kv_row = [&](const uint16_t* base, int key) {
-    return base + ((kv_seg + key) * Hkv + g) * D;
-  };
-
-  constexpr int VB = S::V_BLOCKS > kAttnThreads ? S::V_BLOCKS / kAttnThreads : 1;
-  // V staging block of this thread: 4 keys x 8 dims.  Within each 16-lane group, lanes 0-7
-  // take 8 consecutive dim-chunks of one 4-key group and lanes 8-15 the next key group, so the
-  // global reads are whole 128-byte lines and the transposed LDS writes hit 16 distinct slots.
-  const int v_kg = ((tid >> 3) & 1) + 2 * (tid >> (D == 128 ? 5 : 4));
-  const int v_dc = (tid & 7) + (D == 128 ? 8 * ((tid >> 4) & 1) : 0);
-  const bool v_act = tid < S::V_BLOCKS;
-  u32x4 kreg[S::K_VECS];
-  u32x4 vreg[4];
-  static_assert(VB == 1, "one V block per thread");
-  auto load_tile = [&](int t) {
+  // Direct global -> LDS copy of tile t into buffer `buf`: this wave's CALLS 1 KB pieces of K
+  // and of V.  Rows past n_ctx are clamped to a valid row here and zeroed after arrival.
+  auto issue_tile = [&](int t, int buf) {
     const int j0 = t * kKT;
-    if (j0 + kKT <= nctx) {   // interior tile: every row exists
+    uint16_t* base = lds + buf * S::BUF_ELEMS;
 #pragma unroll
-      for (int i = 0; i < S::K_VECS; ++i) {
-        const int idx = tid + kAttnThreads * i;
-        kreg[i] = ld16(kv_row(k, j0 + idx / S::CHUNKS) + 8 * (idx % S::CHUNKS));
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        vreg[r] = v_act ? ld16(kv_row(v, j0 + 4 * v_kg + r) + 8 * v_dc) : u32x4{0, 0, 0, 0};
-      return;
-    }
-#pragma unroll
-    for (int i = 0; i < S::K_VECS; ++i) {
-      const int idx = tid + kAttnThreads * i;
-      const int key = idx / S::CHUNKS, c8 = idx % S::CHUNKS;
-      kreg[i] = (j0 + key < nctx) ? ld16(kv_row(k, j0 + key) + 8 * c8) : u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int key = j0 + 4 * v_kg + r;
-      vreg[r] = (v_act && key < nctx) ? ld16(kv_row(v, key) + 8 * v_dc) : u32x4{0, 0, 0, 0};
+    for (int cq = 0; cq < S::CALLS; ++cq) {
+      const int call = wave + kAttnWaves * cq;
+      const int lc = call * kWave + lane;          // linear 16-byte chunk in the tile
+      const int key = lc / S::CHUNKS, pc = lc % S::CHUNKS;
+      const int row = min(j0 + key, nctx - 1);
+      const size_t roff = ((kv_seg + row) * Hkv + g) * D;
+      const int kchunk = pc ^ (kswz(key) & (S::CHUNKS - 1));
+      const int vchunk = 2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1);
+      __builtin_amdgcn_global_load_lds(k + roff + 8 * kchunk,
+                                       (lds_void*)(base + call * kWave * 8), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(v + roff + 8 * vchunk,
+                                       (lds_void*)(base + S::TILE_ELEMS + call * kWave * 8), 16,
+                                       0, 0);
     }
   };
-  auto store_tile = [&](uint16_t* buf) {
-    uint16_t* Ks = buf;
-    uint16_t* Vt = buf + S::K_ELEMS;
-#pragma unroll
-    for (int i = 0; i < S::K_VECS; ++i) {
-      const int idx = tid + kAttnThreads * i;
-      const int key = idx / S::CHUNKS, c8 = idx % S::CHUNKS;
-      *reinterpret_cast<u32x4*>(Ks + key * D + 8 * (c8 ^ (kswz(key) & (S::CHUNKS - 1)))) =
-          kreg[i];
-    }
-    if (v_act) {
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const uint32_t sel = e ? 0x07060302u : 0x05040100u;
-          uint32_t lo = __builtin_amdgcn_perm(vreg[1][a], vreg[0][a], sel);
-          uint32_t hi = __builtin_amdgcn_perm(vreg[3][a], vreg[2][a], sel);
-          const int row = 8 * v_dc + 2 * a + e;
-          const int c16 = (v_kg >> 1) ^ vswz(row);
-          *reinterpret_cast<uint2*>(Vt + row * kKT + 8 * c16 + 4 * (v_kg & 1)) = make_uint2(lo, hi);
-        }
-      }
+  // Zero the rows at or past n_ctx of a boundary tile (after its loads have landed).
+  auto zero_tail = [&](int t, int buf) {
+    const int j0 = t * kKT;
+    uint16_t* base = lds + buf * S::BUF_ELEMS;
+    for (int idx = tid; idx < 2 * kKT * S::CHUNKS; idx += kAttnThreads) {
+      const int tensor = idx / (kKT * S::CHUNKS);
+      const int key = (idx / S::CHUNKS) % kKT;
+      if (j0 + key >= nctx)
+        *reinterpret_cast<u32x4*>(base + tensor * S::TILE_ELEMS + 8 * (idx % (kKT * S::CHUNKS))) =
+            u32x4{0, 0, 0, 0};
     }
   };
 
@@ -194,18 +178,25 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   for (int dt = 0; dt < D / 32; ++dt) o[dt] = floatx16{};
   float m_run = -INFINITY, l_run = 0.f;
   const int krow = perm_key(col);
-
   const int fk = kswz(krow) & (S::CHUNKS - 1);
-  if (t_begin < t_end) {
-    load_tile(t_begin);
-    store_tile(lds);
-    if (t_begin + 1 < t_end) load_tile(t_begin + 1);
-  }
-  __syncthreads();
+  // transposing V reads: this lane's role inside its 16-lane group
+  const int gi = lane & 15, gq = (lane >> 4) & 1;
+  const int vsl = vswz<D>(gi >> 2);
+  const int v_lane_off = (gi >> 2) * D + 8 * ((gi & 3) >> 1) + 4 * (gi & 1);
+
+  if (t_begin < t_end) issue_tile(t_begin, 0);
   for (int t = t_begin; t < t_end; ++t) {
     const int j0 = t * kKT;
-    const uint16_t* Ks = lds + ((t - t_begin) & 1) * S::BUF_ELEMS;
-    const uint16_t* Vt = Ks + S::K_ELEMS;
+    const int buf = (t - t_begin) & 1;
+    __builtin_amdgcn_s_waitcnt(0);        // this wave's pieces of tile t have landed
+    __syncthreads();                      // tile t visible; everyone is done with tile t-1
+    if (j0 + kKT > nctx) {                // boundary tile: clear rows past n_ctx
+      zero_tail(t, buf);
+      __syncthreads();
+    }
+    if (t + 1 < t_end) issue_tile(t + 1, buf ^ 1);
+    const uint16_t* Ks = lds + buf * S::BUF_ELEMS;
+    const uint16_t* Vs = Ks + S::TILE_ELEMS;
 
     floatx16 s[2] = {floatx16{}, floatx16{}};
 #pragma unroll
@@ -259,26 +250,24 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       }
     }
     l_run += lsum;
+    // O^T += V^T P^T: the V^T operand (dims 32dt.., keys 32st+16h+8cc..+8) from two
+    // transposing reads of four keys each.
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
-      const int row = 32 * dt + col;
-      const int sw = vswz(row);
+      const int unit = (2 * dt + gq) ^ vsl;
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
-          const int c16 = (4 * st + 2 * h + cc) ^ sw;
-          const bf16x8 a = __builtin_bit_cast(bf16x8, ld16(Vt + row * kKT + 8 * c16));
+          const uint16_t* vp = Vs + (32 * st + 16 * h + 8 * cc) * D + 16 * unit + v_lane_off;
+          const shortx4 lo = ld_tr(vp);
+          const shortx4 hi = ld_tr(vp + 4 * D);
+          const bf16x8 a = __builtin_bit_cast(
+              bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
           o[dt] = mfma(a, pf[st][cc], o[dt]);
         }
       }
     }
-    // Stage the prefetched tile into the other buffer, then prefetch the one after it.
-    if (t + 1 < t_end) {
-      store_tile(lds + ((t + 1 - t_begin) & 1) * S::BUF_ELEMS);
-      if (t + 2 < t_end) load_tile(t + 2);
-    }
-    __syncthreads();
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
