@@ -37,7 +37,7 @@ constexpr int kRowsWG = kAttnWaves * 32; // query rows per workgroup
 constexpr int kNumXcd = 8;
 constexpr int kTargetWGs = 512;          // two resident workgroups on each of 256 CUs
 
-// LDS layout (per buffer; two buffers alternate between tiles), both row-major [64 keys][D]:
+// LDS layout: two K and two V tile buffers, each row-major [64 keys][D]:
 //   K  16-byte chunks XOR-swizzled by kswz(key), so the 8 (and 16) lanes one LDS cycle serves
 //      read distinct bank groups when they fetch rows perm_key(0..31) of the S^T tile.
 //   V  32-byte units XOR-swizzled by vswz(key); the V^T operand of O^T = V^T P^T is gathered
@@ -51,7 +51,6 @@ constexpr int kTargetWGs = 512;          // two resident workgroups on each of 2
 template <int D>
 struct Smem {
   static constexpr int TILE_ELEMS = kKT * D;
-  static constexpr int BUF_ELEMS = 2 * TILE_ELEMS;             // K then V
   static constexpr int CHUNKS = D / 8;                         // 16-byte chunks per row
   static constexpr int CALLS = TILE_ELEMS / 8 / kWave / kAttnWaves;  // 1 KB loads per wave
 };
@@ -88,7 +87,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status) {
   using S = Smem<D>;
-  __shared__ __attribute__((aligned(1024))) uint16_t lds[2 * S::BUF_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[4 * S::TILE_ELEMS];
 
   const int seg = blockIdx.y;
   const int nctx = n_ctx_g[seg];
@@ -139,38 +138,32 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   }
 
   const size_t kv_seg = static_cast<size_t>(seg) * cap;
-  // Direct global -> LDS copy of tile t into buffer `buf`: this wave's CALLS 1 KB pieces of K
-  // and of V.  Rows past n_ctx are clamped to a valid row here and zeroed after arrival.
-  auto issue_tile = [&](int t, int buf) {
+  // Buffers: K tiles alternate between kbuf 0/1 and V tiles between vbuf 0/1.  Iteration t
+  // reads K(t+1) (scores of the next tile) and V(t) (output of this tile) while K(t+2) and
+  // V(t+1) are in flight.
+  auto kbuf = [&](int i) { return lds + i * S::TILE_ELEMS; };
+  auto vbuf = [&](int i) { return lds + (2 + i) * S::TILE_ELEMS; };
+  // Direct global -> LDS copy of one tensor's tile (this wave's CALLS 1 KB pieces).  Rows past
+  // n_ctx are clamped to a valid row here and zeroed after arrival.
+  auto issue = [&](const uint16_t* src, bool is_v, int t, uint16_t* dst) {
     const int j0 = t * kKT;
-    uint16_t* base = lds + buf * S::BUF_ELEMS;
 #pragma unroll
     for (int cq = 0; cq < S::CALLS; ++cq) {
       const int call = wave + kAttnWaves * cq;
       const int lc = call * kWave + lane;          // linear 16-byte chunk in the tile
       const int key = lc / S::CHUNKS, pc = lc % S::CHUNKS;
       const int row = min(j0 + key, nctx - 1);
-      const size_t roff = ((kv_seg + row) * Hkv + g) * D;
-      const int kchunk = pc ^ (kswz(key) & (S::CHUNKS - 1));
-      const int vchunk = 2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1);
-      __builtin_amdgcn_global_load_lds(k + roff + 8 * kchunk,
-                                       (lds_void*)(base + call * kWave * 8), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(v + roff + 8 * vchunk,
-                                       (lds_void*)(base + S::TILE_ELEMS + call * kWave * 8), 16,
-                                       0, 0);
+      const int chunk = is_v ? 2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1)
+                             : pc ^ (kswz(key) & (S::CHUNKS - 1));
+      __builtin_amdgcn_global_load_lds(src + ((kv_seg + row) * Hkv + g) * D + 8 * chunk,
+                                       (lds_void*)(dst + call * kWave * 8), 16, 0, 0);
     }
   };
-  // Zero the rows at or past n_ctx of a boundary tile (after its loads have landed).
-  auto zero_tail = [&](int t, int buf) {
+  auto zero_rows = [&](int t, uint16_t* buf) {
     const int j0 = t * kKT;
-    uint16_t* base = lds + buf * S::BUF_ELEMS;
-    for (int idx = tid; idx < 2 * kKT * S::CHUNKS; idx += kAttnThreads) {
-      const int tensor = idx / (kKT * S::CHUNKS);
-      const int key = (idx / S::CHUNKS) % kKT;
-      if (j0 + key >= nctx)
-        *reinterpret_cast<u32x4*>(base + tensor * S::TILE_ELEMS + 8 * (idx % (kKT * S::CHUNKS))) =
-            u32x4{0, 0, 0, 0};
-    }
+    for (int idx = tid; idx < kKT * S::CHUNKS; idx += kAttnThreads)
+      if (j0 + idx / S::CHUNKS >= nctx)
+        *reinterpret_cast<u32x4*>(buf + 8 * idx) = u32x4{0, 0, 0, 0};
   };
 
   floatx16 o[D / 32];
@@ -183,90 +176,120 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   const int gi = lane & 15, gq = (lane >> 4) & 1;
   const int vsl = vswz<D>(gi >> 2);
   const int v_lane_off = (gi >> 2) * D + 8 * ((gi & 3) >> 1) + 4 * (gi & 1);
+  constexpr int NQK = 2 * (D / 16);                // score MFMAs per tile (two 32-key halves)
+  constexpr int EPS = 32 / NQK;                    // exponentials per interleave segment
 
-  if (t_begin < t_end) issue_tile(t_begin, 0);
-  for (int t = t_begin; t < t_end; ++t) {
-    const int j0 = t * kKT;
-    const int buf = (t - t_begin) & 1;
-    __builtin_amdgcn_s_waitcnt(0);        // this wave's pieces of tile t have landed
-    __syncthreads();                      // tile t visible; everyone is done with tile t-1
-    if (j0 + kKT > nctx) {                // boundary tile: clear rows past n_ctx
-      zero_tail(t, buf);
+  auto kop = [&](const uint16_t* kb, int i) {      // K operand of score MFMA i
+    const int st = i & 1, c = i >> 1;
+    return __builtin_bit_cast(bf16x8, ld16(kb + (32 * st + krow) * D + 8 * ((2 * c + h) ^ fk)));
+  };
+
+  if (t_begin < t_end) {
+    issue(k, false, t_begin, kbuf(0));
+    issue(v, true, t_begin, vbuf(0));
+    if (t_begin + 1 < t_end) issue(k, false, t_begin + 1, kbuf(1));
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t_begin * kKT + kKT > nctx) {
+      zero_rows(t_begin, kbuf(0));
       __syncthreads();
     }
-    if (t + 1 < t_end) issue_tile(t + 1, buf ^ 1);
-    const uint16_t* Ks = lds + buf * S::BUF_ELEMS;
-    const uint16_t* Vs = Ks + S::TILE_ELEMS;
+    floatx16 s_cur[2] = {floatx16{}, floatx16{}};
+#pragma unroll
+    for (int i = 0; i < NQK; ++i) s_cur[i & 1] = mfma(kop(kbuf(0), i), qf[i >> 1], s_cur[i & 1]);
 
-    floatx16 s[2] = {floatx16{}, floatx16{}};
+    for (int t = t_begin; t < t_end; ++t) {
+      const int r = t - t_begin;
+      const int j0 = t * kKT;
+      const bool has_next = t + 1 < t_end;
+      __builtin_amdgcn_s_waitcnt(0);      // this wave's pieces of K(t+1) and V(t) have landed
+      __syncthreads();                    // ... everyone's; iteration t-1 is finished
+      if ((has_next && j0 + 2 * kKT > nctx) || j0 + kKT > nctx) {
+        if (has_next) zero_rows(t + 1, kbuf((r + 1) & 1));
+        zero_rows(t, vbuf(r & 1));
+        __syncthreads();
+      }
+      if (t + 2 < t_end) issue(k, false, t + 2, kbuf(r & 1));
+      if (has_next) issue(v, true, t + 1, vbuf((r + 1) & 1));
+
+      // causal mask of this tile's scores (only tiles past the first row's limit)
+      if (j0 + kKT - 1 > full_lim) {
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      bf16x8 ka[D / 16];
+        for (int st = 0; st < 2; ++st) {
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c)
-        ka[c] = __builtin_bit_cast(bf16x8,
-                                   ld16(Ks + (32 * st + krow) * D + 8 * ((2 * c + h) ^ fk)));
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c) s[st] = mfma(ka[c], qf[c], s[st]);
-    }
-    // Row maximum of the raw scores (scale > 0 commutes with max); mask only boundary tiles.
-    float mx = -INFINITY;
-    if (j0 + kKT - 1 > full_lim) {
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          if (j0 + 32 * st + 16 * h + i > lim) s[st][i] = -INFINITY;
-          mx = fmaxf(mx, s[st][i]);
+          for (int i = 0; i < 16; ++i)
+            if (j0 + 32 * st + 16 * h + i > lim) s_cur[st][i] = -INFINITY;
         }
       }
-    } else {
+      float mx = -INFINITY;
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s_cur[st][i]);
       }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    // Rescale the running output only when some row's maximum moved.
-    if (__any(m_new > m_run)) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-      l_run *= alpha;
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
+      const float m_new = fmaxf(m_run, mx);
+      // Rescale the running output only when some row's maximum moved.
+      if (__any(m_new > m_run)) {
+        const float m_u = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_u);
+        l_run *= alpha;
 #pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
-    }
-    m_run = m_new;
-    float lsum = 0.f;
-    bf16x8 pf[2][2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[st][i], scale_log2, -m_use));
-        lsum += e;
-        pf[st][i / 8][i % 8] = static_cast<__bf16>(e);
+        for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
       }
-    }
-    l_run += lsum;
-    // O^T += V^T P^T: the V^T operand (dims 32dt.., keys 32st+16h+8cc..+8) from two
-    // transposing reads of four keys each.
+      m_run = m_new;
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+
+      // Interleave: segment i issues score MFMA i of the next tile and then EPS exponentials
+      // of this tile, so the vector ALU works while the matrix core runs (a wave issues in
+      // order).  In the last iteration the next-K buffer holds a stale tile; the scores
+      // computed from it are discarded, which keeps the loop body branch-free.
+      const uint16_t* kn = kbuf((r + 1) & 1);
+      floatx16 s_nxt[2] = {floatx16{}, floatx16{}};
+      float e[32];
+      float lsum = 0.f;
+      bf16x8 ka0 = kop(kn, 0), ka1 = kop(kn, 1);
 #pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) {
-      const int unit = (2 * dt + gq) ^ vsl;
+      for (int i = 0; i < NQK; ++i) {
+        const bf16x8 ka = (i & 1) ? ka1 : ka0;
+        s_nxt[i & 1] = mfma(ka, qf[i >> 1], s_nxt[i & 1]);
+        if (i + 2 < NQK) {
+          if (i & 1) ka1 = kop(kn, i + 2); else ka0 = kop(kn, i + 2);
+        }
+#pragma unroll
+        for (int j = 0; j < EPS; ++j) {
+          const int x = i * EPS + j;
+          e[x] = __builtin_amdgcn_exp2f(fmaf(s_cur[x >> 4][x & 15], scale_log2, -m_use));
+          lsum += e[x];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      l_run += lsum;
+      bf16x8 pf[2][2];
+#pragma unroll
+      for (int x = 0; x < 32; ++x) pf[x >> 4][(x >> 3) & 1][x & 7] = static_cast<__bf16>(e[x]);
+
+      // O^T += V^T P^T: the V^T operand (dims 32dt.., keys 32st+16h+8cc..+8) from two
+      // transposing reads of four keys each.
+      const uint16_t* Vs = vbuf(r & 1);
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
-          const uint16_t* vp = Vs + (32 * st + 16 * h + 8 * cc) * D + 16 * unit + v_lane_off;
-          const shortx4 lo = ld_tr(vp);
-          const shortx4 hi = ld_tr(vp + 4 * D);
-          const bf16x8 a = __builtin_bit_cast(
-              bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-          o[dt] = mfma(a, pf[st][cc], o[dt]);
+#pragma unroll
+          for (int dt = 0; dt < D / 32; ++dt) {
+            const int unit = (2 * dt + gq) ^ vsl;
+            const uint16_t* vp = Vs + (32 * st + 16 * h + 8 * cc) * D + 16 * unit + v_lane_off;
+            const shortx4 lo = ld_tr(vp);
+            const shortx4 hi = ld_tr(vp + 4 * D);
+            const bf16x8 av = __builtin_bit_cast(
+                bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            o[dt] = mfma(av, pf[st][cc], o[dt]);
+          }
         }
       }
+      s_cur[0] = s_nxt[0];
+      s_cur[1] = s_nxt[1];
     }
   }
 
