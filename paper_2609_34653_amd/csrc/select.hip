@@ -1,4 +1,5 @@
-// Budgeted whole-unit selection: one workgroup of 1024 threads per segment, all state in LDS.
+// Budgeted whole-unit selection, one workgroup per segment.  Up to 512 units: a single wave
+// (select_small_kernel); beyond: 1024 threads with all state in LDS (select_kernel).
 //
 // Groups (paper: must-keep, recent-context, selected-history):
 //   protected  units holding a system token (all kept; over budget -> OMNITIDE_E_BUDGET)
@@ -44,26 +45,28 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   uint64_t sc[kPer];
   bool bad = false;
   int my_max_first = -1;
+  uint32_t fl[kPer];
+  uint64_t ws[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {           // all loads first: one memory round trip
+    const int u = min(u0 + i, U - 1);
+    ln[i] = len_g[base + u];
+    fs[i] = first_g[base + u];
+    ls[i] = last_g[base + u];
+    fl[i] = flags_g[base + u];
+    ws[i] = wsum_g[base + u];
+  }
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int u = u0 + i;
-    ln[i] = 0;
-    fs[i] = 0;
-    ls[i] = -1;
-    sys[i] = false;
-    sc[i] = 0;
-    if (i < per && u < U) {
-      ln[i] = len_g[base + u];
-      fs[i] = first_g[base + u];
-      ls[i] = last_g[base + u];
-      if (ln[i] > 0) {
-        sys[i] = (flags_g[base + u] & 1u) != 0;
-        sc[i] = wsum_g[base + u] / static_cast<uint64_t>(ln[i]);
-        bad |= (ls[i] - fs[i] + 1) != ln[i];
-        my_max_first = max(my_max_first, fs[i]);
-      } else {
-        ln[i] = 0;
-      }
+    const bool mine = i < per && u < U;
+    if (!mine || ln[i] <= 0) ln[i] = 0;
+    const bool live = ln[i] > 0;
+    sys[i] = live && (fl[i] & 1u) != 0;
+    sc[i] = live ? ws[i] / static_cast<uint32_t>(ln[i]) : 0;
+    bad |= live && (ls[i] - fs[i] + 1) != ln[i];
+    if (live) my_max_first = max(my_max_first, fs[i]);
+    if (mine) {
       score_g[base + u] = sc[i];
       chosen[u] = 0;
       lens[u] = ln[i];
@@ -178,14 +181,220 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   if (tid == 0) kept_tokens_g[seg] = t_sys + t_rec + t_sel;
 }
 
+
+// Single-wave variant for U <= 512 (every lane owns 8 consecutive units): the same plan with
+// wave-level scans (no workgroup barriers) and, instead of a full sort, an MSD radix select of
+// the cut.  The walk "rank order, stop at the first misfit" keeps exactly the candidates whose
+// key exceeds the first misfit's key; the misfit is found digit by digit: a histogram of
+// candidate lengths over the next 8 key bits (LDS atomics) and a scan in descending digit order
+// locate the bucket where the running total first exceeds the cap; higher buckets are kept,
+// lower ones dropped, and the search continues inside that bucket until it holds one key.
+constexpr int kSmallUnits = 512;
+constexpr int kSmallPer = kSmallUnits / kWave;
+
+__device__ inline int wave_exclusive_sum(int v, int* total) {
+  const int inc = wave_inclusive_scan(v);
+  *total = __shfl(inc, kWave - 1, kWave);
+  return inc - v;
+}
+
+__global__ __launch_bounds__(kWave) void select_small_kernel(
+    const uint64_t* __restrict__ wsum_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, const int32_t* __restrict__ last_g,
+    const uint32_t* __restrict__ flags_g, int n_units, int budget, int recent,
+    uint64_t* __restrict__ score_g, uint8_t* __restrict__ keep_g,
+    int32_t* __restrict__ kept_tokens_g, int32_t* __restrict__ status) {
+  __shared__ int32_t hist[256];
+  const int seg = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int U = n_units;
+  const int u0 = lane * kSmallPer;
+  const size_t base = static_cast<size_t>(seg) * U;
+
+  int ln[kSmallPer], fs[kSmallPer], ls[kSmallPer];
+  uint32_t fl[kSmallPer];
+  uint64_t ws[kSmallPer];
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {      // all loads first: one memory round trip
+    const int u = min(u0 + i, U - 1);
+    ln[i] = len_g[base + u];
+    fs[i] = first_g[base + u];
+    ls[i] = last_g[base + u];
+    fl[i] = flags_g[base + u];
+    ws[i] = wsum_g[base + u];
+  }
+  bool sys[kSmallPer];
+  uint64_t key[kSmallPer];
+  bool bad = false;
+  int my_max_first = -1;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    const int u = u0 + i;
+    if (u >= U || ln[i] <= 0) ln[i] = 0;
+    const bool live = ln[i] > 0;
+    sys[i] = live && (fl[i] & 1u) != 0;
+    const uint64_t sc = live ? ws[i] / static_cast<uint32_t>(ln[i]) : 0;
+    bad |= live && (ls[i] - fs[i] + 1) != ln[i];
+    if (live) my_max_first = max(my_max_first, fs[i]);
+    if (u < U) score_g[base + u] = sc;
+    key[i] = (sc << kIdBits) | static_cast<uint64_t>(u);
+  }
+  // unit order: every live unit's first slot exceeds all earlier live units' first slots
+  int run = my_max_first;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(run, off, kWave);
+    if (lane >= off) run = max(run, o);
+  }
+  run = lane == 0 ? -1 : __shfl_up(run, 1, kWave);
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    if (ln[i] > 0) {
+      bad |= fs[i] <= run;
+      run = max(run, fs[i]);
+    }
+  }
+  int my_sys = 0, my_elig = 0;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    my_sys += sys[i] ? ln[i] : 0;
+    my_elig += (ln[i] > 0 && !sys[i]) ? ln[i] : 0;
+  }
+  int t_sys, elig_total;
+  wave_exclusive_sum(my_sys, &t_sys);
+  const int elig_before = wave_exclusive_sum(my_elig, &elig_total);
+  const bool any_bad = __any(bad);
+  if (any_bad || t_sys > budget) {
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i)
+      if (u0 + i < U) keep_g[base + u0 + i] = 0;
+    if (lane == 0) {
+      kept_tokens_g[seg] = 0;
+      set_status(status, any_bad ? OMNITIDE_E_TAGS : OMNITIDE_E_BUDGET);
+    }
+    return;
+  }
+  // recent window: suffix sums of eligible lengths, newest unit first
+  const int cap_rec = min(recent, budget - t_sys);
+  int suffix = elig_total - elig_before - my_elig;
+  bool rec[kSmallPer];
+  int my_rec = 0;
+#pragma unroll
+  for (int i = kSmallPer - 1; i >= 0; --i) {
+    rec[i] = false;
+    if (ln[i] > 0 && !sys[i]) {
+      suffix += ln[i];
+      rec[i] = suffix <= cap_rec;
+      my_rec += rec[i] ? ln[i] : 0;
+    }
+  }
+  int t_rec;
+  wave_exclusive_sum(my_rec, &t_rec);
+  const int cap_sel = budget - t_sys - t_rec;
+
+  // radix select of the first misfit among candidates (state: 1 active, 2 kept, 0 dropped)
+  int state[kSmallPer];
+  uint64_t kmax = 0;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    state[i] = (ln[i] > 0 && !sys[i] && !rec[i]) ? 1 : 0;
+    if (state[i]) kmax = max(kmax, key[i]);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) kmax = max(kmax, __shfl_xor(kmax, off, kWave));
+  int taken = 0;                                   // tokens already kept by the search
+  int hi = 64 - __builtin_clzll(kmax | 1);         // key bits in use
+  while (hi > 0) {
+    const int lo = max(hi - 8, 0);
+    const uint64_t mask = (1ull << (hi - lo)) - 1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hist[lane + kWave * j] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i)
+      if (state[i] == 1) atomicAdd(&hist[(key[i] >> lo) & mask], ln[i]);
+    __syncthreads();
+    // descending digit order: lane owns digits 255-4*lane .. 252-4*lane
+    int hv[4], hsum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      hv[j] = hist[255 - 4 * lane - j];
+      hsum += hv[j];
+    }
+    int tot;
+    int acc = taken + wave_exclusive_sum(hsum, &tot);
+    (void)tot;
+    int cut = -1;                                  // first digit whose bucket overflows
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (cut < 0 && acc + hv[j] > cap_sel) cut = 255 - 4 * lane - j;
+      acc += hv[j];
+    }
+    const uint64_t cut_lanes = __ballot(cut >= 0);
+    if (cut_lanes == 0) {                          // every active candidate fits
+#pragma unroll
+      for (int i = 0; i < kSmallPer; ++i)
+        if (state[i] == 1) state[i] = 2;
+      break;
+    }
+    const int d_cut = __shfl(cut, __builtin_ctzll(cut_lanes), kWave);
+    int my_above = 0;
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) {
+      if (state[i] == 1) {
+        const int dg = static_cast<int>((key[i] >> lo) & mask);
+        if (dg > d_cut) {
+          state[i] = 2;
+          my_above += ln[i];
+        } else if (dg < d_cut) {
+          state[i] = 0;
+        }
+      }
+    }
+    int above, my_left = 0, left;
+#pragma unroll
+    for (int i = 0; i < kSmallPer; ++i) my_left += state[i] == 1 ? 1 : 0;
+    wave_exclusive_sum(my_above, &above);
+    wave_exclusive_sum(my_left, &left);
+    taken += above;
+    hi = lo;
+    __syncthreads();
+    if (hi == 0 || left <= 1) {                    // one key left in the bucket: the misfit
+#pragma unroll
+      for (int i = 0; i < kSmallPer; ++i)
+        if (state[i] == 1) state[i] = 0;
+      break;
+    }
+  }
+  int my_sel = 0;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    const int u = u0 + i;
+    if (u < U) {
+      const bool kp = sys[i] || rec[i] || state[i] == 2;
+      keep_g[base + u] = kp ? 1 : 0;
+      my_sel += state[i] == 2 ? ln[i] : 0;
+    }
+  }
+  int t_sel;
+  wave_exclusive_sum(my_sel, &t_sel);
+  if (lane == 0) kept_tokens_g[seg] = t_sys + t_rec + t_sel;
+}
+
 }  // namespace
 
 hipError_t launch_select(const uint64_t* wsum, const int32_t* len, const int32_t* first,
                          const int32_t* last, const uint32_t* flags, int n_seg, int n_units,
                          int budget, int recent, uint64_t* score, uint8_t* keep,
                          int32_t* kept_tokens, int32_t* status, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3(n_seg), dim3(kSelThreads), 0, stream, wsum, len, first,
-                     last, flags, n_units, budget, recent, score, keep, kept_tokens, status);
+  if (n_units <= kSmallUnits)
+    hipLaunchKernelGGL(select_small_kernel, dim3(n_seg), dim3(kWave), 0, stream, wsum, len,
+                       first, last, flags, n_units, budget, recent, score, keep, kept_tokens,
+                       status);
+  else
+    hipLaunchKernelGGL(select_kernel, dim3(n_seg), dim3(kSelThreads), 0, stream, wsum, len,
+                       first, last, flags, n_units, budget, recent, score, keep, kept_tokens,
+                       status);
   return hipGetLastError();
 }
 

@@ -416,3 +416,47 @@ def test_full_budget_matches_uncompacted_attention_bitwise():
     ot.omnitide_chunk_attn(seg.q.cuda()[None], k_all, v_all, nctx, cfg.scale, out2, st.attn_ws)
     torch.cuda.synchronize()
     assert torch.equal(out2, st.out)
+
+
+def _random_plans(rng, n_seg, U, tie_levels):
+    lens = rng.integers(0, 40, size=(n_seg, U))
+    first = np.zeros((n_seg, U), np.int64)
+    last = np.zeros((n_seg, U), np.int64)
+    for si in range(n_seg):
+        s = 0
+        for u in range(U):
+            first[si, u], last[si, u] = (s, s + lens[si, u] - 1) if lens[si, u] else (10 ** 6, -1)
+            s += lens[si, u]
+    wsum = lens * rng.integers(0, tie_levels, size=(n_seg, U)) * 977 \
+        + rng.integers(0, 5, size=(n_seg, U)) * (tie_levels > 4)
+    flags = (rng.random((n_seg, U)) < 0.02).astype(np.int64)
+    return lens, first, last, wsum, flags
+
+
+@pytest.mark.parametrize("U,tie_levels", [(500, 3), (512, 1000000), (37, 2), (600, 4), (1500, 10 ** 6)])
+def test_select_random_instances_many_segments(U, tie_levels):
+    """Many random plans in one multi-segment call: heavy ties, empty units, system units."""
+    from paper_2609_34653_amd import omnitide as ot
+    rng = np.random.default_rng(U * 7 + tie_levels % 97)
+    n_seg = 48
+    lens, first, last, wsum, flags = _random_plans(rng, n_seg, U, tie_levels)
+    budget = int(np.median(lens.sum(1)) * 0.5)
+    recent = 60
+    i32 = lambda a: dev(np.asarray(a, np.int32).reshape(-1))   # noqa: E731
+    sc_d = torch.zeros(n_seg * U, dtype=torch.int64, device="cuda")
+    keep_d = torch.zeros(n_seg * U, dtype=torch.uint8, device="cuda")
+    kept_d = torch.zeros(n_seg, dtype=torch.int32, device="cuda")
+    stat = torch.zeros(1, dtype=torch.int32, device="cuda")
+    flags[:, :] = np.where((lens * flags).sum(1, keepdims=True) > budget, 0, flags)
+    ot.omnitide_select_units(dev(wsum.astype(np.int64).reshape(-1)), i32(lens), i32(first),
+                             i32(last), i32(flags), n_seg, U, budget, recent, sc_d, keep_d, kept_d,
+                             stat)
+    torch.cuda.synchronize()
+    assert int(host(stat)[0]) == 0
+    keep_h, sc_h, kept_h = host(keep_d).reshape(n_seg, U), host(sc_d).reshape(n_seg, U), host(kept_d)
+    for si in range(n_seg):
+        score, keep, kept = oracle.select_units(wsum[si], lens[si], first[si], last[si],
+                                                flags[si], budget, recent)
+        assert np.array_equal(sc_h[si], score)
+        assert np.array_equal(keep_h[si], keep), si
+        assert int(kept_h[si]) == kept
