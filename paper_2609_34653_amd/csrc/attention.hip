@@ -145,18 +145,32 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   auto vbuf = [&](int i) { return lds + (2 + i) * S::TILE_ELEMS; };
   // Direct global -> LDS copy of one tensor's tile (this wave's CALLS 1 KB pieces).  Rows past
   // n_ctx are clamped to a valid row here and zeroed after arrival.
-  auto issue = [&](const uint16_t* src, bool is_v, int t, uint16_t* dst) {
+  // Per-lane offsets of this lane's 16-byte pieces inside a tile (the same for every tile):
+  // piece cq covers linear chunk (wave + kAttnWaves*cq)*64 + lane of the swizzled LDS tile.
+  const int row_stride = Hkv * D;
+  int koff[S::CALLS], voff[S::CALLS], krowl[S::CALLS];
+#pragma unroll
+  for (int cq = 0; cq < S::CALLS; ++cq) {
+    const int lc = (wave + kAttnWaves * cq) * kWave + lane;
+    const int key = lc / S::CHUNKS, pc = lc % S::CHUNKS;
+    krowl[cq] = key;
+    koff[cq] = key * row_stride + 8 * (pc ^ (kswz(key) & (S::CHUNKS - 1)));
+    voff[cq] = key * row_stride + 8 * (2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1));
+  }
+  const uint16_t* k_head = k + (kv_seg * Hkv + g) * D;
+  const uint16_t* v_head = v + (kv_seg * Hkv + g) * D;
+  // Direct global -> LDS copy of one tensor's tile (this wave's CALLS 1 KB pieces).  In a
+  // boundary tile, rows past n_ctx are clamped to a valid row here and zeroed after arrival.
+  auto issue = [&](const uint16_t* head_base, bool is_v, int t, uint16_t* dst) {
     const int j0 = t * kKT;
+    const uint16_t* tile = head_base + static_cast<size_t>(j0) * row_stride;
+    const bool inner = j0 + kKT <= nctx;
 #pragma unroll
     for (int cq = 0; cq < S::CALLS; ++cq) {
       const int call = wave + kAttnWaves * cq;
-      const int lc = call * kWave + lane;          // linear 16-byte chunk in the tile
-      const int key = lc / S::CHUNKS, pc = lc % S::CHUNKS;
-      const int row = min(j0 + key, nctx - 1);
-      const int chunk = is_v ? 2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1)
-                             : pc ^ (kswz(key) & (S::CHUNKS - 1));
-      __builtin_amdgcn_global_load_lds(src + ((kv_seg + row) * Hkv + g) * D + 8 * chunk,
-                                       (lds_void*)(dst + call * kWave * 8), 16, 0, 0);
+      int off = is_v ? voff[cq] : koff[cq];
+      if (!inner) off += (min(j0 + krowl[cq], nctx - 1) - j0 - krowl[cq]) * row_stride;
+      __builtin_amdgcn_global_load_lds(tile + off, (lds_void*)(dst + call * kWave * 8), 16, 0, 0);
     }
   };
   auto zero_rows = [&](int t, uint16_t* buf) {
@@ -185,9 +199,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   };
 
   if (t_begin < t_end) {
-    issue(k, false, t_begin, kbuf(0));
-    issue(v, true, t_begin, vbuf(0));
-    if (t_begin + 1 < t_end) issue(k, false, t_begin + 1, kbuf(1));
+    issue(k_head, false, t_begin, kbuf(0));
+    issue(v_head, true, t_begin, vbuf(0));
+    if (t_begin + 1 < t_end) issue(k_head, false, t_begin + 1, kbuf(1));
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (t_begin * kKT + kKT > nctx) {
@@ -209,8 +223,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         zero_rows(t, vbuf(r & 1));
         __syncthreads();
       }
-      if (t + 2 < t_end) issue(k, false, t + 2, kbuf(r & 1));
-      if (has_next) issue(v, true, t + 1, vbuf((r + 1) & 1));
+      if (t + 2 < t_end) issue(k_head, false, t + 2, kbuf(r & 1));
+      if (has_next) issue(v_head, true, t + 1, vbuf((r + 1) & 1));
 
       // causal mask of this tile's scores (only tiles past the first row's limit)
       if (j0 + kKT - 1 > full_lim) {
