@@ -1,10 +1,11 @@
 // Eager, order-preserving, out-of-place compaction of the retained rows plus the chunk append.
 //
 // Two kernels on the caller's stream:
-//   plan  one workgroup per segment.  Exclusive scans over units give each kept unit its
-//         destination offset, its rank (= new unit id) and the number of deleted live tokens
-//         before it; a rank table {offset, first slot, deleted-before} with a sentinel, and for
-//         every destination tile the rank of the unit holding its first row, go to the workspace.
+//   plan  one workgroup per segment (a single wave up to 512 units).  Exclusive scans over
+//         units give each kept unit its destination offset, its rank (= new unit id) and the
+//         number of deleted live tokens before it; a rank table {offset, first slot,
+//         deleted-before} with a sentinel, and for every destination tile the rank of the unit
+//         holding its first row, go to the workspace.
 //   copy  one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
 //         source slots from the rank table (short forward walk from the tile's hint), tags are
 //         written, then every thread moves 16-byte vectors of the K and V rows.  Rows are whole
@@ -18,7 +19,7 @@ namespace {
 
 constexpr int kPlanThreads = 1024;
 constexpr int kPer = OMNITIDE_MAX_UNITS / kPlanThreads;
-constexpr int kTile = 32;           // destination rows per copy workgroup
+constexpr int kTile = 16;           // destination rows per copy workgroup
 constexpr int kCopyThreads = 256;
 
 struct RankRec {
@@ -99,6 +100,109 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
     del += dl[i];
   }
   if (tid == 0) {
+    rank[n_kept] = RankRec{kept, 0, 0, 0};
+    const int nctx = kept + chunk_len;
+    meta[0] = kept;
+    meta[1] = n_kept;
+    if (nctx > cap_dst) {
+      set_status(status, OMNITIDE_E_CAPACITY);
+      n_ctx_g[seg] = 0;
+      n_pages_g[seg] = 0;
+    } else {
+      n_ctx_g[seg] = nctx;
+      n_pages_g[seg] = (nctx + page_size - 1) / page_size;
+    }
+  }
+}
+
+// Single-wave plan for U <= 512 (each lane owns 8 consecutive units): the same tables as
+// compact_plan_kernel with wave-level scans, no workgroup barriers.
+constexpr int kSmallUnits = 512;
+constexpr int kSmallPer = kSmallUnits / kWave;
+
+__device__ inline int wave_excl(int v, int* total) {
+  const int inc = wave_inclusive_scan(v);
+  *total = __shfl(inc, kWave - 1, kWave);
+  return inc - v;
+}
+
+__global__ __launch_bounds__(kWave) void compact_plan_small_kernel(
+    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, int n_units, int chunk_len, int cap_dst, int page_size,
+    int32_t* __restrict__ remap_g, int32_t* __restrict__ n_ctx_g,
+    int32_t* __restrict__ n_pages_g, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
+  const int seg = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int U = n_units;
+  const int u0 = lane * kSmallPer;
+  const size_t base = static_cast<size_t>(seg) * U;
+  const WsLayout L = ws_layout(U, cap_dst);
+  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+  RankRec* rank = reinterpret_cast<RankRec*>(wseg + L.rank_off);
+  int32_t* tile_hint = reinterpret_cast<int32_t*>(wseg + L.tile_off);
+  int32_t* meta = reinterpret_cast<int32_t*>(wseg + L.meta_off);
+
+  int nl[kSmallPer], fs[kSmallPer];
+  uint8_t kp[kSmallPer];
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {      // all loads first: one memory round trip
+    const int u = min(u0 + i, U - 1);
+    nl[i] = len_g[base + u];
+    fs[i] = first_g[base + u];
+    kp[i] = keep_g[base + u];
+  }
+  int kl[kSmallPer], dl[kSmallPer];
+  int my_k = 0, my_d = 0, my_n = 0;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    const int n = (u0 + i < U) ? max(nl[i], 0) : 0;
+    kl[i] = kp[i] ? n : 0;
+    dl[i] = kp[i] ? 0 : n;
+    my_k += kl[i];
+    my_d += dl[i];
+    my_n += kl[i] > 0 ? 1 : 0;
+  }
+  __shared__ int32_t roff[kSmallUnits + 1];      // destination offset of each kept rank
+  int kept, dropped, n_kept;
+  int off = wave_excl(my_k, &kept);
+  int del = wave_excl(my_d, &dropped);
+  int rk = wave_excl(my_n, &n_kept);
+  (void)dropped;
+#pragma unroll
+  for (int i = 0; i < kSmallPer; ++i) {
+    const int u = u0 + i;
+    if (u < U) {
+      if (kl[i] > 0) {
+        rank[rk] = RankRec{off, fs[i], del, 0};
+        roff[rk] = off;
+        remap_g[base + u] = rk;
+        ++rk;
+      } else {
+        remap_g[base + u] = -1;
+      }
+    }
+    off += kl[i];
+    del += dl[i];
+  }
+  if (lane == 0) roff[n_kept] = kept;
+  __syncthreads();
+  // Tile hints: lane takes a contiguous range of destination tiles, binary-searches the rank of
+  // its first tile's first row, then walks forward.
+  const int n_tiles = (kept + kTile - 1) / kTile;
+  const int per_lane = (n_tiles + kWave - 1) / kWave;
+  const int t0 = lane * per_lane, t1 = min(t0 + per_lane, n_tiles);
+  if (t0 < t1) {
+    int lo = 0, hi = n_kept - 1;                  // largest k with roff[k] <= t0 * kTile
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (roff[mid] <= t0 * kTile) lo = mid; else hi = mid - 1;
+    }
+    for (int t = t0; t < t1; ++t) {
+      while (roff[lo + 1] <= t * kTile) ++lo;
+      tile_hint[t] = lo;
+    }
+  }
+  if (lane == 0) {
     rank[n_kept] = RankRec{kept, 0, 0, 0};
     const int nctx = kept + chunk_len;
     meta[0] = kept;
@@ -241,10 +345,16 @@ size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
 }
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream, a.keep,
-                     a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst, a.page_size,
-                     a.unit_remap, a.n_ctx, a.n_pages, static_cast<uint8_t*>(a.workspace),
-                     a.d_status);
+  if (a.n_units <= kSmallUnits)
+    hipLaunchKernelGGL(compact_plan_small_kernel, dim3(a.n_seg), dim3(kWave), 0, stream, a.keep,
+                       a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst, a.page_size,
+                       a.unit_remap, a.n_ctx, a.n_pages, static_cast<uint8_t*>(a.workspace),
+                       a.d_status);
+  else
+    hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream,
+                       a.keep, a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst,
+                       a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
+                       static_cast<uint8_t*>(a.workspace), a.d_status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int vecs2 = 2 * a.row_bytes / 16;
