@@ -12,9 +12,8 @@
 //            are lane-local (plus one exchange between the two 32-lane halves).
 //   layout   the keys of an S^T tile are permuted when K rows are read from LDS so that lane half
 //            h holds keys 16h..16h+15 of the tile in register order; its probabilities then form
-//            the B operand of the P*V product directly (8 consecutive keys per operand).  V is
-//            stored transposed in LDS (V^T, keys contiguous) by an in-register 4x8 transpose
-//            while staging, so each V^T operand is one 16-byte LDS read.
+//            the B operand of the P*V product directly (8 consecutive keys per operand).  V
+//            stays row-major in LDS; its V^T operand is gathered by transposing LDS reads.
 //   softmax  fp32, base-2 exponent with scale*log2(e) folded into the scores; the causal mask is
 //            applied only to tiles that reach past the workgroup's first row's limit.
 //   order    workgroups that share a (KV head, split) are mapped onto one XCD (workgroups are
