@@ -15,7 +15,12 @@
 //            the B operand of the P*V product directly (8 consecutive keys per operand).  V
 //            stays row-major in LDS; its V^T operand is gathered by transposing LDS reads.
 //   softmax  fp32, base-2 exponent with scale*log2(e) folded into the scores; the causal mask is
-//            applied only to tiles that reach past the workgroup's first row's limit.
+//            applied only to tiles that reach past the workgroup's first row's limit.  The
+//            exponentials are taken against a reference that moves only when a row's tile sum
+//            would leave a bounded range (no per-tile row maximum, rare rescaling); row sums are
+//            taken over the rounded bf16 probabilities with dot2 instructions.
+//   loop     unrolled by two, so every LDS buffer is addressed statically; the score MFMAs of the
+//            next tile are interleaved with this tile's exponentials.
 //   order    workgroups that share a (KV head, split) are mapped onto one XCD (workgroups are
 //            dealt round-robin over 8 XCDs), so their K/V re-reads hit that XCD's L2.
 #include <algorithm>
@@ -28,6 +33,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = kAttnWaves * kWave;
@@ -79,6 +85,42 @@ __device__ inline shortx4 ld_tr(const uint16_t* p) {
       (__attribute__((address_space(3))) shortx4*)(p));
 }
 
+__device__ inline uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<size_t>((const lds_void*)p));
+}
+
+// 16-byte direct global -> LDS load: lane i reads base + voff_i and writes 16 bytes at LDS byte
+// address lds_base + 16 i.  Written as inline assembly (uniform base in SGPRs, per-lane 32-bit
+// offset) so that issuing it costs no vector instructions and so that the compiler's wait
+// insertion does not treat it as a pending LDS write (it would otherwise make later LDS reads of
+// other buffers wait for it).  Callers wait for it explicitly (s_waitcnt vmcnt(0) + barrier)
+// before any lane reads the buffer it fills.  One wait state is required between the M0 write
+// and the load.  M0 is not listed as clobbered (the compiler reserves it and ignores such
+// clobbers): this file's kernels have no other M0 user, so no compiler value lives in M0.
+__device__ inline void dma16(const void* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_base)
+               : "memory");
+}
+
+// max(x over both 32-lane halves): v_permlane32_swap exchanges the halves without LDS.
+__device__ inline float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int B, class T>
+__device__ inline T& pick(T& a, T& b) {
+  if constexpr (B == 0) return a; else return b;
+}
+
 template <int D>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -86,6 +128,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status) {
   using S = Smem<D>;
+  // Tile buffers K0, K1, V0, V1 at fixed offsets (every access below names its buffer at
+  // compile time, so LDS addresses are immediates).
   __shared__ __attribute__((aligned(1024))) uint16_t lds[4 * S::TILE_ELEMS];
 
   const int seg = blockIdx.y;
@@ -116,7 +160,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int col = lane & 31;
   const int h = lane >> 5;
   const int m = m0 + wave * 32 + col;
@@ -137,51 +181,59 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   }
 
   const size_t kv_seg = static_cast<size_t>(seg) * cap;
-  // Buffers: K tiles alternate between kbuf 0/1 and V tiles between vbuf 0/1.  Iteration t
-  // reads K(t+1) (scores of the next tile) and V(t) (output of this tile) while K(t+2) and
-  // V(t+1) are in flight.
-  auto kbuf = [&](int i) { return lds + i * S::TILE_ELEMS; };
-  auto vbuf = [&](int i) { return lds + (2 + i) * S::TILE_ELEMS; };
-  // Direct global -> LDS copy of one tensor's tile (this wave's CALLS 1 KB pieces).  Rows past
-  // n_ctx are clamped to a valid row here and zeroed after arrival.
-  // Per-lane offsets of this lane's 16-byte pieces inside a tile (the same for every tile):
-  // piece cq covers linear chunk (wave + kAttnWaves*cq)*64 + lane of the swizzled LDS tile.
   const int row_stride = Hkv * D;
-  int koff[S::CALLS], voff[S::CALLS], krowl[S::CALLS];
+  // Per-lane byte offsets of this lane's 16-byte pieces inside a tile (the same for every
+  // tile): piece cq covers linear chunk (wave + kAttnWaves*cq)*64 + lane of the swizzled tile.
+  uint32_t koff[S::CALLS], voff[S::CALLS];
+  int krowl[S::CALLS];
 #pragma unroll
   for (int cq = 0; cq < S::CALLS; ++cq) {
     const int lc = (wave + kAttnWaves * cq) * kWave + lane;
     const int key = lc / S::CHUNKS, pc = lc % S::CHUNKS;
     krowl[cq] = key;
-    koff[cq] = key * row_stride + 8 * (pc ^ (kswz(key) & (S::CHUNKS - 1)));
-    voff[cq] = key * row_stride + 8 * (2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1));
+    koff[cq] = 2u * (key * row_stride + 8 * (pc ^ (kswz(key) & (S::CHUNKS - 1))));
+    voff[cq] = 2u * (key * row_stride + 8 * (2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1)));
   }
   const uint16_t* k_head = k + (kv_seg * Hkv + g) * D;
   const uint16_t* v_head = v + (kv_seg * Hkv + g) * D;
-  // Direct global -> LDS copy of one tensor's tile (this wave's CALLS 1 KB pieces).  In a
+  const uint32_t lds_wave = lds_addr(lds) + static_cast<uint32_t>(wave * kWave * 16);
+  // Direct global -> LDS copy of one tensor's tile t into buffer `buf` (0,1 = K; 2,3 = V).  In a
   // boundary tile, rows past n_ctx are clamped to a valid row here and zeroed after arrival.
-  auto issue = [&](const uint16_t* head_base, bool is_v, int t, uint16_t* dst) {
+  auto issue = [&](const uint16_t* head_base, const uint32_t* offs, int t, int buf) {
     const int j0 = t * kKT;
     const uint16_t* tile = head_base + static_cast<size_t>(j0) * row_stride;
-    const bool inner = j0 + kKT <= nctx;
+    const uint32_t dst = lds_wave + static_cast<uint32_t>(buf * S::TILE_ELEMS * 2);
+    if (j0 + kKT <= nctx) {
 #pragma unroll
-    for (int cq = 0; cq < S::CALLS; ++cq) {
-      const int call = wave + kAttnWaves * cq;
-      int off = is_v ? voff[cq] : koff[cq];
-      if (!inner) off += (min(j0 + krowl[cq], nctx - 1) - j0 - krowl[cq]) * row_stride;
-      __builtin_amdgcn_global_load_lds(tile + off, (lds_void*)(dst + call * kWave * 8), 16, 0, 0);
+      for (int cq = 0; cq < S::CALLS; ++cq)
+        dma16(tile, offs[cq], dst + static_cast<uint32_t>(cq * kAttnWaves * kWave * 16));
+    } else {
+#pragma unroll
+      for (int cq = 0; cq < S::CALLS; ++cq) {
+        const int clamp = min(j0 + krowl[cq], nctx - 1) - j0 - krowl[cq];   // <= 0
+        dma16(tile, offs[cq] + 2u * static_cast<uint32_t>(clamp * row_stride),
+              dst + static_cast<uint32_t>(cq * kAttnWaves * kWave * 16));
+      }
     }
   };
-  auto zero_rows = [&](int t, uint16_t* buf) {
+  auto zero_rows = [&](int t, int buf) {
     const int j0 = t * kKT;
+    uint16_t* base = lds + buf * S::TILE_ELEMS;
     for (int idx = tid; idx < kKT * S::CHUNKS; idx += kAttnThreads)
       if (j0 + idx / S::CHUNKS >= nctx)
-        *reinterpret_cast<u32x4*>(buf + 8 * idx) = u32x4{0, 0, 0, 0};
+        *reinterpret_cast<u32x4*>(base + 8 * idx) = u32x4{0, 0, 0, 0};
   };
 
   floatx16 o[D / 32];
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt) o[dt] = floatx16{};
+  // m_run: the reference the exponentials are taken against (-inf until this row has seen a
+  // visible key).  It is not kept equal to the running maximum: the exponentials of a tile are
+  // computed optimistically against it and only if some row's tile sum reaches 2^32 (or is not
+  // finite: no reference yet) does the wave fall back to the exact tile maximum, move the
+  // reference, rescale and recompute.  Every probability and every partial sum therefore stays
+  // below 2^32 x tile count, far from fp32 overflow, and the final division by the sum taken
+  // against the same reference makes the result independent of where the reference sits.
   float m_run = -INFINITY, l_run = 0.f;
   const int krow = perm_key(col);
   const int fk = kswz(krow) & (S::CHUNKS - 1);
@@ -191,6 +243,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   const int v_lane_off = (gi >> 2) * D + 8 * ((gi & 3) >> 1) + 4 * (gi & 1);
   constexpr int NQK = 2 * (D / 16);                // score MFMAs per tile (two 32-key halves)
   constexpr int EPS = 32 / NQK;                    // exponentials per interleave segment
+  constexpr float kSumLimit = 4294967296.f;        // 2^32
 
   auto kop = [&](const uint16_t* kb, int i) {      // K operand of score MFMA i
     const int st = i & 1, c = i >> 1;
@@ -198,32 +251,39 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   };
 
   if (t_begin < t_end) {
-    issue(k_head, false, t_begin, kbuf(0));
-    issue(v_head, true, t_begin, vbuf(0));
-    if (t_begin + 1 < t_end) issue(k_head, false, t_begin + 1, kbuf(1));
+    issue(k_head, koff, t_begin, 0);
+    issue(v_head, voff, t_begin, 2);
+    if (t_begin + 1 < t_end) issue(k_head, koff, t_begin + 1, 1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (t_begin * kKT + kKT > nctx) {
-      zero_rows(t_begin, kbuf(0));
+      zero_rows(t_begin, 0);
       __syncthreads();
     }
-    floatx16 s_cur[2] = {floatx16{}, floatx16{}};
+    floatx16 sA[2] = {floatx16{}, floatx16{}}, sB[2];
 #pragma unroll
-    for (int i = 0; i < NQK; ++i) s_cur[i & 1] = mfma(kop(kbuf(0), i), qf[i >> 1], s_cur[i & 1]);
+    for (int i = 0; i < NQK; ++i) sA[i & 1] = mfma(kop(lds, i), qf[i >> 1], sA[i & 1]);
 
-    for (int t = t_begin; t < t_end; ++t) {
-      const int r = t - t_begin;
+    // One iteration for tile t with B = (t - t_begin) & 1: scores of t are in s_cur (computed
+    // by the previous iteration); K(t+1) is in K buffer 1-B, V(t) in V buffer B.  The iteration
+    // issues K(t+2) into K buffer B and V(t+1) into V buffer 1-B.
+    auto step = [&](auto par, int t) {
+      constexpr int B = decltype(par)::value;
+      floatx16(&s_cur)[2] = pick<B>(sA, sB);
+      floatx16(&s_nxt)[2] = pick<B>(sB, sA);
+      const uint16_t* Kn = lds + (1 - B) * S::TILE_ELEMS;
+      const uint16_t* Vs = lds + (2 + B) * S::TILE_ELEMS;
       const int j0 = t * kKT;
       const bool has_next = t + 1 < t_end;
       __builtin_amdgcn_s_waitcnt(0);      // this wave's pieces of K(t+1) and V(t) have landed
       __syncthreads();                    // ... everyone's; iteration t-1 is finished
       if ((has_next && j0 + 2 * kKT > nctx) || j0 + kKT > nctx) {
-        if (has_next) zero_rows(t + 1, kbuf((r + 1) & 1));
-        zero_rows(t, vbuf(r & 1));
+        if (has_next) zero_rows(t + 1, 1 - B);
+        zero_rows(t, 2 + B);
         __syncthreads();
       }
-      if (t + 2 < t_end) issue(k_head, false, t + 2, kbuf(r & 1));
-      if (has_next) issue(v_head, true, t + 1, vbuf((r + 1) & 1));
+      if (t + 2 < t_end) issue(k_head, koff, t + 2, B);
+      if (has_next) issue(v_head, voff, t + 1, 3 - B);
 
       // causal mask of this tile's scores (only tiles past the first row's limit)
       if (j0 + kKT - 1 > full_lim) {
@@ -234,57 +294,79 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
             if (j0 + 32 * st + 16 * h + i > lim) s_cur[st][i] = -INFINITY;
         }
       }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s_cur[st][i]);
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
-      const float m_new = fmaxf(m_run, mx);
-      // Rescale the running output only when some row's maximum moved.
-      if (__any(m_new > m_run)) {
-        const float m_u = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_u);
-        l_run *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
-      }
-      m_run = m_new;
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
 
       // Interleave: segment i issues score MFMA i of the next tile and then EPS exponentials
       // of this tile, so the vector ALU works while the matrix core runs (a wave issues in
       // order).  In the last iteration the next-K buffer holds a stale tile; the scores
       // computed from it are discarded, which keeps the loop body branch-free.
-      const uint16_t* kn = kbuf((r + 1) & 1);
-      floatx16 s_nxt[2] = {floatx16{}, floatx16{}};
       float e[32];
-      float lsum = 0.f;
-      bf16x8 ka0 = kop(kn, 0), ka1 = kop(kn, 1);
+      {
+        s_nxt[0] = floatx16{};
+        s_nxt[1] = floatx16{};
+        const float m_use = m_run;
+        bf16x8 ka0 = kop(Kn, 0), ka1 = kop(Kn, 1);
 #pragma unroll
-      for (int i = 0; i < NQK; ++i) {
-        const bf16x8 ka = (i & 1) ? ka1 : ka0;
-        s_nxt[i & 1] = mfma(ka, qf[i >> 1], s_nxt[i & 1]);
-        if (i + 2 < NQK) {
-          if (i & 1) ka1 = kop(kn, i + 2); else ka0 = kop(kn, i + 2);
+        for (int i = 0; i < NQK; ++i) {
+          const bf16x8 ka = (i & 1) ? ka1 : ka0;
+          s_nxt[i & 1] = mfma(ka, qf[i >> 1], s_nxt[i & 1]);
+          if (i + 2 < NQK) {
+            if (i & 1) ka1 = kop(Kn, i + 2); else ka0 = kop(Kn, i + 2);
+          }
+#pragma unroll
+          for (int j = 0; j < EPS; ++j) {
+            const int x = i * EPS + j;
+            e[x] = __builtin_amdgcn_exp2f(fmaf(s_cur[x >> 4][x & 15], scale_log2, -m_use));
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
+      }
+      bf16x8 pf[2][2];
+      auto pack = [&]() {
 #pragma unroll
-        for (int j = 0; j < EPS; ++j) {
-          const int x = i * EPS + j;
+        for (int x = 0; x < 32; ++x) pf[x >> 4][(x >> 3) & 1][x & 7] = static_cast<__bf16>(e[x]);
+      };
+      // Row sum of the rounded probabilities (exactly the weights the P*V product uses), two
+      // bf16 pairs per instruction against (1, 1), in two chains.
+      auto rowsum = [&]() {
+        const bf16x2 one2 = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+        float ls[2] = {0.f, 0.f};
+#pragma unroll
+        for (int x = 0; x < 16; ++x) {
+          const bf16x8 v8 = pf[x >> 3][(x >> 2) & 1];
+          const int j = x & 3;
+          const bf16x2 pr = {v8[2 * j], v8[2 * j + 1]};
+          ls[x & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one2, ls[x & 1], false);
+        }
+        return ls[0] + ls[1];
+      };
+      pack();
+      float lsum = rowsum();
+      if (__any(!(lsum < kSumLimit))) {
+        // Slow path: exact tile maximum, move the reference, rescale, recompute the tile.
+        float mx = -INFINITY;
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s_cur[st][i]);
+        }
+        mx = max_halves(mx) * scale_log2;
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) o[dt] *= alpha;
+        m_run = m_new;
+#pragma unroll
+        for (int x = 0; x < 32; ++x)
           e[x] = __builtin_amdgcn_exp2f(fmaf(s_cur[x >> 4][x & 15], scale_log2, -m_use));
-          lsum += e[x];
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        pack();
+        lsum = rowsum();
       }
       l_run += lsum;
-      bf16x8 pf[2][2];
-#pragma unroll
-      for (int x = 0; x < 32; ++x) pf[x >> 4][(x >> 3) & 1][x & 7] = static_cast<__bf16>(e[x]);
 
       // O^T += V^T P^T: the V^T operand (dims 32dt.., keys 32st+16h+8cc..+8) from two
       // transposing reads of four keys each.
-      const uint16_t* Vs = vbuf(r & 1);
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
@@ -301,12 +383,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
           }
         }
       }
-      s_cur[0] = s_nxt[0];
-      s_cur[1] = s_nxt[1];
+    };
+    int t = t_begin;
+    for (; t + 1 < t_end; t += 2) {
+      step(std::integral_constant<int, 0>{}, t);
+      step(std::integral_constant<int, 1>{}, t + 1);
     }
+    if (t < t_end) step(std::integral_constant<int, 0>{}, t);
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  const float l_tot = sum_halves(l_run);
   if (!row_ok) return;
   const size_t orow = (static_cast<size_t>(seg) * L + p) * Hq + head;
   if (n_split == 1) {
