@@ -210,8 +210,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     } else {
 #pragma unroll
       for (int cq = 0; cq < S::CALLS; ++cq) {
-        const int clamp = min(j0 + krowl[cq], nctx - 1) - j0 - krowl[cq];   // <= 0
-        dma16(tile, offs[cq] + 2u * static_cast<uint32_t>(clamp * row_stride),
+        // Base at row min(j0, n_ctx-1) so every lane offset stays non-negative (the hardware
+        // zero-extends it): lane row min(j0+key, n_ctx-1) lies 0..kKT-1 rows past the base.
+        const int r0 = min(j0, nctx - 1);
+        const int shift = min(j0 + krowl[cq], nctx - 1) - r0 - krowl[cq];
+        dma16(head_base + static_cast<size_t>(r0) * row_stride,
+              offs[cq] + 2u * static_cast<uint32_t>(shift * row_stride),
               dst + static_cast<uint32_t>(cq * kAttnWaves * kWave * 16));
       }
     }
