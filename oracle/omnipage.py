@@ -40,12 +40,18 @@ def page_span(n_ctx: int, page_size: int) -> int:
 
 
 def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
-               k_chunk, v_chunk, chunk_modality, chunk_unit, cap_dst: int, page_size: int):
+               k_chunk, v_chunk, chunk_modality, chunk_unit, cap_dst: int, page_size: int,
+               rope=None):
     """Order-preserving out-of-place packing of the kept units' rows, then the chunk.
 
     k_src/v_src: [n_slots, H_kv, d] (any dtype; rows are copied verbatim).
     Returns a dict: k, v ([n_ctx, H_kv, d]), unit_id, modality, pos, src_of_dst (per destination
     row), unit_remap [n_units], n_ctx, n_pages.
+
+    rope: optional dict(base, dims, style, dtype) -- the keys are rotary-encoded at their
+    positions; the result then also holds "k_f64": the destination keys as float64 with every
+    history row re-rotated by its position shift (new - old position, see rope.shift_keys) and
+    the chunk rows unchanged (they are encoded at their new positions by the caller).
     """
     unit_id = np.asarray(unit_id, np.int64)
     n_slots = unit_id.shape[0]
@@ -91,6 +97,14 @@ def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
                           np.asarray(chunk_modality, np.int64)])
     p = np.concatenate([np.array(new_pos, np.int64), kept + np.arange(L, dtype=np.int64)])
     src = np.concatenate([rows, np.full(L, -1, np.int64)])
-    return {"k": k, "v": v, "unit_id": uid, "modality": mod, "pos": p, "src_of_dst": src,
-            "unit_remap": unit_remap, "n_ctx": n_ctx, "n_pages": n_pages(n_ctx, page_size),
-            "kept": kept, "n_kept_units": n_kept_units}
+    out = {"k": k, "v": v, "unit_id": uid, "modality": mod, "pos": p, "src_of_dst": src,
+           "unit_remap": unit_remap, "n_ctx": n_ctx, "n_pages": n_pages(n_ctx, page_size),
+           "kept": kept, "n_kept_units": n_kept_units}
+    if rope is not None:
+        from .omnipick import to_f64
+        from .rope import shift_keys
+        shift = np.zeros(n_ctx, np.int64)
+        shift[:kept] = p[:kept] - np.asarray(pos, np.int64)[rows]
+        out["k_f64"] = shift_keys(to_f64(k, rope["dtype"]), shift, rope["base"], rope["dims"],
+                                  rope["style"])
+    return out
