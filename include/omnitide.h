@@ -56,6 +56,9 @@ enum {
 };
 
 enum { OMNITIDE_BF16 = 0, OMNITIDE_F32 = 1 };
+/* rotary dimension pairing for omnitide_compact_kv_rope */
+enum { OMNITIDE_ROPE_HALF = 0,          /* pairs (j, j + rope_dims/2) */
+       OMNITIDE_ROPE_INTERLEAVED = 1 }; /* pairs (2j, 2j + 1) */
 enum { OMNITIDE_MOD_SYS = 0, OMNITIDE_MOD_VIDEO = 1, OMNITIDE_MOD_AUDIO = 2, OMNITIDE_MOD_TEXT = 3 };
 
 /* Limits checked on the host. */
@@ -162,6 +165,40 @@ int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_s
                         int32_t* pos_dst, int32_t* src_of_dst, int32_t* unit_remap,
                         int32_t* n_ctx, int32_t* n_pages, void* workspace,
                         size_t workspace_bytes, int32_t* d_status, void* stream);
+
+/*
+ * omnitide_compact_kv_rope -- omnitide_compact_kv plus the rotary re-encoding of the moved keys
+ * (paper: Applying the retention plan -- a retained token's position drops by the number of
+ * deleted tokens before it, and the runtime applies the matching RoPE adjustment to the cached
+ * keys).  Same arguments, outputs and errors as omnitide_compact_kv, except:
+ *   k_dst   history row r (source slot s) holds K[s] with each pair (x, y) of its first
+ *           rope_dims dimensions (per head) turned by shift * theta_j:
+ *           (x cos - y sin, x sin + y cos), shift = pos_dst[r] - pos_src[s] (<= 0, minus the
+ *           deleted live slots before s), theta_j = rope_base^(-2j / rope_dims),
+ *           j < rope_dims / 2; the pairing is rope_style.  Chunk rows, dimensions >= rope_dims,
+ *           rows with shift 0 and all of V are copied unchanged, bit for bit.
+ *   rope_base    finite and > 1 (e.g. 10000 or 1e6)
+ *   rope_dims    even, 2..head_dim; with OMNITIDE_ROPE_HALF a multiple of 16 (bf16) or 8 (f32)
+ *   rope_style   OMNITIDE_ROPE_HALF or OMNITIDE_ROPE_INTERLEAVED
+ * Precision: the angle shift * theta_j is reduced modulo 2 pi in double precision, its sine and
+ * cosine and the rotation are computed in float, and the result is rounded to the storage type
+ * (round to nearest even): within half a unit in the last place of the exactly rotated value
+ * plus 2^-21 of the length of the rotated pair.
+ * Invalid rope arguments return OMNITIDE_E_SHAPE (checked after null pointers and dtype).
+ */
+int omnitide_compact_kv_rope(const void* k_src, const void* v_src, int dtype, int n_seg,
+                             int n_slots_src, int n_kv_heads, int head_dim, int page_size,
+                             const int32_t* unit_id_src, const uint8_t* modality_src,
+                             const int32_t* pos_src, const uint8_t* keep,
+                             const int32_t* unit_len, const int32_t* unit_first_slot,
+                             int n_units, const void* k_chunk, const void* v_chunk,
+                             const uint8_t* chunk_modality, const int32_t* chunk_unit,
+                             int chunk_len, void* k_dst, void* v_dst, int cap_dst,
+                             int32_t* unit_id_dst, uint8_t* modality_dst, int32_t* pos_dst,
+                             int32_t* src_of_dst, int32_t* unit_remap, int32_t* n_ctx,
+                             int32_t* n_pages, void* workspace, size_t workspace_bytes,
+                             double rope_base, int rope_dims, int rope_style,
+                             int32_t* d_status, void* stream);
 
 size_t omnitide_compact_workspace_bytes(int n_seg, int n_units, int cap_dst);
 

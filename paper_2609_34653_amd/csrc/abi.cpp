@@ -120,17 +120,18 @@ size_t omnitide_compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
   return omnitide::compact_workspace_bytes(n_seg, n_units, cap_dst);
 }
 
-int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_seg,
-                        int n_slots_src, int n_kv_heads, int head_dim, int page_size,
-                        const int32_t* unit_id_src, const uint8_t* modality_src,
-                        const int32_t* pos_src, const uint8_t* keep, const int32_t* unit_len,
-                        const int32_t* unit_first_slot, int n_units, const void* k_chunk,
-                        const void* v_chunk, const uint8_t* chunk_modality,
-                        const int32_t* chunk_unit, int chunk_len, void* k_dst, void* v_dst,
-                        int cap_dst, int32_t* unit_id_dst, uint8_t* modality_dst,
-                        int32_t* pos_dst, int32_t* src_of_dst, int32_t* unit_remap,
-                        int32_t* n_ctx, int32_t* n_pages, void* workspace,
-                        size_t workspace_bytes, int32_t* d_status, void* stream) {
+namespace {
+
+int compact_impl(const void* k_src, const void* v_src, int dtype, int n_seg, int n_slots_src,
+                 int n_kv_heads, int head_dim, int page_size, const int32_t* unit_id_src,
+                 const uint8_t* modality_src, const int32_t* pos_src, const uint8_t* keep,
+                 const int32_t* unit_len, const int32_t* unit_first_slot, int n_units,
+                 const void* k_chunk, const void* v_chunk, const uint8_t* chunk_modality,
+                 const int32_t* chunk_unit, int chunk_len, void* k_dst, void* v_dst, int cap_dst,
+                 int32_t* unit_id_dst, uint8_t* modality_dst, int32_t* pos_dst,
+                 int32_t* src_of_dst, int32_t* unit_remap, int32_t* n_ctx, int32_t* n_pages,
+                 void* workspace, size_t workspace_bytes, bool rope, double rope_base,
+                 int rope_dims, int rope_style, int32_t* d_status, void* stream) {
   if (!all_set({keep, unit_len, unit_first_slot, k_dst, v_dst, unit_id_dst, modality_dst,
                 pos_dst, src_of_dst, unit_remap, n_ctx, n_pages}))
     return OMNITIDE_E_NULL;
@@ -140,6 +141,14 @@ int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_s
     return OMNITIDE_E_NULL;
   const int eb = elt_bytes(dtype);
   if (eb == 0) return OMNITIDE_E_DTYPE;
+  if (rope) {
+    const int chunk_elems = 16 / eb;
+    if (!(rope_style == OMNITIDE_ROPE_HALF || rope_style == OMNITIDE_ROPE_INTERLEAVED) ||
+        rope_dims < 2 || rope_dims % 2 != 0 || rope_dims > head_dim ||
+        (rope_style == OMNITIDE_ROPE_HALF && (rope_dims / 2) % chunk_elems != 0) ||
+        !(std::isfinite(rope_base) && rope_base > 1.0))
+      return OMNITIDE_E_SHAPE;
+  }
   if (n_seg < 1 || n_seg > kMaxGridY || n_slots_src < 0 || n_units < 1 ||
       n_units > OMNITIDE_MAX_UNITS || !row_ok(n_kv_heads, head_dim) || chunk_len < 0 ||
       !(page_size == 32 || page_size == 64 || page_size == 128 || page_size == 256) ||
@@ -195,7 +204,54 @@ int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_s
   a.n_pages = n_pages;
   a.workspace = workspace;
   a.d_status = d_status;
+  a.n_kv_heads = n_kv_heads;
+  a.head_dim = head_dim;
+  a.rope_base = rope_base;
+  a.rope_dims = rope ? rope_dims : 0;
+  a.rope_half = rope_style == OMNITIDE_ROPE_HALF;
   return hip_status(omnitide::launch_compact(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_seg,
+                        int n_slots_src, int n_kv_heads, int head_dim, int page_size,
+                        const int32_t* unit_id_src, const uint8_t* modality_src,
+                        const int32_t* pos_src, const uint8_t* keep, const int32_t* unit_len,
+                        const int32_t* unit_first_slot, int n_units, const void* k_chunk,
+                        const void* v_chunk, const uint8_t* chunk_modality,
+                        const int32_t* chunk_unit, int chunk_len, void* k_dst, void* v_dst,
+                        int cap_dst, int32_t* unit_id_dst, uint8_t* modality_dst,
+                        int32_t* pos_dst, int32_t* src_of_dst, int32_t* unit_remap,
+                        int32_t* n_ctx, int32_t* n_pages, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream) {
+  return compact_impl(k_src, v_src, dtype, n_seg, n_slots_src, n_kv_heads, head_dim, page_size,
+                      unit_id_src, modality_src, pos_src, keep, unit_len, unit_first_slot,
+                      n_units, k_chunk, v_chunk, chunk_modality, chunk_unit, chunk_len, k_dst,
+                      v_dst, cap_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
+                      unit_remap, n_ctx, n_pages, workspace, workspace_bytes, false, 0.0, 0, 0,
+                      d_status, stream);
+}
+
+int omnitide_compact_kv_rope(const void* k_src, const void* v_src, int dtype, int n_seg,
+                             int n_slots_src, int n_kv_heads, int head_dim, int page_size,
+                             const int32_t* unit_id_src, const uint8_t* modality_src,
+                             const int32_t* pos_src, const uint8_t* keep,
+                             const int32_t* unit_len, const int32_t* unit_first_slot,
+                             int n_units, const void* k_chunk, const void* v_chunk,
+                             const uint8_t* chunk_modality, const int32_t* chunk_unit,
+                             int chunk_len, void* k_dst, void* v_dst, int cap_dst,
+                             int32_t* unit_id_dst, uint8_t* modality_dst, int32_t* pos_dst,
+                             int32_t* src_of_dst, int32_t* unit_remap, int32_t* n_ctx,
+                             int32_t* n_pages, void* workspace, size_t workspace_bytes,
+                             double rope_base, int rope_dims, int rope_style,
+                             int32_t* d_status, void* stream) {
+  return compact_impl(k_src, v_src, dtype, n_seg, n_slots_src, n_kv_heads, head_dim, page_size,
+                      unit_id_src, modality_src, pos_src, keep, unit_len, unit_first_slot,
+                      n_units, k_chunk, v_chunk, chunk_modality, chunk_unit, chunk_len, k_dst,
+                      v_dst, cap_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
+                      unit_remap, n_ctx, n_pages, workspace, workspace_bytes, true, rope_base,
+                      rope_dims, rope_style, d_status, stream);
 }
 
 size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,

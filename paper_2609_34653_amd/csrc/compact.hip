@@ -218,26 +218,24 @@ __global__ __launch_bounds__(kWave) void compact_plan_small_kernel(
   }
 }
 
-template <int VPT>
-__global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
-    const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
-    int row_bytes, const uint8_t* __restrict__ mod_src,
-    const int32_t* __restrict__ pos_src, const uint8_t* __restrict__ k_chunk,
-    const uint8_t* __restrict__ v_chunk, const uint8_t* __restrict__ chunk_mod,
-    const int32_t* __restrict__ chunk_unit, int chunk_len, uint8_t* __restrict__ k_dst,
-    uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
-    uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
-    int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
-    const uint8_t* __restrict__ ws) {
-  constexpr int RB = VPT >= 16 ? 1 : 16 / VPT;
-  __shared__ int32_t src_row[kTile];
-  const int seg = blockIdx.y;
-  const int t = blockIdx.x;
+// Writes the tags of destination tile t and resolves its rows: src_row[i] is the source slot of
+// row r0 + i, or -1 - c for chunk row c; shift_row[i] (if given) is the row's position change
+// (minus the deleted live slots before it; 0 for chunk rows).  Rows [n_ctx, cap_dst) become empty
+// slots, so the destination is a complete pool.  Returns the tile's row count (0: nothing to
+// copy).  Ends with a workgroup barrier.
+__device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int chunk_len,
+                                   int cap_dst, int n_units, const uint8_t* __restrict__ mod_src,
+                                   const int32_t* __restrict__ pos_src,
+                                   const uint8_t* __restrict__ chunk_mod,
+                                   const int32_t* __restrict__ chunk_unit,
+                                   int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst,
+                                   int32_t* __restrict__ pos_dst,
+                                   int32_t* __restrict__ src_of_dst,
+                                   const uint8_t* __restrict__ ws, int32_t* src_row,
+                                   int32_t* shift_row) {
   const int tid = threadIdx.x;
-  const int nctx = n_ctx_g[seg];
   const int r0 = t * kTile;
   const size_t dst_tag = static_cast<size_t>(seg) * cap_dst;
-  // Rows [n_ctx, cap_dst) become empty slots, so the destination is a complete pool.
   {
     const int r = r0 + tid;
     if (tid < kTile && r >= nctx && r < cap_dst) {
@@ -247,7 +245,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
       src_of_dst[dst_tag + r] = -1;
     }
   }
-  if (r0 >= nctx) return;
+  if (r0 >= nctx) return 0;
   const int nrows = min(kTile, nctx - r0);
   const int kept = nctx - chunk_len;
   const WsLayout L = ws_layout(n_units, cap_dst);
@@ -269,6 +267,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
       pos_dst[dst_tag + r] = pos_src[src_tag + s] - rec.del;
       src_of_dst[dst_tag + r] = s;
       src_row[tid] = s;
+      if (shift_row) shift_row[tid] = -rec.del;
     } else {
       const int i = r - kept;
       uid_dst[dst_tag + r] = meta[1] + chunk_unit[i];
@@ -276,9 +275,35 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
       pos_dst[dst_tag + r] = kept + i;
       src_of_dst[dst_tag + r] = -1;
       src_row[tid] = -1 - i;
+      if (shift_row) shift_row[tid] = 0;
     }
   }
   __syncthreads();
+  return nrows;
+}
+
+template <int VPT>
+__global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
+    const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
+    int row_bytes, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, const uint8_t* __restrict__ k_chunk,
+    const uint8_t* __restrict__ v_chunk, const uint8_t* __restrict__ chunk_mod,
+    const int32_t* __restrict__ chunk_unit, int chunk_len, uint8_t* __restrict__ k_dst,
+    uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
+    uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
+    const uint8_t* __restrict__ ws) {
+  constexpr int RB = VPT >= 16 ? 1 : 16 / VPT;
+  __shared__ int32_t src_row[kTile];
+  const int seg = blockIdx.y;
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int nctx = n_ctx_g[seg];
+  const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
+                                 pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
+                                 src_of_dst, ws, src_row, nullptr);
+  if (nrows == 0) return;
+  const int r0 = t * kTile;
 
   const int row_vecs = row_bytes / 16;
   const int vecs2 = 2 * row_vecs;       // K row then V row
@@ -338,6 +363,171 @@ hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Copy with rotary re-encoding of the moved keys (paper: Applying the retention plan -- the
+// position of each retained token drops by the deleted tokens before it and the cached keys get
+// the matching RoPE adjustment).  A history row whose position changes by `shift` has each pair
+// (x, y) of its first rot_dims key dimensions turned by shift * theta_j, theta_j =
+// base^(-2j/rot_dims): (x cos - y sin, x sin + y cos).  Pairs are (j, j + rot_dims/2) (HALF) or
+// (2j, 2j+1).  V rows, chunk rows and unshifted rows are copied unchanged.
+// Angles: theta_j and the reduction of shift * theta_j modulo 2 pi in double precision, then a
+// float sine/cosine of the reduced angle; the rotation itself in float, rounded to the storage
+// type (round to nearest even).  One workgroup per 16-row destination tile; the tile's cos/sin
+// table (rows x rot_dims/2) is built in LDS once and shared by all heads.
+constexpr int kMaxHalfRot = 64;     // rot_dims <= head_dim <= 128
+
+template <int EB, bool HALF>
+__global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
+    const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
+    int n_kv_heads, int head_dim, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, const uint8_t* __restrict__ k_chunk,
+    const uint8_t* __restrict__ v_chunk, const uint8_t* __restrict__ chunk_mod,
+    const int32_t* __restrict__ chunk_unit, int chunk_len, uint8_t* __restrict__ k_dst,
+    uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
+    uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
+    const uint8_t* __restrict__ ws, double rope_base, int rot_dims) {
+  constexpr int EPC = 16 / EB;                    // elements per 16-byte chunk
+  __shared__ int32_t src_row[kTile];
+  __shared__ int32_t shift_row[kTile];
+  __shared__ double theta[kMaxHalfRot];
+  __shared__ float2 cs[kTile][kMaxHalfRot];
+  const int seg = blockIdx.y;
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int nctx = n_ctx_g[seg];
+  const int half = rot_dims / 2;
+  if (tid < half) theta[tid] = pow(rope_base, -2.0 * tid / rot_dims);
+  const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
+                                 pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
+                                 src_of_dst, ws, src_row, shift_row);
+  if (nrows == 0) return;
+  const int r0 = t * kTile;
+  constexpr double kTwoPi = 6.283185307179586476925286766559;
+  for (int idx = tid; idx < nrows * half; idx += kCopyThreads) {
+    const int row = idx / half, j = idx % half;
+    const int sh = shift_row[row];
+    float c = 1.f, sn = 0.f;
+    if (sh != 0) {
+      const double phi = static_cast<double>(sh) * theta[j];
+      const double red = fma(-rint(phi * (1.0 / kTwoPi)), kTwoPi, phi);
+      sincosf(static_cast<float>(red), &sn, &c);
+    }
+    cs[row][j] = make_float2(c, sn);
+  }
+  __syncthreads();
+
+  const int row_bytes = n_kv_heads * head_dim * EB;
+  const int row_vecs = row_bytes / 16;
+  const size_t src_base = static_cast<size_t>(seg) * n_slots;
+  const size_t chunk_base = static_cast<size_t>(seg) * chunk_len;
+  const size_t dst_base = static_cast<size_t>(seg) * cap_dst;
+  auto row_src = [&](const uint8_t* pool, const uint8_t* chunk, int row) {
+    const int s = src_row[row];
+    return s >= 0 ? pool + (src_base + s) * row_bytes
+                  : chunk + (chunk_base + (-1 - s)) * row_bytes;
+  };
+  // V rows: verbatim.
+  for (int f = tid; f < nrows * row_vecs; f += kCopyThreads) {
+    const int row = f / row_vecs, vec = f % row_vecs;
+    const u32x4 x = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x4*>(row_src(v_src, v_chunk, row)) + vec);
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(v_dst + (dst_base + r0 + row) *
+                                                            row_bytes) + vec);
+  }
+  // K rows: work items per head.  HALF: item i < rot_dims/(2 EPC) is the chunk pair (i, i +
+  // rot_dims/(2 EPC)); the remaining items are the unrotated chunks past rot_dims.  Otherwise
+  // every chunk is one item whose dimension pairs below rot_dims rotate.
+  const int chunks = head_dim / EPC;
+  const int pair_items = HALF ? half / EPC : 0;
+  const int items = HALF ? pair_items + (head_dim - rot_dims) / EPC : chunks;
+  auto unpack = [](const u32x4& v, float* f) {
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      const uint32_t w = v[e * EB / 4];
+      if constexpr (EB == 2) f[e] = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+      else f[e] = __uint_as_float(w);
+    }
+  };
+  auto pack = [](const float* f) {
+    u32x4 v;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if constexpr (EB == 2) {
+        const __bf16 lo = static_cast<__bf16>(f[2 * q]), hi = static_cast<__bf16>(f[2 * q + 1]);
+        v[q] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, lo)) |
+               (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, hi)) << 16);
+      } else {
+        v[q] = __float_as_uint(f[q]);
+      }
+    }
+    return v;
+  };
+  for (int w = tid; w < nrows * n_kv_heads * items; w += kCopyThreads) {
+    const int row = w / (n_kv_heads * items);
+    const int rem = w % (n_kv_heads * items);
+    const int hd = rem / items, it = rem % items;
+    const u32x4* src = reinterpret_cast<const u32x4*>(row_src(k_src, k_chunk, row)) +
+                       hd * chunks;
+    u32x4* dst = reinterpret_cast<u32x4*>(k_dst + (dst_base + r0 + row) * row_bytes) +
+                 hd * chunks;
+    const float2* tab = cs[row];
+    const bool moved = shift_row[row] != 0;        // unmoved rows are copied bit for bit
+    if (HALF && it < pair_items) {
+      const int ca = it, cb = it + pair_items;
+      u32x4 va = __builtin_nontemporal_load(src + ca), vb = __builtin_nontemporal_load(src + cb);
+      if (moved) {
+        float a[EPC], bv[EPC];
+        unpack(va, a);
+        unpack(vb, bv);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) {
+          const float2 r = tab[ca * EPC + e];
+          const float x = a[e], y = bv[e];
+          a[e] = fmaf(x, r.x, -y * r.y);
+          bv[e] = fmaf(x, r.y, y * r.x);
+        }
+        va = pack(a);
+        vb = pack(bv);
+      }
+      __builtin_nontemporal_store(va, dst + ca);
+      __builtin_nontemporal_store(vb, dst + cb);
+    } else {
+      const int c = HALF ? 2 * pair_items + (it - pair_items) : it;
+      u32x4 v = __builtin_nontemporal_load(src + c);
+      if (!HALF && moved && c * EPC < rot_dims) {
+        float f[EPC];
+        unpack(v, f);
+#pragma unroll
+        for (int m = 0; m < EPC / 2; ++m) {
+          const int d0 = c * EPC + 2 * m;
+          if (d0 < rot_dims) {
+            const float2 r = tab[d0 / 2];
+            const float x = f[2 * m], y = f[2 * m + 1];
+            f[2 * m] = fmaf(x, r.x, -y * r.y);
+            f[2 * m + 1] = fmaf(x, r.y, y * r.x);
+          }
+        }
+        v = pack(f);
+      }
+      __builtin_nontemporal_store(v, dst + c);
+    }
+  }
+}
+
+template <int EB, bool HALF>
+hipError_t launch_copy_rope(const CompactArgs& a, hipStream_t stream) {
+  const dim3 grid((a.cap_dst + kTile - 1) / kTile, a.n_seg);
+  hipLaunchKernelGGL((compact_copy_rope_kernel<EB, HALF>), grid, dim3(kCopyThreads), 0, stream,
+                     static_cast<const uint8_t*>(a.k_src), static_cast<const uint8_t*>(a.v_src),
+                     a.n_slots_src, a.n_kv_heads, a.head_dim, a.modality_src, a.pos_src,
+                     static_cast<const uint8_t*>(a.k_chunk), static_cast<const uint8_t*>(a.v_chunk),
+                     a.chunk_modality, a.chunk_unit, a.chunk_len, static_cast<uint8_t*>(a.k_dst),
+                     static_cast<uint8_t*>(a.v_dst), a.cap_dst, a.n_units, a.unit_id_dst,
+                     a.modality_dst, a.pos_dst, a.src_of_dst, a.n_ctx,
+                     static_cast<const uint8_t*>(a.workspace), a.rope_base, a.rope_dims);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
@@ -357,6 +547,13 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
                        static_cast<uint8_t*>(a.workspace), a.d_status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.rope_dims > 0) {
+    const int eb = a.row_bytes / (a.n_kv_heads * a.head_dim);
+    if (eb == 2) return a.rope_half ? launch_copy_rope<2, true>(a, stream)
+                                    : launch_copy_rope<2, false>(a, stream);
+    return a.rope_half ? launch_copy_rope<4, true>(a, stream)
+                       : launch_copy_rope<4, false>(a, stream);
+  }
   const int vecs2 = 2 * a.row_bytes / 16;
   const int vpt = (vecs2 + kCopyThreads - 1) / kCopyThreads;
   if (vpt <= 1) return launch_copy<1>(a, stream);

@@ -47,6 +47,11 @@ struct CompactArgs {
   int32_t* n_pages;
   void* workspace;
   int32_t* d_status;
+  // rotary re-encoding of moved keys: off when rope_dims == 0
+  int n_kv_heads = 0, head_dim = 0;
+  double rope_base = 0.0;
+  int rope_dims = 0;
+  bool rope_half = true;
 };
 
 size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst);

@@ -24,8 +24,10 @@ OK, E_NULL, E_SHAPE, E_DTYPE, E_WEIGHT, E_CAPACITY, E_WORKSPACE, E_ALIAS, E_HIP 
     0, -1, -2, -3, -4, -5, -6, -7, -8
 E_BUDGET, E_TAGS = -16, -17
 BF16, F32 = 0, 1
+ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 
 EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
+           "omnitide_compact_kv_rope",
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
            "omnitide_attn_workspace_bytes", "omnitide_status_string", "omnitide_version")
 
@@ -58,6 +60,8 @@ def lib() -> ctypes.CDLL:
         L.omnitide_compact_kv.argtypes = [_P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P,
                                           _I, _P, _P, _P, _P, _I, _P, _P, _I, _P, _P, _P, _P, _P,
                                           _P, _P, _P, _SZ, _P, _P]
+        L.omnitide_compact_kv_rope.argtypes = (L.omnitide_compact_kv.argtypes[:-2] +
+                                               [ctypes.c_double, _I, _I, _P, _P])
         L.omnitide_compact_workspace_bytes.argtypes = [_I, _I, _I]
         L.omnitide_compact_workspace_bytes.restype = _SZ
         L.omnitide_chunk_attn.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
@@ -68,7 +72,7 @@ def lib() -> ctypes.CDLL:
         L.omnitide_status_string.restype = ctypes.c_char_p
         L.omnitide_version.restype = ctypes.c_char_p
         for name in ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
-                     "omnitide_chunk_attn"):
+                     "omnitide_compact_kv_rope", "omnitide_chunk_attn"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -173,10 +177,11 @@ def omnitide_compact_workspace_bytes(n_seg, n_units, cap_dst) -> int:
     return int(lib().omnitide_compact_workspace_bytes(n_seg, n_units, cap_dst))
 
 
-def omnitide_compact_kv(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
-                        unit_len, unit_first_slot, n_units, k_chunk, v_chunk, chunk_modality,
-                        chunk_unit, k_dst, v_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
-                        unit_remap, n_ctx, n_pages, workspace, d_status=None, stream=None):
+def _compact_call_args(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
+                       unit_len, unit_first_slot, n_units, k_chunk, v_chunk, chunk_modality,
+                       chunk_unit, k_dst, v_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
+                       unit_remap, n_ctx, n_pages, workspace, d_status):
+    """Checked C arguments shared by the two compaction entry points (all but the stream)."""
     n_seg, n_slots, H, d = _pool_dims(k_src, "k_src")
     dt = (k_src.dtype,)
     _need(k_src, "k_src", (torch.bfloat16, torch.float32))
@@ -211,15 +216,41 @@ def omnitide_compact_kv(k_src, v_src, page_size, unit_id_src, modality_src, pos_
     _need(workspace, "workspace", U8)
     if d_status is not None:
         _need(d_status, "d_status", I32, 1)
-    _check(lib().omnitide_compact_kv(
-        _ptr(k_src), _ptr(v_src), _kv_dtype(k_src), n_seg, n_slots, H, d, page_size,
-        _ptr(unit_id_src), _ptr(modality_src), _ptr(pos_src), _ptr(keep), _ptr(unit_len),
-        _ptr(unit_first_slot), n_units, _ptr(k_chunk) if L else None,
-        _ptr(v_chunk) if L else None, _ptr(chunk_modality) if L else None,
-        _ptr(chunk_unit) if L else None, L, _ptr(k_dst), _ptr(v_dst), cap, _ptr(unit_id_dst),
-        _ptr(modality_dst), _ptr(pos_dst), _ptr(src_of_dst), _ptr(unit_remap), _ptr(n_ctx),
-        _ptr(n_pages), _ptr(workspace), workspace.numel(), _ptr(d_status), _stream(stream)),
-        "omnitide_compact_kv")
+    return (_ptr(k_src), _ptr(v_src), _kv_dtype(k_src), n_seg, n_slots, H, d, page_size,
+            _ptr(unit_id_src), _ptr(modality_src), _ptr(pos_src), _ptr(keep), _ptr(unit_len),
+            _ptr(unit_first_slot), n_units, _ptr(k_chunk), _ptr(v_chunk), _ptr(chunk_modality),
+            _ptr(chunk_unit), L, _ptr(k_dst), _ptr(v_dst), cap, _ptr(unit_id_dst),
+            _ptr(modality_dst), _ptr(pos_dst), _ptr(src_of_dst), _ptr(unit_remap), _ptr(n_ctx),
+            _ptr(n_pages), _ptr(workspace), workspace.numel())
+
+
+def omnitide_compact_kv(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
+                        unit_len, unit_first_slot, n_units, k_chunk, v_chunk, chunk_modality,
+                        chunk_unit, k_dst, v_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
+                        unit_remap, n_ctx, n_pages, workspace, d_status=None, stream=None):
+    args = _compact_call_args(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
+                              unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
+                              chunk_modality, chunk_unit, k_dst, v_dst, unit_id_dst,
+                              modality_dst, pos_dst, src_of_dst, unit_remap, n_ctx, n_pages,
+                              workspace, d_status)
+    _check(lib().omnitide_compact_kv(*args, _ptr(d_status), _stream(stream)),
+           "omnitide_compact_kv")
+
+
+def omnitide_compact_kv_rope(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
+                             unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
+                             chunk_modality, chunk_unit, k_dst, v_dst, unit_id_dst,
+                             modality_dst, pos_dst, src_of_dst, unit_remap, n_ctx, n_pages,
+                             workspace, rope_base, rope_dims, rope_style=ROPE_HALF,
+                             d_status=None, stream=None):
+    args = _compact_call_args(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
+                              unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
+                              chunk_modality, chunk_unit, k_dst, v_dst, unit_id_dst,
+                              modality_dst, pos_dst, src_of_dst, unit_remap, n_ctx, n_pages,
+                              workspace, d_status)
+    _check(lib().omnitide_compact_kv_rope(*args, float(rope_base), int(rope_dims),
+                                          int(rope_style), _ptr(d_status), _stream(stream)),
+           "omnitide_compact_kv_rope")
 
 
 def omnitide_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim) -> int:

@@ -74,13 +74,17 @@ class StreamStep:
                                  self.d_status, stream)
 
     def compact(self, k_hist, v_hist, unit_id, modality, pos, k_chunk, v_chunk, chunk_modality,
-                chunk_unit, stream=None, keep=None):
-        ot.omnitide_compact_kv(k_hist, v_hist, self.page_size, unit_id, modality, pos,
-                               self.keep if keep is None else keep, self.unit_len,
-                               self.unit_first, self.n_units, k_chunk, v_chunk, chunk_modality,
-                               chunk_unit, self.k_dst, self.v_dst, self.unit_id_dst,
-                               self.modality_dst, self.pos_dst, self.src_of_dst, self.unit_remap,
-                               self.n_ctx, self.n_pages, self.compact_ws, self.d_status, stream)
+                chunk_unit, stream=None, keep=None, rope=None):
+        """rope: optional (base, rotary dims, pairing) -- re-encode the moved keys."""
+        args = (k_hist, v_hist, self.page_size, unit_id, modality, pos,
+                self.keep if keep is None else keep, self.unit_len, self.unit_first, self.n_units,
+                k_chunk, v_chunk, chunk_modality, chunk_unit, self.k_dst, self.v_dst,
+                self.unit_id_dst, self.modality_dst, self.pos_dst, self.src_of_dst,
+                self.unit_remap, self.n_ctx, self.n_pages, self.compact_ws)
+        if rope is None:
+            ot.omnitide_compact_kv(*args, self.d_status, stream)
+        else:
+            ot.omnitide_compact_kv_rope(*args, *rope, d_status=self.d_status, stream=stream)
 
     def attend(self, q, scale, k=None, v=None, stream=None):
         ot.omnitide_chunk_attn(q, self.k_dst if k is None else k, self.v_dst if v is None else v,

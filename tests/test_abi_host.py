@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 8
+    assert len(names) == 9
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -116,6 +116,36 @@ def compact(L, **kw):
                                  a["kd"], a["vd"], a["cap"], a["uidd"], a["modd"], a["posd"],
                                  a["src"], a["rm"], a["nctx"], a["npg"], a["ws"], a["wsb"],
                                  a["st"], None)
+
+
+def compact_rope(L, base=10000.0, rdims=128, style=0, **kw):
+    a = dict(ks=fake(0), vs=fake(1), dtype=0, n_seg=1, n=1000, H=8, d=128, P=64, uid=fake(2),
+             mod=fake(3), pos=fake(4), keep=fake(5), ln=fake(6), fs=fake(7), U=10, kc=fake(8),
+             vc=fake(9), cm=fake(10), cu=fake(11), Lc=16, kd=fake(12), vd=fake(13), cap=600,
+             uidd=fake(14), modd=fake(15), posd=fake(16), src=fake(17), rm=fake(18), nctx=fake(19),
+             npg=fake(20), ws=None, wsb=1 << 20, st=fake(22))
+    a.update(kw)
+    return L.omnitide_compact_kv_rope(a["ks"], a["vs"], a["dtype"], a["n_seg"], a["n"], a["H"],
+                                      a["d"], a["P"], a["uid"], a["mod"], a["pos"], a["keep"],
+                                      a["ln"], a["fs"], a["U"], a["kc"], a["vc"], a["cm"],
+                                      a["cu"], a["Lc"], a["kd"], a["vd"], a["cap"], a["uidd"],
+                                      a["modd"], a["posd"], a["src"], a["rm"], a["nctx"],
+                                      a["npg"], a["ws"], a["wsb"], base, rdims, style, a["st"],
+                                      None)
+
+
+def test_compact_rope_validation(L):
+    # valid rotary arguments get past their check (the missing workspace is reported next)
+    assert compact_rope(L) == ot.E_WORKSPACE
+    assert compact_rope(L, rdims=64, style=1) == ot.E_WORKSPACE
+    assert compact_rope(L, rdims=24, style=1) == ot.E_WORKSPACE   # interleaved: any even width
+    assert compact_rope(L, rdims=24, style=0, dtype=1) == ot.E_WORKSPACE   # f32 chunks: 4 dims
+    for bad in (dict(rdims=0), dict(rdims=7), dict(rdims=130), dict(rdims=24, style=0),
+                dict(style=2), dict(base=1.0), dict(base=float("inf")), dict(base=float("nan"))):
+        assert compact_rope(L, **bad) == ot.E_SHAPE, bad
+    # pointer and dtype errors come first
+    assert compact_rope(L, rdims=7, kd=None) == ot.E_NULL
+    assert compact_rope(L, rdims=7, dtype=3) == ot.E_DTYPE
 
 
 def test_compact_validation(L):
