@@ -46,6 +46,39 @@ COUNTER_TRAFFIC = {
 }
 
 
+def graph_time_us(fn, reps, dev):
+    """(mean GPU time in us, method) of fn() over `reps` calls: captured in one HIP graph and
+    replayed (the calls are too short for host-side launches to keep the GPU busy); if capture
+    fails, timed with events around host launches instead."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    try:
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn(0)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(reps):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3, "graph replay"
+    except Exception:  # pragma: no cover - capture unsupported
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3, "events around host launches"
+
+
 def counter_traffic(stage, config):
     """Calibrated HBM bytes per call of `stage`, or None if not measured on this code/config."""
     import hashlib
@@ -195,21 +228,35 @@ def main():
     rope = (1.0e6, d, 0)
     st.compact(c["k"], c["v"], c["uid"], c["mod"], c["pos"], c["kc"], c["vc"], c["cm"], c["cu"],
                rope=rope)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(s)
-    for i in range(args.steps):
+    def rope_call(i):
         c = copies[i % len(copies)]
         st.compact(c["k"], c["v"], c["uid"], c["mod"], c["pos"], c["kc"], c["vc"], c["cm"],
                    c["cu"], rope=rope)
-    e1.record(s)
-    torch.cuda.synchronize()
-    rope_us = e0.elapsed_time(e1) / args.steps * 1e3
-    kernels["compact_rope"] = {"us": round(rope_us, 4), "bytes": cbytes,
+    rope_us, rope_how = graph_time_us(rope_call, args.steps, dev)
+    kernels["compact_rope"] = {"us": round(rope_us, 4), "bytes": cbytes, "timing": rope_how,
                                "GBps": round(cbytes / (rope_us * 1e-6) / 1e9, 4),
                                "frac_hbm": round(cbytes / (rope_us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
                                                  4),
                                "in_step": False}
+
+    # Decode attention of one new token (all 32 query heads) over the compacted pool of this
+    # workload (n_ctx rows), timed on its own: four copies of the pool are rotated so that the
+    # reads come from HBM, not the 256 MB last-level cache.
+    pools = [(st.k_dst.clone(), st.v_dst.clone()) for _ in range(4)]
+    qd = torch.randn(1, 1, Hq, d, device=dev).to(torch.bfloat16)
+    od = torch.empty(1, 1, Hq, d, device=dev)
+    nbd = ot.omnitide_decode_workspace_bytes(1, st.cap_dst, 1, Hq, H, d)
+    wsd = torch.zeros(max(nbd, 1), dtype=torch.uint8, device=dev)
+    def dec_call(i):
+        kp, vp = pools[i % len(pools)]
+        ot.omnitide_decode_attn(qd, kp, vp, st.n_ctx, cfg.scale, od, wsd, st.d_status)
+    dec_us, dec_how = graph_time_us(dec_call, 4 * args.steps, dev)
+    dbytes = n_ctx * H * d * elt * 2 + Hq * d * (2 + 4)
+    kernels["decode"] = {"us": round(dec_us, 4), "bytes": dbytes, "timing": dec_how,
+                         "GBps": round(dbytes / (dec_us * 1e-6) / 1e9, 4),
+                         "frac_hbm": round(dbytes / (dec_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                         "n_ctx": n_ctx, "in_step": False}
+    del pools
 
     value = flops / (ms_per_step * 1e-3) / 1e12
     result = {

@@ -6,6 +6,8 @@
  *   2. omnitide_select_units  budgeted whole-unit retention plan (OmniPick planning)
  *   3. omnitide_compact_kv    order-preserving packing of the kept rows + chunk (OmniPage)
  *   4. omnitide_chunk_attn    GQA prefill attention of the chunk over [history || chunk]
+ * plus omnitide_compact_kv_rope (compaction with rotary re-encoding of the moved keys) and
+ * omnitide_decode_attn (decode attention of the last few tokens over the compacted pool).
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers into memory the caller allocated (hipMalloc or a
@@ -226,6 +228,33 @@ int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32
 
 size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                      int n_kv_heads, int head_dim);
+
+/*
+ * omnitide_decode_attn -- decode attention over the compacted pool (paper: Background, decode
+ * generates one token at a time reusing the cached states; OmniPage ablation, decode attention
+ * time over the native, OmniPage and eagerly compacted layouts).  The chunk attention above
+ * with chunk_len = n_q small: for query token i in [0, n_q) (the segment's last n_q positions)
+ * and query head h,
+ *   out[i][h] = sum_j softmax_j(scale * <q[i][h], k[j][g]>) v[j][g],  g = h / (n_q_heads/n_kv_heads)
+ *   over keys j <= n_ctx - n_q + i.
+ *   q            bf16 [n_seg][n_q][n_q_heads][head_dim]
+ *   k, v         bf16 [n_seg][cap][n_kv_heads][head_dim] (rows [0, n_ctx) are read)
+ *   n_ctx        int32 [n_seg] device; n_q <= n_ctx <= cap, else OMNITIDE_E_CAPACITY on the
+ *                device and that segment's output is not written
+ *   out          float32 [n_seg][n_q][n_q_heads][head_dim]
+ *   workspace    device scratch of omnitide_decode_workspace_bytes() bytes (may be NULL when
+ *                that is 0): split partials
+ * Arithmetic: bf16 inputs, float dot products, softmax and accumulation (probabilities are not
+ * rounded).  Bandwidth-bound: each (key, KV head) row is read once per call.
+ * Limits: n_q * (n_q_heads / n_kv_heads) <= 8, head_dim in {64, 128}, scale finite.
+ */
+int omnitide_decode_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                         int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
+                         int head_dim, float scale, float* out, void* workspace,
+                         size_t workspace_bytes, int32_t* d_status, void* stream);
+
+size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,
+                                       int n_kv_heads, int head_dim);
 
 /* Static description of a status code. */
 const char* omnitide_status_string(int code);

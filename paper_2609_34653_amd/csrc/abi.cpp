@@ -15,6 +15,7 @@ namespace {
 
 using omnitide::AttnArgs;
 using omnitide::CompactArgs;
+using omnitide::DecodeArgs;
 
 struct Range {
   const void* p;
@@ -297,6 +298,51 @@ int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32
   a.workspace = need > 0 ? workspace : nullptr;
   a.d_status = d_status;
   return hip_status(omnitide::launch_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,
+                                       int n_kv_heads, int head_dim) {
+  if (n_seg < 1 || cap < 1 || n_q < 1 || n_kv_heads < 1 || n_q_heads < n_kv_heads ||
+      n_q_heads % n_kv_heads != 0 || !(head_dim == 64 || head_dim == 128))
+    return 0;
+  return omnitide::decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim);
+}
+
+int omnitide_decode_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                         int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
+                         int head_dim, float scale, float* out, void* workspace,
+                         size_t workspace_bytes, int32_t* d_status, void* stream) {
+  if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
+  if (n_seg < 1 || n_seg > kMaxGridY || n_q < 1 || n_kv_heads < 1 ||
+      n_q_heads < n_kv_heads || n_q_heads % n_kv_heads != 0 || n_kv_heads > kMaxGridY ||
+      !(head_dim == 64 || head_dim == 128) || !std::isfinite(scale) ||
+      static_cast<long>(n_q) * (n_q_heads / n_kv_heads) > omnitide::decode_max_query_vectors())
+    return OMNITIDE_E_SHAPE;
+  if (cap < n_q) return OMNITIDE_E_CAPACITY;
+  const size_t need =
+      omnitide::decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return OMNITIDE_E_WORKSPACE;
+  const size_t qrows = static_cast<size_t>(n_seg) * n_q * n_q_heads;
+  const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * 2;
+  if (any_alias({{out, qrows * head_dim * 4}, {workspace, need}, {d_status, 4}},
+                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull}}))
+    return OMNITIDE_E_ALIAS;
+  DecodeArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.n_ctx = n_ctx;
+  a.n_seg = n_seg;
+  a.cap = cap;
+  a.n_q = n_q;
+  a.n_q_heads = n_q_heads;
+  a.n_kv_heads = n_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  a.out = out;
+  a.workspace = need > 0 ? workspace : nullptr;
+  a.d_status = d_status;
+  return hip_status(omnitide::launch_decode(a, static_cast<hipStream_t>(stream)));
 }
 
 const char* omnitide_status_string(int code) {

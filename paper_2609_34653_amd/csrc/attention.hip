@@ -27,6 +27,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "combine.h"
 
 namespace omnitide {
 namespace {
@@ -428,40 +429,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   }
 }
 
-// Merge split partials: out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, splits in order.
-template <int D>
-__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
-                                                           const float* __restrict__ part_ml,
-                                                           int n_split, size_t n_rows,
-                                                           const int32_t* __restrict__ n_ctx_g,
-                                                           int L, int Hq, int cap,
-                                                           float* __restrict__ out) {
-  constexpr int TPR = D / 4;                       // threads per row, 4 floats each
-  const size_t row = static_cast<size_t>(blockIdx.x) * (256 / TPR) + threadIdx.x / TPR;
-  if (row >= n_rows) return;
-  const int seg = static_cast<int>(row / (static_cast<size_t>(L) * Hq));
-  const int nctx = n_ctx_g[seg];
-  if (nctx < L || nctx > cap) return;
-  const int d4 = threadIdx.x % TPR;
-  float M = -INFINITY;
-  for (int s = 0; s < n_split; ++s) M = fmaxf(M, part_ml[2 * (s * n_rows + row)]);
-  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-  float den = 0.f;
-  for (int s = 0; s < n_split; ++s) {
-    const float ms = part_ml[2 * (s * n_rows + row)];
-    const float w = ms == -INFINITY ? 0.f : exp2f(ms - M);
-    den += w * part_ml[2 * (s * n_rows + row) + 1];
-    const float4 ov = *reinterpret_cast<const float4*>(part_o + (s * n_rows + row) * D + 4 * d4);
-    num.x += w * ov.x;
-    num.y += w * ov.y;
-    num.z += w * ov.z;
-    num.w += w * ov.w;
-  }
-  const float inv = den > 0.f ? 1.f / den : 0.f;
-  *reinterpret_cast<float4*>(out + row * D + 4 * d4) =
-      make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
-}
-
 template <int D>
 hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
   const int G = a.n_q_heads / a.n_kv_heads;
@@ -478,11 +445,8 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
                      n_split, a.d_status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_split == 1) return e;
-  constexpr int rows_per_block = 256 / (D / 4);
-  const unsigned blocks = static_cast<unsigned>((n_rows + rows_per_block - 1) / rows_per_block);
-  hipLaunchKernelGGL((attn_combine_kernel<D>), dim3(blocks), dim3(256), 0, stream, part_o,
-                     part_ml, n_split, n_rows, a.n_ctx, a.chunk_len, a.n_q_heads, a.cap, a.out);
-  return hipGetLastError();
+  return launch_combine<D>(part_o, part_ml, n_split, n_rows, a.n_ctx, a.chunk_len, a.n_q_heads, a.cap,
+                           a.out, stream);
 }
 
 }  // namespace

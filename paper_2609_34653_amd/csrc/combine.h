@@ -1,0 +1,89 @@
+// Split-KV combine shared by the chunk and decode attention kernels (one instantiation per
+// translation unit).  Partials: part_o [n_split][n_rows][D] (unnormalised output against the
+// split's reference m) and part_ml [n_split][n_rows] (m, l); rows are (segment, query token,
+// query head) with L query tokens per segment.
+#pragma once
+
+#include "common.h"
+
+namespace omnitide {
+namespace {
+
+// Merge split partials: out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, M = max_s m_s,
+// splits in order.
+// CH = splits loaded per step (4 for a few splits, 16 for many).
+template <int D, int CH>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
+                                                           const float* __restrict__ part_ml,
+                                                           int n_split, size_t n_rows,
+                                                           const int32_t* __restrict__ n_ctx_g,
+                                                           int L, int Hq, int cap,
+                                                           float* __restrict__ out) {
+  constexpr int TPR = D / 4;                       // threads per row, 4 floats each
+  const size_t row = static_cast<size_t>(blockIdx.x) * (256 / TPR) + threadIdx.x / TPR;
+  if (row >= n_rows) return;
+  const int seg = static_cast<int>(row / (static_cast<size_t>(L) * Hq));
+  const int nctx = n_ctx_g[seg];
+  if (nctx < L || nctx > cap) return;
+  const int d4 = threadIdx.x % TPR;
+  // One pass in fixed split order, kChunk splits at a time with all their loads in flight; the
+  // running (M, num, den) is rescaled to each chunk's new maximum.
+  constexpr int kChunk = CH;
+  float M = -INFINITY, den = 0.f;
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = 0; s0 < n_split; s0 += kChunk) {
+    float2 ml[kChunk];
+    float4 ov[kChunk];
+#pragma unroll
+    for (int c = 0; c < kChunk; ++c) {
+      const size_t pr = static_cast<size_t>(s0 + c) * n_rows + row;
+      const bool in = s0 + c < n_split;
+      ml[c] = in ? *reinterpret_cast<const float2*>(part_ml + 2 * pr) : make_float2(-INFINITY, 0.f);
+      ov[c] = in ? *reinterpret_cast<const float4*>(part_o + pr * D + 4 * d4)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    float cm = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < kChunk; ++c) cm = fmaxf(cm, ml[c].x);
+    const float Mn = fmaxf(M, cm);
+    if (Mn == -INFINITY) continue;              // nothing visible in any split so far
+    const float a = M == -INFINITY ? 0.f : exp2f(M - Mn);
+    den *= a;
+    num.x *= a;
+    num.y *= a;
+    num.z *= a;
+    num.w *= a;
+#pragma unroll
+    for (int c = 0; c < kChunk; ++c) {
+      const float w = ml[c].x == -INFINITY ? 0.f : exp2f(ml[c].x - Mn);
+      den = fmaf(w, ml[c].y, den);
+      num.x = fmaf(w, ov[c].x, num.x);
+      num.y = fmaf(w, ov[c].y, num.y);
+      num.z = fmaf(w, ov[c].z, num.z);
+      num.w = fmaf(w, ov[c].w, num.w);
+    }
+    M = Mn;
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  *reinterpret_cast<float4*>(out + row * D + 4 * d4) =
+      make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
+}
+
+// Launch the combine for n_rows rows.
+template <int D>
+hipError_t launch_combine(const float* part_o, const float* part_ml, int n_split, size_t n_rows,
+                          const int32_t* n_ctx, int L, int Hq, int cap, float* out,
+                          hipStream_t stream) {
+  constexpr int rows_per_block = 256 / (D / 4);
+  const unsigned blocks = static_cast<unsigned>((n_rows + rows_per_block - 1) / rows_per_block);
+  if (n_split <= 4)
+    hipLaunchKernelGGL((attn_combine_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, part_o,
+                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
+  else
+    hipLaunchKernelGGL((attn_combine_kernel<D, 16>), dim3(blocks), dim3(256), 0, stream, part_o,
+                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
+  return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace omnitide

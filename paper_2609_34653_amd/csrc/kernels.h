@@ -75,4 +75,22 @@ size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, in
                             int head_dim);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
 
+struct DecodeArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* n_ctx;
+  int n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim;
+  float scale;
+  float* out;
+  void* workspace;
+  int32_t* d_status;
+};
+
+int decode_num_splits(int n_seg, int cap, int n_kv_heads);
+size_t decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
+                              int head_dim);
+int decode_max_query_vectors();
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+
 }  // namespace omnitide

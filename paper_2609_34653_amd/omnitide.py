@@ -29,7 +29,8 @@ ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
            "omnitide_compact_kv_rope",
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
-           "omnitide_attn_workspace_bytes", "omnitide_status_string", "omnitide_version")
+           "omnitide_attn_workspace_bytes", "omnitide_decode_attn",
+           "omnitide_decode_workspace_bytes", "omnitide_status_string", "omnitide_version")
 
 
 class OmnitideError(RuntimeError):
@@ -68,11 +69,15 @@ def lib() -> ctypes.CDLL:
                                           ctypes.c_float, _P, _P, _SZ, _P, _P]
         L.omnitide_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_attn_workspace_bytes.restype = _SZ
+        L.omnitide_decode_attn.argtypes = L.omnitide_chunk_attn.argtypes
+        L.omnitide_decode_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
+        L.omnitide_decode_workspace_bytes.restype = _SZ
         L.omnitide_status_string.argtypes = [_I]
         L.omnitide_status_string.restype = ctypes.c_char_p
         L.omnitide_version.restype = ctypes.c_char_p
         for name in ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
-                     "omnitide_compact_kv_rope", "omnitide_chunk_attn"):
+                     "omnitide_compact_kv_rope", "omnitide_chunk_attn",
+                     "omnitide_decode_attn"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -279,3 +284,34 @@ def omnitide_chunk_attn(q, k, v, n_ctx, scale, out, workspace=None, d_status=Non
                                      Hkv, d, float(scale), _ptr(out), _ptr(workspace),
                                      0 if workspace is None else workspace.numel(),
                                      _ptr(d_status), _stream(stream)), "omnitide_chunk_attn")
+
+
+def omnitide_decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim) -> int:
+    return int(lib().omnitide_decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                                                     head_dim))
+
+
+def omnitide_decode_attn(q, k, v, n_ctx, scale, out, workspace=None, d_status=None,
+                         stream=None):
+    """q [n_seg, n_q, Hq, d] bf16 (the last n_q tokens), k/v [n_seg, cap, Hkv, d] bf16,
+    n_ctx int32 [n_seg] (device), out float32 like q."""
+    if q.dim() == 3:
+        q = q.unsqueeze(0)
+    n_seg, n_q, Hq, d = q.shape
+    ns, cap, Hkv, dk = _pool_dims(k, "k")
+    if ns != n_seg or dk != d:
+        raise ValueError("k does not match q")
+    _need(q, "q", (torch.bfloat16,))
+    _need(k, "k", (torch.bfloat16,))
+    _need(v, "v", (torch.bfloat16,), k.numel())
+    _need(n_ctx, "n_ctx", I32, n_seg)
+    _need(out, "out", (torch.float32,), q.numel())
+    if workspace is not None:
+        _need(workspace, "workspace", U8)
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_decode_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(n_ctx), n_seg, cap, n_q,
+                                      Hq, Hkv, d, float(scale), _ptr(out), _ptr(workspace),
+                                      0 if workspace is None else workspace.numel(),
+                                      _ptr(d_status), _stream(stream)), "omnitide_decode_attn")
+

@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 9
+    assert len(names) == 11
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -182,3 +182,26 @@ def test_attention_validation(L):
     assert need > 0 and attn(L, wsb=need - 1) == ot.E_WORKSPACE
     # split count: 21 row tiles x 8 KV heads -> 3 splits on the 80K-history shape
     assert need == 3 * 665 * 32 * 130 * 4
+
+
+def decode(L, **kw):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), n_ctx=fake(3), n_seg=1, cap=1000, nq=1, Hq=32,
+             Hkv=8, d=128, scale=0.088, out=fake(4), ws=fake(5), wsb=1 << 24, st=fake(6))
+    a.update(kw)
+    return L.omnitide_decode_attn(a["q"], a["k"], a["v"], a["n_ctx"], a["n_seg"], a["cap"],
+                                  a["nq"], a["Hq"], a["Hkv"], a["d"], a["scale"], a["out"],
+                                  a["ws"], a["wsb"], a["st"], None)
+
+
+def test_decode_validation(L):
+    assert decode(L, q=None) == ot.E_NULL
+    assert decode(L, nq=3) == ot.E_SHAPE          # 3 tokens x 4 heads > 8 query vectors
+    assert decode(L, Hq=30) == ot.E_SHAPE         # not a multiple of the KV heads
+    assert decode(L, d=96) == ot.E_SHAPE
+    assert decode(L, scale=float("nan")) == ot.E_SHAPE
+    assert decode(L, cap=0) == ot.E_CAPACITY
+    assert decode(L, ws=None) == ot.E_WORKSPACE
+    assert decode(L, out=P(fake(1).value + 64)) == ot.E_ALIAS
+    assert ot.omnitide_decode_workspace_bytes(1, 1000, 1, 32, 8, 128) > 0
+    assert ot.omnitide_decode_workspace_bytes(1, 1000, 1, 30, 8, 128) == 0
+
