@@ -31,27 +31,31 @@ WORKLOAD = "history_80k"
 CSRC = os.path.join(ROOT, "paper_2609_34653_amd", "csrc")
 
 # HBM traffic of one call of each stage on the default workload, from two rocprofv3 --pmc passes
-# over `bench.py --steps 5 --warmup 1 --no-cpu-baseline --copy-calibration-mb 1024` (FETCH_SIZE,
-# then WRITE_SIZE; KiB per dispatch, summed over the stage's kernels).  Scaled by what the same
+# over `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --copy-calibration-mb 1024`
+# (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, summed over the stage's kernels).  Scaled by what the same
 # counters read for the calibration copy (1 GiB read + 1 GiB written by one elementwise kernel):
 # FETCH_SIZE reads 524,297 KiB for 1,048,576 KiB fetched (x2.000), WRITE_SIZE reads 1,048,576 KiB
 # (x1.000).  Each entry carries a hash of the sources of its kernels and is reported only while
 # they are unchanged (otherwise null: the counters describe other code).
 FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 COUNTER_TRAFFIC = {
-    "score": (("score.hip", "common.h"), "096c5fd963427f8e", 57084.9, 490.7),
+    "score": (("score.hip", "common.h"), "096c5fd963427f8e", 57085.0, 490.7),
     "select": (("select.hip", "common.h"), "0baf3f02762d4c67", 19.7, 3.0),
-    "compact": (("compact.hip", "common.h"), "8fc570369f165b50", 34203.4, 68136.9),
-    "attend": (("attention.hip", "common.h"), "f915373dbdb90c5a", 54274.9, 43058.8),
+    "compact": (("compact.hip", "common.h"), "d273d21cf4e00496", 34203.2, 68151.4),
+    "attend": (("attention.hip", "combine.h", "common.h"), "7afbf524c48c2f3b", 55539.9, 45074.8),
+    "compact_rope": (("compact.hip", "common.h"), "d273d21cf4e00496", 34208.5, 68035.2),
+    "decode": (("decode.hip", "combine.h", "common.h"), "25878bb4cb9068be", 34371.6, 536.0),
 }
 
 
-def graph_time_us(fn, reps, dev):
+def graph_time_us(fn, reps, dev, use_graph=True):
     """(mean GPU time in us, method) of fn() over `reps` calls: captured in one HIP graph and
     replayed (the calls are too short for host-side launches to keep the GPU busy); if capture
-    fails, timed with events around host launches instead."""
+    fails, or use_graph is False, timed with events around host launches instead."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     try:
+        if not use_graph:
+            raise RuntimeError("graph capture disabled")
         side = torch.cuda.Stream(device=dev)
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
@@ -69,7 +73,7 @@ def graph_time_us(fn, reps, dev):
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps * 1e3, "graph replay"
-    except Exception:  # pragma: no cover - capture unsupported
+    except Exception:  # pragma: no cover - capture unsupported or disabled
         torch.cuda.synchronize()
         e0.record()
         for i in range(reps):
@@ -120,6 +124,9 @@ def main():
                     help="run a plain elementwise copy kernel (reads and writes this many MiB) "
                          "three times before the warmup: a known-size reference for hardware "
                          "byte counters")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time the standalone calls with events around host launches instead of "
+                         "one captured HIP graph (for counter passes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the stream step "
@@ -232,11 +239,12 @@ def main():
         c = copies[i % len(copies)]
         st.compact(c["k"], c["v"], c["uid"], c["mod"], c["pos"], c["kc"], c["vc"], c["cm"],
                    c["cu"], rope=rope)
-    rope_us, rope_how = graph_time_us(rope_call, args.steps, dev)
+    rope_us, rope_how = graph_time_us(rope_call, args.steps, dev, not args.no_graph)
     kernels["compact_rope"] = {"us": round(rope_us, 4), "bytes": cbytes, "timing": rope_how,
                                "GBps": round(cbytes / (rope_us * 1e-6) / 1e9, 4),
                                "frac_hbm": round(cbytes / (rope_us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
                                                  4),
+                               "traffic": counter_traffic("compact_rope", cfg.name),
                                "in_step": False}
 
     # Decode attention of one new token (all 32 query heads) over the compacted pool of this
@@ -250,12 +258,13 @@ def main():
     def dec_call(i):
         kp, vp = pools[i % len(pools)]
         ot.omnitide_decode_attn(qd, kp, vp, st.n_ctx, cfg.scale, od, wsd, st.d_status)
-    dec_us, dec_how = graph_time_us(dec_call, 4 * args.steps, dev)
+    dec_us, dec_how = graph_time_us(dec_call, 4 * args.steps, dev, not args.no_graph)
     dbytes = n_ctx * H * d * elt * 2 + Hq * d * (2 + 4)
     kernels["decode"] = {"us": round(dec_us, 4), "bytes": dbytes, "timing": dec_how,
                          "GBps": round(dbytes / (dec_us * 1e-6) / 1e9, 4),
                          "frac_hbm": round(dbytes / (dec_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-                         "n_ctx": n_ctx, "in_step": False}
+                         "traffic": counter_traffic("decode", cfg.name), "n_ctx": n_ctx,
+                         "in_step": False}
     del pools
 
     value = flops / (ms_per_step * 1e-3) / 1e12
