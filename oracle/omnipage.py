@@ -41,8 +41,12 @@ def page_span(n_ctx: int, page_size: int) -> int:
 
 def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
                k_chunk, v_chunk, chunk_modality, chunk_unit, cap_dst: int, page_size: int,
-               rope=None):
+               rope=None, keep_len=None):
     """Order-preserving out-of-place packing of the kept units' rows, then the chunk.
+
+    keep: per unit, nonzero = kept whole.  keep_len (instead of keep, which is then ignored):
+    per unit, the number of its leading live slots (in slot order) that stay -- the span plan's
+    partially retained units.
 
     k_src/v_src: [n_slots, H_kv, d] (any dtype; rows are copied verbatim).
     Returns a dict: k, v ([n_ctx, H_kv, d]), unit_id, modality, pos, src_of_dst (per destination
@@ -57,12 +61,15 @@ def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
     n_slots = unit_id.shape[0]
     if np.any(unit_id < -1) or np.any(unit_id >= n_units):
         raise TagError("unit id out of range")
-    keep = np.asarray(keep)
     L = len(chunk_modality)
 
     has_rows = np.zeros(n_units, bool)
     has_rows[unit_id[unit_id >= 0]] = True
-    kept_unit = (keep != 0) & has_rows
+    if keep_len is not None:
+        quota = np.asarray(keep_len, np.int64).copy()
+    else:
+        quota = np.where(np.asarray(keep) != 0, np.iinfo(np.int64).max, 0)
+    kept_unit = (quota > 0) & has_rows
     unit_remap = np.full(n_units, -1, np.int64)
     nxt = 0
     for u in range(n_units):
@@ -78,7 +85,8 @@ def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
         u = unit_id[s]
         if u < 0:
             continue
-        if kept_unit[u]:
+        if quota[u] > 0:
+            quota[u] -= 1
             rows.append(s)
             new_pos.append(int(pos[s]) - deleted)
         else:
