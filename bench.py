@@ -267,6 +267,39 @@ def main():
                          "in_step": False}
     del pools
 
+    # Span plan (recent units whole; older units keep 256 video / 16 audio leading tokens; 1,024
+    # text tokens oldest first; trimmed toward the budget) and compaction of its kept prefixes,
+    # each timed on its own after the step loop on the same pool.
+    sp = dict(low=cfg.budget, high=cfg.budget, recent=cfg.recent, sink_video=256, sink_audio=16,
+              text_budget=1024)
+    c = copies[0]
+    st.score(c["k"], c["uid"], c["mod"])
+    def plan_call(i):
+        st.plan_spans(copies[i % len(copies)]["mod"], sp["low"], sp["high"], sp["recent"],
+                      sp["sink_video"], sp["sink_audio"], sp["text_budget"])
+    plan_us, plan_how = graph_time_us(plan_call, args.steps, dev, not args.no_graph)
+    torch.cuda.synchronize()
+    kept_sp = int(st.kept_tokens.item())
+    def span_compact_call(i):
+        c = copies[i % len(copies)]
+        st.compact_spans(c["k"], c["v"], c["uid"], c["mod"], c["pos"], c["kc"], c["vc"],
+                         c["cm"], c["cu"])
+    sc_us, sc_how = graph_time_us(span_compact_call, args.steps, dev, not args.no_graph)
+    torch.cuda.synchronize()
+    status = int(st.d_status.item())
+    if status != 0:
+        raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
+    plan_bytes = lay.n_units * (4 * 4 + 1 + 4) + 4
+    sbytes_c = compact_bytes(kept_sp, L, H, d, elt, st.cap_dst, lay.n_units)
+    kernels["span_plan"] = {"us": round(plan_us, 4), "bytes": plan_bytes, "timing": plan_how,
+                            "GBps": round(plan_bytes / (plan_us * 1e-6) / 1e9, 4),
+                            "params": sp, "kept_tokens": kept_sp, "in_step": False}
+    kernels["compact_spans"] = {"us": round(sc_us, 4), "bytes": sbytes_c, "timing": sc_how,
+                                "GBps": round(sbytes_c / (sc_us * 1e-6) / 1e9, 4),
+                                "frac_hbm": round(sbytes_c / (sc_us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+                                                  4),
+                                "kept_tokens": kept_sp, "in_step": False}
+
     value = flops / (ms_per_step * 1e-3) / 1e12
     result = {
         "metric": "chunk-attn TFLOP/s + score/compact GB/s (% roofline), 80K-token history, 1 GPU",

@@ -6,8 +6,11 @@
  *   2. omnitide_select_units  budgeted whole-unit retention plan (OmniPick planning)
  *   3. omnitide_compact_kv    order-preserving packing of the kept rows + chunk (OmniPage)
  *   4. omnitide_chunk_attn    GQA prefill attention of the chunk over [history || chunk]
- * plus omnitide_compact_kv_rope (compaction with rotary re-encoding of the moved keys) and
- * omnitide_decode_attn (decode attention of the last few tokens over the compacted pool).
+ * plus omnitide_compact_kv_rope (compaction with rotary re-encoding of the moved keys),
+ * omnitide_plan_spans + omnitide_compact_kv_spans (the span plan: recent units whole, sink
+ * prefixes of older units, a shared text budget, oldest-first trimming, then compaction of the
+ * kept prefixes) and omnitide_decode_attn (decode attention of the last few tokens over the
+ * compacted pool).
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers into memory the caller allocated (hipMalloc or a
@@ -203,6 +206,69 @@ int omnitide_compact_kv_rope(const void* k_src, const void* v_src, int dtype, in
                              int32_t* d_status, void* stream);
 
 size_t omnitide_compact_workspace_bytes(int n_seg, int n_units, int cap_dst);
+
+/*
+ * omnitide_plan_spans -- span retention plan (paper: Structure-aware retention planning:
+ * retention starts above the high watermark and trims toward the low watermark; the system
+ * prefix is protected; recent units are kept in full; older units, oldest to newest, keep short
+ * image and audio prefixes as sinks, with separate lengths per modality; text is kept oldest to
+ * newest until a shared budget is used up; then units are dropped oldest first, partially
+ * retained ones before complete ones, until the target is met or one unit remains).
+ * Per segment, with len_u > 0 marking live units and class_u = modality[first slot of u]:
+ *   sum len_u <= high_watermark  -> keep_len = len (nothing removed)
+ *   otherwise keep_len_u =
+ *     len_u                              if u holds a system token (flag bit 0; never dropped)
+ *     len_u                              if u is recent: newest live non-system units walked
+ *                                        newest to oldest while their total <= recent_tokens,
+ *                                        stopping at the first misfit
+ *     min(len_u, sink_video)             older video unit
+ *     min(len_u, sink_audio)             older audio unit
+ *     min(len_u, text_budget - T)        older text unit, T = older text tokens before u
+ *                                        (clamped at 0: the budget is used up to the token)
+ *   then, while sum keep_len > low_watermark and more than one unit has keep_len > 0, the next
+ *   unit of the drop order gets keep_len 0: partially retained units (0 < keep_len < len) by
+ *   id, then complete non-system units by id.  The low watermark is a target, not a bound.
+ *   Inputs: omnitide_score_units' unit_len, unit_first_slot, unit_last_slot, unit_flags
+ *   ([n_seg][n_units]) and the slot modality tags [n_seg][n_slots].
+ *   keep_len     int32 [n_seg][n_units]   leading tokens of each unit that stay
+ *   kept_tokens  int32 [n_seg]            sum of keep_len
+ *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run inside
+ *                [0, n_slots), runs are out of unit order, or a unit's first modality is > 3;
+ *                the segment's keep_len is then all 0 and kept_tokens 0.
+ * Limits: 1 <= n_units <= 8192, n_slots >= 0, 0 <= low_watermark <= high_watermark, and
+ * recent_tokens, sink_video, sink_audio, text_budget >= 0.  One workgroup per segment.
+ */
+int omnitide_plan_spans(const int32_t* unit_len, const int32_t* unit_first_slot,
+                        const int32_t* unit_last_slot, const uint32_t* unit_flags,
+                        const uint8_t* modality, int n_seg, int n_slots, int n_units,
+                        int low_watermark, int high_watermark, int recent_tokens,
+                        int sink_video, int sink_audio, int text_budget, int32_t* keep_len,
+                        int32_t* kept_tokens, int32_t* d_status, void* stream);
+
+/*
+ * omnitide_compact_kv_spans -- compaction of a span plan (paper: Applying the retention plan --
+ * unselected ranges are deleted, every retained token moves down by the deleted tokens before
+ * it, a partially retained unit keeps its identity with its new length).  Same arguments,
+ * outputs and errors as omnitide_compact_kv_rope with `keep` replaced by
+ *   keep_len  int32 [n_seg][n_units]: unit u keeps its first min(max(keep_len_u, 0), len_u)
+ *             live slots (omnitide_plan_spans' output); units with 0 are dropped and renumbered
+ *             -1, the others keep their order and are renumbered densely.
+ * and rope_dims == 0 meaning no rotary re-encoding (keys copied verbatim, rope_base and
+ * rope_style ignored); otherwise the rope arguments are as for omnitide_compact_kv_rope.
+ */
+int omnitide_compact_kv_spans(const void* k_src, const void* v_src, int dtype, int n_seg,
+                              int n_slots_src, int n_kv_heads, int head_dim, int page_size,
+                              const int32_t* unit_id_src, const uint8_t* modality_src,
+                              const int32_t* pos_src, const int32_t* keep_len,
+                              const int32_t* unit_len, const int32_t* unit_first_slot,
+                              int n_units, const void* k_chunk, const void* v_chunk,
+                              const uint8_t* chunk_modality, const int32_t* chunk_unit,
+                              int chunk_len, void* k_dst, void* v_dst, int cap_dst,
+                              int32_t* unit_id_dst, uint8_t* modality_dst, int32_t* pos_dst,
+                              int32_t* src_of_dst, int32_t* unit_remap, int32_t* n_ctx,
+                              int32_t* n_pages, void* workspace, size_t workspace_bytes,
+                              double rope_base, int rope_dims, int rope_style,
+                              int32_t* d_status, void* stream);
 
 /*
  * omnitide_chunk_attn -- grouped-query prefill attention of the new chunk over the compacted

@@ -1,4 +1,7 @@
 // Eager, order-preserving, out-of-place compaction of the retained rows plus the chunk append.
+// A unit keeps its first k live tokens: k = len for a unit kept whole (keep flag), or the
+// span plan's kept-prefix length; a partially kept unit's deleted tail counts among the
+// deleted tokens before every later unit.
 //
 // Two kernels on the caller's stream:
 //   plan  one workgroup per segment (a single wave up to 512 units).  Exclusive scans over
@@ -44,8 +47,9 @@ __host__ __device__ inline WsLayout ws_layout(int n_units, int cap_dst) {
 }
 
 __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
-    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ len_g,
-    const int32_t* __restrict__ first_g, int n_units, int chunk_len, int cap_dst, int page_size,
+    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ keep_len_g,
+    const int32_t* __restrict__ len_g, const int32_t* __restrict__ first_g, int n_units,
+    int chunk_len, int cap_dst, int page_size,
     int32_t* __restrict__ remap_g, int32_t* __restrict__ n_ctx_g,
     int32_t* __restrict__ n_pages_g, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
   __shared__ int32_t scr[kPlanThreads / kWave + 1];
@@ -69,9 +73,9 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
     kl[i] = dl[i] = fs[i] = 0;
     if (i < per && u < U) {
       const int n = max(len_g[base + u], 0);
-      const bool kp = keep_g[base + u] != 0;
-      kl[i] = kp ? n : 0;
-      dl[i] = kp ? 0 : n;
+      kl[i] = keep_len_g != nullptr ? min(max(keep_len_g[base + u], 0), n)
+                                    : (keep_g[base + u] != 0 ? n : 0);
+      dl[i] = n - kl[i];
       fs[i] = first_g[base + u];
     }
     my_k += kl[i];
@@ -127,8 +131,9 @@ __device__ inline int wave_excl(int v, int* total) {
 }
 
 __global__ __launch_bounds__(kWave) void compact_plan_small_kernel(
-    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ len_g,
-    const int32_t* __restrict__ first_g, int n_units, int chunk_len, int cap_dst, int page_size,
+    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ keep_len_g,
+    const int32_t* __restrict__ len_g, const int32_t* __restrict__ first_g, int n_units,
+    int chunk_len, int cap_dst, int page_size,
     int32_t* __restrict__ remap_g, int32_t* __restrict__ n_ctx_g,
     int32_t* __restrict__ n_pages_g, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
   const int seg = blockIdx.x;
@@ -142,22 +147,22 @@ __global__ __launch_bounds__(kWave) void compact_plan_small_kernel(
   int32_t* tile_hint = reinterpret_cast<int32_t*>(wseg + L.tile_off);
   int32_t* meta = reinterpret_cast<int32_t*>(wseg + L.meta_off);
 
-  int nl[kSmallPer], fs[kSmallPer];
-  uint8_t kp[kSmallPer];
+  int nl[kSmallPer], fs[kSmallPer], kq[kSmallPer];
 #pragma unroll
   for (int i = 0; i < kSmallPer; ++i) {      // all loads first: one memory round trip
     const int u = min(u0 + i, U - 1);
     nl[i] = len_g[base + u];
     fs[i] = first_g[base + u];
-    kp[i] = keep_g[base + u];
+    kq[i] = keep_len_g != nullptr ? keep_len_g[base + u]
+                                  : (keep_g[base + u] != 0 ? INT32_MAX : 0);
   }
   int kl[kSmallPer], dl[kSmallPer];
   int my_k = 0, my_d = 0, my_n = 0;
 #pragma unroll
   for (int i = 0; i < kSmallPer; ++i) {
     const int n = (u0 + i < U) ? max(nl[i], 0) : 0;
-    kl[i] = kp[i] ? n : 0;
-    dl[i] = kp[i] ? 0 : n;
+    kl[i] = min(max(kq[i], 0), n);
+    dl[i] = n - kl[i];
     my_k += kl[i];
     my_d += dl[i];
     my_n += kl[i] > 0 ? 1 : 0;
@@ -537,13 +542,13 @@ size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
   if (a.n_units <= kSmallUnits)
     hipLaunchKernelGGL(compact_plan_small_kernel, dim3(a.n_seg), dim3(kWave), 0, stream, a.keep,
-                       a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst, a.page_size,
-                       a.unit_remap, a.n_ctx, a.n_pages, static_cast<uint8_t*>(a.workspace),
-                       a.d_status);
+                       a.keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst,
+                       a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
+                       static_cast<uint8_t*>(a.workspace), a.d_status);
   else
     hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream,
-                       a.keep, a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst,
-                       a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
+                       a.keep, a.keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len,
+                       a.cap_dst, a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
                        static_cast<uint8_t*>(a.workspace), a.d_status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -27,6 +27,7 @@ struct CompactArgs {
   const uint8_t* modality_src;
   const int32_t* pos_src;
   const uint8_t* keep;
+  const int32_t* keep_len = nullptr;   // kept leading tokens per unit; replaces keep when set
   const int32_t* unit_len;
   const int32_t* unit_first;
   int n_units;
@@ -55,6 +56,21 @@ struct CompactArgs {
 };
 
 size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst);
+
+struct SpanPlanArgs {
+  const int32_t* unit_len;
+  const int32_t* unit_first;
+  const int32_t* unit_last;
+  const uint32_t* unit_flags;
+  const uint8_t* modality;
+  int n_seg, n_slots, n_units;
+  int low, high, recent, sink_video, sink_audio, text_budget;
+  int32_t* keep_len;
+  int32_t* kept_tokens;
+  int32_t* d_status;
+};
+
+hipError_t launch_plan_spans(const SpanPlanArgs& a, hipStream_t stream);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 
 struct AttnArgs {

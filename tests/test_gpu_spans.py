@@ -1,0 +1,301 @@
+"""HIP span plan and span compaction vs the CPU oracle, through the C ABI.
+
+Bar: keep_len, kept_tokens and every compaction output bit-exact (integers and raw KV bytes);
+with rotary re-encoding, the rotated key elements within the bound of the rotary compaction
+tests (half a storage ulp plus 2^-21 of the pair's length).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import streamgen as sg
+from tests._util import storage_np
+from tests.test_gpu_parity import dev, gpu_inputs, host, make_step
+from tests.test_gpu_rope import pair_norm, ulp
+
+pytestmark = pytest.mark.gpu
+
+SYS, VIDEO, AUDIO, TEXT = 0, 1, 2, 3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_34653_amd import omnitide
+    omnitide.lib()
+    yield
+
+
+def i32(a):
+    return dev(np.asarray(a, np.int32))
+
+
+def gpu_plan(length, first, last, flags, modality, n_slots, params, n_seg=1):
+    """Run omnitide_plan_spans on host arrays laid out [n_seg][U]; returns (keep_len, kept,
+    status)."""
+    from paper_2609_34653_amd import omnitide as ot
+    U = len(length) // n_seg
+    kl = torch.full((n_seg * U,), -7, dtype=torch.int32, device="cuda")
+    kt = torch.full((n_seg,), -7, dtype=torch.int32, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ot.omnitide_plan_spans(i32(length), i32(first), i32(last), i32(flags),
+                           dev(np.asarray(modality, np.uint8)), n_seg, n_slots, U,
+                           params["low"], params["high"], params["recent"], params["sv"],
+                           params["sa"], params["tb"], kl, kt, st)
+    torch.cuda.synchronize()
+    return host(kl), host(kt), int(host(st)[0])
+
+
+def oracle_plan(sc, modality, p):
+    um = oracle.unit_modality(modality, np.minimum(sc["first"], len(modality) - 1), sc["len"])
+    return oracle.plan_spans(sc["len"], sc["first"], sc["last"], sc["flags"], um, p["low"],
+                             p["high"], p["recent"], p["sv"], p["sa"], p["tb"])
+
+
+def random_layout(rng, U, hole_p=0.2):
+    """Contiguous unit runs in id order with empty slots between some of them."""
+    length = rng.integers(1, 40, U)
+    length[rng.random(U) < 0.05] = 0                     # some units without slots
+    mod_u = rng.choice([SYS, VIDEO, AUDIO, TEXT], U, p=[0.03, 0.45, 0.37, 0.15])
+    unit_id, modality = [], []
+    for u in range(U):
+        if rng.random() < hole_p:
+            gap = int(rng.integers(1, 5))
+            unit_id += [-1] * gap
+            modality += [VIDEO] * gap
+        unit_id += [u] * int(length[u])
+        modality += [int(mod_u[u])] * int(length[u])
+    unit_id = np.array(unit_id, np.int64)
+    modality = np.array(modality, np.int64)
+    n = len(unit_id)
+    first = np.full(U, n, np.int64)
+    last = np.full(U, -1, np.int64)
+    for s in range(n):
+        u = unit_id[s]
+        if u >= 0:
+            first[u] = min(first[u], s)
+            last[u] = s
+    flags = np.zeros(U, np.int64)
+    for u in range(U):
+        if length[u] and mod_u[u] == SYS:
+            flags[u] = 1
+    return dict(len=length.astype(np.int64), first=first, last=last, flags=flags), modality
+
+
+def random_params(rng, total):
+    high = int(rng.integers(0, total + 10))
+    return dict(high=high, low=int(rng.integers(0, high + 1)),
+                recent=int(rng.integers(0, max(total // 3, 1))), sv=int(rng.integers(0, 20)),
+                sa=int(rng.integers(0, 8)), tb=int(rng.integers(0, 80)))
+
+
+@pytest.mark.parametrize("U,seed", [(1, 0), (2, 1), (7, 2), (60, 3), (512, 4), (513, 5),
+                                    (3000, 6), (8192, 7)])
+def test_plan_parity_random(U, seed):
+    rng = np.random.default_rng(seed)
+    for trial in range(6):
+        sc, modality = random_layout(rng, U)
+        p = random_params(rng, int(sc["len"].sum()))
+        if trial == 0:
+            p["high"] = int(sc["len"].sum())             # nothing to trim
+        want, wkept = oracle_plan(sc, modality, p)
+        got, kept, status = gpu_plan(sc["len"], sc["first"], sc["last"], sc["flags"], modality,
+                                     len(modality), p)
+        assert status == 0
+        assert np.array_equal(got, want), (U, seed, trial, p)
+        assert int(kept[0]) == wkept
+
+
+def test_plan_several_segments():
+    rng = np.random.default_rng(11)
+    scs, mods = [], []
+    n_slots = None
+    for _ in range(3):
+        while True:
+            sc, m = random_layout(rng, 300, hole_p=0.0)
+            if n_slots is None or len(m) <= n_slots:
+                break
+        n_slots = n_slots or len(m) + 50
+        scs.append(sc)
+        mods.append(np.concatenate([m, np.full(n_slots - len(m), VIDEO)]))
+    p = dict(high=500, low=400, recent=200, sv=6, sa=3, tb=40)
+    cat = lambda key: np.concatenate([s[key] for s in scs])  # noqa: E731
+    got, kept, status = gpu_plan(cat("len"), cat("first"), cat("last"), cat("flags"),
+                                 np.concatenate(mods), n_slots, p, n_seg=3)
+    assert status == 0
+    for i, sc in enumerate(scs):
+        want, wkept = oracle_plan(sc, mods[i], p)
+        assert np.array_equal(got[i * 300:(i + 1) * 300], want)
+        assert int(kept[i]) == wkept
+
+
+def test_plan_tag_errors():
+    rng = np.random.default_rng(12)
+    sc, modality = random_layout(rng, 20, hole_p=0.0)
+    p = dict(high=0, low=0, recent=10, sv=2, sa=2, tb=5)
+    live = np.nonzero(sc["len"] > 0)[0]
+    bad = {k: v.copy() for k, v in sc.items()}
+    bad["first"][live[3]], bad["first"][live[4]] = sc["first"][live[4]], sc["first"][live[3]]
+    bad["last"][live[3]], bad["last"][live[4]] = sc["last"][live[4]], sc["last"][live[3]]
+    got, kept, status = gpu_plan(bad["len"], bad["first"], bad["last"], bad["flags"], modality,
+                                 len(modality), p)
+    assert status == -17 and np.all(got == 0) and int(kept[0]) == 0
+    bad = {k: v.copy() for k, v in sc.items()}
+    bad["last"][live[2]] += 1                            # run longer than its token count
+    assert gpu_plan(bad["len"], bad["first"], bad["last"], bad["flags"], modality,
+                    len(modality), p)[2] == -17
+    m2 = modality.copy()
+    m2[sc["first"][live[5]]] = 9                         # modality out of range
+    assert gpu_plan(sc["len"], sc["first"], sc["last"], sc["flags"], m2, len(m2), p)[2] == -17
+
+
+SPAN_PARAMS = {
+    "tiny_1p6k_f32": dict(high=600, low=512, sv=8, sa=4, tb=16),
+    "single_layer_8k": dict(high=4096, low=4096, sv=64, sa=8, tb=64),
+    "history_80k": dict(high=16384, low=16384, sv=256, sa=16, tb=1024),
+    "hires_32k_36layer": dict(high=8192, low=6000, sv=256, sa=8, tb=32),
+}
+
+
+def run_span_step(cfg, lay, segs, p, cap_dst=None, rope=None):
+    st = make_step(cfg, lay, n_seg=len(segs), cap_dst=cap_dst)
+    g = gpu_inputs(lay, segs)
+    st.score(g["k_hist"], g["unit_id"], g["modality"])
+    st.plan_spans(g["modality"], p["low"], p["high"], cfg.recent, p["sv"], p["sa"], p["tb"])
+    st.compact_spans(g["k_hist"], g["v_hist"], g["unit_id"], g["modality"], g["pos"],
+                     g["k_chunk"], g["v_chunk"], g["chunk_modality"], g["chunk_unit"], rope=rope)
+    torch.cuda.synchronize()
+    assert int(host(st.d_status)[0]) == 0
+    return st
+
+
+def check_span_segment(cfg, lay, seg, st, si, p, rope=None):
+    U = lay.n_units
+    sl = slice(si * U, (si + 1) * U)
+    k = storage_np(seg.k_hist)
+    sc = oracle.score_units(k, cfg.dtype, lay.unit_id, lay.modality, cfg.weights, U)
+    want, wkept = oracle_plan(sc, np.asarray(lay.modality), dict(p, recent=cfg.recent))
+    assert np.array_equal(host(st.keep_len)[sl], want)
+    assert int(host(st.kept_tokens)[si]) == wkept
+    rope_o = None
+    if rope is not None:
+        rope_o = dict(base=rope[0], dims=rope[1], style=("half", "interleaved")[rope[2]],
+                      dtype=cfg.dtype)
+    cp = oracle.compact_kv(k, storage_np(seg.v_hist), lay.unit_id, lay.modality, lay.pos, None, U,
+                           storage_np(seg.k_chunk), storage_np(seg.v_chunk), lay.chunk_modality,
+                           lay.chunk_unit, st.cap_dst, st.page_size, rope=rope_o, keep_len=want)
+    n = cp["n_ctx"]
+    assert int(host(st.n_ctx)[si]) == n and int(host(st.n_pages)[si]) == cp["n_pages"]
+    cap = st.cap_dst
+    tags = slice(si * cap, (si + 1) * cap)
+    uid = host(st.unit_id_dst)[tags]
+    assert np.array_equal(uid[:n], cp["unit_id"]) and np.all(uid[n:] == -1)
+    assert np.array_equal(host(st.modality_dst)[tags][:n], cp["modality"])
+    assert np.array_equal(host(st.pos_dst)[tags][:n], cp["pos"])
+    assert np.array_equal(host(st.src_of_dst)[tags][:n], cp["src_of_dst"])
+    assert np.array_equal(host(st.unit_remap)[sl], cp["unit_remap"])
+    assert np.array_equal(storage_np(st.v_dst[si])[:n], cp["v"])
+    kd = storage_np(st.k_dst[si])[:n]
+    if rope is None:
+        assert np.array_equal(kd, cp["k"])
+    else:
+        R = rope[1]
+        assert np.array_equal(kd[..., R:], cp["k"][..., R:])
+        got = oracle.to_f64(kd, cfg.dtype)[..., :R]
+        w = cp["k_f64"][..., :R]
+        src = oracle.to_f64(cp["k"], cfg.dtype)
+        bound = 0.5 * ulp(w, cfg.dtype) + 2.0 ** -21 * pair_norm(src, R, rope_o["style"])[..., :R]
+        assert np.all(np.abs(got - w) <= bound)
+    return cp, want
+
+
+@pytest.mark.parametrize("cfg_name", ["tiny_1p6k_f32", "single_layer_8k", "history_80k"])
+def test_span_step_parity(cfg_name):
+    cfg = sg.CONFIG_BY_NAME[cfg_name]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    p = SPAN_PARAMS[cfg_name]
+    st = run_span_step(cfg, lay, [seg], p)
+    _, kl = check_span_segment(cfg, lay, seg, st, 0, p)
+    length = np.bincount(np.asarray(lay.unit_id)[np.asarray(lay.unit_id) >= 0],
+                         minlength=lay.n_units)
+    assert np.any((kl > 0) & (kl < length)), "the plan must shorten some units"
+
+
+def test_span_step_three_layers():
+    cfg = sg.CONFIG_BY_NAME["hires_32k_36layer"]
+    stream = sg.make_stream(cfg)
+    lay = stream.layout
+    segs = [stream.segment(i) for i in (0, 17, 35)]
+    p = SPAN_PARAMS[cfg.name]
+    st = run_span_step(cfg, lay, segs, p)
+    for i, seg in enumerate(segs):
+        check_span_segment(cfg, lay, seg, st, i, p)
+
+
+@pytest.mark.parametrize("cfg_name,rope", [("single_layer_8k", (1.0e6, 128, 0)),
+                                           ("tiny_1p6k_f32", (10000.0, 32, 1))])
+def test_span_step_with_rope(cfg_name, rope):
+    cfg = sg.CONFIG_BY_NAME[cfg_name]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    p = SPAN_PARAMS[cfg_name]
+    st = run_span_step(cfg, lay, [seg], p, rope=rope)
+    check_span_segment(cfg, lay, seg, st, 0, p, rope=rope)
+
+
+def test_compaction_of_arbitrary_prefixes():
+    """Any keep_len (negative and oversized values clamp to [0, len]) against the oracle."""
+    cfg = sg.CONFIG_BY_NAME["single_layer_8k"]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    rng = np.random.default_rng(13)
+    U = lay.n_units
+    length = np.bincount(np.asarray(lay.unit_id)[np.asarray(lay.unit_id) >= 0], minlength=U)
+    kl = rng.integers(-3, length + 4)
+    kl[rng.random(U) < 0.3] = 0
+    st = make_step(cfg, lay, cap_dst=lay.n_slots + lay.chunk_len)
+    g = gpu_inputs(lay, [seg])
+    st.score(g["k_hist"], g["unit_id"], g["modality"])
+    st.compact_spans(g["k_hist"], g["v_hist"], g["unit_id"], g["modality"], g["pos"],
+                     g["k_chunk"], g["v_chunk"], g["chunk_modality"], g["chunk_unit"],
+                     keep_len=i32(kl))
+    torch.cuda.synchronize()
+    assert int(host(st.d_status)[0]) == 0
+    cp = oracle.compact_kv(storage_np(seg.k_hist), storage_np(seg.v_hist), lay.unit_id,
+                           lay.modality, lay.pos, None, U, storage_np(seg.k_chunk),
+                           storage_np(seg.v_chunk), lay.chunk_modality, lay.chunk_unit,
+                           st.cap_dst, st.page_size, keep_len=kl)
+    n = cp["n_ctx"]
+    assert int(host(st.n_ctx)[0]) == n
+    assert np.array_equal(storage_np(st.k_dst[0])[:n], cp["k"])
+    assert np.array_equal(storage_np(st.v_dst[0])[:n], cp["v"])
+    assert np.array_equal(host(st.pos_dst)[:n], cp["pos"])
+    assert np.array_equal(host(st.src_of_dst)[:n], cp["src_of_dst"])
+    assert np.array_equal(host(st.unit_id_dst)[:n], cp["unit_id"])
+    assert np.array_equal(host(st.unit_remap), cp["unit_remap"])
+
+
+def test_whole_units_match_the_keep_flag_compaction():
+    """keep_len = len for the selected units gives the whole-unit compaction bit for bit."""
+    cfg = sg.CONFIG_BY_NAME["single_layer_8k"]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    st = make_step(cfg, lay)
+    g = gpu_inputs(lay, [seg])
+    st.score(g["k_hist"], g["unit_id"], g["modality"])
+    st.select()
+    st.compact(g["k_hist"], g["v_hist"], g["unit_id"], g["modality"], g["pos"], g["k_chunk"],
+               g["v_chunk"], g["chunk_modality"], g["chunk_unit"])
+    torch.cuda.synchronize()
+    ref = {k: getattr(st, k).clone() for k in ("k_dst", "v_dst", "unit_id_dst", "pos_dst",
+                                               "src_of_dst", "unit_remap", "n_ctx")}
+    kl = torch.where(st.keep != 0, st.unit_len, torch.zeros_like(st.unit_len))
+    st.compact_spans(g["k_hist"], g["v_hist"], g["unit_id"], g["modality"], g["pos"],
+                     g["k_chunk"], g["v_chunk"], g["chunk_modality"], g["chunk_unit"],
+                     keep_len=kl.contiguous())
+    torch.cuda.synchronize()
+    for k, v in ref.items():
+        assert torch.equal(getattr(st, k), v), k
