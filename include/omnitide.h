@@ -296,6 +296,35 @@ size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_
                                      int n_kv_heads, int head_dim);
 
 /*
+ * omnitide_span_attn -- chunk attention over a pool with holes (paper: Fragmentation after
+ * logical eviction -- deletion leaves holes between retained entries, attention is presented
+ * the physical span, and a tile can be skipped only when every entry in it is masked).
+ * For query position i in [0, chunk_len) and query head h:
+ *   out[i][h] = sum_j softmax_j(scale * <q[i][h], k[j][g]>) v[j][g],  g as omnitide_chunk_attn
+ *   over slots j < span[seg] with 0 <= key_pos[j] <= q_pos0[seg] + i.
+ *   key_pos  int32 [n_seg][cap], device: logical position of each slot's entry, -1 = empty.
+ *            The chunk's own keys must be in the pool with positions q_pos0 + i.
+ *   span     int32 [n_seg], device: slots presented to attention; chunk_len <= span <= cap
+ *            (device check: OMNITIDE_E_CAPACITY, the segment's output is then not written)
+ *   q_pos0   int32 [n_seg], device: logical position of chunk query 0
+ *   q, k, v, out, scale: as omnitide_chunk_attn.  The K/V bytes of empty slots are never used
+ *   (they may hold anything, NaN included).
+ *   workspace  device scratch of omnitide_span_attn_workspace_bytes() bytes (always > 0).
+ * 64-slot tiles without an entry are skipped; tiles whose entries are all visible to every
+ * query of a workgroup run unmasked.  With key_pos[j] = j for j < span and q_pos0 = span -
+ * chunk_len this computes omnitide_chunk_attn with n_ctx = span (up to summation order).
+ * Limits: as omnitide_chunk_attn, and cap <= 2,097,152.
+ */
+int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_t* key_pos,
+                       const int32_t* span, const int32_t* q_pos0, int n_seg, int cap,
+                       int chunk_len, int n_q_heads, int n_kv_heads, int head_dim, float scale,
+                       float* out, void* workspace, size_t workspace_bytes, int32_t* d_status,
+                       void* stream);
+
+size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
+                                          int n_kv_heads, int head_dim);
+
+/*
  * omnitide_decode_attn -- decode attention over the compacted pool (paper: Background, decode
  * generates one token at a time reusing the cached states; OmniPage ablation, decode attention
  * time over the native, OmniPage and eagerly compacted layouts).  The chunk attention above

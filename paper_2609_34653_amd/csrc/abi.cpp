@@ -333,24 +333,34 @@ size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_
   return omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
 }
 
-int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
-                        int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
-                        int head_dim, float scale, float* out, void* workspace,
-                        size_t workspace_bytes, int32_t* d_status, void* stream) {
+namespace {
+
+// Chunk attention over contiguous rows (key_pos == nullptr) or over a span with holes.
+int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+              const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int chunk_len,
+              int n_q_heads, int n_kv_heads, int head_dim, float scale, float* out,
+              void* workspace, size_t workspace_bytes, int32_t* d_status, void* stream) {
+  const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
+  if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
   if (n_seg < 1 || n_seg > kMaxGridY || chunk_len < 1 || n_kv_heads < 1 ||
       n_q_heads < n_kv_heads || n_q_heads % n_kv_heads != 0 ||
       !(head_dim == 64 || head_dim == 128) || !std::isfinite(scale) ||
       static_cast<long>(chunk_len) * (n_q_heads / n_kv_heads) > (1L << 30))
     return OMNITIDE_E_SHAPE;
-  if (cap < chunk_len) return OMNITIDE_E_CAPACITY;
+  if (cap < chunk_len || (span && cap > omnitide::span_attn_max_cap()))
+    return OMNITIDE_E_CAPACITY;
   const size_t need =
-      omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
+      span ? omnitide::span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
+                                                 head_dim)
+           : omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
+                                            head_dim);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return OMNITIDE_E_WORKSPACE;
   const size_t qrows = static_cast<size_t>(n_seg) * chunk_len * n_q_heads;
   const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * 2;
   if (any_alias({{out, qrows * head_dim * 4}, {workspace, need}, {d_status, 4}},
-                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull}}))
+                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull},
+                 {key_pos, static_cast<size_t>(n_seg) * cap * 4}, {q_pos0, n_seg * 4ull}}))
     return OMNITIDE_E_ALIAS;
   AttnArgs a;
   a.q = q;
@@ -367,7 +377,38 @@ int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32
   a.out = out;
   a.workspace = need > 0 ? workspace : nullptr;
   a.d_status = d_status;
+  a.key_pos = key_pos;
+  a.q_pos0 = q_pos0;
   return hip_status(omnitide::launch_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                        int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                        int head_dim, float scale, float* out, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream) {
+  return attn_impl(q, k, v, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len, n_q_heads,
+                   n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream);
+}
+
+size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
+                                          int n_kv_heads, int head_dim) {
+  if (n_seg < 1 || cap < 1 || chunk_len < 1 || n_kv_heads < 1 || n_q_heads < n_kv_heads ||
+      n_q_heads % n_kv_heads != 0 || !(head_dim == 64 || head_dim == 128))
+    return 0;
+  return omnitide::span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
+                                             head_dim);
+}
+
+int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_t* key_pos,
+                       const int32_t* span, const int32_t* q_pos0, int n_seg, int cap,
+                       int chunk_len, int n_q_heads, int n_kv_heads, int head_dim, float scale,
+                       float* out, void* workspace, size_t workspace_bytes, int32_t* d_status,
+                       void* stream) {
+  if (key_pos == nullptr || q_pos0 == nullptr) return OMNITIDE_E_NULL;
+  return attn_impl(q, k, v, span, key_pos, q_pos0, n_seg, cap, chunk_len, n_q_heads,
+                   n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream);
 }
 
 size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,

@@ -122,19 +122,28 @@ __device__ inline T& pick(T& a, T& b) {
   if constexpr (B == 0) return a; else return b;
 }
 
-template <int D>
+// SPAN = false: keys are the contiguous rows [0, n_ctx) of the compacted pool, the chunk last.
+// SPAN = true: keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span);
+// slot j is visible to query i iff 0 <= key_pos[j] <= q_pos0 + i; only the active tiles listed
+// by span_tiles_kernel are visited, and a tile is masked only if it holds an empty slot or a
+// position past the workgroup's first row.
+template <int D, bool SPAN>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int L, int Hq,
     int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
-    float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status) {
+    float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status,
+    const int32_t* __restrict__ key_pos, const int32_t* __restrict__ qpos0_g,
+    const int2* __restrict__ tile_info, const int32_t* __restrict__ tile_list,
+    const int32_t* __restrict__ n_active_g, int max_tiles) {
   using S = Smem<D>;
   // Tile buffers K0, K1, V0, V1 at fixed offsets (every access below names its buffer at
   // compile time, so LDS addresses are immediates).
   __shared__ __attribute__((aligned(1024))) uint16_t lds[4 * S::TILE_ELEMS];
+  __shared__ int32_t kpos_lds[SPAN ? kKT : 1];     // positions of the current tile's keys
 
   const int seg = blockIdx.y;
-  const int nctx = n_ctx_g[seg];
+  const int nctx = n_ctx_g[seg];                   // SPAN: the span
   if (nctx < L || nctx > cap) {
     if (threadIdx.x == 0) set_status(status, OMNITIDE_E_CAPACITY);
     return;
@@ -149,12 +158,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
 
   const int G = Hq / Hkv;
   const int rows = L * G;
-  const int kept = nctx - L;
+  const int kept = SPAN ? qpos0_g[seg] : nctx - L;  // logical position of chunk query 0
   const int m0 = mt * kRowsWG;
   const int p_lo = m0 / G;
   const int p_hi = min(L - 1, (m0 + kRowsWG - 1) / G);
   const int kmax = kept + p_hi + 1;               // keys [0, kmax) are needed by this workgroup
-  const int n_tiles = (kmax + kKT - 1) / kKT;
+  const int n_tiles = SPAN ? n_active_g[seg] : (kmax + kKT - 1) / kKT;
   const int t_begin = static_cast<int>(static_cast<long>(n_tiles) * split / n_split);
   const int t_end = static_cast<int>(static_cast<long>(n_tiles) * (split + 1) / n_split);
   const int full_lim = kept + p_lo;               // keys <= full_lim are visible to every row
@@ -229,6 +238,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         *reinterpret_cast<u32x4*>(base + 8 * idx) = u32x4{0, 0, 0, 0};
   };
 
+  // SPAN: the a-th visited tile is tile_list[a]; its (largest position, has an empty slot).
+  const size_t tl_base = static_cast<size_t>(seg) * max_tiles;
+  auto tile_of = [&](int a) -> int {
+    if constexpr (SPAN) return tile_list[tl_base + a]; else return a;
+  };
+  // SPAN: wave 0 holds the positions of the next V tile's keys (one per lane, -1 past the span)
+  int kp_next = -1;
+  auto load_kpos = [&](int t) {
+    const int j = t * kKT + lane;
+    kp_next = j < nctx ? key_pos[static_cast<size_t>(seg) * cap + j] : -1;
+  };
+
   floatx16 o[D / 32];
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt) o[dt] = floatx16{};
@@ -256,12 +277,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   };
 
   if (t_begin < t_end) {
-    issue(k_head, koff, t_begin, 0);
-    issue(v_head, voff, t_begin, 2);
-    if (t_begin + 1 < t_end) issue(k_head, koff, t_begin + 1, 1);
+    issue(k_head, koff, tile_of(t_begin), 0);
+    issue(v_head, voff, tile_of(t_begin), 2);
+    if constexpr (SPAN) {
+      if (wave == 0) load_kpos(tile_of(t_begin));
+    }
+    if (t_begin + 1 < t_end) issue(k_head, koff, tile_of(t_begin + 1), 1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (t_begin * kKT + kKT > nctx) {
+    if (!SPAN && t_begin * kKT + kKT > nctx) {
       zero_rows(t_begin, 0);
       __syncthreads();
     }
@@ -282,21 +306,51 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       const bool has_next = t + 1 < t_end;
       __builtin_amdgcn_s_waitcnt(0);      // this wave's pieces of K(t+1) and V(t) have landed
       __syncthreads();                    // ... everyone's; iteration t-1 is finished
-      if ((has_next && j0 + 2 * kKT > nctx) || j0 + kKT > nctx) {
-        if (has_next) zero_rows(t + 1, 1 - B);
-        zero_rows(t, 2 + B);
-        __syncthreads();
+      bool masked;
+      if constexpr (SPAN) {
+        // t indexes the tile list: publish this tile's key positions, zero the V rows of its
+        // empty slots (their contents are arbitrary), then mask per key.
+        const int2 info = tile_info[tl_base + tile_of(t)];
+        masked = info.y != 0 || info.x > full_lim;
+        if (masked) {
+          if (wave == 0) kpos_lds[lane] = kp_next;
+          __syncthreads();
+          if (info.y != 0) {
+            uint16_t* vb = lds + (2 + B) * S::TILE_ELEMS;
+            for (int idx = tid; idx < kKT * S::CHUNKS; idx += kAttnThreads)
+              if (kpos_lds[idx / S::CHUNKS] < 0)
+                *reinterpret_cast<u32x4*>(vb + 8 * idx) = u32x4{0, 0, 0, 0};
+            __syncthreads();
+          }
+        }
+        if (t + 2 < t_end) issue(k_head, koff, tile_of(t + 2), B);
+        if (has_next) {
+          issue(v_head, voff, tile_of(t + 1), 3 - B);
+          if (wave == 0) load_kpos(tile_of(t + 1));
+        }
+      } else {
+        if ((has_next && j0 + 2 * kKT > nctx) || j0 + kKT > nctx) {
+          if (has_next) zero_rows(t + 1, 1 - B);
+          zero_rows(t, 2 + B);
+          __syncthreads();
+        }
+        if (t + 2 < t_end) issue(k_head, koff, t + 2, B);
+        if (has_next) issue(v_head, voff, t + 1, 3 - B);
+        masked = j0 + kKT - 1 > full_lim;  // causal mask: only tiles past the first row's limit
       }
-      if (t + 2 < t_end) issue(k_head, koff, t + 2, B);
-      if (has_next) issue(v_head, voff, t + 1, 3 - B);
 
-      // causal mask of this tile's scores (only tiles past the first row's limit)
-      if (j0 + kKT - 1 > full_lim) {
+      if (masked) {
 #pragma unroll
         for (int st = 0; st < 2; ++st) {
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            if (j0 + 32 * st + 16 * h + i > lim) s_cur[st][i] = -INFINITY;
+          for (int i = 0; i < 16; ++i) {
+            if constexpr (SPAN) {
+              const int kp = kpos_lds[32 * st + 16 * h + i];
+              if (kp < 0 || kp > lim) s_cur[st][i] = -INFINITY;
+            } else {
+              if (j0 + 32 * st + 16 * h + i > lim) s_cur[st][i] = -INFINITY;
+            }
+          }
         }
       }
 
@@ -429,24 +483,94 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   }
 }
 
+// Active tiles of a span, one workgroup per segment: per 64-slot tile of [0, span) the largest
+// key position and whether it holds an empty slot (or slots past the span), and the ordered
+// list of tiles holding at least one entry.
+constexpr int kSpanThreads = 1024;
+constexpr int kMaxSpanTiles = 32768;
+
+__global__ __launch_bounds__(kSpanThreads) void span_tiles_kernel(
+    const int32_t* __restrict__ key_pos, const int32_t* __restrict__ span_g, int cap, int L,
+    int max_tiles, int2* __restrict__ tile_info, int32_t* __restrict__ tile_list,
+    int32_t* __restrict__ n_active_g) {
+  __shared__ uint8_t act[kMaxSpanTiles];
+  __shared__ int32_t scr[kSpanThreads / kWave + 1];
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int span = span_g[seg];
+  const size_t tb = static_cast<size_t>(seg) * max_tiles;
+  if (span < L || span > cap) {                  // reported by the attention kernel
+    if (tid == 0) n_active_g[seg] = 0;
+    return;
+  }
+  const int n_tiles = (span + kKT - 1) / kKT;
+  for (int t = wave; t < n_tiles; t += kSpanThreads / kWave) {
+    const int j = t * kKT + lane;
+    const int p = j < span ? key_pos[static_cast<size_t>(seg) * cap + j] : -1;
+    const uint64_t valid = __ballot(p >= 0);
+    int mx = p;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off, kWave));
+    if (lane == 0) {
+      tile_info[tb + t] = make_int2(mx, valid != ~0ull ? 1 : 0);
+      act[t] = valid != 0 ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  int running = 0;
+  for (int base = 0; base < n_tiles; base += kSpanThreads) {
+    const int t = base + tid;
+    const int f = t < n_tiles ? act[t] : 0;
+    int total;
+    const int off = block_exclusive_scan(f, scr, &total);
+    if (f) tile_list[tb + running + off] = t;
+    running += total;
+  }
+  if (tid == 0) n_active_g[seg] = running;
+}
+
 template <int D>
 hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
   const int G = a.n_q_heads / a.n_kv_heads;
   const int n_mt = (a.chunk_len * G + kRowsWG - 1) / kRowsWG;
   const dim3 grid(n_mt * a.n_kv_heads * n_split, a.n_seg);
   const size_t n_rows = static_cast<size_t>(a.n_seg) * a.chunk_len * a.n_q_heads;
-  float* part_o = static_cast<float*>(a.workspace);
+  float* part_o = n_split > 1 ? static_cast<float*>(a.workspace) : nullptr;
   float* part_ml = part_o ? part_o + static_cast<size_t>(n_split) * n_rows * D : nullptr;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  hipLaunchKernelGGL((attn_kernel<D>), grid, dim3(kAttnThreads), 0, stream,
-                     static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
-                     static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
-                     a.n_q_heads, a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_mt,
-                     n_split, a.d_status);
+  if (a.key_pos != nullptr) {
+    // span mode: tile table after the partials
+    const int max_tiles = (a.cap + kKT - 1) / kKT;
+    uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
+                   (n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
+    int2* tile_info = reinterpret_cast<int2*>(tbl);
+    int32_t* tile_list = reinterpret_cast<int32_t*>(
+        tbl + static_cast<size_t>(a.n_seg) * max_tiles * sizeof(int2));
+    int32_t* n_active = tile_list + static_cast<size_t>(a.n_seg) * max_tiles;
+    hipLaunchKernelGGL(span_tiles_kernel, dim3(a.n_seg), dim3(kSpanThreads), 0, stream,
+                       a.key_pos, a.n_ctx, a.cap, a.chunk_len, max_tiles, tile_info, tile_list,
+                       n_active);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_kernel<D, true>), grid, dim3(kAttnThreads), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                       static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
+                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_mt,
+                       n_split, a.d_status, a.key_pos, a.q_pos0, tile_info, tile_list, n_active,
+                       max_tiles);
+  } else {
+    hipLaunchKernelGGL((attn_kernel<D, false>), grid, dim3(kAttnThreads), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                       static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
+                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_mt,
+                       n_split, a.d_status, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_split == 1) return e;
-  return launch_combine<D>(part_o, part_ml, n_split, n_rows, a.n_ctx, a.chunk_len, a.n_q_heads, a.cap,
-                           a.out, stream);
+  return launch_combine<D>(part_o, part_ml, n_split, n_rows, a.n_ctx, a.chunk_len, a.n_q_heads,
+                           a.cap, a.out, stream);
 }
 
 }  // namespace
@@ -470,6 +594,16 @@ size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, in
   const size_t rows = static_cast<size_t>(n_seg) * chunk_len * n_q_heads;
   return static_cast<size_t>(s) * rows * (static_cast<size_t>(head_dim) + 2) * sizeof(float);
 }
+
+size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
+                                 int n_kv_heads, int head_dim) {
+  const size_t max_tiles = (static_cast<size_t>(cap) + kKT - 1) / kKT;
+  return attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim) +
+         static_cast<size_t>(n_seg) * max_tiles * (sizeof(int2) + sizeof(int32_t)) +
+         static_cast<size_t>(n_seg) * sizeof(int32_t);
+}
+
+int span_attn_max_cap() { return kMaxSpanTiles * kKT; }
 
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
   const int s = attn_num_splits(a.n_seg, a.cap, a.chunk_len, a.n_q_heads, a.n_kv_heads,

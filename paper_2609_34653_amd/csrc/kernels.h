@@ -83,6 +83,9 @@ struct AttnArgs {
   float* out;
   void* workspace;
   int32_t* d_status;
+  // span mode (keys = the slots [0, span) of a pool with holes; n_ctx holds the span):
+  const int32_t* key_pos = nullptr;   // [n_seg][cap] logical position, -1 = empty slot
+  const int32_t* q_pos0 = nullptr;    // [n_seg] logical position of chunk query 0
 };
 
 int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
@@ -90,6 +93,9 @@ int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_h
 size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
                             int head_dim);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
+size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
+                                 int n_kv_heads, int head_dim);
+int span_attn_max_cap();
 
 struct DecodeArgs {
   const void* q;

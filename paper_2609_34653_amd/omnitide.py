@@ -29,7 +29,8 @@ ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
            "omnitide_compact_kv_rope", "omnitide_plan_spans", "omnitide_compact_kv_spans",
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
-           "omnitide_attn_workspace_bytes", "omnitide_decode_attn",
+           "omnitide_attn_workspace_bytes", "omnitide_span_attn",
+           "omnitide_span_attn_workspace_bytes", "omnitide_decode_attn",
            "omnitide_decode_workspace_bytes", "omnitide_status_string", "omnitide_version")
 
 
@@ -72,6 +73,10 @@ def lib() -> ctypes.CDLL:
                                           ctypes.c_float, _P, _P, _SZ, _P, _P]
         L.omnitide_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_attn_workspace_bytes.restype = _SZ
+        L.omnitide_span_attn.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
+                                         ctypes.c_float, _P, _P, _SZ, _P, _P]
+        L.omnitide_span_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
+        L.omnitide_span_attn_workspace_bytes.restype = _SZ
         L.omnitide_decode_attn.argtypes = L.omnitide_chunk_attn.argtypes
         L.omnitide_decode_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_decode_workspace_bytes.restype = _SZ
@@ -80,7 +85,7 @@ def lib() -> ctypes.CDLL:
         L.omnitide_version.restype = ctypes.c_char_p
         for name in ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
                      "omnitide_compact_kv_rope", "omnitide_compact_kv_spans",
-                     "omnitide_plan_spans", "omnitide_chunk_attn",
+                     "omnitide_plan_spans", "omnitide_chunk_attn", "omnitide_span_attn",
                      "omnitide_decode_attn"):
             getattr(L, name).restype = _I
         _lib = L
@@ -327,6 +332,39 @@ def omnitide_chunk_attn(q, k, v, n_ctx, scale, out, workspace=None, d_status=Non
                                      Hkv, d, float(scale), _ptr(out), _ptr(workspace),
                                      0 if workspace is None else workspace.numel(),
                                      _ptr(d_status), _stream(stream)), "omnitide_chunk_attn")
+
+
+def omnitide_span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
+                                       head_dim) -> int:
+    return int(lib().omnitide_span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads,
+                                                        n_kv_heads, head_dim))
+
+
+def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_status=None,
+                       stream=None):
+    """q [n_seg, L, Hq, d] bf16; k/v [n_seg, cap, Hkv, d] bf16; key_pos int32 [n_seg * cap]
+    (-1 = empty slot); span, q_pos0 int32 [n_seg] (device); out float32 like q."""
+    if q.dim() == 3:
+        n_seg, (L, Hq, d) = 1, q.shape
+    else:
+        n_seg, L, Hq, d = q.shape
+    ds, cap, Hkv, dd = _pool_dims(k, "k")
+    if ds != n_seg or dd != d:
+        raise ValueError("k shape does not match q")
+    _need(q, "q", (torch.bfloat16,))
+    _need(k, "k", (torch.bfloat16,))
+    _need(v, "v", (torch.bfloat16,), k.numel())
+    _need(key_pos, "key_pos", I32, n_seg * cap)
+    _need(span, "span", I32, n_seg)
+    _need(q_pos0, "q_pos0", I32, n_seg)
+    _need(out, "out", (torch.float32,), q.numel())
+    _need(workspace, "workspace", U8)
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_span_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(key_pos), _ptr(span),
+                                    _ptr(q_pos0), n_seg, cap, L, Hq, Hkv, d, float(scale),
+                                    _ptr(out), _ptr(workspace), workspace.numel(),
+                                    _ptr(d_status), _stream(stream)), "omnitide_span_attn")
 
 
 def omnitide_decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim) -> int:

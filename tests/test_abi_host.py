@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 13
+    assert len(names) == 15
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -231,6 +231,31 @@ def test_attention_validation(L):
     assert need > 0 and attn(L, wsb=need - 1) == ot.E_WORKSPACE
     # split count: 21 row tiles x 8 KV heads -> 3 splits on the 80K-history shape
     assert need == 3 * 665 * 32 * 130 * 4
+
+
+def span_attn(L, **kw):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), kp=fake(3), span=fake(4), qp=fake(5), n_seg=1,
+             cap=81920, Lc=665, Hq=32, Hkv=8, d=128, scale=0.0884, out=fake(6), ws=fake(7),
+             wsb=1 << 30, st=fake(8))
+    a.update(kw)
+    return L.omnitide_span_attn(a["q"], a["k"], a["v"], a["kp"], a["span"], a["qp"], a["n_seg"],
+                                a["cap"], a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"],
+                                a["out"], a["ws"], a["wsb"], a["st"], None)
+
+
+def test_span_attention_validation(L):
+    for k in ("q", "kp", "span", "qp", "out"):
+        assert span_attn(L, **{k: None}) == ot.E_NULL, k
+    assert span_attn(L, Hq=30) == ot.E_SHAPE
+    assert span_attn(L, cap=600) == ot.E_CAPACITY            # smaller than the chunk
+    assert span_attn(L, cap=(1 << 21) + 1) == ot.E_CAPACITY  # over the tile-table limit
+    assert span_attn(L, ws=None) == ot.E_WORKSPACE
+    need = ot.omnitide_span_attn_workspace_bytes(1, 81920, 665, 32, 8, 128)
+    assert need > ot.omnitide_attn_workspace_bytes(1, 81920, 665, 32, 8, 128)
+    assert span_attn(L, wsb=need - 1) == ot.E_WORKSPACE
+    assert span_attn(L, out=P(fake(3).value + 256)) == ot.E_ALIAS   # output over key_pos
+    # chunk_attn keeps its own (smaller) workspace and needs no positions
+    assert ot.omnitide_span_attn_workspace_bytes(1, 81920, 665, 30, 8, 128) == 0
 
 
 def decode(L, **kw):

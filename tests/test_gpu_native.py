@@ -1,0 +1,188 @@
+"""Native (logical-only) layout on the GPU vs the CPU oracle, through the C ABI: attention over a
+holey span.
+
+Bar: attention within max |err| <= 1e-2 and mean |err| <= 1e-3 of the float64 oracle on the
+same bf16 inputs (the prefill bar); full-size pools compare sampled query rows the oracle
+computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import streamgen as sg
+from tests._util import storage_np
+from tests.test_gpu_parity import dev, host, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 1e-2, 1e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_34653_amd import omnitide
+    omnitide.lib()
+    yield
+
+
+def bf16(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16)
+
+
+def run_span_attn(q, k, v, key_pos, span, q_pos0, scale, expect_status=0):
+    """q [n_seg, L, Hq, d], k/v [n_seg, cap, Hkv, d] bf16 (CPU); key_pos [n_seg, cap]."""
+    from paper_2609_34653_amd import omnitide as ot
+    n_seg, L, Hq, d = q.shape
+    cap, Hkv = k.shape[1], k.shape[2]
+    out = torch.full((n_seg, L, Hq, d), float("nan"), device="cuda")
+    nb = ot.omnitide_span_attn_workspace_bytes(n_seg, cap, L, Hq, Hkv, d)
+    ws = torch.zeros(nb, dtype=torch.uint8, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ot.omnitide_span_attn(q.cuda(), k.cuda(), v.cuda(),
+                          dev(np.asarray(key_pos, np.int32).reshape(-1)),
+                          dev(np.asarray(span, np.int32)), dev(np.asarray(q_pos0, np.int32)),
+                          scale, out, ws, st)
+    torch.cuda.synchronize()
+    assert int(host(st)[0]) == expect_status
+    return host(out)
+
+
+def check(out, q, k, v, key_pos, span, q_pos0, scale, rows=None):
+    f = lambda t: oracle.to_f64(storage_np(t), "bf16")  # noqa: E731
+    L = q.shape[0]
+    if rows is not None:
+        # only occupied slots can be visible: hand the oracle those (in slot order)
+        occ = np.nonzero(np.asarray(key_pos)[:span] >= 0)[0]
+        k, v, key_pos, span = k[occ], v[occ], np.asarray(key_pos)[occ], len(occ)
+    q64, k64, v64 = f(q), f(k), f(v)
+    if rows is None:
+        ref = oracle.span_attention(q64, k64, v64, key_pos, span, q_pos0, scale)
+        got = out
+    else:
+        ref = np.stack([oracle.span_attention(q64[i:i + 1], k64, v64, key_pos, span,
+                                              q_pos0 + i, scale)[0] for i in rows])
+        got = out[rows]
+    assert got.shape[0] == (L if rows is None else len(rows))
+    err = np.abs(got.astype(np.float64) - ref)
+    assert np.isfinite(got).all()
+    assert err.max() <= MAX_ABS, err.max()
+    assert err.mean() <= MEAN_ABS, err.mean()
+
+
+def random_span_pool(rng, cap, L, Hkv, d, fill, empty_tiles=True, nan_holes=True):
+    """Entries at random slots (some whole 64-slot tiles empty), dense positions in a random
+    temporal order of runs, the chunk in the lowest free run of L slots."""
+    occ = rng.random(cap - L) < fill
+    if empty_tiles:
+        for t in range(0, cap - L, 64):
+            if rng.random() < 0.25:
+                occ[t:t + 64] = False
+    uid = np.full(cap, -1)
+    uid[:cap - L][occ] = 0
+    s0 = oracle.place_chunk(uid, L, cap)
+    hist = np.nonzero(uid >= 0)[0]
+    key_pos = np.full(cap, -1)
+    key_pos[hist] = rng.permutation(len(hist))          # any physical order of positions
+    key_pos[s0:s0 + L] = len(hist) + np.arange(L)
+    span = int(np.nonzero(key_pos >= 0)[0][-1]) + 1
+    k = rng.standard_normal((cap, Hkv, d)).astype(np.float32)
+    v = rng.standard_normal((cap, Hkv, d)).astype(np.float32)
+    if nan_holes:
+        k[key_pos < 0] = np.nan
+        v[key_pos < 0] = np.inf
+    return bf16(k), bf16(v), key_pos, span, len(hist)
+
+
+@pytest.mark.parametrize("cap,L,Hq,Hkv,d,fill,seed", [
+    (700, 37, 8, 2, 128, 0.5, 0),       # ragged span, several tiles, GQA 4
+    (2000, 100, 4, 4, 64, 0.3, 1),      # no grouping, d = 64
+    (1500, 200, 32, 8, 128, 0.9, 2),    # nearly full, chunk 200
+    (5000, 64, 8, 1, 128, 0.1, 3),      # sparse: many empty tiles
+])
+def test_span_attention_random_pools(cap, L, Hq, Hkv, d, fill, seed):
+    rng = np.random.default_rng(seed)
+    k, v, key_pos, span, q_pos0 = random_span_pool(rng, cap, L, Hkv, d, fill)
+    q = bf16(rng.standard_normal((L, Hq, d)))
+    scale = d ** -0.5
+    out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0], scale)
+    check(out[0], q, k, v, key_pos, span, q_pos0, scale)
+
+
+def test_span_attention_several_segments():
+    rng = np.random.default_rng(5)
+    cap, L, Hq, Hkv, d = 1200, 50, 8, 2, 128
+    pools = [random_span_pool(rng, cap, L, Hkv, d, f) for f in (0.2, 0.6, 0.95)]
+    q = bf16(rng.standard_normal((3, L, Hq, d)))
+    out = run_span_attn(q, torch.stack([p[0] for p in pools]), torch.stack([p[1] for p in pools]),
+                        np.stack([p[2] for p in pools]), [p[3] for p in pools],
+                        [p[4] for p in pools], 0.1)
+    for i, (k, v, kp, span, qp) in enumerate(pools):
+        check(out[i], q[i], k, v, kp, span, qp, 0.1)
+
+
+def test_dense_positions_match_chunk_attention():
+    """key_pos = slot index and q_pos0 = span - L: the contiguous chunk attention."""
+    from paper_2609_34653_amd import omnitide as ot
+    rng = np.random.default_rng(6)
+    cap, L, Hq, Hkv, d, n = 3000, 300, 16, 4, 128, 2345
+    k = bf16(rng.standard_normal((1, cap, Hkv, d)))
+    v = bf16(rng.standard_normal((1, cap, Hkv, d)))
+    q = bf16(rng.standard_normal((1, L, Hq, d)))
+    kp = np.where(np.arange(cap) < n, np.arange(cap), -1)
+    out = run_span_attn(q, k, v, kp[None], [n], [n - L], 0.09)
+    ref = torch.zeros(1, L, Hq, d, device="cuda")
+    nb = ot.omnitide_attn_workspace_bytes(1, cap, L, Hq, Hkv, d)
+    ws = torch.zeros(max(nb, 1), dtype=torch.uint8, device="cuda")
+    ot.omnitide_chunk_attn(q.cuda(), k.cuda(), v.cuda(), dev(np.array([n], np.int32)), 0.09, ref,
+                           ws)
+    torch.cuda.synchronize()
+    assert np.abs(out - host(ref)).max() <= 2e-3
+    check(out[0], q[0], k[0], v[0], kp, n, n - L, 0.09, rows=sample_rows(L, rng, 12))
+
+
+def native_80k(keep_whole=True):
+    """The 80K history after the whole-unit plan, evicted in place, the chunk in the lowest run
+    of empty slots."""
+    cfg = sg.CONFIG_BY_NAME["history_80k"]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    k = storage_np(seg.k_hist)
+    sc = oracle.score_units(k, cfg.dtype, lay.unit_id, lay.modality, cfg.weights, lay.n_units)
+    _, keep, kept = oracle.select_units(sc["wsum"], sc["len"], sc["first"], sc["last"],
+                                        sc["flags"], cfg.budget, cfg.recent)
+    ev = oracle.evict_logical(lay.unit_id, lay.pos, np.where(keep != 0, sc["len"], 0),
+                              lay.n_units)
+    L = lay.chunk_len
+    cap = lay.n_slots + L
+    uid = np.concatenate([ev["unit_id"], np.full(L, -1)])
+    s0 = oracle.place_chunk(uid, L, cap)
+    key_pos = np.concatenate([ev["pos"], np.full(L, -1)])
+    key_pos[s0:s0 + L] = ev["kept"] + np.arange(L)
+    kk = torch.cat([seg.k_hist, torch.zeros(L, *seg.k_hist.shape[1:], dtype=torch.bfloat16)])
+    vv = torch.cat([seg.v_hist, torch.zeros(L, *seg.v_hist.shape[1:], dtype=torch.bfloat16)])
+    kk[s0:s0 + L] = seg.k_chunk
+    vv[s0:s0 + L] = seg.v_chunk
+    span = int(np.nonzero(key_pos >= 0)[0][-1]) + 1
+    return cfg, seg.q, kk, vv, key_pos, span, ev["kept"], s0
+
+
+def test_span_attention_native_80k():
+    cfg, q, k, v, key_pos, span, q_pos0, s0 = native_80k()
+    assert s0 < span - 665 and span > 60000, "the chunk fills a hole, the span stays long"
+    out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0], cfg.scale)
+    rows = sample_rows(q.shape[0], np.random.default_rng(8), 16)
+    check(out[0], q, k, v, key_pos, span, q_pos0, cfg.scale, rows=rows)
+
+
+def test_span_attention_capacity_error():
+    rng = np.random.default_rng(9)
+    k, v, kp, span, qp = random_span_pool(rng, 500, 40, 2, 64, 0.5, nan_holes=False)
+    q = bf16(rng.standard_normal((1, 40, 4, 64)))
+    out = run_span_attn(q, k[None], v[None], kp[None], [501], [qp], 0.1,
+                        expect_status=-5)
+    assert np.all(np.isnan(out))
+    out = run_span_attn(q, k[None], v[None], kp[None], [39], [qp], 0.1, expect_status=-5)
+    assert np.all(np.isnan(out))
