@@ -10,7 +10,8 @@
  * omnitide_plan_spans + omnitide_compact_kv_spans (the span plan: recent units whole, sink
  * prefixes of older units, a shared text budget, oldest-first trimming, then compaction of the
  * kept prefixes) and omnitide_decode_attn (decode attention of the last few tokens over the
- * compacted pool).
+ * compacted pool); omnitide_evict_native, omnitide_pack_suffix, omnitide_place_chunk and
+ * omnitide_span_attn keep the native (logical-only) layout with holes instead.
  *
  * Conventions shared by every entry point
  *   - Array arguments are DEVICE pointers into memory the caller allocated (hipMalloc or a
@@ -294,6 +295,67 @@ int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32
 
 size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                      int n_kv_heads, int head_dim);
+
+/*
+ * Native (logical-only) layout: the retained entries stay in their slots after eviction, the
+ * new chunk fills the lowest run of empty slots, and attention runs over the physical span
+ * (omnitide_span_attn).  Paper: Applying the retention plan (logical deletion, positions shift
+ * down, entries stay in place); Fragmentation after logical eviction (holes, physical span);
+ * Selective and efficient KV migration, ordered-suffix mode.
+ *
+ * Preconditions on the tags of a native pool ([n_seg][cap], cap <= 131,072): live entries carry
+ * the logical positions 0..n-1 of their segment, each unit's tokens hold consecutive positions
+ * and units follow each other in id (temporal) order; slots may be in any physical order.
+ *
+ * omnitide_evict_native -- logical eviction in place.  Unit u keeps its first keep_len[u] tokens
+ * in position order (keep_len NULL: keep[u] != 0 keeps the whole unit).  Kept entries get the
+ * unit's new id (kept units renumbered 0.. in order, unit_remap[u], -1 when dropped) and their
+ * position minus the tokens deleted before them; evicted slots get unit id -1 and position -1
+ * (their K/V bytes stay).  Outputs per segment: kept_tokens, n_kept_units, span (last occupied
+ * slot + 1).  unit_len is omnitide_score_units' output.  d_status: OMNITIDE_E_TAGS for an entry
+ * whose position lies outside its unit's range (tags then partly rewritten).
+ */
+int omnitide_evict_native(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
+                          const uint8_t* keep, const int32_t* keep_len, const int32_t* unit_len,
+                          int n_units, int32_t* unit_remap, int32_t* kept_tokens,
+                          int32_t* n_kept_units, int32_t* span, void* workspace,
+                          size_t workspace_bytes, int32_t* d_status, void* stream);
+size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units);
+
+/*
+ * omnitide_pack_suffix -- ordered-suffix migration in place (paper: scanning back from the end
+ * of the cache, the suffix whose packing shortens the page-rounded span by at least a threshold
+ * of pages is packed, order kept, everything before it untouched; no qualifying suffix, no
+ * move).  Per segment, with span = last occupied slot + 1 and P = page_size: the packed span of
+ * cut c is c + (entries at or after c); the largest c < span whose packed span needs at least
+ * min_pages fewer pages of P slots than span is taken.  The entries at or after c move to
+ * c, c+1, ... in slot order with their tags (positions unchanged); vacated slots become empty.
+ * Outputs per segment: cut (-1: nothing moved), moved (entries whose slot changed), span (after
+ * packing).  Rows are staged through the workspace (a destination can be an earlier entry's
+ * source).  Limits: page_size >= 1, min_pages >= 1, cap <= 131,072.
+ */
+int omnitide_pack_suffix(void* k, void* v, int dtype, int n_seg, int cap, int n_kv_heads,
+                         int head_dim, int page_size, int min_pages, int32_t* unit_id,
+                         uint8_t* modality, int32_t* pos, int32_t* span, int32_t* cut,
+                         int32_t* moved, void* workspace, size_t workspace_bytes, void* stream);
+size_t omnitide_pack_suffix_workspace_bytes(int dtype, int n_seg, int cap, int n_kv_heads,
+                                            int head_dim);
+
+/*
+ * omnitide_place_chunk -- the new chunk into the lowest run of chunk_len empty slots of the
+ * pool (the free space past the span counts).  Row i goes to slot chunk_slot + i with unit id
+ * n_kept_units + chunk_unit[i], modality chunk_modality[i] and position kept_tokens + i
+ * (kept_tokens, n_kept_units: omnitide_evict_native's outputs).  Outputs per segment:
+ * chunk_slot and span (covering the chunk).  d_status: OMNITIDE_E_CAPACITY when no run fits
+ * (chunk_slot = -1, nothing written).
+ */
+int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_kv_heads,
+                         int head_dim, int32_t* unit_id, uint8_t* modality, int32_t* pos,
+                         const void* k_chunk, const void* v_chunk,
+                         const uint8_t* chunk_modality, const int32_t* chunk_unit,
+                         int chunk_len, const int32_t* kept_tokens,
+                         const int32_t* n_kept_units, int32_t* chunk_slot, int32_t* span,
+                         int32_t* d_status, void* stream);
 
 /*
  * omnitide_span_attn -- chunk attention over a pool with holes (paper: Fragmentation after

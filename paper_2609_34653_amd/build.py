@@ -19,8 +19,8 @@ LIB_NAME = "libomnitide.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["abi.cpp", "score.hip", "select.hip", "spans.hip", "compact.hip", "attention.hip",
-           "decode.hip"]
+SOURCES = ["abi.cpp", "score.hip", "select.hip", "spans.hip", "compact.hip", "native.hip",
+           "attention.hip", "decode.hip"]
 
 # Packed fp32 instructions are kept out of the device code (-packed-fp32-ops).
 HIP_FLAGS = ["-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

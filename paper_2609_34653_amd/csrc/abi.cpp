@@ -411,6 +411,143 @@ int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_
                    n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream);
 }
 
+size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units) {
+  if (n_seg < 1 || n_units < 1 || n_units > OMNITIDE_MAX_UNITS) return 0;
+  return omnitide::evict_workspace_bytes(n_seg, n_units);
+}
+
+int omnitide_evict_native(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
+                          const uint8_t* keep, const int32_t* keep_len, const int32_t* unit_len,
+                          int n_units, int32_t* unit_remap, int32_t* kept_tokens,
+                          int32_t* n_kept_units, int32_t* span, void* workspace,
+                          size_t workspace_bytes, int32_t* d_status, void* stream) {
+  if (!all_set({unit_len, unit_remap, kept_tokens, n_kept_units, span}) ||
+      (keep == nullptr && keep_len == nullptr))
+    return OMNITIDE_E_NULL;
+  if (cap > 0 && !all_set({unit_id, pos})) return OMNITIDE_E_NULL;
+  if (n_seg < 1 || n_seg > kMaxGridY || cap < 0 || cap > omnitide::native_max_cap() ||
+      n_units < 1 || n_units > OMNITIDE_MAX_UNITS)
+    return OMNITIDE_E_SHAPE;
+  const size_t need = omnitide::evict_workspace_bytes(n_seg, n_units);
+  if (workspace == nullptr || workspace_bytes < need) return OMNITIDE_E_WORKSPACE;
+  const size_t slots = static_cast<size_t>(n_seg) * cap;
+  const size_t units = static_cast<size_t>(n_seg) * n_units;
+  if (any_alias({{unit_id, slots * 4}, {pos, slots * 4}, {unit_remap, units * 4},
+                 {kept_tokens, n_seg * 4ull}, {n_kept_units, n_seg * 4ull}, {span, n_seg * 4ull},
+                 {workspace, need}, {d_status, 4}},
+                {{keep, keep_len ? 0 : units}, {keep_len, units * 4}, {unit_len, units * 4}}))
+    return OMNITIDE_E_ALIAS;
+  omnitide::EvictArgs a;
+  a.n_seg = n_seg;
+  a.cap = cap;
+  a.n_units = n_units;
+  a.unit_id = unit_id;
+  a.pos = pos;
+  a.keep = keep;
+  a.keep_len = keep_len;
+  a.unit_len = unit_len;
+  a.unit_remap = unit_remap;
+  a.kept_tokens = kept_tokens;
+  a.n_kept_units = n_kept_units;
+  a.span = span;
+  a.workspace = workspace;
+  a.d_status = d_status;
+  return hip_status(omnitide::launch_evict(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t omnitide_pack_suffix_workspace_bytes(int dtype, int n_seg, int cap, int n_kv_heads,
+                                            int head_dim) {
+  const int eb = elt_bytes(dtype);
+  if (eb == 0 || n_seg < 1 || cap < 1 || !row_ok(n_kv_heads, head_dim)) return 0;
+  return omnitide::suffix_workspace_bytes(n_seg, cap, n_kv_heads * head_dim * eb);
+}
+
+int omnitide_pack_suffix(void* k, void* v, int dtype, int n_seg, int cap, int n_kv_heads,
+                         int head_dim, int page_size, int min_pages, int32_t* unit_id,
+                         uint8_t* modality, int32_t* pos, int32_t* span, int32_t* cut,
+                         int32_t* moved, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!all_set({k, v, unit_id, modality, pos, span, cut, moved})) return OMNITIDE_E_NULL;
+  const int eb = elt_bytes(dtype);
+  if (eb == 0) return OMNITIDE_E_DTYPE;
+  if (n_seg < 1 || n_seg > kMaxGridY || cap < 1 || cap > omnitide::native_max_cap() ||
+      !row_ok(n_kv_heads, head_dim) || page_size < 1 || min_pages < 1)
+    return OMNITIDE_E_SHAPE;
+  const int row = n_kv_heads * head_dim * eb;
+  const size_t need = omnitide::suffix_workspace_bytes(n_seg, cap, row);
+  if (workspace == nullptr || workspace_bytes < need) return OMNITIDE_E_WORKSPACE;
+  const size_t slots = static_cast<size_t>(n_seg) * cap;
+  if (any_alias({{k, slots * row}, {v, slots * row}, {unit_id, slots * 4}, {modality, slots},
+                 {pos, slots * 4}, {span, n_seg * 4ull}, {cut, n_seg * 4ull},
+                 {moved, n_seg * 4ull}, {workspace, need}},
+                {}))
+    return OMNITIDE_E_ALIAS;
+  omnitide::SuffixArgs a;
+  a.n_seg = n_seg;
+  a.cap = cap;
+  a.row_bytes = row;
+  a.page_size = page_size;
+  a.min_pages = min_pages;
+  a.k = k;
+  a.v = v;
+  a.unit_id = unit_id;
+  a.modality = modality;
+  a.pos = pos;
+  a.span = span;
+  a.cut = cut;
+  a.moved = moved;
+  a.workspace = workspace;
+  return hip_status(omnitide::launch_pack_suffix(a, static_cast<hipStream_t>(stream)));
+}
+
+int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_kv_heads,
+                         int head_dim, int32_t* unit_id, uint8_t* modality, int32_t* pos,
+                         const void* k_chunk, const void* v_chunk,
+                         const uint8_t* chunk_modality, const int32_t* chunk_unit,
+                         int chunk_len, const int32_t* kept_tokens,
+                         const int32_t* n_kept_units, int32_t* chunk_slot, int32_t* span,
+                         int32_t* d_status, void* stream) {
+  if (!all_set({k, v, unit_id, modality, pos, k_chunk, v_chunk, chunk_modality, chunk_unit,
+                kept_tokens, n_kept_units, chunk_slot, span}))
+    return OMNITIDE_E_NULL;
+  const int eb = elt_bytes(dtype);
+  if (eb == 0) return OMNITIDE_E_DTYPE;
+  if (n_seg < 1 || n_seg > kMaxGridY || cap < 1 || cap > omnitide::native_max_cap() ||
+      !row_ok(n_kv_heads, head_dim) || chunk_len < 1)
+    return OMNITIDE_E_SHAPE;
+  if (chunk_len > cap) return OMNITIDE_E_CAPACITY;
+  const int row = n_kv_heads * head_dim * eb;
+  const size_t slots = static_cast<size_t>(n_seg) * cap;
+  const size_t crow = static_cast<size_t>(n_seg) * chunk_len;
+  if (any_alias({{k, slots * row}, {v, slots * row}, {unit_id, slots * 4}, {modality, slots},
+                 {pos, slots * 4}, {chunk_slot, n_seg * 4ull}, {span, n_seg * 4ull},
+                 {d_status, 4}},
+                {{k_chunk, crow * row}, {v_chunk, crow * row},
+                 {chunk_modality, static_cast<size_t>(chunk_len)},
+                 {chunk_unit, static_cast<size_t>(chunk_len) * 4}, {kept_tokens, n_seg * 4ull},
+                 {n_kept_units, n_seg * 4ull}}))
+    return OMNITIDE_E_ALIAS;
+  omnitide::PlaceArgs a;
+  a.n_seg = n_seg;
+  a.cap = cap;
+  a.row_bytes = row;
+  a.chunk_len = chunk_len;
+  a.k = k;
+  a.v = v;
+  a.unit_id = unit_id;
+  a.modality = modality;
+  a.pos = pos;
+  a.k_chunk = k_chunk;
+  a.v_chunk = v_chunk;
+  a.chunk_modality = chunk_modality;
+  a.chunk_unit = chunk_unit;
+  a.kept_tokens = kept_tokens;
+  a.n_kept_units = n_kept_units;
+  a.chunk_slot = chunk_slot;
+  a.span = span;
+  a.d_status = d_status;
+  return hip_status(omnitide::launch_place_chunk(a, static_cast<hipStream_t>(stream)));
+}
+
 size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,
                                        int n_kv_heads, int head_dim) {
   if (n_seg < 1 || cap < 1 || n_q < 1 || n_kv_heads < 1 || n_q_heads < n_kv_heads ||

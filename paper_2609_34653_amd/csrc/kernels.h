@@ -71,6 +71,57 @@ struct SpanPlanArgs {
 };
 
 hipError_t launch_plan_spans(const SpanPlanArgs& a, hipStream_t stream);
+
+// Native layout: logical eviction in place, ordered-suffix packing, chunk placement.
+struct EvictArgs {
+  int n_seg, cap, n_units;
+  int32_t* unit_id;          // [n_seg][cap], in place
+  int32_t* pos;              // [n_seg][cap], in place
+  const uint8_t* keep;       // one of keep / keep_len
+  const int32_t* keep_len;
+  const int32_t* unit_len;
+  int32_t* unit_remap;
+  int32_t* kept_tokens;
+  int32_t* n_kept_units;
+  int32_t* span;
+  void* workspace;
+  int32_t* d_status;
+};
+struct SuffixArgs {
+  int n_seg, cap, row_bytes, page_size, min_pages;
+  void* k;
+  void* v;
+  int32_t* unit_id;
+  uint8_t* modality;
+  int32_t* pos;
+  int32_t* span;
+  int32_t* cut;
+  int32_t* moved;
+  void* workspace;
+};
+struct PlaceArgs {
+  int n_seg, cap, row_bytes, chunk_len;
+  void* k;
+  void* v;
+  int32_t* unit_id;
+  uint8_t* modality;
+  int32_t* pos;
+  const void* k_chunk;
+  const void* v_chunk;
+  const uint8_t* chunk_modality;
+  const int32_t* chunk_unit;
+  const int32_t* kept_tokens;
+  const int32_t* n_kept_units;
+  int32_t* chunk_slot;
+  int32_t* span;
+  int32_t* d_status;
+};
+int native_max_cap();
+size_t evict_workspace_bytes(int n_seg, int n_units);
+size_t suffix_workspace_bytes(int n_seg, int cap, int row_bytes);
+hipError_t launch_evict(const EvictArgs& a, hipStream_t stream);
+hipError_t launch_pack_suffix(const SuffixArgs& a, hipStream_t stream);
+hipError_t launch_place_chunk(const PlaceArgs& a, hipStream_t stream);
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream);
 
 struct AttnArgs {

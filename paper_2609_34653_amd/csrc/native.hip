@@ -1,0 +1,439 @@
+// Native (logical-only) layout: logical eviction in place, ordered-suffix migration and chunk
+// placement into the lowest run of empty slots.
+//
+//   evict_plan     one workgroup per segment: scans over units give each unit its first
+//                  logical position (exclusive sum of lengths), kept length, deleted tokens
+//                  before it and new id; the table goes to the workspace.
+//   evict_apply    one thread per slot: rewrites the tags in place (kept: new id, position minus
+//                  the deleted tokens before its unit; otherwise empty); the span (last occupied
+//                  slot + 1) is a per-wave maximum published with one atomic per wave.
+//   The single-workgroup scans below first pack the segment's occupancy into an LDS bitmap
+//   (one bit per slot, all loads in flight at once), then work on bits: counts are popcounts
+//   and "last occupied slot" is a bit scan.
+//   suffix_plan    one workgroup per segment: the packed span of cut c is c + (entries at or
+//                  after c), or the span of what precedes c when that suffix is empty; it never
+//                  decreases with c, so the cuts that save >= min_pages pages form a prefix of
+//                  [0, span) and the largest is a block-wide maximum.  Lists the suffix entries
+//                  in slot order.
+//   suffix_gather  suffix entries whose slot changes -> workspace (rows and tags), in order;
+//   suffix_scatter workspace -> slots c + rank, vacated slots marked empty.  A destination can
+//                  be the source of an earlier entry, hence the round trip through scratch.
+//   place_plan     one workgroup per segment: the lowest slot s with [s, s + L) empty, from a
+//                  running "last occupied slot" carried across threads.
+//   chunk_write    the chunk's K/V rows and tags into [s, s + L).
+#include "common.h"
+#include "kernels.h"
+
+namespace omnitide {
+namespace {
+
+constexpr int kNatThreads = 1024;
+constexpr int kNatPer = OMNITIDE_MAX_UNITS / kNatThreads;
+constexpr int kRowsPerBlock = 16;
+constexpr int kCopyThreads = 256;
+
+struct UnitRec {
+  int32_t pos0;   // logical position of the unit's first token
+  int32_t kl;     // kept leading tokens
+  int32_t del;    // deleted tokens of earlier units
+  int32_t rank;   // new id, -1 when dropped
+};
+
+__global__ __launch_bounds__(kNatThreads) void evict_plan_kernel(
+    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ keep_len_g,
+    const int32_t* __restrict__ len_g, int n_units, UnitRec* __restrict__ table,
+    int32_t* __restrict__ remap_g, int32_t* __restrict__ kept_g,
+    int32_t* __restrict__ n_kept_units_g, int32_t* __restrict__ span_g) {
+  __shared__ int32_t scr[kNatThreads / kWave + 1];
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int U = n_units;
+  const int per = (U + kNatThreads - 1) / kNatThreads;
+  const int u0 = tid * per;
+  const size_t base = static_cast<size_t>(seg) * U;
+  int ln[kNatPer], kl[kNatPer];
+  int my_len = 0, my_kept = 0, my_del = 0, my_n = 0;
+#pragma unroll
+  for (int i = 0; i < kNatPer; ++i) {
+    const int u = u0 + i;
+    ln[i] = kl[i] = 0;
+    if (i < per && u < U) {
+      ln[i] = max(len_g[base + u], 0);
+      kl[i] = keep_len_g != nullptr ? min(max(keep_len_g[base + u], 0), ln[i])
+                                    : (keep_g[base + u] != 0 ? ln[i] : 0);
+    }
+    my_len += ln[i];
+    my_kept += kl[i];
+    my_del += ln[i] - kl[i];
+    my_n += kl[i] > 0 ? 1 : 0;
+  }
+  int total_len, kept, dropped, n_kept;
+  int pos0 = block_exclusive_scan(my_len, scr, &total_len);
+  int del = block_exclusive_scan(my_del, scr, &dropped);
+  int rk = block_exclusive_scan(my_n, scr, &n_kept);
+  (void)block_exclusive_scan(my_kept, scr, &kept);
+#pragma unroll
+  for (int i = 0; i < kNatPer; ++i) {
+    const int u = u0 + i;
+    if (i < per && u < U) {
+      const int r = kl[i] > 0 ? rk++ : -1;
+      table[base + u] = UnitRec{pos0, kl[i], del, r};
+      remap_g[base + u] = r;
+    }
+    pos0 += ln[i];
+    del += ln[i] - kl[i];
+  }
+  if (tid == 0) {
+    kept_g[seg] = kept;
+    n_kept_units_g[seg] = n_kept;
+    span_g[seg] = 0;                               // raised by evict_apply
+  }
+}
+
+// Occupancy bitmap of one segment's slots [0, cap) in LDS: bit j of word w is slot 32 w + j.
+constexpr int kMaxNatWords = 4096;                 // 131,072 slots
+__device__ inline void load_bitmap(const int32_t* __restrict__ uid, int cap, uint32_t* bits,
+                                   int nwords) {
+  for (int w = threadIdx.x; w < nwords; w += kNatThreads) {
+    int u[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const int s = 32 * w + j;
+      u[j] = s < cap ? uid[s] : -1;
+    }
+    uint32_t word = 0;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) word |= (u[j] >= 0 ? 1u : 0u) << j;
+    bits[w] = word;
+  }
+  __syncthreads();
+}
+__device__ inline bool bit(const uint32_t* bits, int s) {
+  return (bits[s >> 5] >> (s & 31)) & 1u;
+}
+
+__global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
+    int32_t* __restrict__ uid_g, int32_t* __restrict__ pos_g, int cap, int n_units,
+    const UnitRec* __restrict__ table, const int32_t* __restrict__ len_g,
+    int32_t* __restrict__ span_g, int32_t* __restrict__ status) {
+  const int seg = blockIdx.y;
+  const int s = blockIdx.x * kCopyThreads + threadIdx.x;
+  const size_t sb = static_cast<size_t>(seg) * cap;
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  int end = 0;                                    // slot + 1 if this slot stays occupied
+  if (s < cap) {
+    const int u = uid_g[sb + s];
+    if (u >= 0) {
+      bool bad = u >= n_units;
+      if (!bad) {
+        const UnitRec rec = table[ub + u];
+        const int p = pos_g[sb + s];
+        const int r = p - rec.pos0;               // rank of the token inside its unit
+        bad = r < 0 || r >= len_g[ub + u];
+        if (!bad && r < rec.kl) {
+          uid_g[sb + s] = rec.rank;
+          pos_g[sb + s] = p - rec.del;
+          end = s + 1;
+        } else if (!bad) {
+          uid_g[sb + s] = -1;
+          pos_g[sb + s] = -1;
+        }
+      }
+      if (bad) set_status(status, OMNITIDE_E_TAGS);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) end = max(end, __shfl_xor(end, off, kWave));
+  if ((threadIdx.x & (kWave - 1)) == 0 && end > 0) atomicMax(span_g + seg, end);
+}
+
+__global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
+    const int32_t* __restrict__ uid_g, int cap, int page_size, int min_pages,
+    int32_t* __restrict__ list, int32_t* __restrict__ meta, int32_t* __restrict__ span_g,
+    int32_t* __restrict__ cut_g, int32_t* __restrict__ moved_g) {
+  __shared__ uint32_t bits[kMaxNatWords];
+  __shared__ int32_t scr[kNatThreads / kWave + 1];
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  const size_t sb = static_cast<size_t>(seg) * cap;
+  const int nwords = (cap + 31) / 32;
+  load_bitmap(uid_g + sb, cap, bits, nwords);
+  // thread t owns words [w0, w1), i.e. slots [32 w0, 32 w1)
+  const int wpt = (nwords + kNatThreads - 1) / kNatThreads;
+  const int w0 = min(tid * wpt, nwords), w1 = min(w0 + wpt, nwords);
+  int my_live = 0, my_last = -1;
+  for (int w = w0; w < w1; ++w) {
+    my_live += __popc(bits[w]);
+    if (bits[w]) my_last = 32 * w + 31 - __clz(bits[w]);
+  }
+  int total;
+  const int live_before = block_exclusive_scan(my_live, scr, &total);
+  int span_m1;
+  const int last_before = block_exclusive_max(my_last, -1, scr, &span_m1);
+  const int span = span_m1 + 1;
+  const int pages_now = (span + page_size - 1) / page_size;
+  // largest qualifying cut c < span in this thread's slots
+  int best = -1;
+  {
+    int lb = last_before, live_lt = live_before;   // state before slot s
+    for (int s = 32 * w0; s < 32 * w1 && s < span; ++s) {
+      const int suffix = total - live_lt;            // entries at or after s
+      const int ps = suffix > 0 ? s + suffix : lb + 1;
+      if (pages_now - (ps + page_size - 1) / page_size >= min_pages) best = s;
+      if (bit(bits, s)) {
+        ++live_lt;
+        lb = s;
+      }
+    }
+  }
+  int c;
+  (void)block_exclusive_max(best, -1, scr, &c);
+  int n_suffix = 0, new_span = span, moved = 0;
+  if (c >= 0) {
+    // entries before c, counted by the thread whose range holds c
+    int mine = 0;
+    if (c >= 32 * w0 && c < 32 * w1) {
+      mine = live_before;
+      for (int s = 32 * w0; s < c; ++s) mine += bit(bits, s) ? 1 : 0;
+    }
+    const int before_c = block_sum(mine, scr);
+    n_suffix = total - before_c;
+    new_span = c + n_suffix;
+    int live_lt = live_before, moved_here = 0;
+    for (int s = 32 * w0; s < 32 * w1 && s < span; ++s) {
+      if (bit(bits, s)) {
+        if (s >= c) {
+          const int r = live_lt - before_c;
+          list[sb + r] = s;
+          moved_here += (c + r != s) ? 1 : 0;
+        }
+        ++live_lt;
+      }
+    }
+    moved = block_sum(moved_here, scr);
+  }
+  if (tid == 0) {
+    cut_g[seg] = c;
+    moved_g[seg] = moved;
+    span_g[seg] = new_span;
+    meta[2 * seg] = n_suffix;
+    meta[2 * seg + 1] = span;                       // span before packing
+  }
+}
+
+// Rows and tags of the suffix entries whose slot changes: src -> scratch (SCATTER = false) or
+// scratch -> c + rank (SCATTER = true, which also empties the vacated slots).
+template <bool SCATTER>
+__global__ __launch_bounds__(kCopyThreads) void suffix_copy_kernel(
+    uint8_t* __restrict__ k, uint8_t* __restrict__ v, int cap, int row_bytes,
+    int32_t* __restrict__ uid_g, uint8_t* __restrict__ mod_g, int32_t* __restrict__ pos_g,
+    const int32_t* __restrict__ list, const int32_t* __restrict__ meta,
+    const int32_t* __restrict__ cut_g, uint8_t* __restrict__ scr_rows,
+    int32_t* __restrict__ scr_tags) {
+  __shared__ int32_t src_row[kRowsPerBlock];
+  const int seg = blockIdx.y;
+  const int c = cut_g[seg];
+  if (c < 0) return;
+  const int n_suffix = meta[2 * seg];
+  const int old_span = meta[2 * seg + 1];
+  const size_t sb = static_cast<size_t>(seg) * cap;
+  const int r0 = blockIdx.x * kRowsPerBlock;
+  const int tid = threadIdx.x;
+  if (SCATTER) {
+    // vacated slots [c + n_suffix, old_span): this block's share
+    for (int i = tid; i < kRowsPerBlock; i += kCopyThreads) {
+      const int s = c + n_suffix + r0 + i;
+      if (s < old_span) {
+        uid_g[sb + s] = -1;
+        pos_g[sb + s] = -1;
+      }
+    }
+  }
+  if (r0 >= n_suffix) return;
+  const int nr = min(kRowsPerBlock, n_suffix - r0);
+  if (tid < nr) {
+    const int r = r0 + tid;
+    const int s = list[sb + r];
+    src_row[tid] = s != c + r ? s : -1;            // -1: already in place
+    if (s != c + r) {
+      int32_t* t = scr_tags + 3 * (sb + r);
+      if (SCATTER) {
+        uid_g[sb + c + r] = t[0];
+        mod_g[sb + c + r] = static_cast<uint8_t>(t[1]);
+        pos_g[sb + c + r] = t[2];
+      } else {
+        t[0] = uid_g[sb + s];
+        t[1] = mod_g[sb + s];
+        t[2] = pos_g[sb + s];
+      }
+    }
+  }
+  __syncthreads();
+  const int vecs = row_bytes / 16;
+  for (int f = tid; f < nr * vecs; f += kCopyThreads) {
+    const int i = f / vecs, e = f % vecs;
+    const int s = src_row[i];
+    if (s < 0) continue;
+    const int r = r0 + i;
+    const size_t scr_off = ((sb + r) * 2) * static_cast<size_t>(row_bytes);
+    const u32x4* ks = reinterpret_cast<const u32x4*>(
+        SCATTER ? scr_rows + scr_off : k + (sb + s) * static_cast<size_t>(row_bytes));
+    const u32x4* vs = reinterpret_cast<const u32x4*>(
+        SCATTER ? scr_rows + scr_off + row_bytes : v + (sb + s) * static_cast<size_t>(row_bytes));
+    u32x4* kd = reinterpret_cast<u32x4*>(
+        SCATTER ? k + (sb + c + r) * static_cast<size_t>(row_bytes) : scr_rows + scr_off);
+    u32x4* vd = reinterpret_cast<u32x4*>(
+        SCATTER ? v + (sb + c + r) * static_cast<size_t>(row_bytes)
+                : scr_rows + scr_off + row_bytes);
+    kd[e] = __builtin_nontemporal_load(ks + e);
+    vd[e] = __builtin_nontemporal_load(vs + e);
+  }
+}
+
+__global__ __launch_bounds__(kNatThreads) void place_plan_kernel(
+    const int32_t* __restrict__ uid_g, int cap, int chunk_len, int32_t* __restrict__ slot_g,
+    int32_t* __restrict__ span_g, int32_t* __restrict__ status) {
+  __shared__ uint32_t bits[kMaxNatWords];
+  __shared__ int32_t scr[kNatThreads / kWave + 1];
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  const size_t sb = static_cast<size_t>(seg) * cap;
+  const int nwords = (cap + 31) / 32;
+  load_bitmap(uid_g + sb, cap, bits, nwords);
+  const int wpt = (nwords + kNatThreads - 1) / kNatThreads;
+  const int w0 = min(tid * wpt, nwords), w1 = min(w0 + wpt, nwords);
+  int my_last = -1;
+  for (int w = w0; w < w1; ++w)
+    if (bits[w]) my_last = 32 * w + 31 - __clz(bits[w]);
+  int last_all;
+  int last = block_exclusive_max(my_last, -1, scr, &last_all);
+  // first slot s of this range where the empty run ending at s reaches chunk_len
+  int cand = -1;
+  for (int s = 32 * w0; s < 32 * w1 && s < cap; ++s) {
+    if (bit(bits, s)) {
+      last = s;
+    } else if (s - last >= chunk_len) {
+      cand = s - chunk_len + 1;
+      break;
+    }
+  }
+  // lowest candidate over all threads = -(largest of the negated candidates)
+  int best;
+  (void)block_exclusive_max(cand >= 0 ? -cand : -INT32_MAX, -INT32_MAX, scr, &best);
+  if (tid == 0) {
+    if (best == -INT32_MAX) {
+      slot_g[seg] = -1;
+      set_status(status, OMNITIDE_E_CAPACITY);
+    } else {
+      const int s = -best;
+      slot_g[seg] = s;
+      span_g[seg] = max(last_all + 1, s + chunk_len);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kCopyThreads) void chunk_write_kernel(
+    uint8_t* __restrict__ k, uint8_t* __restrict__ v, int cap, int row_bytes,
+    int32_t* __restrict__ uid_g, uint8_t* __restrict__ mod_g, int32_t* __restrict__ pos_g,
+    const uint8_t* __restrict__ k_chunk, const uint8_t* __restrict__ v_chunk,
+    const uint8_t* __restrict__ chunk_mod, const int32_t* __restrict__ chunk_unit,
+    int chunk_len, const int32_t* __restrict__ slot_g, const int32_t* __restrict__ kept_g,
+    const int32_t* __restrict__ n_kept_units_g) {
+  const int seg = blockIdx.y;
+  const int s = slot_g[seg];
+  if (s < 0) return;
+  const size_t sb = static_cast<size_t>(seg) * cap;
+  const size_t cb = static_cast<size_t>(seg) * chunk_len;
+  const int r0 = blockIdx.x * kRowsPerBlock;
+  const int nr = min(kRowsPerBlock, chunk_len - r0);
+  const int tid = threadIdx.x;
+  if (nr <= 0) return;
+  if (tid < nr) {
+    const int i = r0 + tid;
+    uid_g[sb + s + i] = n_kept_units_g[seg] + chunk_unit[i];
+    mod_g[sb + s + i] = chunk_mod[i];
+    pos_g[sb + s + i] = kept_g[seg] + i;
+  }
+  const int vecs = row_bytes / 16;
+  for (int f = tid; f < nr * vecs; f += kCopyThreads) {
+    const int i = r0 + f / vecs, e = f % vecs;
+    const u32x4* ks = reinterpret_cast<const u32x4*>(k_chunk + (cb + i) * row_bytes);
+    const u32x4* vs = reinterpret_cast<const u32x4*>(v_chunk + (cb + i) * row_bytes);
+    reinterpret_cast<u32x4*>(k + (sb + s + i) * static_cast<size_t>(row_bytes))[e] = ks[e];
+    reinterpret_cast<u32x4*>(v + (sb + s + i) * static_cast<size_t>(row_bytes))[e] = vs[e];
+  }
+}
+
+}  // namespace
+
+int native_max_cap() { return kMaxNatWords * 32; }
+
+size_t evict_workspace_bytes(int n_seg, int n_units) {
+  return static_cast<size_t>(n_seg) * n_units * sizeof(UnitRec);
+}
+
+hipError_t launch_evict(const EvictArgs& a, hipStream_t stream) {
+  UnitRec* table = static_cast<UnitRec*>(a.workspace);
+  hipLaunchKernelGGL(evict_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream, a.keep,
+                     a.keep_len, a.unit_len, a.n_units, table, a.unit_remap, a.kept_tokens,
+                     a.n_kept_units, a.span);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 grid((a.cap + kCopyThreads - 1) / kCopyThreads, a.n_seg);
+  hipLaunchKernelGGL(evict_apply_kernel, grid, dim3(kCopyThreads), 0, stream, a.unit_id, a.pos,
+                     a.cap, a.n_units, table, a.unit_len, a.span, a.d_status);
+  return hipGetLastError();
+}
+
+size_t suffix_workspace_bytes(int n_seg, int cap, int row_bytes) {
+  const size_t slots = static_cast<size_t>(n_seg) * cap;
+  const size_t list = ((slots * 4 + 255) / 256) * 256;
+  const size_t meta = 256 + ((static_cast<size_t>(n_seg) * 8 + 255) / 256) * 256;
+  const size_t tags = ((slots * 12 + 255) / 256) * 256;
+  return list + meta + tags + slots * 2 * static_cast<size_t>(row_bytes);
+}
+
+hipError_t launch_pack_suffix(const SuffixArgs& a, hipStream_t stream) {
+  const size_t slots = static_cast<size_t>(a.n_seg) * a.cap;
+  uint8_t* w = static_cast<uint8_t*>(a.workspace);
+  int32_t* list = reinterpret_cast<int32_t*>(w);
+  w += ((slots * 4 + 255) / 256) * 256;
+  int32_t* meta = reinterpret_cast<int32_t*>(w);
+  w += 256 + ((static_cast<size_t>(a.n_seg) * 8 + 255) / 256) * 256;
+  int32_t* tags = reinterpret_cast<int32_t*>(w);
+  w += ((slots * 12 + 255) / 256) * 256;
+  uint8_t* rows = w;
+  hipLaunchKernelGGL(suffix_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream,
+                     a.unit_id, a.cap, a.page_size, a.min_pages, list, meta, a.span, a.cut,
+                     a.moved);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 grid((a.cap + kRowsPerBlock - 1) / kRowsPerBlock, a.n_seg);
+  uint8_t* k = static_cast<uint8_t*>(a.k);
+  uint8_t* v = static_cast<uint8_t*>(a.v);
+  hipLaunchKernelGGL(suffix_copy_kernel<false>, grid, dim3(kCopyThreads), 0, stream, k, v,
+                     a.cap, a.row_bytes, a.unit_id, a.modality, a.pos, list, meta, a.cut, rows,
+                     tags);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(suffix_copy_kernel<true>, grid, dim3(kCopyThreads), 0, stream, k, v,
+                     a.cap, a.row_bytes, a.unit_id, a.modality, a.pos, list, meta, a.cut, rows,
+                     tags);
+  return hipGetLastError();
+}
+
+hipError_t launch_place_chunk(const PlaceArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(place_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream, a.unit_id,
+                     a.cap, a.chunk_len, a.chunk_slot, a.span, a.d_status);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 grid((a.chunk_len + kRowsPerBlock - 1) / kRowsPerBlock, a.n_seg);
+  hipLaunchKernelGGL(chunk_write_kernel, grid, dim3(kCopyThreads), 0, stream,
+                     static_cast<uint8_t*>(a.k), static_cast<uint8_t*>(a.v), a.cap, a.row_bytes,
+                     a.unit_id, a.modality, a.pos, static_cast<const uint8_t*>(a.k_chunk),
+                     static_cast<const uint8_t*>(a.v_chunk), a.chunk_modality, a.chunk_unit,
+                     a.chunk_len, a.chunk_slot, a.kept_tokens, a.n_kept_units);
+  return hipGetLastError();
+}
+
+}  // namespace omnitide

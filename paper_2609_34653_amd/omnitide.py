@@ -29,7 +29,9 @@ ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
            "omnitide_compact_kv_rope", "omnitide_plan_spans", "omnitide_compact_kv_spans",
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
-           "omnitide_attn_workspace_bytes", "omnitide_span_attn",
+           "omnitide_attn_workspace_bytes", "omnitide_span_attn", "omnitide_evict_native",
+           "omnitide_evict_native_workspace_bytes", "omnitide_pack_suffix",
+           "omnitide_pack_suffix_workspace_bytes", "omnitide_place_chunk",
            "omnitide_span_attn_workspace_bytes", "omnitide_decode_attn",
            "omnitide_decode_workspace_bytes", "omnitide_status_string", "omnitide_version")
 
@@ -77,6 +79,16 @@ def lib() -> ctypes.CDLL:
                                          ctypes.c_float, _P, _P, _SZ, _P, _P]
         L.omnitide_span_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_span_attn_workspace_bytes.restype = _SZ
+        L.omnitide_evict_native.argtypes = [_I, _I, _P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P,
+                                            _SZ, _P, _P]
+        L.omnitide_evict_native_workspace_bytes.argtypes = [_I, _I]
+        L.omnitide_evict_native_workspace_bytes.restype = _SZ
+        L.omnitide_pack_suffix.argtypes = [_P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P,
+                                           _P, _P, _P, _SZ, _P]
+        L.omnitide_pack_suffix_workspace_bytes.argtypes = [_I, _I, _I, _I, _I]
+        L.omnitide_pack_suffix_workspace_bytes.restype = _SZ
+        L.omnitide_place_chunk.argtypes = [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P,
+                                           _P, _I, _P, _P, _P, _P, _P, _P]
         L.omnitide_decode_attn.argtypes = L.omnitide_chunk_attn.argtypes
         L.omnitide_decode_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_decode_workspace_bytes.restype = _SZ
@@ -86,6 +98,7 @@ def lib() -> ctypes.CDLL:
         for name in ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
                      "omnitide_compact_kv_rope", "omnitide_compact_kv_spans",
                      "omnitide_plan_spans", "omnitide_chunk_attn", "omnitide_span_attn",
+                     "omnitide_evict_native", "omnitide_pack_suffix", "omnitide_place_chunk",
                      "omnitide_decode_attn"):
             getattr(L, name).restype = _I
         _lib = L
@@ -365,6 +378,89 @@ def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_
                                     _ptr(q_pos0), n_seg, cap, L, Hq, Hkv, d, float(scale),
                                     _ptr(out), _ptr(workspace), workspace.numel(),
                                     _ptr(d_status), _stream(stream)), "omnitide_span_attn")
+
+
+def omnitide_evict_native_workspace_bytes(n_seg, n_units) -> int:
+    return int(lib().omnitide_evict_native_workspace_bytes(n_seg, n_units))
+
+
+def omnitide_evict_native(unit_id, pos, n_seg, n_units, unit_len, unit_remap, kept_tokens,
+                          n_kept_units, span, workspace, keep=None, keep_len=None,
+                          d_status=None, stream=None):
+    """Logical eviction in place of the tags unit_id / pos ([n_seg * cap] int32)."""
+    cap = unit_id.numel() // n_seg
+    nu = n_seg * n_units
+    _need(unit_id, "unit_id", I32, n_seg * cap)
+    _need(pos, "pos", I32, n_seg * cap)
+    if keep_len is not None:
+        _need(keep_len, "keep_len", I32, nu)
+    else:
+        _need(keep, "keep", U8, nu)
+    for t, nm in ((unit_len, "unit_len"), (unit_remap, "unit_remap")):
+        _need(t, nm, I32, nu)
+    for t, nm in ((kept_tokens, "kept_tokens"), (n_kept_units, "n_kept_units"), (span, "span")):
+        _need(t, nm, I32, n_seg)
+    _need(workspace, "workspace", U8)
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_evict_native(n_seg, cap, _ptr(unit_id), _ptr(pos),
+                                       _ptr(keep) if keep_len is None else None, _ptr(keep_len),
+                                       _ptr(unit_len), n_units, _ptr(unit_remap),
+                                       _ptr(kept_tokens), _ptr(n_kept_units), _ptr(span),
+                                       _ptr(workspace), workspace.numel(), _ptr(d_status),
+                                       _stream(stream)), "omnitide_evict_native")
+
+
+def omnitide_pack_suffix_workspace_bytes(dtype, n_seg, cap, n_kv_heads, head_dim) -> int:
+    return int(lib().omnitide_pack_suffix_workspace_bytes(dtype, n_seg, cap, n_kv_heads,
+                                                          head_dim))
+
+
+def omnitide_pack_suffix(k, v, page_size, min_pages, unit_id, modality, pos, span, cut, moved,
+                         workspace, stream=None):
+    """Ordered-suffix packing in place of pools k/v [n_seg, cap, H, d] and their tags."""
+    n_seg, cap, H, d = _pool_dims(k, "k")
+    _need(k, "k", (torch.bfloat16, torch.float32))
+    _need(v, "v", (k.dtype,), k.numel())
+    _need(unit_id, "unit_id", I32, n_seg * cap)
+    _need(modality, "modality", U8, n_seg * cap)
+    _need(pos, "pos", I32, n_seg * cap)
+    for t, nm in ((span, "span"), (cut, "cut"), (moved, "moved")):
+        _need(t, nm, I32, n_seg)
+    _need(workspace, "workspace", U8)
+    _check(lib().omnitide_pack_suffix(_ptr(k), _ptr(v), _kv_dtype(k), n_seg, cap, H, d,
+                                      page_size, min_pages, _ptr(unit_id), _ptr(modality),
+                                      _ptr(pos), _ptr(span), _ptr(cut), _ptr(moved),
+                                      _ptr(workspace), workspace.numel(), _stream(stream)),
+           "omnitide_pack_suffix")
+
+
+def omnitide_place_chunk(k, v, unit_id, modality, pos, k_chunk, v_chunk, chunk_modality,
+                         chunk_unit, kept_tokens, n_kept_units, chunk_slot, span,
+                         d_status=None, stream=None):
+    """The chunk into the lowest run of empty slots of pools k/v [n_seg, cap, H, d]."""
+    n_seg, cap, H, d = _pool_dims(k, "k")
+    L = chunk_modality.numel()
+    _need(k, "k", (torch.bfloat16, torch.float32))
+    _need(v, "v", (k.dtype,), k.numel())
+    _need(unit_id, "unit_id", I32, n_seg * cap)
+    _need(modality, "modality", U8, n_seg * cap)
+    _need(pos, "pos", I32, n_seg * cap)
+    _need(k_chunk, "k_chunk", (k.dtype,), n_seg * L * H * d)
+    _need(v_chunk, "v_chunk", (k.dtype,), n_seg * L * H * d)
+    _need(chunk_modality, "chunk_modality", U8, L)
+    _need(chunk_unit, "chunk_unit", I32, L)
+    for t, nm in ((kept_tokens, "kept_tokens"), (n_kept_units, "n_kept_units"),
+                  (chunk_slot, "chunk_slot"), (span, "span")):
+        _need(t, nm, I32, n_seg)
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_place_chunk(_ptr(k), _ptr(v), _kv_dtype(k), n_seg, cap, H, d,
+                                      _ptr(unit_id), _ptr(modality), _ptr(pos), _ptr(k_chunk),
+                                      _ptr(v_chunk), _ptr(chunk_modality), _ptr(chunk_unit), L,
+                                      _ptr(kept_tokens), _ptr(n_kept_units), _ptr(chunk_slot),
+                                      _ptr(span), _ptr(d_status), _stream(stream)),
+           "omnitide_place_chunk")
 
 
 def omnitide_decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim) -> int:

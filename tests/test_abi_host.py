@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 15
+    assert len(names) == 20
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -256,6 +256,69 @@ def test_span_attention_validation(L):
     assert span_attn(L, out=P(fake(3).value + 256)) == ot.E_ALIAS   # output over key_pos
     # chunk_attn keeps its own (smaller) workspace and needs no positions
     assert ot.omnitide_span_attn_workspace_bytes(1, 81920, 665, 30, 8, 128) == 0
+
+
+def evict(L, **kw):
+    a = dict(n_seg=1, cap=1000, uid=fake(0), pos=fake(1), keep=fake(2), kl=None, ln=fake(3), U=10,
+             rm=fake(4), kt=fake(5), nk=fake(6), span=fake(7), ws=fake(8), wsb=1 << 20,
+             st=fake(9))
+    a.update(kw)
+    return L.omnitide_evict_native(a["n_seg"], a["cap"], a["uid"], a["pos"], a["keep"], a["kl"],
+                                   a["ln"], a["U"], a["rm"], a["kt"], a["nk"], a["span"],
+                                   a["ws"], a["wsb"], a["st"], None)
+
+
+def test_evict_native_validation(L):
+    assert evict(L, keep=None) == ot.E_NULL               # neither keep nor keep_len
+    assert evict(L, span=None) == ot.E_NULL
+    assert evict(L, cap=131073) == ot.E_SHAPE
+    assert evict(L, U=8193) == ot.E_SHAPE
+    assert evict(L, ws=None) == ot.E_WORKSPACE
+    assert evict(L, wsb=16) == ot.E_WORKSPACE
+    assert evict(L, rm=fake(3)) == ot.E_ALIAS              # output over unit_len
+    assert evict(L, pos=P(fake(0).value + 8)) == ot.E_ALIAS   # in-place tags overlap
+    assert ot.omnitide_evict_native_workspace_bytes(1, 10) == 160
+
+
+def pack(L, **kw):
+    a = dict(k=fake(0), v=fake(1), dtype=0, n_seg=1, cap=1000, H=8, d=128, P=256, T=1,
+             uid=fake(2), mod=fake(3), pos=fake(4), span=fake(5), cut=fake(6), mv=fake(7),
+             ws=fake(8), wsb=1 << 30)
+    a.update(kw)
+    return L.omnitide_pack_suffix(a["k"], a["v"], a["dtype"], a["n_seg"], a["cap"], a["H"],
+                                  a["d"], a["P"], a["T"], a["uid"], a["mod"], a["pos"],
+                                  a["span"], a["cut"], a["mv"], a["ws"], a["wsb"], None)
+
+
+def test_pack_suffix_validation(L):
+    assert pack(L, cut=None) == ot.E_NULL
+    assert pack(L, dtype=2) == ot.E_DTYPE
+    assert pack(L, T=0) == ot.E_SHAPE
+    assert pack(L, P=0) == ot.E_SHAPE
+    assert pack(L, cap=131073) == ot.E_SHAPE
+    assert pack(L, ws=None) == ot.E_WORKSPACE
+    need = ot.omnitide_pack_suffix_workspace_bytes(0, 1, 1000, 8, 128)
+    assert need >= 1000 * 2 * 2048 and pack(L, wsb=need - 1) == ot.E_WORKSPACE
+    assert pack(L, v=P(fake(0).value + 4096)) == ot.E_ALIAS
+
+
+def place(L, **kw):
+    a = dict(k=fake(0), v=fake(1), dtype=0, n_seg=1, cap=1000, H=8, d=128, uid=fake(2),
+             mod=fake(3), pos=fake(4), kc=fake(5), vc=fake(6), cm=fake(7), cu=fake(8), Lc=16,
+             kt=fake(9), nk=fake(10), slot=fake(11), span=fake(12), st=fake(13))
+    a.update(kw)
+    return L.omnitide_place_chunk(a["k"], a["v"], a["dtype"], a["n_seg"], a["cap"], a["H"],
+                                  a["d"], a["uid"], a["mod"], a["pos"], a["kc"], a["vc"],
+                                  a["cm"], a["cu"], a["Lc"], a["kt"], a["nk"], a["slot"],
+                                  a["span"], a["st"], None)
+
+
+def test_place_chunk_validation(L):
+    assert place(L, kc=None) == ot.E_NULL
+    assert place(L, dtype=5) == ot.E_DTYPE
+    assert place(L, Lc=0) == ot.E_SHAPE
+    assert place(L, Lc=1001) == ot.E_CAPACITY
+    assert place(L, slot=fake(9)) == ot.E_ALIAS            # output over kept_tokens
 
 
 def decode(L, **kw):

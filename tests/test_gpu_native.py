@@ -186,3 +186,184 @@ def test_span_attention_capacity_error():
     assert np.all(np.isnan(out))
     out = run_span_attn(q, k[None], v[None], kp[None], [39], [qp], 0.1, expect_status=-5)
     assert np.all(np.isnan(out))
+
+
+# ------------------------------------------------------------------------------ layout kernels
+
+def i32(a):
+    return dev(np.asarray(a, np.int32))
+
+
+def native_state(cfg_name, extra=None, plan="whole", seed_keep=None):
+    """GPU pool of capacity n_slots + L (+extra) with the stream's tags, scored on the GPU, and
+    the retention plan (whole-unit select, or arbitrary kept prefixes) on the host."""
+    from paper_2609_34653_amd import omnitide as ot
+    cfg = sg.CONFIG_BY_NAME[cfg_name]
+    stream = sg.make_stream(cfg)
+    lay, seg = stream.layout, stream.segment(0)
+    L = lay.chunk_len
+    cap = lay.n_slots + L + (extra or 0)
+    pad = cap - lay.n_slots
+    uid = np.concatenate([lay.unit_id, np.full(pad, -1)]).astype(np.int32)
+    pos = np.concatenate([lay.pos, np.full(pad, -1)]).astype(np.int32)
+    mod = np.concatenate([lay.modality, np.full(pad, 1)]).astype(np.uint8)
+    kdt = seg.k_hist.dtype
+    k = torch.cat([seg.k_hist, torch.zeros(pad, *seg.k_hist.shape[1:], dtype=kdt)])
+    v = torch.cat([seg.v_hist, torch.zeros(pad, *seg.v_hist.shape[1:], dtype=kdt)])
+    k[lay.n_slots:] = 3.0                               # recognisable bytes in the free tail
+    k_np, v_np = storage_np(k), storage_np(v)
+    sc = oracle.score_units(storage_np(seg.k_hist), cfg.dtype, lay.unit_id, lay.modality,
+                            cfg.weights, lay.n_units)
+    if plan == "whole":
+        _, keep, _ = oracle.select_units(sc["wsum"], sc["len"], sc["first"], sc["last"],
+                                         sc["flags"], cfg.budget, cfg.recent)
+        keep_len = np.where(keep != 0, sc["len"], 0)
+    else:
+        rng = np.random.default_rng(seed_keep)
+        keep_len = rng.integers(-2, sc["len"] + 3)
+        keep_len[rng.random(lay.n_units) < 0.3] = 0
+    g = dict(k=k.cuda()[None].contiguous(), v=v.cuda()[None].contiguous(), uid=i32(uid),
+             pos=i32(pos), mod=dev(mod), len=i32(sc["len"]), keep_len=i32(keep_len),
+             keep=dev((keep_len > 0).astype(np.uint8)),
+             remap=i32(np.zeros(lay.n_units)), kept=i32([0]), nku=i32([0]), span=i32([0]),
+             ws=torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, lay.n_units),
+                            dtype=torch.uint8, device="cuda"),
+             st=i32([0]))
+    h = dict(uid=uid, pos=pos, mod=mod, k=k_np, v=v_np, keep_len=keep_len, sc=sc)
+    return cfg, lay, seg, g, h
+
+
+def gpu_evict(lay, g, use_len=True):
+    from paper_2609_34653_amd import omnitide as ot
+    ot.omnitide_evict_native(g["uid"], g["pos"], 1, lay.n_units, g["len"], g["remap"], g["kept"],
+                             g["nku"], g["span"], g["ws"],
+                             keep=None if use_len else g["keep"],
+                             keep_len=g["keep_len"] if use_len else None, d_status=g["st"])
+    torch.cuda.synchronize()
+
+
+def check_evict(lay, g, h):
+    kl = np.minimum(np.maximum(h["keep_len"], 0), h["sc"]["len"])
+    ev = oracle.evict_logical(h["uid"], h["pos"], kl, lay.n_units)
+    assert int(host(g["st"])[0]) == 0
+    assert np.array_equal(host(g["uid"]), ev["unit_id"])
+    assert np.array_equal(host(g["pos"]), ev["pos"])
+    assert np.array_equal(host(g["remap"]), ev["unit_remap"])
+    assert int(host(g["kept"])[0]) == ev["kept"]
+    assert int(host(g["nku"])[0]) == ev["n_kept_units"]
+    assert int(host(g["span"])[0]) == oracle.span_of(ev["unit_id"])
+    return ev
+
+
+@pytest.mark.parametrize("cfg_name,plan", [("tiny_1p6k_f32", "whole"),
+                                           ("single_layer_8k", "prefix"),
+                                           ("history_80k", "whole"), ("history_80k", "prefix")])
+def test_evict_native_parity(cfg_name, plan):
+    cfg, lay, seg, g, h = native_state(cfg_name, plan=plan, seed_keep=3)
+    gpu_evict(lay, g, use_len=plan == "prefix")
+    check_evict(lay, g, h)
+    # K/V are not touched by logical eviction
+    assert np.array_equal(storage_np(g["k"][0]), h["k"])
+
+
+def test_evict_native_tag_error():
+    cfg, lay, seg, g, h = native_state("single_layer_8k")
+    bad = h["pos"].copy()
+    s = int(np.nonzero(h["uid"] == 3)[0][0])
+    bad[s] = bad[s] + 10_000                             # outside unit 3's positions
+    g["pos"] = i32(bad)
+    gpu_evict(lay, g)
+    assert int(host(g["st"])[0]) == -17
+
+
+@pytest.mark.parametrize("cfg_name,P,T", [("single_layer_8k", 64, 1), ("single_layer_8k", 64, 8),
+                                          ("history_80k", 256, 1), ("history_80k", 256, 40),
+                                          ("history_80k", 256, 10_000)])
+def test_pack_suffix_parity(cfg_name, P, T):
+    from paper_2609_34653_amd import omnitide as ot
+    cfg, lay, seg, g, h = native_state(cfg_name, plan="whole")
+    gpu_evict(lay, g)
+    ev = check_evict(lay, g, h)
+    cap = len(h["uid"])
+    H, d = seg.k_hist.shape[1], seg.k_hist.shape[2]
+    nb = ot.omnitide_pack_suffix_workspace_bytes(0 if cfg.dtype == "bf16" else 1, 1, cap, H, d)
+    ws = torch.zeros(nb, dtype=torch.uint8, device="cuda")
+    cut, moved = i32([7]), i32([7])
+    ot.omnitide_pack_suffix(g["k"], g["v"], P, T, g["uid"], g["mod"], g["pos"], g["span"], cut,
+                            moved, ws)
+    torch.cuda.synchronize()
+    c, ns = oracle.plan_suffix(ev["unit_id"] >= 0, P, T)
+    assert int(host(cut)[0]) == c
+    assert int(host(g["span"])[0]) == ns
+    if c < 0:
+        assert int(host(moved)[0]) == 0
+        assert np.array_equal(host(g["uid"]), ev["unit_id"])
+        return
+    pk = oracle.pack_suffix(h["k"], h["v"], ev["unit_id"], h["mod"], ev["pos"], c)
+    assert int(host(moved)[0]) == pk["moved"] and pk["moved"] > 0
+    assert np.array_equal(host(g["uid"]), pk["unit_id"])
+    assert np.array_equal(host(g["pos"]), pk["pos"])
+    assert np.array_equal(host(g["mod"]), pk["modality"])
+    assert np.array_equal(storage_np(g["k"][0]), pk["k"])
+    assert np.array_equal(storage_np(g["v"][0]), pk["v"])
+
+
+def test_place_chunk_parity_and_native_attention():
+    """80K history: eviction, the chunk into the lowest empty run, attention over the span."""
+    from paper_2609_34653_amd import omnitide as ot
+    cfg, lay, seg, g, h = native_state("history_80k")
+    gpu_evict(lay, g)
+    ev = check_evict(lay, g, h)
+    L = lay.chunk_len
+    slot, = [i32([-9])]
+    ot.omnitide_place_chunk(g["k"], g["v"], g["uid"], g["mod"], g["pos"],
+                            seg.k_chunk.cuda()[None].contiguous(),
+                            seg.v_chunk.cuda()[None].contiguous(), dev(lay.chunk_modality),
+                            dev(lay.chunk_unit), g["kept"], g["nku"], slot, g["span"],
+                            d_status=g["st"])
+    torch.cuda.synchronize()
+    assert int(host(g["st"])[0]) == 0
+    cap = len(h["uid"])
+    s0 = oracle.place_chunk(ev["unit_id"], L, cap)
+    assert int(host(slot)[0]) == s0
+    uid = ev["unit_id"].copy()
+    pos = ev["pos"].copy()
+    uid[s0:s0 + L] = ev["n_kept_units"] + lay.chunk_unit
+    pos[s0:s0 + L] = ev["kept"] + np.arange(L)
+    assert np.array_equal(host(g["uid"]), uid) and np.array_equal(host(g["pos"]), pos)
+    assert np.array_equal(host(g["mod"])[s0:s0 + L], lay.chunk_modality)
+    kk = h["k"].copy()
+    kk[s0:s0 + L] = storage_np(seg.k_chunk)
+    assert np.array_equal(storage_np(g["k"][0]), kk)
+    span = int(host(g["span"])[0])
+    assert span == oracle.span_of(uid)
+    # attention over the span with the device-built layout
+    nb = ot.omnitide_span_attn_workspace_bytes(1, cap, L, cfg.n_q_heads, cfg.n_kv_heads,
+                                               cfg.head_dim)
+    ws = torch.zeros(nb, dtype=torch.uint8, device="cuda")
+    out = torch.zeros(1, L, cfg.n_q_heads, cfg.head_dim, device="cuda")
+    ot.omnitide_span_attn(seg.q.cuda()[None].contiguous(), g["k"], g["v"], g["pos"], g["span"],
+                          g["kept"], cfg.scale, out, ws, g["st"])
+    torch.cuda.synchronize()
+    assert int(host(g["st"])[0]) == 0
+    rows = sample_rows(L, np.random.default_rng(10), 8)
+    kt, vt = torch.from_numpy(kk.view(np.int16)).view(torch.bfloat16), g["v"][0].cpu()
+    check(host(out)[0], seg.q, kt, vt, pos, span, ev["kept"], cfg.scale, rows=rows)
+
+
+def test_place_chunk_capacity_error():
+    from paper_2609_34653_amd import omnitide as ot
+    cfg, lay, seg, g, h = native_state("single_layer_8k")
+    # nothing evicted and no free tail: the pool is full
+    uid = np.where(h["uid"] >= 0, h["uid"], 0).astype(np.int32)
+    g["uid"] = i32(uid)
+    slot = i32([5])
+    span = i32([5])
+    ot.omnitide_place_chunk(g["k"], g["v"], g["uid"], g["mod"], g["pos"],
+                            seg.k_chunk.cuda()[None].contiguous(),
+                            seg.v_chunk.cuda()[None].contiguous(), dev(lay.chunk_modality),
+                            dev(lay.chunk_unit), g["kept"], g["nku"], slot, span,
+                            d_status=g["st"])
+    torch.cuda.synchronize()
+    assert int(host(g["st"])[0]) == -5 and int(host(slot)[0]) == -1
+    assert np.array_equal(host(g["uid"]), uid)
