@@ -300,6 +300,9 @@ def main():
                                                   4),
                                 "kept_tokens": kept_sp, "in_step": False}
 
+    kernels["layouts"] = layout_ablation(ot, st, copies[0], lay, cfg, L, H, Hq, d, dev,
+                                         args.steps, n_ctx, not args.no_graph)
+
     value = flops / (ms_per_step * 1e-3) / 1e12
     result = {
         "metric": "chunk-attn TFLOP/s + score/compact GB/s (% roofline), 80K-token history, 1 GPU",
@@ -322,6 +325,115 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, stream, seg, flops)
     print(json.dumps(result), flush=True)
+
+
+def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_graph=True):
+    """The same retention plan (the step's whole-unit selection) under three physical layouts:
+    native (logical eviction, the chunk in the lowest empty run, attention over the holey span),
+    ordered-suffix packing (eviction, then the suffix whose packing saves >= 1 page of 256
+    slots, then the chunk) and eager compaction (the step's own compact + attend).  Each
+    maintenance call is timed from its layout's state before it: `reps` repetitions of
+    [restore the tags from a snapshot, call] in one captured graph, minus the same graph without
+    the call; attention is `reps` calls over the final layout."""
+    cap = lay.n_slots + L
+    pad = cap - lay.n_slots
+    i32 = dict(dtype=torch.int32, device=dev)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    tags0 = (t(np.concatenate([lay.unit_id, np.full(pad, -1)]).astype(np.int32)),
+             t(np.concatenate([lay.pos, np.full(pad, -1)]).astype(np.int32)),
+             t(np.concatenate([lay.modality, np.full(pad, 1)]).astype(np.uint8)))
+    k = torch.cat([c["k"][0], torch.zeros(pad, H, d, dtype=c["k"].dtype, device=dev)])[None]
+    v = torch.cat([c["v"][0], torch.zeros(pad, H, d, dtype=c["v"].dtype, device=dev)])[None]
+    k, v = k.contiguous(), v.contiguous()
+    uid, pos, mod = (x.clone() for x in tags0)
+    remap = torch.zeros(lay.n_units, **i32)
+    kept, nku, span, slot, cut, moved = (torch.zeros(1, **i32) for _ in range(6))
+    ws_e = torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, lay.n_units),
+                       dtype=torch.uint8, device=dev)
+    ws_p = torch.zeros(ot.omnitide_pack_suffix_workspace_bytes(0, 1, cap, H, d),
+                       dtype=torch.uint8, device=dev)
+    ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap, L, Hq, H, d),
+                       dtype=torch.uint8, device=dev)
+    ws_c = torch.zeros(ot.omnitide_place_chunk_workspace_bytes(1, cap), dtype=torch.uint8,
+                       device=dev)
+    out = torch.zeros(1, L, Hq, d, device=dev)
+
+    def restore(snap):
+        for dst, src in zip((uid, pos, mod), snap):
+            dst.copy_(src)
+
+    def evict():
+        ot.omnitide_evict_native(uid, pos, 1, lay.n_units, st.unit_len, remap, kept, nku, span,
+                                 ws_e, keep=st.keep, d_status=st.d_status)
+
+    def pack():
+        ot.omnitide_pack_suffix(k, v, 256, 1, uid, mod, pos, span, cut, moved, ws_p)
+
+    def place():
+        ot.omnitide_place_chunk(k, v, uid, mod, pos, c["kc"], c["vc"], c["cm"], c["cu"], kept,
+                                nku, slot, span, ws_c, d_status=st.d_status)
+
+    def attend():
+        ot.omnitide_span_attn(c["q"], k, v, pos, span, kept, cfg.scale, out, ws_a, st.d_status)
+
+    def staged(snap, call):
+        """(us per call, method): graph of [restore, call] minus graph of [restore]."""
+        span0 = span.clone()
+        def with_call(i):
+            restore(snap)
+            span.copy_(span0)
+            call()
+        def without(i):
+            restore(snap)
+            span.copy_(span0)
+        t1, how = graph_time_us(with_call, reps, dev, use_graph)
+        t0, _ = graph_time_us(without, reps, dev, use_graph)
+        return max(t1 - t0, 0.0), how
+
+    res = {}
+    for name, packed in (("native", False), ("ordered_suffix", True)):
+        restore(tags0)
+        evict()
+        snap_ev = tuple(x.clone() for x in (uid, pos, mod))
+        span_ev = span.clone()
+        if packed:
+            pack()
+        snap_pk = tuple(x.clone() for x in (uid, pos, mod))
+        span_pk = span.clone()
+        place()
+        torch.cuda.synchronize()
+        status = int(st.d_status.item())
+        if status != 0:
+            raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
+        u = uid.cpu().numpy()
+        occ = np.nonzero(u >= 0)[0]
+        sp = int(span.item())
+        r = {"span": sp, "pages_256": -(-sp // 256),
+             "active_pages_256": int(len(np.unique(occ // 256))),
+             "active_tiles_64": int(len(np.unique(occ // 64))),
+             "chunk_slot": int(slot.item())}
+        if packed:
+            r.update(cut=int(cut.item()), moved_rows=int(moved.item()))
+        attn_us, how = graph_time_us(lambda i: attend(), reps, dev, use_graph)
+        final = tuple(x.clone() for x in (uid, pos, mod))
+        span_final = span.clone()
+        span.copy_(torch.zeros_like(span))
+        r["evict_us"], _ = staged(tags0, evict)
+        span.copy_(span_ev)
+        if packed:
+            r["pack_us"], _ = staged(snap_ev, pack)
+        span.copy_(span_pk)
+        r["place_us"], _ = staged(snap_pk, place)
+        restore(final)
+        span.copy_(span_final)
+        r["attend_us"] = attn_us
+        r["timing"] = how
+        r = {a: (round(b, 3) if isinstance(b, float) else b) for a, b in r.items()}
+        res[name] = r
+    res["eager"] = {"span": n_ctx, "pages_256": -(-n_ctx // 256),
+                    "active_pages_256": -(-n_ctx // 256), "active_tiles_64": -(-n_ctx // 64),
+                    "note": "the step's compact + attend (kernels.compact, kernels.attend)"}
+    return res
 
 
 def cpu_baseline(cfg, stream, seg, flops):

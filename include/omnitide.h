@@ -347,7 +347,8 @@ size_t omnitide_pack_suffix_workspace_bytes(int dtype, int n_seg, int cap, int n
  * n_kept_units + chunk_unit[i], modality chunk_modality[i] and position kept_tokens + i
  * (kept_tokens, n_kept_units: omnitide_evict_native's outputs).  Outputs per segment:
  * chunk_slot and span (covering the chunk).  d_status: OMNITIDE_E_CAPACITY when no run fits
- * (chunk_slot = -1, nothing written).
+ * (chunk_slot = -1, nothing written).  workspace: omnitide_place_chunk_workspace_bytes() bytes
+ * (an occupancy bitmap).
  */
 int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_kv_heads,
                          int head_dim, int32_t* unit_id, uint8_t* modality, int32_t* pos,
@@ -355,7 +356,9 @@ int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_
                          const uint8_t* chunk_modality, const int32_t* chunk_unit,
                          int chunk_len, const int32_t* kept_tokens,
                          const int32_t* n_kept_units, int32_t* chunk_slot, int32_t* span,
-                         int32_t* d_status, void* stream);
+                         void* workspace, size_t workspace_bytes, int32_t* d_status,
+                         void* stream);
+size_t omnitide_place_chunk_workspace_bytes(int n_seg, int cap);
 
 /*
  * omnitide_span_attn -- chunk attention over a pool with holes (paper: Fragmentation after

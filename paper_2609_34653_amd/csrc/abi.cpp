@@ -505,7 +505,8 @@ int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_
                          const uint8_t* chunk_modality, const int32_t* chunk_unit,
                          int chunk_len, const int32_t* kept_tokens,
                          const int32_t* n_kept_units, int32_t* chunk_slot, int32_t* span,
-                         int32_t* d_status, void* stream) {
+                         void* workspace, size_t workspace_bytes, int32_t* d_status,
+                         void* stream) {
   if (!all_set({k, v, unit_id, modality, pos, k_chunk, v_chunk, chunk_modality, chunk_unit,
                 kept_tokens, n_kept_units, chunk_slot, span}))
     return OMNITIDE_E_NULL;
@@ -515,12 +516,14 @@ int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_
       !row_ok(n_kv_heads, head_dim) || chunk_len < 1)
     return OMNITIDE_E_SHAPE;
   if (chunk_len > cap) return OMNITIDE_E_CAPACITY;
+  const size_t need = omnitide::place_workspace_bytes(n_seg, cap);
+  if (workspace == nullptr || workspace_bytes < need) return OMNITIDE_E_WORKSPACE;
   const int row = n_kv_heads * head_dim * eb;
   const size_t slots = static_cast<size_t>(n_seg) * cap;
   const size_t crow = static_cast<size_t>(n_seg) * chunk_len;
   if (any_alias({{k, slots * row}, {v, slots * row}, {unit_id, slots * 4}, {modality, slots},
                  {pos, slots * 4}, {chunk_slot, n_seg * 4ull}, {span, n_seg * 4ull},
-                 {d_status, 4}},
+                 {workspace, need}, {d_status, 4}},
                 {{k_chunk, crow * row}, {v_chunk, crow * row},
                  {chunk_modality, static_cast<size_t>(chunk_len)},
                  {chunk_unit, static_cast<size_t>(chunk_len) * 4}, {kept_tokens, n_seg * 4ull},
@@ -544,8 +547,14 @@ int omnitide_place_chunk(void* k, void* v, int dtype, int n_seg, int cap, int n_
   a.n_kept_units = n_kept_units;
   a.chunk_slot = chunk_slot;
   a.span = span;
+  a.workspace = workspace;
   a.d_status = d_status;
   return hip_status(omnitide::launch_place_chunk(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t omnitide_place_chunk_workspace_bytes(int n_seg, int cap) {
+  if (n_seg < 1 || cap < 1) return 0;
+  return omnitide::place_workspace_bytes(n_seg, cap);
 }
 
 size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,

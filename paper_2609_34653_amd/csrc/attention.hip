@@ -483,46 +483,52 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   }
 }
 
-// Active tiles of a span, one workgroup per segment: per 64-slot tile of [0, span) the largest
-// key position and whether it holds an empty slot (or slots past the span), and the ordered
-// list of tiles holding at least one entry.
+// Active tiles of a span.  span_info_kernel: one wave per 64-slot tile of [0, span) (a grid of
+// workgroups) records the tile's largest key position, whether it holds an empty slot (or
+// slots past the span) and whether it holds any entry.  span_list_kernel: one workgroup per
+// segment lists the tiles holding an entry, in order.
 constexpr int kSpanThreads = 1024;
-constexpr int kMaxSpanTiles = 32768;
+constexpr int kInfoThreads = 256;
 
-__global__ __launch_bounds__(kSpanThreads) void span_tiles_kernel(
+__global__ __launch_bounds__(kInfoThreads) void span_info_kernel(
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ span_g, int cap, int L,
-    int max_tiles, int2* __restrict__ tile_info, int32_t* __restrict__ tile_list,
-    int32_t* __restrict__ n_active_g) {
-  __shared__ uint8_t act[kMaxSpanTiles];
+    int max_tiles, int2* __restrict__ tile_info, uint8_t* __restrict__ act_g) {
+  const int seg = blockIdx.y;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t = blockIdx.x * (kInfoThreads / kWave) + threadIdx.x / kWave;
+  const int span = span_g[seg];
+  if (span < L || span > cap) return;            // reported by the attention kernel
+  if (t * kKT >= span) return;
+  const int j = t * kKT + lane;
+  const int p = j < span ? key_pos[static_cast<size_t>(seg) * cap + j] : -1;
+  const uint64_t valid = __ballot(p >= 0);
+  int mx = p;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off, kWave));
+  if (lane == 0) {
+    const size_t tb = static_cast<size_t>(seg) * max_tiles;
+    tile_info[tb + t] = make_int2(mx, valid != ~0ull ? 1 : 0);
+    act_g[tb + t] = valid != 0 ? 1 : 0;
+  }
+}
+
+__global__ __launch_bounds__(kSpanThreads) void span_list_kernel(
+    const uint8_t* __restrict__ act_g, const int32_t* __restrict__ span_g, int cap, int L,
+    int max_tiles, int32_t* __restrict__ tile_list, int32_t* __restrict__ n_active_g) {
   __shared__ int32_t scr[kSpanThreads / kWave + 1];
   const int seg = blockIdx.x;
   const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
   const int span = span_g[seg];
   const size_t tb = static_cast<size_t>(seg) * max_tiles;
-  if (span < L || span > cap) {                  // reported by the attention kernel
+  if (span < L || span > cap) {
     if (tid == 0) n_active_g[seg] = 0;
     return;
   }
   const int n_tiles = (span + kKT - 1) / kKT;
-  for (int t = wave; t < n_tiles; t += kSpanThreads / kWave) {
-    const int j = t * kKT + lane;
-    const int p = j < span ? key_pos[static_cast<size_t>(seg) * cap + j] : -1;
-    const uint64_t valid = __ballot(p >= 0);
-    int mx = p;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off, kWave));
-    if (lane == 0) {
-      tile_info[tb + t] = make_int2(mx, valid != ~0ull ? 1 : 0);
-      act[t] = valid != 0 ? 1 : 0;
-    }
-  }
-  __syncthreads();
   int running = 0;
   for (int base = 0; base < n_tiles; base += kSpanThreads) {
     const int t = base + tid;
-    const int f = t < n_tiles ? act[t] : 0;
+    const int f = t < n_tiles ? act_g[tb + t] : 0;
     int total;
     const int off = block_exclusive_scan(f, scr, &total);
     if (f) tile_list[tb + running + off] = t;
@@ -545,14 +551,20 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
     const int max_tiles = (a.cap + kKT - 1) / kKT;
     uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
                    (n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
+    const size_t nt = static_cast<size_t>(a.n_seg) * max_tiles;
     int2* tile_info = reinterpret_cast<int2*>(tbl);
-    int32_t* tile_list = reinterpret_cast<int32_t*>(
-        tbl + static_cast<size_t>(a.n_seg) * max_tiles * sizeof(int2));
-    int32_t* n_active = tile_list + static_cast<size_t>(a.n_seg) * max_tiles;
-    hipLaunchKernelGGL(span_tiles_kernel, dim3(a.n_seg), dim3(kSpanThreads), 0, stream,
-                       a.key_pos, a.n_ctx, a.cap, a.chunk_len, max_tiles, tile_info, tile_list,
-                       n_active);
+    int32_t* tile_list = reinterpret_cast<int32_t*>(tbl + nt * sizeof(int2));
+    int32_t* n_active = tile_list + nt;
+    uint8_t* act = reinterpret_cast<uint8_t*>(n_active + a.n_seg);
+    const int per_block = kInfoThreads / kWave;
+    hipLaunchKernelGGL(span_info_kernel, dim3((max_tiles + per_block - 1) / per_block, a.n_seg),
+                       dim3(kInfoThreads), 0, stream, a.key_pos, a.n_ctx, a.cap, a.chunk_len,
+                       max_tiles, tile_info, act);
     hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(span_list_kernel, dim3(a.n_seg), dim3(kSpanThreads), 0, stream, act,
+                       a.n_ctx, a.cap, a.chunk_len, max_tiles, tile_list, n_active);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_kernel<D, true>), grid, dim3(kAttnThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
@@ -599,11 +611,11 @@ size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_head
                                  int n_kv_heads, int head_dim) {
   const size_t max_tiles = (static_cast<size_t>(cap) + kKT - 1) / kKT;
   return attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim) +
-         static_cast<size_t>(n_seg) * max_tiles * (sizeof(int2) + sizeof(int32_t)) +
+         static_cast<size_t>(n_seg) * max_tiles * (sizeof(int2) + sizeof(int32_t) + 1) +
          static_cast<size_t>(n_seg) * sizeof(int32_t);
 }
 
-int span_attn_max_cap() { return kMaxSpanTiles * kKT; }
+int span_attn_max_cap() { return 32768 * kKT; }
 
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
   const int s = attn_num_splits(a.n_seg, a.cap, a.chunk_len, a.n_q_heads, a.n_kv_heads,

@@ -114,9 +114,11 @@ struct PlaceArgs {
   const int32_t* n_kept_units;
   int32_t* chunk_slot;
   int32_t* span;
+  void* workspace;
   int32_t* d_status;
 };
 int native_max_cap();
+size_t place_workspace_bytes(int n_seg, int cap);
 size_t evict_workspace_bytes(int n_seg, int n_units);
 size_t suffix_workspace_bytes(int n_seg, int cap, int row_bytes);
 hipError_t launch_evict(const EvictArgs& a, hipStream_t stream);

@@ -90,28 +90,43 @@ __global__ __launch_bounds__(kNatThreads) void evict_plan_kernel(
   }
 }
 
-// Occupancy bitmap of one segment's slots [0, cap) in LDS: bit j of word w is slot 32 w + j.
+// Occupancy bitmap of one segment's slots [0, cap): bit j of word w is slot 32 w + j.  Built by
+// a grid of waves (one coalesced 64-slot load and a ballot per wave), then loaded into LDS by
+// the single-workgroup scans.
 constexpr int kMaxNatWords = 4096;                 // 131,072 slots
-__device__ inline void load_bitmap(const int32_t* __restrict__ uid, int cap, uint32_t* bits,
+
+__global__ __launch_bounds__(kCopyThreads) void occupancy_kernel(const int32_t* __restrict__ uid_g,
+                                                                 int cap, int nwords,
+                                                                 uint32_t* __restrict__ bits_g) {
+  const int seg = blockIdx.y;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int ch = blockIdx.x * (kCopyThreads / kWave) + threadIdx.x / kWave;
+  const int s = ch * kWave + lane;
+  const bool occ = s < cap && uid_g[static_cast<size_t>(seg) * cap + s] >= 0;
+  const uint64_t m = __ballot(occ);
+  if (lane == 0 && 2 * ch < nwords) {
+    bits_g[static_cast<size_t>(seg) * nwords + 2 * ch] = static_cast<uint32_t>(m);
+    if (2 * ch + 1 < nwords)
+      bits_g[static_cast<size_t>(seg) * nwords + 2 * ch + 1] = static_cast<uint32_t>(m >> 32);
+  }
+}
+
+__device__ inline void load_bitmap(const uint32_t* __restrict__ bits_g, uint32_t* bits,
                                    int nwords) {
-  for (int w = threadIdx.x; w < nwords; w += kNatThreads) {
-    int u[32];
+  constexpr int kIter = kMaxNatWords / kNatThreads;
+  uint32_t w[kIter];
 #pragma unroll
-    for (int j = 0; j < 32; ++j) {
-      const int s = 32 * w + j;
-      u[j] = s < cap ? uid[s] : -1;
-    }
-    uint32_t word = 0;
+  for (int i = 0; i < kIter; ++i) {                // all loads in flight, then the LDS writes
+    const int idx = threadIdx.x + i * kNatThreads;
+    w[i] = idx < nwords ? bits_g[idx] : 0u;
+  }
 #pragma unroll
-    for (int j = 0; j < 32; ++j) word |= (u[j] >= 0 ? 1u : 0u) << j;
-    bits[w] = word;
+  for (int i = 0; i < kIter; ++i) {
+    const int idx = threadIdx.x + i * kNatThreads;
+    if (idx < nwords) bits[idx] = w[i];
   }
   __syncthreads();
 }
-__device__ inline bool bit(const uint32_t* bits, int s) {
-  return (bits[s >> 5] >> (s & 31)) & 1u;
-}
-
 __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
     int32_t* __restrict__ uid_g, int32_t* __restrict__ pos_g, int cap, int n_units,
     const UnitRec* __restrict__ table, const int32_t* __restrict__ len_g,
@@ -148,7 +163,7 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
 }
 
 __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
-    const int32_t* __restrict__ uid_g, int cap, int page_size, int min_pages,
+    const uint32_t* __restrict__ bits_g, int cap, int page_size, int min_pages,
     int32_t* __restrict__ list, int32_t* __restrict__ meta, int32_t* __restrict__ span_g,
     int32_t* __restrict__ cut_g, int32_t* __restrict__ moved_g) {
   __shared__ uint32_t bits[kMaxNatWords];
@@ -157,7 +172,7 @@ __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
   const int tid = threadIdx.x;
   const size_t sb = static_cast<size_t>(seg) * cap;
   const int nwords = (cap + 31) / 32;
-  load_bitmap(uid_g + sb, cap, bits, nwords);
+  load_bitmap(bits_g + static_cast<size_t>(seg) * nwords, bits, nwords);
   // thread t owns words [w0, w1), i.e. slots [32 w0, 32 w1)
   const int wpt = (nwords + kNatThreads - 1) / kNatThreads;
   const int w0 = min(tid * wpt, nwords), w1 = min(w0 + wpt, nwords);
@@ -172,17 +187,20 @@ __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
   const int last_before = block_exclusive_max(my_last, -1, scr, &span_m1);
   const int span = span_m1 + 1;
   const int pages_now = (span + page_size - 1) / page_size;
-  // largest qualifying cut c < span in this thread's slots
+  // A cut c < span qualifies iff its packed span c + (entries at or after c) fits in
+  // pages_now - min_pages pages, i.e. is at most `limit` slots.  Largest such c in this
+  // thread's slots (the packed span never decreases with c).
+  const long limit = static_cast<long>(pages_now - min_pages) * page_size;
+  (void)last_before;
   int best = -1;
-  {
-    int lb = last_before, live_lt = live_before;   // state before slot s
-    for (int s = 32 * w0; s < 32 * w1 && s < span; ++s) {
-      const int suffix = total - live_lt;            // entries at or after s
-      const int ps = suffix > 0 ? s + suffix : lb + 1;
-      if (pages_now - (ps + page_size - 1) / page_size >= min_pages) best = s;
-      if (bit(bits, s)) {
-        ++live_lt;
-        lb = s;
+  if (limit >= 0) {
+    int live_lt = live_before;                      // entries before slot s
+    for (int w = w0; w < w1 && 32 * w < span; ++w) {
+      const uint32_t word = bits[w];
+      for (int j = 0; j < 32 && 32 * w + j < span; ++j) {
+        const int s = 32 * w + j;
+        if (s + (total - live_lt) <= limit) best = s;
+        live_lt += (word >> j) & 1u;
       }
     }
   }
@@ -194,14 +212,19 @@ __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
     int mine = 0;
     if (c >= 32 * w0 && c < 32 * w1) {
       mine = live_before;
-      for (int s = 32 * w0; s < c; ++s) mine += bit(bits, s) ? 1 : 0;
+      for (int w = w0; w < c / 32; ++w) mine += __popc(bits[w]);
+      mine += __popc(bits[c / 32] & ((1u << (c % 32)) - 1u));
     }
     const int before_c = block_sum(mine, scr);
     n_suffix = total - before_c;
     new_span = c + n_suffix;
     int live_lt = live_before, moved_here = 0;
-    for (int s = 32 * w0; s < 32 * w1 && s < span; ++s) {
-      if (bit(bits, s)) {
+    for (int w = w0; w < w1 && 32 * w < span; ++w) {
+      uint32_t word = bits[w];
+      while (word) {
+        const int j = __ffs(word) - 1;
+        word &= word - 1;
+        const int s = 32 * w + j;
         if (s >= c) {
           const int r = live_lt - before_c;
           list[sb + r] = s;
@@ -291,15 +314,14 @@ __global__ __launch_bounds__(kCopyThreads) void suffix_copy_kernel(
 }
 
 __global__ __launch_bounds__(kNatThreads) void place_plan_kernel(
-    const int32_t* __restrict__ uid_g, int cap, int chunk_len, int32_t* __restrict__ slot_g,
+    const uint32_t* __restrict__ bits_g, int cap, int chunk_len, int32_t* __restrict__ slot_g,
     int32_t* __restrict__ span_g, int32_t* __restrict__ status) {
   __shared__ uint32_t bits[kMaxNatWords];
   __shared__ int32_t scr[kNatThreads / kWave + 1];
   const int seg = blockIdx.x;
   const int tid = threadIdx.x;
-  const size_t sb = static_cast<size_t>(seg) * cap;
   const int nwords = (cap + 31) / 32;
-  load_bitmap(uid_g + sb, cap, bits, nwords);
+  load_bitmap(bits_g + static_cast<size_t>(seg) * nwords, bits, nwords);
   const int wpt = (nwords + kNatThreads - 1) / kNatThreads;
   const int w0 = min(tid * wpt, nwords), w1 = min(w0 + wpt, nwords);
   int my_last = -1;
@@ -309,12 +331,20 @@ __global__ __launch_bounds__(kNatThreads) void place_plan_kernel(
   int last = block_exclusive_max(my_last, -1, scr, &last_all);
   // first slot s of this range where the empty run ending at s reaches chunk_len
   int cand = -1;
-  for (int s = 32 * w0; s < 32 * w1 && s < cap; ++s) {
-    if (bit(bits, s)) {
-      last = s;
-    } else if (s - last >= chunk_len) {
-      cand = s - chunk_len + 1;
-      break;
+  for (int w = w0; w < w1 && cand < 0; ++w) {
+    const uint32_t word = bits[w];
+    const int end = min(32 * w + 32, cap);          // slots of this word: [32 w, end)
+    if (word == 0u) {                               // all empty: the run only grows
+      if (last + chunk_len < end) cand = last + 1;
+      continue;
+    }
+    for (int s = 32 * w; s < end; ++s) {
+      if ((word >> (s - 32 * w)) & 1u) {
+        last = s;
+      } else if (s - last >= chunk_len) {
+        cand = s - chunk_len + 1;
+        break;
+      }
     }
   }
   // lowest candidate over all threads = -(largest of the negated candidates)
@@ -385,13 +415,30 @@ hipError_t launch_evict(const EvictArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+static size_t bitmap_bytes(int n_seg, int cap) {
+  return ((static_cast<size_t>(n_seg) * ((cap + 31) / 32) * 4 + 255) / 256) * 256;
+}
+
+static hipError_t launch_occupancy(const int32_t* uid, int n_seg, int cap, uint32_t* bits,
+                                   hipStream_t stream) {
+  const int nwords = (cap + 31) / 32;
+  const int chunks = (cap + kWave - 1) / kWave;
+  const int per_block = kCopyThreads / kWave;
+  hipLaunchKernelGGL(occupancy_kernel, dim3((chunks + per_block - 1) / per_block, n_seg),
+                     dim3(kCopyThreads), 0, stream, uid, cap, nwords, bits);
+  return hipGetLastError();
+}
+
 size_t suffix_workspace_bytes(int n_seg, int cap, int row_bytes) {
   const size_t slots = static_cast<size_t>(n_seg) * cap;
   const size_t list = ((slots * 4 + 255) / 256) * 256;
   const size_t meta = 256 + ((static_cast<size_t>(n_seg) * 8 + 255) / 256) * 256;
   const size_t tags = ((slots * 12 + 255) / 256) * 256;
-  return list + meta + tags + slots * 2 * static_cast<size_t>(row_bytes);
+  return list + meta + tags + bitmap_bytes(n_seg, cap) +
+         slots * 2 * static_cast<size_t>(row_bytes);
 }
+
+size_t place_workspace_bytes(int n_seg, int cap) { return bitmap_bytes(n_seg, cap); }
 
 hipError_t launch_pack_suffix(const SuffixArgs& a, hipStream_t stream) {
   const size_t slots = static_cast<size_t>(a.n_seg) * a.cap;
@@ -402,11 +449,14 @@ hipError_t launch_pack_suffix(const SuffixArgs& a, hipStream_t stream) {
   w += 256 + ((static_cast<size_t>(a.n_seg) * 8 + 255) / 256) * 256;
   int32_t* tags = reinterpret_cast<int32_t*>(w);
   w += ((slots * 12 + 255) / 256) * 256;
+  uint32_t* bits = reinterpret_cast<uint32_t*>(w);
+  w += bitmap_bytes(a.n_seg, a.cap);
   uint8_t* rows = w;
-  hipLaunchKernelGGL(suffix_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream,
-                     a.unit_id, a.cap, a.page_size, a.min_pages, list, meta, a.span, a.cut,
-                     a.moved);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_occupancy(a.unit_id, a.n_seg, a.cap, bits, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(suffix_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream, bits,
+                     a.cap, a.page_size, a.min_pages, list, meta, a.span, a.cut, a.moved);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 grid((a.cap + kRowsPerBlock - 1) / kRowsPerBlock, a.n_seg);
   uint8_t* k = static_cast<uint8_t*>(a.k);
@@ -423,9 +473,12 @@ hipError_t launch_pack_suffix(const SuffixArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_place_chunk(const PlaceArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(place_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream, a.unit_id,
-                     a.cap, a.chunk_len, a.chunk_slot, a.span, a.d_status);
-  hipError_t e = hipGetLastError();
+  uint32_t* bits = static_cast<uint32_t*>(a.workspace);
+  hipError_t e = launch_occupancy(a.unit_id, a.n_seg, a.cap, bits, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(place_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream, bits, a.cap,
+                     a.chunk_len, a.chunk_slot, a.span, a.d_status);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   const dim3 grid((a.chunk_len + kRowsPerBlock - 1) / kRowsPerBlock, a.n_seg);
   hipLaunchKernelGGL(chunk_write_kernel, grid, dim3(kCopyThreads), 0, stream,

@@ -32,6 +32,7 @@ EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv
            "omnitide_attn_workspace_bytes", "omnitide_span_attn", "omnitide_evict_native",
            "omnitide_evict_native_workspace_bytes", "omnitide_pack_suffix",
            "omnitide_pack_suffix_workspace_bytes", "omnitide_place_chunk",
+           "omnitide_place_chunk_workspace_bytes",
            "omnitide_span_attn_workspace_bytes", "omnitide_decode_attn",
            "omnitide_decode_workspace_bytes", "omnitide_status_string", "omnitide_version")
 
@@ -88,7 +89,9 @@ def lib() -> ctypes.CDLL:
         L.omnitide_pack_suffix_workspace_bytes.argtypes = [_I, _I, _I, _I, _I]
         L.omnitide_pack_suffix_workspace_bytes.restype = _SZ
         L.omnitide_place_chunk.argtypes = [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P,
-                                           _P, _I, _P, _P, _P, _P, _P, _P]
+                                           _P, _I, _P, _P, _P, _P, _P, _SZ, _P, _P]
+        L.omnitide_place_chunk_workspace_bytes.argtypes = [_I, _I]
+        L.omnitide_place_chunk_workspace_bytes.restype = _SZ
         L.omnitide_decode_attn.argtypes = L.omnitide_chunk_attn.argtypes
         L.omnitide_decode_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_decode_workspace_bytes.restype = _SZ
@@ -435,8 +438,12 @@ def omnitide_pack_suffix(k, v, page_size, min_pages, unit_id, modality, pos, spa
            "omnitide_pack_suffix")
 
 
+def omnitide_place_chunk_workspace_bytes(n_seg, cap) -> int:
+    return int(lib().omnitide_place_chunk_workspace_bytes(n_seg, cap))
+
+
 def omnitide_place_chunk(k, v, unit_id, modality, pos, k_chunk, v_chunk, chunk_modality,
-                         chunk_unit, kept_tokens, n_kept_units, chunk_slot, span,
+                         chunk_unit, kept_tokens, n_kept_units, chunk_slot, span, workspace,
                          d_status=None, stream=None):
     """The chunk into the lowest run of empty slots of pools k/v [n_seg, cap, H, d]."""
     n_seg, cap, H, d = _pool_dims(k, "k")
@@ -453,13 +460,15 @@ def omnitide_place_chunk(k, v, unit_id, modality, pos, k_chunk, v_chunk, chunk_m
     for t, nm in ((kept_tokens, "kept_tokens"), (n_kept_units, "n_kept_units"),
                   (chunk_slot, "chunk_slot"), (span, "span")):
         _need(t, nm, I32, n_seg)
+    _need(workspace, "workspace", U8)
     if d_status is not None:
         _need(d_status, "d_status", I32, 1)
     _check(lib().omnitide_place_chunk(_ptr(k), _ptr(v), _kv_dtype(k), n_seg, cap, H, d,
                                       _ptr(unit_id), _ptr(modality), _ptr(pos), _ptr(k_chunk),
                                       _ptr(v_chunk), _ptr(chunk_modality), _ptr(chunk_unit), L,
                                       _ptr(kept_tokens), _ptr(n_kept_units), _ptr(chunk_slot),
-                                      _ptr(span), _ptr(d_status), _stream(stream)),
+                                      _ptr(span), _ptr(workspace), workspace.numel(),
+                                      _ptr(d_status), _stream(stream)),
            "omnitide_place_chunk")
 
 

@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 20
+    assert len(names) == 21
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -305,12 +305,13 @@ def test_pack_suffix_validation(L):
 def place(L, **kw):
     a = dict(k=fake(0), v=fake(1), dtype=0, n_seg=1, cap=1000, H=8, d=128, uid=fake(2),
              mod=fake(3), pos=fake(4), kc=fake(5), vc=fake(6), cm=fake(7), cu=fake(8), Lc=16,
-             kt=fake(9), nk=fake(10), slot=fake(11), span=fake(12), st=fake(13))
+             kt=fake(9), nk=fake(10), slot=fake(11), span=fake(12), ws=fake(14), wsb=1 << 20,
+             st=fake(13))
     a.update(kw)
     return L.omnitide_place_chunk(a["k"], a["v"], a["dtype"], a["n_seg"], a["cap"], a["H"],
                                   a["d"], a["uid"], a["mod"], a["pos"], a["kc"], a["vc"],
                                   a["cm"], a["cu"], a["Lc"], a["kt"], a["nk"], a["slot"],
-                                  a["span"], a["st"], None)
+                                  a["span"], a["ws"], a["wsb"], a["st"], None)
 
 
 def test_place_chunk_validation(L):
@@ -319,6 +320,9 @@ def test_place_chunk_validation(L):
     assert place(L, Lc=0) == ot.E_SHAPE
     assert place(L, Lc=1001) == ot.E_CAPACITY
     assert place(L, slot=fake(9)) == ot.E_ALIAS            # output over kept_tokens
+    assert place(L, ws=None) == ot.E_WORKSPACE
+    assert place(L, wsb=8) == ot.E_WORKSPACE
+    assert ot.omnitide_place_chunk_workspace_bytes(1, 1000) >= 125
 
 
 def decode(L, **kw):

@@ -194,6 +194,12 @@ def i32(a):
     return dev(np.asarray(a, np.int32))
 
 
+def place_ws(cap):
+    from paper_2609_34653_amd import omnitide as ot
+    return torch.zeros(ot.omnitide_place_chunk_workspace_bytes(1, cap), dtype=torch.uint8,
+                       device="cuda")
+
+
 def native_state(cfg_name, extra=None, plan="whole", seed_keep=None):
     """GPU pool of capacity n_slots + L (+extra) with the stream's tags, scored on the GPU, and
     the retention plan (whole-unit select, or arbitrary kept prefixes) on the host."""
@@ -315,15 +321,15 @@ def test_place_chunk_parity_and_native_attention():
     gpu_evict(lay, g)
     ev = check_evict(lay, g, h)
     L = lay.chunk_len
-    slot, = [i32([-9])]
+    cap = len(h["uid"])
+    slot = i32([-9])
     ot.omnitide_place_chunk(g["k"], g["v"], g["uid"], g["mod"], g["pos"],
                             seg.k_chunk.cuda()[None].contiguous(),
                             seg.v_chunk.cuda()[None].contiguous(), dev(lay.chunk_modality),
                             dev(lay.chunk_unit), g["kept"], g["nku"], slot, g["span"],
-                            d_status=g["st"])
+                            place_ws(cap), d_status=g["st"])
     torch.cuda.synchronize()
     assert int(host(g["st"])[0]) == 0
-    cap = len(h["uid"])
     s0 = oracle.place_chunk(ev["unit_id"], L, cap)
     assert int(host(slot)[0]) == s0
     uid = ev["unit_id"].copy()
@@ -363,7 +369,7 @@ def test_place_chunk_capacity_error():
                             seg.k_chunk.cuda()[None].contiguous(),
                             seg.v_chunk.cuda()[None].contiguous(), dev(lay.chunk_modality),
                             dev(lay.chunk_unit), g["kept"], g["nku"], slot, span,
-                            d_status=g["st"])
+                            place_ws(len(uid)), d_status=g["st"])
     torch.cuda.synchronize()
     assert int(host(g["st"])[0]) == -5 and int(host(slot)[0]) == -1
     assert np.array_equal(host(g["uid"]), uid)
