@@ -124,6 +124,8 @@ def main():
                     help="run a plain elementwise copy kernel (reads and writes this many MiB) "
                          "three times before the warmup: a known-size reference for hardware "
                          "byte counters")
+    ap.add_argument("--loop-steps", type=int, default=64,
+                    help="steps of the stream-loop layout comparison (0 = skip)")
     ap.add_argument("--no-graph", action="store_true",
                     help="time the standalone calls with events around host launches instead of "
                          "one captured HIP graph (for counter passes)")
@@ -303,6 +305,9 @@ def main():
     kernels["layouts"] = layout_ablation(ot, st, copies[0], lay, cfg, L, H, Hq, d, dev,
                                          args.steps, n_ctx, not args.no_graph)
 
+    if args.loop_steps > 0:
+        kernels["stream_loop_layouts"] = stream_loop_ablation(ot, dev, args.loop_steps)
+
     value = flops / (ms_per_step * 1e-3) / 1e12
     result = {
         "metric": "chunk-attn TFLOP/s + score/compact GB/s (% roofline), 80K-token history, 1 GPU",
@@ -433,6 +438,152 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
     res["eager"] = {"span": n_ctx, "pages_256": -(-n_ctx // 256),
                     "active_pages_256": -(-n_ctx // 256), "active_tiles_64": -(-n_ctx // 64),
                     "note": "the step's compact + attend (kernels.compact, kernels.attend)"}
+    return res
+
+
+def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
+    """The 64-step stream loop (prefill 16,384 tokens, then 665-token chunks, budget 16,384)
+    with the same selections under three layouts: eager (the step: compact + chunk attention,
+    ping-pong pools), native (logical eviction, the chunk in the lowest empty run, attention
+    over the holey span) and ordered-suffix packing (native plus, after each eviction, the
+    suffix whose packing saves >= T pages of `page` slots, for each T in `suffix_pages`).  The
+    eager path's score + select decide each step's plan; the native pools apply the same keep
+    flags (their unit ids and positions coincide with the eager pool's).  Attention over a
+    native pool runs twice per step: skipping empty 64-slot tiles, and traversing the whole
+    span (as kernels without tile skipping do).  Attention and maintenance are timed with events
+    around their launches; spans and active pages are recorded per step."""
+    from paper_2609_34653_amd.step import StreamStep
+    cfg = sg.CONFIG_BY_NAME["stream_loop_64x665"]
+    stream = sg.make_stream(cfg)
+    lay, seg0 = stream.layout, stream.segment(0)
+    U, L = 512, 665
+    H, d, Hq = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads
+    cap_e, cap_n = cfg.budget + L, 131072
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    chunks = []
+    for i in range(steps):
+        clay, cseg = sg.loop_chunk(cfg, i)
+        chunks.append(dict(kc=cseg.k_chunk.to(dev)[None].contiguous(),
+                           vc=cseg.v_chunk.to(dev)[None].contiguous(),
+                           q=cseg.q.to(dev)[None].contiguous(), cm=t(clay.chunk_modality),
+                           cu=t(clay.chunk_unit)))
+    mk = lambda n: StreamStep(n_seg=1, n_slots=n, n_units=U, n_q_heads=Hq, n_kv_heads=H,  # noqa
+                              head_dim=d, chunk_len=L, budget=cfg.budget, recent=cfg.recent,
+                              page_size=cfg.page_size, weights=cfg.weights, cap_dst=cap_e,
+                              device=dev)
+    st_first, st_a, st_b = mk(lay.n_slots), mk(cap_e), mk(cap_e)
+    src = dict(k=seg0.k_hist.to(dev)[None].contiguous(), v=seg0.v_hist.to(dev)[None].contiguous(),
+               uid=t(lay.unit_id), mod=t(lay.modality), pos=t(lay.pos))
+    i32 = dict(dtype=torch.int32, device=dev)
+    pad = cap_n - lay.n_slots
+
+    def native_pool(min_pages):
+        k = torch.zeros(1, cap_n, H, d, dtype=torch.bfloat16, device=dev)
+        v = torch.zeros_like(k)
+        k[0, :lay.n_slots] = src["k"][0]
+        v[0, :lay.n_slots] = src["v"][0]
+        return dict(k=k, v=v, min_pages=min_pages,
+                    uid=t(np.concatenate([lay.unit_id, np.full(pad, -1)]).astype(np.int32)),
+                    pos=t(np.concatenate([lay.pos, np.full(pad, -1)]).astype(np.int32)),
+                    mod=t(np.concatenate([lay.modality, np.full(pad, 1)]).astype(np.uint8)),
+                    remap=torch.zeros(U, **i32), kept=torch.zeros(1, **i32),
+                    nku=torch.zeros(1, **i32), span=torch.zeros(1, **i32),
+                    slot=torch.zeros(1, **i32), cut=torch.zeros(1, **i32),
+                    moved=torch.zeros(1, **i32), out=torch.zeros(1, L, Hq, d, device=dev),
+                    moved_sum=torch.zeros(1, **i32), migrations=torch.zeros(1, **i32))
+    pools = {"native": native_pool(0)}
+    for T in suffix_pages:
+        pools[f"ordered_suffix_T{T}"] = native_pool(T)
+    ws_e = torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, U), dtype=torch.uint8,
+                       device=dev)
+    ws_p = torch.zeros(ot.omnitide_pack_suffix_workspace_bytes(0, 1, cap_n, H, d),
+                       dtype=torch.uint8, device=dev)
+    ws_c = torch.zeros(ot.omnitide_place_chunk_workspace_bytes(1, cap_n), dtype=torch.uint8,
+                       device=dev)
+    ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap_n, L, Hq, H, d),
+                       dtype=torch.uint8, device=dev)
+    names = ["eager"] + list(pools)
+    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+          for n in names}
+    spans = {n: torch.zeros(steps, **i32) for n in names}
+    active = {n: torch.zeros(steps, **i32) for n in names}
+    diff = torch.zeros(len(pools), device=dev)
+    s = torch.cuda.current_stream()
+    d_status = st_first.d_status
+    for i in range(steps):
+        c = chunks[i]
+        st = st_first if i == 0 else (st_a if i % 2 else st_b)
+        st.d_status = d_status
+        e = ev["eager"][i]
+        st.score(src["k"], src["uid"], src["mod"])
+        st.select()
+        e[0].record(s)
+        st.compact(src["k"], src["v"], src["uid"], src["mod"], src["pos"], c["kc"], c["vc"],
+                   c["cm"], c["cu"])
+        e[1].record(s)
+        st.attend(c["q"], cfg.scale)
+        e[2].record(s)
+        spans["eager"][i:i + 1].copy_(st.n_ctx)
+        active["eager"][i:i + 1].copy_((st.n_ctx + page - 1) // page)
+        for j, (n, pl) in enumerate(pools.items()):
+            e = ev[n][i]
+            e[0].record(s)
+            ot.omnitide_evict_native(pl["uid"], pl["pos"], 1, U, st.unit_len, pl["remap"],
+                                     pl["kept"], pl["nku"], pl["span"], ws_e, keep=st.keep,
+                                     d_status=d_status)
+            if pl["min_pages"] > 0:
+                ot.omnitide_pack_suffix(pl["k"], pl["v"], page, pl["min_pages"], pl["uid"],
+                                        pl["mod"], pl["pos"], pl["span"], pl["cut"],
+                                        pl["moved"], ws_p)
+                pl["moved_sum"] += pl["moved"]
+                pl["migrations"] += (pl["cut"] >= 0).to(torch.int32)
+            ot.omnitide_place_chunk(pl["k"], pl["v"], pl["uid"], pl["mod"], pl["pos"], c["kc"],
+                                    c["vc"], c["cm"], c["cu"], pl["kept"], pl["nku"], pl["slot"],
+                                    pl["span"], ws_c, d_status=d_status)
+            e[1].record(s)
+            ot.omnitide_span_attn(c["q"], pl["k"], pl["v"], pl["pos"], pl["span"], pl["kept"],
+                                  cfg.scale, pl["out"], ws_a, d_status, skip_empty_tiles=True)
+            e[2].record(s)
+            ot.omnitide_span_attn(c["q"], pl["k"], pl["v"], pl["pos"], pl["span"], pl["kept"],
+                                  cfg.scale, pl["out"], ws_a, d_status, skip_empty_tiles=False)
+            e[3].record(s)
+            spans[n][i:i + 1].copy_(pl["span"])
+            occ = (pl["uid"] >= 0).view(-1, page).any(dim=1)
+            active[n][i:i + 1].copy_(occ.sum().view(1).to(torch.int32))
+            diff[j] = torch.maximum(diff[j], (pl["out"] - st.out).abs().max())
+        src = dict(k=st.k_dst, v=st.v_dst, uid=st.unit_id_dst, mod=st.modality_dst,
+                   pos=st.pos_dst)
+    torch.cuda.synchronize()
+    status = int(d_status.item())
+    if status != 0:
+        raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
+    res = {"steps": steps, "page_size": page,
+           "max_abs_diff_vs_eager": round(float(diff.max().item()), 6)}
+    for n in names:
+        ms = lambda a, b: sum(ev[n][i][a].elapsed_time(ev[n][i][b]) for i in range(steps))  # noqa
+        sp = spans[n].cpu().numpy()
+        ac = active[n].cpu().numpy()
+        r = {"maintenance_ms_total": round(ms(0, 1), 3), "mean_span": round(float(sp.mean()), 1),
+             "max_span": int(sp.max()), "final_span": int(sp[-1]),
+             "mean_active_pages": round(float(ac.mean()), 1)}
+        if n == "eager":
+            r["attend_ms_total"] = round(ms(1, 2), 3)
+        else:
+            r["attend_skip_ms_total"] = round(ms(1, 2), 3)
+            r["attend_full_span_ms_total"] = round(ms(2, 3), 3)
+            if pools[n]["min_pages"] > 0:
+                r["min_pages"] = pools[n]["min_pages"]
+                r["moved_rows_total"] = int(pools[n]["moved_sum"].item())
+                r["migrations"] = int(pools[n]["migrations"].item())
+        res[n] = r
+    nat = res["native"]
+    for n in names[1:]:
+        for mode in ("skip", "full_span"):
+            res[n][f"attend_{mode}_reduction_vs_native"] = round(
+                1 - res[n][f"attend_{mode}_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
+    for mode in ("skip", "full_span"):
+        res["eager"][f"attend_reduction_vs_native_{mode}"] = round(
+            1 - res["eager"]["attend_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
     return res
 
 

@@ -339,7 +339,8 @@ namespace {
 int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
               const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int chunk_len,
               int n_q_heads, int n_kv_heads, int head_dim, float scale, float* out,
-              void* workspace, size_t workspace_bytes, int32_t* d_status, void* stream) {
+              void* workspace, size_t workspace_bytes, int32_t* d_status, void* stream,
+              bool skip_empty = true) {
   const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
   if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
@@ -379,6 +380,7 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
   a.d_status = d_status;
   a.key_pos = key_pos;
   a.q_pos0 = q_pos0;
+  a.skip_empty = skip_empty;
   return hip_status(omnitide::launch_attn(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -404,11 +406,12 @@ size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int
 int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_t* key_pos,
                        const int32_t* span, const int32_t* q_pos0, int n_seg, int cap,
                        int chunk_len, int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                       float* out, void* workspace, size_t workspace_bytes, int32_t* d_status,
-                       void* stream) {
+                       int skip_empty_tiles, float* out, void* workspace,
+                       size_t workspace_bytes, int32_t* d_status, void* stream) {
   if (key_pos == nullptr || q_pos0 == nullptr) return OMNITIDE_E_NULL;
   return attn_impl(q, k, v, span, key_pos, q_pos0, n_seg, cap, chunk_len, n_q_heads,
-                   n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream);
+                   n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream,
+                   skip_empty_tiles != 0);
 }
 
 size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units) {

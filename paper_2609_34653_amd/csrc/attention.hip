@@ -485,14 +485,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
 
 // Active tiles of a span.  span_info_kernel: one wave per 64-slot tile of [0, span) (a grid of
 // workgroups) records the tile's largest key position, whether it holds an empty slot (or
-// slots past the span) and whether it holds any entry.  span_list_kernel: one workgroup per
+// slots past the span) and whether it is visited (it holds an entry, or every tile of the span
+// is visited).  span_list_kernel: one workgroup per
 // segment lists the tiles holding an entry, in order.
 constexpr int kSpanThreads = 1024;
 constexpr int kInfoThreads = 256;
 
 __global__ __launch_bounds__(kInfoThreads) void span_info_kernel(
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ span_g, int cap, int L,
-    int max_tiles, int2* __restrict__ tile_info, uint8_t* __restrict__ act_g) {
+    int max_tiles, int skip_empty, int2* __restrict__ tile_info, uint8_t* __restrict__ act_g) {
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
   const int t = blockIdx.x * (kInfoThreads / kWave) + threadIdx.x / kWave;
@@ -508,7 +509,7 @@ __global__ __launch_bounds__(kInfoThreads) void span_info_kernel(
   if (lane == 0) {
     const size_t tb = static_cast<size_t>(seg) * max_tiles;
     tile_info[tb + t] = make_int2(mx, valid != ~0ull ? 1 : 0);
-    act_g[tb + t] = valid != 0 ? 1 : 0;
+    act_g[tb + t] = (valid != 0 || !skip_empty) ? 1 : 0;
   }
 }
 
@@ -559,7 +560,7 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
     const int per_block = kInfoThreads / kWave;
     hipLaunchKernelGGL(span_info_kernel, dim3((max_tiles + per_block - 1) / per_block, a.n_seg),
                        dim3(kInfoThreads), 0, stream, a.key_pos, a.n_ctx, a.cap, a.chunk_len,
-                       max_tiles, tile_info, act);
+                       max_tiles, a.skip_empty ? 1 : 0, tile_info, act);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(span_list_kernel, dim3(a.n_seg), dim3(kSpanThreads), 0, stream, act,

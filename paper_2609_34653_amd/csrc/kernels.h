@@ -139,6 +139,7 @@ struct AttnArgs {
   // span mode (keys = the slots [0, span) of a pool with holes; n_ctx holds the span):
   const int32_t* key_pos = nullptr;   // [n_seg][cap] logical position, -1 = empty slot
   const int32_t* q_pos0 = nullptr;    // [n_seg] logical position of chunk query 0
+  bool skip_empty = true;             // skip 64-slot tiles without an entry
 };
 
 int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,

@@ -77,7 +77,7 @@ def lib() -> ctypes.CDLL:
         L.omnitide_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_attn_workspace_bytes.restype = _SZ
         L.omnitide_span_attn.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
-                                         ctypes.c_float, _P, _P, _SZ, _P, _P]
+                                         ctypes.c_float, _I, _P, _P, _SZ, _P, _P]
         L.omnitide_span_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_span_attn_workspace_bytes.restype = _SZ
         L.omnitide_evict_native.argtypes = [_I, _I, _P, _P, _P, _P, _P, _I, _P, _P, _P, _P, _P,
@@ -357,7 +357,7 @@ def omnitide_span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_he
 
 
 def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_status=None,
-                       stream=None):
+                       stream=None, skip_empty_tiles=True):
     """q [n_seg, L, Hq, d] bf16; k/v [n_seg, cap, Hkv, d] bf16; key_pos int32 [n_seg * cap]
     (-1 = empty slot); span, q_pos0 int32 [n_seg] (device); out float32 like q."""
     if q.dim() == 3:
@@ -379,7 +379,8 @@ def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_
         _need(d_status, "d_status", I32, 1)
     _check(lib().omnitide_span_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(key_pos), _ptr(span),
                                     _ptr(q_pos0), n_seg, cap, L, Hq, Hkv, d, float(scale),
-                                    _ptr(out), _ptr(workspace), workspace.numel(),
+                                    1 if skip_empty_tiles else 0, _ptr(out), _ptr(workspace),
+                                    workspace.numel(),
                                     _ptr(d_status), _stream(stream)), "omnitide_span_attn")
 
 

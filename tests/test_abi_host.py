@@ -239,7 +239,7 @@ def span_attn(L, **kw):
              wsb=1 << 30, st=fake(8))
     a.update(kw)
     return L.omnitide_span_attn(a["q"], a["k"], a["v"], a["kp"], a["span"], a["qp"], a["n_seg"],
-                                a["cap"], a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"],
+                                a["cap"], a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"], 1,
                                 a["out"], a["ws"], a["wsb"], a["st"], None)
 
 

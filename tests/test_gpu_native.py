@@ -32,7 +32,7 @@ def bf16(a):
     return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16)
 
 
-def run_span_attn(q, k, v, key_pos, span, q_pos0, scale, expect_status=0):
+def run_span_attn(q, k, v, key_pos, span, q_pos0, scale, expect_status=0, skip=True):
     """q [n_seg, L, Hq, d], k/v [n_seg, cap, Hkv, d] bf16 (CPU); key_pos [n_seg, cap]."""
     from paper_2609_34653_amd import omnitide as ot
     n_seg, L, Hq, d = q.shape
@@ -44,7 +44,7 @@ def run_span_attn(q, k, v, key_pos, span, q_pos0, scale, expect_status=0):
     ot.omnitide_span_attn(q.cuda(), k.cuda(), v.cuda(),
                           dev(np.asarray(key_pos, np.int32).reshape(-1)),
                           dev(np.asarray(span, np.int32)), dev(np.asarray(q_pos0, np.int32)),
-                          scale, out, ws, st)
+                          scale, out, ws, st, skip_empty_tiles=skip)
     torch.cuda.synchronize()
     assert int(host(st)[0]) == expect_status
     return host(out)
@@ -96,18 +96,21 @@ def random_span_pool(rng, cap, L, Hkv, d, fill, empty_tiles=True, nan_holes=True
     return bf16(k), bf16(v), key_pos, span, len(hist)
 
 
-@pytest.mark.parametrize("cap,L,Hq,Hkv,d,fill,seed", [
-    (700, 37, 8, 2, 128, 0.5, 0),       # ragged span, several tiles, GQA 4
-    (2000, 100, 4, 4, 64, 0.3, 1),      # no grouping, d = 64
-    (1500, 200, 32, 8, 128, 0.9, 2),    # nearly full, chunk 200
-    (5000, 64, 8, 1, 128, 0.1, 3),      # sparse: many empty tiles
+@pytest.mark.parametrize("cap,L,Hq,Hkv,d,fill,seed,skip", [
+    (700, 37, 8, 2, 128, 0.5, 0, True),       # ragged span, several tiles, GQA 4
+    (2000, 100, 4, 4, 64, 0.3, 1, True),      # no grouping, d = 64
+    (1500, 200, 32, 8, 128, 0.9, 2, True),    # nearly full, chunk 200
+    (5000, 64, 8, 1, 128, 0.1, 3, True),      # sparse: many empty tiles
+    (5000, 64, 8, 1, 128, 0.1, 3, False),     # the same, every tile traversed
+    (2000, 100, 4, 4, 64, 0.3, 1, False),
 ])
-def test_span_attention_random_pools(cap, L, Hq, Hkv, d, fill, seed):
+def test_span_attention_random_pools(cap, L, Hq, Hkv, d, fill, seed, skip):
     rng = np.random.default_rng(seed)
     k, v, key_pos, span, q_pos0 = random_span_pool(rng, cap, L, Hkv, d, fill)
     q = bf16(rng.standard_normal((L, Hq, d)))
     scale = d ** -0.5
-    out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0], scale)
+    out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0], scale,
+                        skip=skip)
     check(out[0], q, k, v, key_pos, span, q_pos0, scale)
 
 
@@ -172,9 +175,11 @@ def native_80k(keep_whole=True):
 def test_span_attention_native_80k():
     cfg, q, k, v, key_pos, span, q_pos0, s0 = native_80k()
     assert s0 < span - 665 and span > 60000, "the chunk fills a hole, the span stays long"
-    out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0], cfg.scale)
     rows = sample_rows(q.shape[0], np.random.default_rng(8), 16)
-    check(out[0], q, k, v, key_pos, span, q_pos0, cfg.scale, rows=rows)
+    for skip in (True, False):
+        out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0],
+                            cfg.scale, skip=skip)
+        check(out[0], q, k, v, key_pos, span, q_pos0, cfg.scale, rows=rows)
 
 
 def test_span_attention_capacity_error():
