@@ -58,7 +58,7 @@ def gpu_inputs(lay, segs):
         q=torch.stack([s.q for s in segs]).cuda())
 
 
-def run_gpu(cfg, st, inp, attend=True):
+def run_gpu(cfg, st, inp, attend=True, sync=True):
     st.score(inp["k_hist"], inp["unit_id"], inp["modality"])
     st.select()
     st.compact(inp["k_hist"], inp["v_hist"], inp["unit_id"], inp["modality"], inp["pos"],
@@ -69,7 +69,8 @@ def run_gpu(cfg, st, inp, attend=True):
         else:   # float32 pools: attention runs on round-to-nearest-even bf16 copies
             st.attend(inp["q"].to(torch.bfloat16), cfg.scale, k=st.k_dst.to(torch.bfloat16),
                       v=st.v_dst.to(torch.bfloat16))
-    torch.cuda.synchronize()
+    if sync:
+        torch.cuda.synchronize()
 
 
 def check_segment(cfg, lay, seg, st, si, n_units=None, sample_rows=None, rng=None):
