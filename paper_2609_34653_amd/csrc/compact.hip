@@ -3,17 +3,16 @@
 // span plan's kept-prefix length; a partially kept unit's deleted tail counts among the
 // deleted tokens before every later unit.
 //
-// Two kernels on the caller's stream:
-//   plan  one workgroup per segment (a single wave up to 512 units).  Exclusive scans over
-//         units give each kept unit its destination offset, its rank (= new unit id) and the
-//         number of deleted live tokens before it; a rank table {offset, first slot,
-//         deleted-before} with a sentinel, and for every destination tile the rank of the unit
-//         holding its first row, go to the workspace.
-//   copy  one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
-//         source slots from the rank table (short forward walk from the tile's hint), tags are
-//         written, then every thread moves 16-byte vectors of the K and V rows.  Rows are whole
-//         2 KB (bf16, 8 heads x 128) runs, so reads and writes are fully coalesced; source and
-//         destination never alias, so a single pass is safe (no scratch round trip).
+// Plan: exclusive scans over units give each kept unit its destination offset, its rank (= new
+// unit id) and the number of deleted live tokens before it.  Up to 512 units every copy
+// workgroup builds this table in LDS itself (wave 0, wave scans), so the compaction is a single
+// kernel; beyond, a plan kernel (1024 threads) writes it to the workspace together with, for
+// every destination tile, the rank of the unit holding the tile's first row.
+// Copy: one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
+// source slots (binary search over the LDS table, or a short forward walk from the workspace
+// hint), tags are written, then every thread moves 16-byte vectors of the K and V rows.  Rows
+// are whole 2 KB (bf16, 8 heads x 128) runs, so reads and writes are fully coalesced; source and
+// destination never alias, so a single pass is safe (no scratch round trip).
 #include "common.h"
 #include "kernels.h"
 
@@ -119,8 +118,7 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
   }
 }
 
-// Single-wave plan for U <= 512 (each lane owns 8 consecutive units): the same tables as
-// compact_plan_kernel with wave-level scans, no workgroup barriers.
+// Up to 512 units one wave plans (each lane owns 8 consecutive units, wave-level scans).
 constexpr int kSmallUnits = 512;
 constexpr int kSmallPer = kSmallUnits / kWave;
 
@@ -130,97 +128,99 @@ __device__ inline int wave_excl(int v, int* total) {
   return inc - v;
 }
 
-__global__ __launch_bounds__(kWave) void compact_plan_small_kernel(
-    const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ keep_len_g,
-    const int32_t* __restrict__ len_g, const int32_t* __restrict__ first_g, int n_units,
-    int chunk_len, int cap_dst, int page_size,
-    int32_t* __restrict__ remap_g, int32_t* __restrict__ n_ctx_g,
-    int32_t* __restrict__ n_pages_g, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
-  const int seg = blockIdx.x;
-  const int lane = threadIdx.x;
-  const int U = n_units;
-  const int u0 = lane * kSmallPer;
-  const size_t base = static_cast<size_t>(seg) * U;
-  const WsLayout L = ws_layout(U, cap_dst);
-  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
-  RankRec* rank = reinterpret_cast<RankRec*>(wseg + L.rank_off);
-  int32_t* tile_hint = reinterpret_cast<int32_t*>(wseg + L.tile_off);
-  int32_t* meta = reinterpret_cast<int32_t*>(wseg + L.meta_off);
+// Fused plan (U <= kSmallUnits): every copy workgroup has wave 0 scan the units into LDS (the
+// tables compact_plan_kernel writes to the workspace), so the compaction is one kernel.
+// Workgroup (0, seg) also writes unit_remap, n_ctx, n_pages and the capacity status.
+template <bool FUSED>
+struct TilePlan {};
+template <>
+struct TilePlan<true> {
+  int32_t roff[kSmallUnits + 1];   // destination offset of each kept rank (+ sentinel)
+  int32_t rfirst[kSmallUnits];     // first source slot of each kept rank
+  int32_t rdel[kSmallUnits];       // deleted live tokens before each kept rank
+  int32_t kept, n_kept;
+};
 
-  int nl[kSmallPer], fs[kSmallPer], kq[kSmallPer];
+struct FusedPlanArgs {
+  const uint8_t* keep;
+  const int32_t* keep_len;
+  const int32_t* len;
+  const int32_t* first;
+  int page_size;
+  int32_t* remap;
+  int32_t* n_ctx;
+  int32_t* n_pages;
+  int32_t* status;
+};
+
+__device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_dst,
+                                   const FusedPlanArgs& f, TilePlan<true>& P) {
+  const bool writer = blockIdx.x == 0;
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    const int U = n_units;
+    const int u0 = lane * kSmallPer;
+    const size_t base = static_cast<size_t>(seg) * U;
+    int nl[kSmallPer], fs[kSmallPer], kq[kSmallPer];
 #pragma unroll
-  for (int i = 0; i < kSmallPer; ++i) {      // all loads first: one memory round trip
-    const int u = min(u0 + i, U - 1);
-    nl[i] = len_g[base + u];
-    fs[i] = first_g[base + u];
-    kq[i] = keep_len_g != nullptr ? keep_len_g[base + u]
-                                  : (keep_g[base + u] != 0 ? INT32_MAX : 0);
-  }
-  int kl[kSmallPer], dl[kSmallPer];
-  int my_k = 0, my_d = 0, my_n = 0;
+    for (int i = 0; i < kSmallPer; ++i) {        // all loads first: one memory round trip
+      const int u = min(u0 + i, U - 1);
+      nl[i] = f.len[base + u];
+      fs[i] = f.first[base + u];
+      kq[i] = f.keep_len != nullptr ? f.keep_len[base + u]
+                                    : (f.keep[base + u] != 0 ? INT32_MAX : 0);
+    }
+    int kl[kSmallPer], dl[kSmallPer];
+    int my_k = 0, my_d = 0, my_n = 0;
 #pragma unroll
-  for (int i = 0; i < kSmallPer; ++i) {
-    const int n = (u0 + i < U) ? max(nl[i], 0) : 0;
-    kl[i] = min(max(kq[i], 0), n);
-    dl[i] = n - kl[i];
-    my_k += kl[i];
-    my_d += dl[i];
-    my_n += kl[i] > 0 ? 1 : 0;
-  }
-  __shared__ int32_t roff[kSmallUnits + 1];      // destination offset of each kept rank
-  int kept, dropped, n_kept;
-  int off = wave_excl(my_k, &kept);
-  int del = wave_excl(my_d, &dropped);
-  int rk = wave_excl(my_n, &n_kept);
-  (void)dropped;
+    for (int i = 0; i < kSmallPer; ++i) {
+      const int n = (u0 + i < U) ? max(nl[i], 0) : 0;
+      kl[i] = min(max(kq[i], 0), n);
+      dl[i] = n - kl[i];
+      my_k += kl[i];
+      my_d += dl[i];
+      my_n += kl[i] > 0 ? 1 : 0;
+    }
+    int kept, dropped, n_kept;
+    int off = wave_excl(my_k, &kept);
+    int del = wave_excl(my_d, &dropped);
+    int rk = wave_excl(my_n, &n_kept);
+    (void)dropped;
 #pragma unroll
-  for (int i = 0; i < kSmallPer; ++i) {
-    const int u = u0 + i;
-    if (u < U) {
-      if (kl[i] > 0) {
-        rank[rk] = RankRec{off, fs[i], del, 0};
-        roff[rk] = off;
-        remap_g[base + u] = rk;
-        ++rk;
-      } else {
-        remap_g[base + u] = -1;
+    for (int i = 0; i < kSmallPer; ++i) {
+      const int u = u0 + i;
+      if (u < U) {
+        if (kl[i] > 0) {
+          P.roff[rk] = off;
+          P.rfirst[rk] = fs[i];
+          P.rdel[rk] = del;
+          if (writer) f.remap[base + u] = rk;
+          ++rk;
+        } else if (writer) {
+          f.remap[base + u] = -1;
+        }
+      }
+      off += kl[i];
+      del += dl[i];
+    }
+    if (lane == 0) {
+      P.roff[n_kept] = kept;
+      P.kept = kept;
+      P.n_kept = n_kept;
+      if (writer) {
+        const int nctx = kept + chunk_len;
+        if (nctx > cap_dst) {
+          set_status(f.status, OMNITIDE_E_CAPACITY);
+          f.n_ctx[seg] = 0;
+          f.n_pages[seg] = 0;
+        } else {
+          f.n_ctx[seg] = nctx;
+          f.n_pages[seg] = (nctx + f.page_size - 1) / f.page_size;
+        }
       }
     }
-    off += kl[i];
-    del += dl[i];
   }
-  if (lane == 0) roff[n_kept] = kept;
   __syncthreads();
-  // Tile hints: lane takes a contiguous range of destination tiles, binary-searches the rank of
-  // its first tile's first row, then walks forward.
-  const int n_tiles = (kept + kTile - 1) / kTile;
-  const int per_lane = (n_tiles + kWave - 1) / kWave;
-  const int t0 = lane * per_lane, t1 = min(t0 + per_lane, n_tiles);
-  if (t0 < t1) {
-    int lo = 0, hi = n_kept - 1;                  // largest k with roff[k] <= t0 * kTile
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (roff[mid] <= t0 * kTile) lo = mid; else hi = mid - 1;
-    }
-    for (int t = t0; t < t1; ++t) {
-      while (roff[lo + 1] <= t * kTile) ++lo;
-      tile_hint[t] = lo;
-    }
-  }
-  if (lane == 0) {
-    rank[n_kept] = RankRec{kept, 0, 0, 0};
-    const int nctx = kept + chunk_len;
-    meta[0] = kept;
-    meta[1] = n_kept;
-    if (nctx > cap_dst) {
-      set_status(status, OMNITIDE_E_CAPACITY);
-      n_ctx_g[seg] = 0;
-      n_pages_g[seg] = 0;
-    } else {
-      n_ctx_g[seg] = nctx;
-      n_pages_g[seg] = (nctx + page_size - 1) / page_size;
-    }
-  }
 }
 
 // Writes the tags of destination tile t and resolves its rows: src_row[i] is the source slot of
@@ -237,7 +237,7 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
                                    int32_t* __restrict__ pos_dst,
                                    int32_t* __restrict__ src_of_dst,
                                    const uint8_t* __restrict__ ws, int32_t* src_row,
-                                   int32_t* shift_row) {
+                                   int32_t* shift_row, const TilePlan<true>* plan = nullptr) {
   const int tid = threadIdx.x;
   const int r0 = t * kTile;
   const size_t dst_tag = static_cast<size_t>(seg) * cap_dst;
@@ -253,19 +253,30 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
   if (r0 >= nctx) return 0;
   const int nrows = min(kTile, nctx - r0);
   const int kept = nctx - chunk_len;
-  const WsLayout L = ws_layout(n_units, cap_dst);
-  const uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
-  const RankRec* rank = reinterpret_cast<const RankRec*>(wseg + L.rank_off);
-  const int32_t* tile_hint = reinterpret_cast<const int32_t*>(wseg + L.tile_off);
-  const int32_t* meta = reinterpret_cast<const int32_t*>(wseg + L.meta_off);
   const size_t src_tag = static_cast<size_t>(seg) * n_slots;
 
   if (tid < nrows) {
     const int r = r0 + tid;
     if (r < kept) {
-      int k = tile_hint[t];
-      while (rank[k + 1].off <= r) ++k;
-      const RankRec rec = rank[k];
+      int k;
+      RankRec rec;
+      if (plan != nullptr) {                      // largest kept rank k with roff[k] <= r
+        int lo = 0, hi = plan->n_kept - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (plan->roff[mid] <= r) lo = mid; else hi = mid - 1;
+        }
+        k = lo;
+        rec = RankRec{plan->roff[k], plan->rfirst[k], plan->rdel[k], 0};
+      } else {
+        const WsLayout L = ws_layout(n_units, cap_dst);
+        const uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+        const RankRec* rank = reinterpret_cast<const RankRec*>(wseg + L.rank_off);
+        const int32_t* tile_hint = reinterpret_cast<const int32_t*>(wseg + L.tile_off);
+        k = tile_hint[t];
+        while (rank[k + 1].off <= r) ++k;
+        rec = rank[k];
+      }
       const int s = rec.first + (r - rec.off);
       uid_dst[dst_tag + r] = k;
       mod_dst[dst_tag + r] = mod_src[src_tag + s];
@@ -275,7 +286,16 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
       if (shift_row) shift_row[tid] = -rec.del;
     } else {
       const int i = r - kept;
-      uid_dst[dst_tag + r] = meta[1] + chunk_unit[i];
+      int n_kept_units;
+      if (plan != nullptr) {
+        n_kept_units = plan->n_kept;
+      } else {
+        const WsLayout L = ws_layout(n_units, cap_dst);
+        const int32_t* meta = reinterpret_cast<const int32_t*>(
+            ws + static_cast<size_t>(seg) * L.seg_bytes + L.meta_off);
+        n_kept_units = meta[1];
+      }
+      uid_dst[dst_tag + r] = n_kept_units + chunk_unit[i];
       mod_dst[dst_tag + r] = chunk_mod[i];
       pos_dst[dst_tag + r] = kept + i;
       src_of_dst[dst_tag + r] = -1;
@@ -287,7 +307,7 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
   return nrows;
 }
 
-template <int VPT>
+template <int VPT, bool FUSED>
 __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
     const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
     int row_bytes, const uint8_t* __restrict__ mod_src,
@@ -297,16 +317,26 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
     uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
     uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
     int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
-    const uint8_t* __restrict__ ws) {
+    const uint8_t* __restrict__ ws, FusedPlanArgs fp) {
   constexpr int RB = VPT >= 16 ? 1 : 16 / VPT;
   __shared__ int32_t src_row[kTile];
+  __shared__ TilePlan<FUSED> plan;
   const int seg = blockIdx.y;
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
-  const int nctx = n_ctx_g[seg];
+  int nctx;
+  const TilePlan<true>* pp = nullptr;
+  if constexpr (FUSED) {
+    plan_in_lds(seg, n_units, chunk_len, cap_dst, fp, plan);
+    nctx = plan.kept + chunk_len;
+    if (nctx > cap_dst) nctx = 0;                 // capacity error: every row becomes empty
+    pp = &plan;
+  } else {
+    nctx = n_ctx_g[seg];
+  }
   const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
                                  pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, nullptr);
+                                 src_of_dst, ws, src_row, nullptr, pp);
   if (nrows == 0) return;
   const int r0 = t * kTile;
 
@@ -354,17 +384,22 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
   }
 }
 
-template <int VPT>
+FusedPlanArgs fused_args(const CompactArgs& a) {
+  return FusedPlanArgs{a.keep, a.keep_len, a.unit_len, a.unit_first, a.page_size,
+                       a.unit_remap, a.n_ctx, a.n_pages, a.d_status};
+}
+
+template <int VPT, bool FUSED>
 hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
   const dim3 grid((a.cap_dst + kTile - 1) / kTile, a.n_seg);
-  hipLaunchKernelGGL((compact_copy_kernel<VPT>), grid, dim3(kCopyThreads), 0, stream,
+  hipLaunchKernelGGL((compact_copy_kernel<VPT, FUSED>), grid, dim3(kCopyThreads), 0, stream,
                      static_cast<const uint8_t*>(a.k_src), static_cast<const uint8_t*>(a.v_src),
                      a.n_slots_src, a.row_bytes, a.modality_src, a.pos_src,
                      static_cast<const uint8_t*>(a.k_chunk), static_cast<const uint8_t*>(a.v_chunk),
                      a.chunk_modality, a.chunk_unit, a.chunk_len, static_cast<uint8_t*>(a.k_dst),
                      static_cast<uint8_t*>(a.v_dst), a.cap_dst, a.n_units, a.unit_id_dst,
                      a.modality_dst, a.pos_dst, a.src_of_dst, a.n_ctx,
-                     static_cast<const uint8_t*>(a.workspace));
+                     static_cast<const uint8_t*>(a.workspace), fused_args(a));
   return hipGetLastError();
 }
 
@@ -380,7 +415,7 @@ hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
 // table (rows x rot_dims/2) is built in LDS once and shared by all heads.
 constexpr int kMaxHalfRot = 64;     // rot_dims <= head_dim <= 128
 
-template <int EB, bool HALF>
+template <int EB, bool HALF, bool FUSED>
 __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
     int n_kv_heads, int head_dim, const uint8_t* __restrict__ mod_src,
@@ -390,21 +425,31 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
     uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
     int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
-    const uint8_t* __restrict__ ws, double rope_base, int rot_dims) {
+    const uint8_t* __restrict__ ws, double rope_base, int rot_dims, FusedPlanArgs fp) {
   constexpr int EPC = 16 / EB;                    // elements per 16-byte chunk
   __shared__ int32_t src_row[kTile];
   __shared__ int32_t shift_row[kTile];
   __shared__ double theta[kMaxHalfRot];
   __shared__ float2 cs[kTile][kMaxHalfRot];
+  __shared__ TilePlan<FUSED> plan;
   const int seg = blockIdx.y;
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
-  const int nctx = n_ctx_g[seg];
   const int half = rot_dims / 2;
   if (tid < half) theta[tid] = pow(rope_base, -2.0 * tid / rot_dims);
+  int nctx;
+  const TilePlan<true>* pp = nullptr;
+  if constexpr (FUSED) {
+    plan_in_lds(seg, n_units, chunk_len, cap_dst, fp, plan);
+    nctx = plan.kept + chunk_len;
+    if (nctx > cap_dst) nctx = 0;
+    pp = &plan;
+  } else {
+    nctx = n_ctx_g[seg];
+  }
   const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
                                  pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, shift_row);
+                                 src_of_dst, ws, src_row, shift_row, pp);
   if (nrows == 0) return;
   const int r0 = t * kTile;
   constexpr double kTwoPi = 6.283185307179586476925286766559;
@@ -519,17 +564,19 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
   }
 }
 
-template <int EB, bool HALF>
+template <int EB, bool HALF, bool FUSED>
 hipError_t launch_copy_rope(const CompactArgs& a, hipStream_t stream) {
   const dim3 grid((a.cap_dst + kTile - 1) / kTile, a.n_seg);
-  hipLaunchKernelGGL((compact_copy_rope_kernel<EB, HALF>), grid, dim3(kCopyThreads), 0, stream,
+  hipLaunchKernelGGL((compact_copy_rope_kernel<EB, HALF, FUSED>), grid, dim3(kCopyThreads), 0,
+                     stream,
                      static_cast<const uint8_t*>(a.k_src), static_cast<const uint8_t*>(a.v_src),
                      a.n_slots_src, a.n_kv_heads, a.head_dim, a.modality_src, a.pos_src,
                      static_cast<const uint8_t*>(a.k_chunk), static_cast<const uint8_t*>(a.v_chunk),
                      a.chunk_modality, a.chunk_unit, a.chunk_len, static_cast<uint8_t*>(a.k_dst),
                      static_cast<uint8_t*>(a.v_dst), a.cap_dst, a.n_units, a.unit_id_dst,
                      a.modality_dst, a.pos_dst, a.src_of_dst, a.n_ctx,
-                     static_cast<const uint8_t*>(a.workspace), a.rope_base, a.rope_dims);
+                     static_cast<const uint8_t*>(a.workspace), a.rope_base, a.rope_dims,
+                     fused_args(a));
   return hipGetLastError();
 }
 
@@ -539,33 +586,35 @@ size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
   return ws_layout(n_units, cap_dst).seg_bytes * static_cast<size_t>(n_seg);
 }
 
-hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
-  if (a.n_units <= kSmallUnits)
-    hipLaunchKernelGGL(compact_plan_small_kernel, dim3(a.n_seg), dim3(kWave), 0, stream, a.keep,
-                       a.keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst,
-                       a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
-                       static_cast<uint8_t*>(a.workspace), a.d_status);
-  else
-    hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream,
-                       a.keep, a.keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len,
-                       a.cap_dst, a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
-                       static_cast<uint8_t*>(a.workspace), a.d_status);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+template <bool FUSED>
+hipError_t launch_copies(const CompactArgs& a, hipStream_t stream) {
   if (a.rope_dims > 0) {
     const int eb = a.row_bytes / (a.n_kv_heads * a.head_dim);
-    if (eb == 2) return a.rope_half ? launch_copy_rope<2, true>(a, stream)
-                                    : launch_copy_rope<2, false>(a, stream);
-    return a.rope_half ? launch_copy_rope<4, true>(a, stream)
-                       : launch_copy_rope<4, false>(a, stream);
+    if (eb == 2) return a.rope_half ? launch_copy_rope<2, true, FUSED>(a, stream)
+                                    : launch_copy_rope<2, false, FUSED>(a, stream);
+    return a.rope_half ? launch_copy_rope<4, true, FUSED>(a, stream)
+                       : launch_copy_rope<4, false, FUSED>(a, stream);
   }
   const int vecs2 = 2 * a.row_bytes / 16;
   const int vpt = (vecs2 + kCopyThreads - 1) / kCopyThreads;
-  if (vpt <= 1) return launch_copy<1>(a, stream);
-  if (vpt <= 2) return launch_copy<2>(a, stream);
-  if (vpt <= 4) return launch_copy<4>(a, stream);
-  if (vpt <= 8) return launch_copy<8>(a, stream);
+  if (vpt <= 1) return launch_copy<1, FUSED>(a, stream);
+  if (vpt <= 2) return launch_copy<2, FUSED>(a, stream);
+  if (vpt <= 4) return launch_copy<4, FUSED>(a, stream);
+  if (vpt <= 8) return launch_copy<8, FUSED>(a, stream);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
+  // Up to 512 units every copy workgroup plans for itself (one kernel); beyond, a plan kernel
+  // writes the rank table and tile hints to the workspace first.
+  if (a.n_units <= kSmallUnits) return launch_copies<true>(a, stream);
+  hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream, a.keep,
+                     a.keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst,
+                     a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
+                     static_cast<uint8_t*>(a.workspace), a.d_status);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_copies<false>(a, stream);
 }
 
 }  // namespace omnitide
