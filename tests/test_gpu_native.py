@@ -378,3 +378,62 @@ def test_place_chunk_capacity_error():
     torch.cuda.synchronize()
     assert int(host(g["st"])[0]) == -5 and int(host(slot)[0]) == -1
     assert np.array_equal(host(g["uid"]), uid)
+
+
+def test_native_kernels_several_segments():
+    """Eviction, suffix packing and placement on two segments in one call each (segment 0: the
+    whole-unit plan, segment 1: arbitrary kept prefixes)."""
+    from paper_2609_34653_amd import omnitide as ot
+    cfg, lay, seg, g0, h0 = native_state("single_layer_8k", plan="whole")
+    _, _, _, g1, h1 = native_state("single_layer_8k", plan="prefix", seed_keep=9)
+    U, cap, L = lay.n_units, len(h0["uid"]), lay.chunk_len
+    cat = lambda key: torch.cat([g0[key].view(-1), g1[key].view(-1)]).contiguous()  # noqa: E731
+    uid, pos, mod = cat("uid"), cat("pos"), cat("mod")
+    k = torch.cat([g0["k"], g1["k"]]).contiguous()
+    v = torch.cat([g0["v"], g1["v"]]).contiguous()
+    remap = i32(np.zeros(2 * U))
+    kept, nku, span, st = i32([0, 0]), i32([0, 0]), i32([0, 0]), i32([0])
+    ws = torch.zeros(ot.omnitide_evict_native_workspace_bytes(2, U), dtype=torch.uint8,
+                     device="cuda")
+    ot.omnitide_evict_native(uid, pos, 2, U, cat("len"), remap, kept, nku, span, ws,
+                             keep_len=cat("keep_len"), d_status=st)
+    H, d = seg.k_hist.shape[1], seg.k_hist.shape[2]
+    wsp = torch.zeros(ot.omnitide_pack_suffix_workspace_bytes(0, 2, cap, H, d),
+                      dtype=torch.uint8, device="cuda")
+    cut, moved = i32([0, 0]), i32([0, 0])
+    ot.omnitide_pack_suffix(k, v, 64, 1, uid, mod, pos, span, cut, moved, wsp)
+    kc = torch.stack([seg.k_chunk, seg.k_chunk]).cuda().contiguous()
+    vc = torch.stack([seg.v_chunk, seg.v_chunk]).cuda().contiguous()
+    slot = i32([0, 0])
+    wsc = torch.zeros(ot.omnitide_place_chunk_workspace_bytes(2, cap), dtype=torch.uint8,
+                      device="cuda")
+    ot.omnitide_place_chunk(k, v, uid, mod, pos, kc, vc, dev(lay.chunk_modality),
+                            dev(lay.chunk_unit), kept, nku, slot, span, wsc, d_status=st)
+    torch.cuda.synchronize()
+    assert int(host(st)[0]) == 0
+    for si, h in enumerate((h0, h1)):
+        kl = np.minimum(np.maximum(h["keep_len"], 0), h["sc"]["len"])
+        ev = oracle.evict_logical(h["uid"], h["pos"], kl, U)
+        assert np.array_equal(host(remap)[si * U:(si + 1) * U], ev["unit_remap"])
+        assert int(host(kept)[si]) == ev["kept"] and int(host(nku)[si]) == ev["n_kept_units"]
+        c, _ = oracle.plan_suffix(ev["unit_id"] >= 0, 64, 1)
+        assert int(host(cut)[si]) == c
+        if c >= 0:
+            pk = oracle.pack_suffix(h["k"], h["v"], ev["unit_id"], h["mod"], ev["pos"], c)
+        else:
+            pk = dict(k=h["k"], v=h["v"], unit_id=ev["unit_id"], modality=h["mod"],
+                      pos=ev["pos"], moved=0)
+        assert int(host(moved)[si]) == pk["moved"]
+        s0 = oracle.place_chunk(pk["unit_id"], L, cap)
+        assert int(host(slot)[si]) == s0
+        want_uid = pk["unit_id"].copy()
+        want_pos = pk["pos"].copy()
+        want_uid[s0:s0 + L] = ev["n_kept_units"] + lay.chunk_unit
+        want_pos[s0:s0 + L] = ev["kept"] + np.arange(L)
+        sl = slice(si * cap, (si + 1) * cap)
+        assert np.array_equal(host(uid)[sl], want_uid)
+        assert np.array_equal(host(pos)[sl], want_pos)
+        want_k = pk["k"].copy()
+        want_k[s0:s0 + L] = storage_np(seg.k_chunk)
+        assert np.array_equal(storage_np(k[si]), want_k)
+        assert int(host(span)[si]) == oracle.span_of(want_uid)
