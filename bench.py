@@ -31,7 +31,7 @@ WORKLOAD = "history_80k"
 CSRC = os.path.join(ROOT, "paper_2609_34653_amd", "csrc")
 
 # HBM traffic of one call of each stage on the default workload, from two rocprofv3 --pmc passes
-# over `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0
+# over `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0 --no-ceilings
 # --copy-calibration-mb 1024` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, summed over the stage's kernels).  Scaled by what the same
 # counters read for the calibration copy (1 GiB read + 1 GiB written by one elementwise kernel):
 # FETCH_SIZE reads 524,297 KiB for 1,048,576 KiB fetched (x2.000), WRITE_SIZE reads 1,048,576 KiB
@@ -124,6 +124,8 @@ def main():
                     help="run a plain elementwise copy kernel (reads and writes this many MiB) "
                          "three times before the warmup: a known-size reference for hardware "
                          "byte counters")
+    ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
+                    help="skip the measured-ceiling probes (library GEMM, device copy)")
     ap.add_argument("--loop-steps", type=int, default=64,
                     help="steps of the stream-loop layout comparison (0 = skip)")
     ap.add_argument("--no-graph", action="store_true",
@@ -398,9 +400,71 @@ def main():
                      "traffic": kernels["attend"]["traffic"]},
         "wall_s_timed_region": round(wall, 4),
     }
+    if args.ceilings:
+        result["measured_ceilings"] = measured_ceilings(dev)
+        c = result["measured_ceilings"]
+        result["roofline"]["frac_of_measured_mfma"] = round(attn_tflops / c["mfma_bf16_tflops"], 4)
+        for k in ("score", "compact"):
+            kernels[k]["frac_of_measured_copy"] = round(kernels[k]["GBps"] / 1e3 /
+                                                        c["copy_tbps"], 4)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, stream, seg, flops)
     print(json.dumps(result), flush=True)
+
+
+def measured_ceilings(dev):
+    """What this chip sustains right now, beside the published peaks: a large bf16 GEMM through
+    the vendor library (torch.matmul; 8192^3, fp32 accumulate), an elementwise copy of 1 GiB in /
+    1 GiB out (torch.neg), each the best of 5 timed launches, and an MFMA-only probe with the
+    shader clock it ran at."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def best(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1))
+        return min(t) * 1e-3
+    n = 8192
+    a = torch.randn(n, n, device=dev).to(torch.bfloat16)
+    b = torch.randn(n, n, device=dev).to(torch.bfloat16)
+    gemm_s = best(lambda: torch.matmul(a, b))
+    del a, b
+    x = torch.ones((1 << 30) // 4, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    copy_s = best(lambda: torch.neg(x, out=y))
+    del x, y
+    out = {"gemm_bf16_tflops": round(2.0 * n ** 3 / gemm_s / 1e12, 1),
+           "copy_tbps": round(2.0 * (1 << 30) / copy_s / 1e12, 3),
+           "method": "torch.matmul bf16 8192^3 and torch.neg over 1 GiB, best of 5"}
+    # Matrix-core probe (libomnitide_probe.so): 1,024 workgroups x 4 waves, each wave four
+    # independent 32x32x16 bf16 MFMA chains; shader clock from wave 0's counters.
+    import ctypes
+    from paper_2609_34653_amd import build as b
+    probe = ctypes.CDLL(b.PROBE_PATH)
+    probe.omnitide_probe_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p]
+    n_wg, iters = 1024, 20000
+    sink = torch.empty(n_wg * 256, device=dev)
+    clocks = torch.zeros(2, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def run_probe():
+        if probe.omnitide_probe_mfma(n_wg, iters, ctypes.c_void_p(sink.data_ptr()),
+                                     ctypes.c_void_p(clocks.data_ptr()), stream) != 0:
+            raise RuntimeError("probe launch failed")
+    probe_s = best(run_probe, 3)
+    cyc, ticks = (int(x) for x in clocks.cpu())
+    out["mfma_bf16_tflops"] = round(n_wg * 4 * iters * 4 * 32768 / probe_s / 1e12, 1)
+    out["sclk_ghz_under_mfma"] = round(cyc / (ticks / 100e6) / 1e9, 3) if ticks else None
+    out["method"] += ("; an MFMA-only probe (1,024 x 4 waves x 20,000 x 4 independent "
+                      "32x32x16 bf16 MFMAs) with the shader clock of its first wave")
+    return out
 
 
 def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_graph=True):

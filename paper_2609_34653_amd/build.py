@@ -1,4 +1,5 @@
-"""Build libomnitide.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Build libomnitide.so (the HIP kernels and the C ABI) and libomnitide_probe.so (a
+matrix-core rate probe used by the benchmark) for gfx950 with hipcc.
 
 Usage: python -m paper_2609_34653_amd.build   (or call build()).  Always recompiles.
 """
@@ -17,6 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_NAME = "libomnitide.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
+PROBE_PATH = os.path.join(PKG, "libomnitide_probe.so")
 ARCH = "gfx950"
 
 SOURCES = ["abi.cpp", "score.hip", "select.hip", "spans.hip", "compact.hip", "native.hip",
@@ -50,18 +52,24 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB_PATH + ".tmp"
+def _link(objs, path: str, verbose: bool) -> None:
+    tmp = path + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"linking {LIB_NAME} failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB_PATH)
+        raise RuntimeError(f"linking {os.path.basename(path)} failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, path)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = SOURCES + ["probe.hip"]
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
+    _link(objs[:-1], LIB_PATH, verbose)
+    _link(objs[-1:], PROBE_PATH, verbose)
     return LIB_PATH
 
 
