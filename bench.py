@@ -48,11 +48,28 @@ COUNTER_TRAFFIC = {
 }
 
 
-def graph_time_us(fn, reps, dev, use_graph=True):
-    """(mean GPU time in us, method) of fn() over `reps` calls: captured in one HIP graph and
-    replayed (the calls are too short for host-side launches to keep the GPU busy); if capture
-    fails, or use_graph is False, timed with events around host launches instead."""
+def graph_time(fn, reps, dev, use_graph=True, replays=5):
+    """GPU time of fn() over `reps` calls, captured in one HIP graph and replayed (the calls are
+    too short for host-side launches to keep the GPU busy); if capture fails, or use_graph is
+    False, timed with events around host launches instead.  After one untimed replay (or loop),
+    `replays` replays are timed one by one: returns {"us": mean per call over all of them,
+    "us_p10"/"us_p50"/"us_p90": percentiles of the per-replay means, "timing": method,
+    "replays", "calls_per_replay"}."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(run):
+        run()
+        torch.cuda.synchronize()
+        per = []
+        for _ in range(replays):
+            e0.record()
+            run()
+            e1.record()
+            torch.cuda.synchronize()
+            per.append(e0.elapsed_time(e1) / reps * 1e3)
+        return per
+
+    how = "graph replay"
     try:
         if not use_graph:
             raise RuntimeError("graph capture disabled")
@@ -66,21 +83,25 @@ def graph_time_us(fn, reps, dev, use_graph=True):
         with torch.cuda.graph(g):
             for i in range(reps):
                 fn(i)
-        g.replay()
-        torch.cuda.synchronize()
-        e0.record()
-        g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / reps * 1e3, "graph replay"
+        per = timed(g.replay)
+        del g
     except Exception:  # pragma: no cover - capture unsupported or disabled
         torch.cuda.synchronize()
-        e0.record()
-        for i in range(reps):
-            fn(i)
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / reps * 1e3, "events around host launches"
+        how = "events around host launches"
+
+        def loop():
+            for i in range(reps):
+                fn(i)
+        per = timed(loop)
+    p10, p50, p90 = np.percentile(per, [10, 50, 90])
+    return {"us": float(np.mean(per)), "us_p10": float(p10), "us_p50": float(p50),
+            "us_p90": float(p90), "timing": how, "replays": replays, "calls_per_replay": reps}
+
+
+def graph_time_us(fn, reps, dev, use_graph=True):
+    """(mean GPU time per call in us, method): graph_time without the distribution."""
+    r = graph_time(fn, reps, dev, use_graph)
+    return r["us"], r["timing"]
 
 
 def counter_traffic(stage, config):
@@ -112,6 +133,11 @@ def compact_bytes(kept, L, H, d, elt, cap, U):
     return 2 * row * (2 * kept + 2 * L) + kept * 9 + L * 5 + cap * 13 + U * 13
 
 
+def progress(msg):
+    """One line on stderr as each part of the run finishes (the JSON result goes to stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,6 +154,8 @@ def main():
                     help="skip the measured-ceiling probes (library GEMM, device copy)")
     ap.add_argument("--loop-steps", type=int, default=64,
                     help="steps of the stream-loop layout comparison (0 = skip)")
+    ap.add_argument("--no-other-configs", dest="other_configs", action="store_false",
+                    help="skip the single-layer 8K and 36-layer 32K measurements")
     ap.add_argument("--no-graph", action="store_true",
                     help="time the standalone calls with events around host launches instead of "
                          "one captured HIP graph (for counter passes)")
@@ -230,6 +258,14 @@ def main():
         torch.cuda.synchronize()
         wall = time.perf_counter() - wall0
         ms_per_step = start.elapsed_time(end) / args.steps
+        # the spread: four more replays of the same K steps, each timed on its own
+        step_replays = [ms_per_step]
+        for _ in range(4):
+            start.record(s)
+            g.replay()
+            end.record(s)
+            torch.cuda.synchronize()
+            step_replays.append(start.elapsed_time(end) / args.steps)
         out_graph = st.out.clone()
         step(args.warmup + args.steps - 1)
         torch.cuda.synchronize()
@@ -240,6 +276,7 @@ def main():
         if not args.no_graph and "differs" in str(exc):
             raise
         step_timing = "host launches"
+        step_replays = None
         wall0 = time.perf_counter()
         start.record(s)
         for i in range(args.steps):
@@ -270,10 +307,11 @@ def main():
             else:
                 st.attend(c["q"], cfg.scale)
         return f
-    us = {}
-    how = "graph replay"
+    progress(f"step: {ms_per_step:.4f} ms per step ({step_timing})")
+    us, dist = {}, {}
     for j, n in enumerate(names):
-        us[n], how = graph_time_us(call(n), 4 * args.steps, dev, not args.no_graph)
+        dist[n] = graph_time(call(n), 4 * args.steps, dev, not args.no_graph)
+        us[n] = dist[n]["us"]
     torch.cuda.synchronize()
 
     flops = attn_flops(L, kept, Hq, d)
@@ -291,7 +329,8 @@ def main():
         "attend": {"us": us["attend"], "flops": flops, "TFLOPs": attn_tflops},
     }
     for j, n in enumerate(names):
-        kernels[n]["timing"] = how
+        for key in ("us_p10", "us_p50", "us_p90", "timing", "replays", "calls_per_replay"):
+            kernels[n][key] = dist[n][key]
         kernels[n]["us_host_launched"] = avg[j] * 1e3
     for k in ("score", "compact"):
         kernels[k]["frac_hbm"] = kernels[k]["GBps"] / HBM_PEAK_GBPS
@@ -373,11 +412,17 @@ def main():
                                                   4),
                                 "kept_tokens": kept_sp, "in_step": False}
 
+    progress("per-call timings done")
     kernels["layouts"] = layout_ablation(ot, st, copies[0], lay, cfg, L, H, Hq, d, dev,
                                          args.steps, n_ctx, not args.no_graph)
 
+    progress("layout comparison done")
     if args.loop_steps > 0:
         kernels["stream_loop_layouts"] = stream_loop_ablation(ot, dev, args.loop_steps)
+        progress("stream loop done")
+    if args.other_configs:
+        kernels["other_configs"] = other_configs(dev, args.steps, not args.no_graph)
+        progress("other workloads done")
 
     value = flops / (ms_per_step * 1e-3) / 1e12
     result = {
@@ -385,6 +430,11 @@ def main():
         "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "step_timing": step_timing,
         "ms_per_step_host_launched": round(launched_ms_per_step, 4), "higher_is_better": True,
+        "ms_per_step_replays": (None if step_replays is None else
+                                {"timed_replay_and_4_more": [round(x, 4) for x in step_replays],
+                                 "p10": round(float(np.percentile(step_replays, 10)), 4),
+                                 "p50": round(float(np.percentile(step_replays, 50)), 4),
+                                 "p90": round(float(np.percentile(step_replays, 90)), 4)}),
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.description}", "history_slots": lay.n_slots,
                    "live_tokens": int((lay.unit_id >= 0).sum()), "units": lay.n_units,
@@ -408,6 +458,7 @@ def main():
             kernels[k]["frac_of_measured_copy"] = round(kernels[k]["GBps"] / 1e3 /
                                                         c["copy_tbps"], 4)
     if not args.no_cpu_baseline:
+        progress("CPU oracle baseline ...")
         result["cpu_baseline"] = cpu_baseline(cfg, stream, seg, flops)
     print(json.dumps(result), flush=True)
 
@@ -586,7 +637,8 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     flags (their unit ids and positions coincide with the eager pool's).  Attention over a
     native pool runs twice per step: skipping empty 64-slot tiles, and traversing the whole
     span (as kernels without tile skipping do).  Attention and maintenance are timed with events
-    around their launches; spans and active pages are recorded per step."""
+    around their launches (the per-step latency percentiles come from the same events); spans
+    and active pages are recorded per step."""
     from paper_2609_34653_amd.step import StreamStep
     cfg = sg.CONFIG_BY_NAME["stream_loop_64x665"]
     stream = sg.make_stream(cfg)
@@ -638,7 +690,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap_n, L, Hq, H, d),
                        dtype=torch.uint8, device=dev)
     names = ["eager"] + list(pools)
-    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
           for n in names}
     spans = {n: torch.zeros(steps, **i32) for n in names}
     active = {n: torch.zeros(steps, **i32) for n in names}
@@ -650,6 +702,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         st = st_first if i == 0 else (st_a if i % 2 else st_b)
         st.d_status = d_status
         e = ev["eager"][i]
+        e[4].record(s)
         st.score(src["k"], src["uid"], src["mod"])
         st.select()
         e[0].record(s)
@@ -701,6 +754,13 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         r = {"maintenance_ms_total": round(ms(0, 1), 3), "mean_span": round(float(sp.mean()), 1),
              "max_span": int(sp.max()), "final_span": int(sp[-1]),
              "mean_active_pages": round(float(ac.mean()), 1)}
+        # per-step latency: eager = score + select + compact + attention; native layouts =
+        # eviction (+ packing) + placement + attention with tile skipping
+        a = 4 if n == "eager" else 0
+        lat = np.array([ev[n][i][a].elapsed_time(ev[n][i][2]) for i in range(steps)])
+        r["step_ms_p50"] = round(float(np.percentile(lat, 50)), 4)
+        r["step_ms_p99"] = round(float(np.percentile(lat, 99)), 4)
+        r["step_ms_max"] = round(float(lat.max()), 4)
         if n == "eager":
             r["attend_ms_total"] = round(ms(1, 2), 3)
         else:
@@ -719,6 +779,117 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     for mode in ("skip", "full_span"):
         res["eager"][f"attend_reduction_vs_native_{mode}"] = round(
             1 - res["eager"]["attend_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
+    return res
+
+
+def device_segments(cfg, lay, dev):
+    """All layers of a multi-layer workload drawn on the device with the host generator's
+    recipe (N(0,1) keys, values and queries plus per-unit offsets drawn from N(0, 0.5^2), stored
+    as bf16), each layer from its own seeded device generator: [n_layers, ...] tensors.  The
+    values differ from the host generator's (a different random stream); the shapes, the
+    distribution and the tags are the same."""
+    H, d, Hq, L, n = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads, lay.chunk_len, lay.n_slots
+    orig = torch.from_numpy(lay.orig_unit.astype(np.int64)).to(dev)
+    cu = torch.from_numpy(lay.chunk_unit.astype(np.int64)).to(dev) + lay.n_orig_units
+    nu = lay.n_orig_units + lay.n_chunk_units
+    out = {key: [] for key in ("k", "v", "kc", "vc", "q")}
+    for layer in range(cfg.n_layers):
+        g = torch.Generator(device=dev)
+        g.manual_seed(cfg.seed * 1000 + layer)
+        off_k = torch.randn(nu, generator=g, device=dev) * 0.5
+        off_v = torch.randn(nu, generator=g, device=dev) * 0.5
+        rn = lambda *shape: torch.randn(*shape, generator=g, device=dev)  # noqa: E731
+        out["k"].append((rn(n, H, d) + off_k[orig][:, None, None]).to(torch.bfloat16))
+        out["v"].append((rn(n, H, d) + off_v[orig][:, None, None]).to(torch.bfloat16))
+        out["kc"].append((rn(L, H, d) + off_k[cu][:, None, None]).to(torch.bfloat16))
+        out["vc"].append((rn(L, H, d) + off_v[cu][:, None, None]).to(torch.bfloat16))
+        out["q"].append(rn(L, Hq, d).to(torch.bfloat16))
+    return {key: torch.stack(val) for key, val in out.items()}
+
+
+def other_configs(dev, steps, use_graph=True):
+    """The four step calls on the single-layer 8K case (host-generated, the parity tests'
+    inputs; input copies rotated so that 512 MB pass between reuses) and on the 36-layer 32K
+    case (all 36 layers in one multi-segment call of each entry point, device-generated with the
+    same recipe).  Rates are algorithmic bytes or flops summed over segments per call time."""
+    from paper_2609_34653_amd.step import StreamStep
+    res = {}
+    for name in ("single_layer_8k", "hires_32k_36layer"):
+        cfg = sg.CONFIG_BY_NAME[name]
+        stream = sg.make_stream(cfg)
+        lay = stream.layout
+        H, d, Hq, L, n_seg = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads, lay.chunk_len, \
+            cfg.n_layers
+        elt = 2
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(np.tile(a, n_seg))).to(dev)  # noqa
+        tags = dict(uid=t(lay.unit_id), mod=t(lay.modality), pos=t(lay.pos),
+                    cm=torch.from_numpy(lay.chunk_modality).to(dev),
+                    cu=torch.from_numpy(lay.chunk_unit).to(dev))
+        if n_seg == 1:
+            seg = stream.segment(0)
+            one = dict(k=seg.k_hist.to(dev)[None], v=seg.v_hist.to(dev)[None],
+                       kc=seg.k_chunk.to(dev)[None], vc=seg.v_chunk.to(dev)[None],
+                       q=seg.q.to(dev)[None])
+            per_copy = 2 * one["k"].numel() * elt
+            n_copies = max(1, -(-(512 << 20) // per_copy))
+            copies = [one] + [{k_: v_.clone() for k_, v_ in one.items()}
+                              for _ in range(n_copies - 1)]
+            data = "host generator (the parity tests' inputs)"
+        else:
+            copies = [device_segments(cfg, lay, dev)]
+            data = "device generator, same recipe, one seed per layer"
+        st = StreamStep(n_seg=n_seg, n_slots=lay.n_slots, n_units=lay.n_units, n_q_heads=Hq,
+                        n_kv_heads=H, head_dim=d, chunk_len=L, budget=cfg.budget,
+                        recent=cfg.recent, page_size=cfg.page_size, weights=cfg.weights,
+                        device=dev)
+
+        def calls(name_):
+            def f(i):
+                c = copies[i % len(copies)]
+                if name_ == "score":
+                    st.score(c["k"], tags["uid"], tags["mod"])
+                elif name_ == "select":
+                    st.select()
+                elif name_ == "compact":
+                    st.compact(c["k"], c["v"], tags["uid"], tags["mod"], tags["pos"], c["kc"],
+                               c["vc"], tags["cm"], tags["cu"])
+                else:
+                    st.attend(c["q"], cfg.scale)
+            return f
+        for nm in ("score", "select", "compact", "attend"):
+            calls(nm)(0)
+        torch.cuda.synchronize()
+        status = int(st.d_status.item())
+        if status != 0:
+            raise RuntimeError(f"{name}: device status {status}")
+        kept = [int(x) for x in st.kept_tokens.cpu().tolist()]
+        reps = 4 * steps if n_seg == 1 else 4
+        tm = {nm: graph_time(calls(nm), reps, dev, use_graph, replays=3)
+              for nm in ("score", "select", "compact", "attend")}
+        flops = sum(attn_flops(L, kp, Hq, d) for kp in kept)
+        sb = score_bytes(lay, H, d, elt, lay.n_units) * n_seg
+        cb = sum(compact_bytes(kp, L, H, d, elt, st.cap_dst, lay.n_units) for kp in kept)
+        r = {"segments": n_seg, "history_slots": lay.n_slots, "units": lay.n_units,
+             "chunk_len": L, "budget": cfg.budget, "kept_tokens": kept if n_seg <= 4 else
+             {"min": min(kept), "max": max(kept)}, "data": data,
+             "input_copies": len(copies)}
+        for nm in ("score", "select", "compact", "attend"):
+            e = {"us": round(tm[nm]["us"], 3), "us_p10": round(tm[nm]["us_p10"], 3),
+                 "us_p90": round(tm[nm]["us_p90"], 3), "timing": tm[nm]["timing"]}
+            sec = tm[nm]["us"] * 1e-6
+            if nm == "score":
+                e.update(bytes=sb, GBps=round(sb / sec / 1e9, 2),
+                         frac_hbm=round(sb / sec / 1e9 / HBM_PEAK_GBPS, 4))
+            elif nm == "compact":
+                e.update(bytes=cb, GBps=round(cb / sec / 1e9, 2),
+                         frac_hbm=round(cb / sec / 1e9 / HBM_PEAK_GBPS, 4))
+            elif nm == "attend":
+                e.update(flops=flops, TFLOPs=round(flops / sec / 1e12, 2),
+                         frac_mfma=round(flops / sec / 1e12 / BF16_PEAK_TFLOPS, 4))
+            r[nm] = e
+        res[name] = r
+        del copies, st
+        torch.cuda.empty_cache()
     return res
 
 
@@ -747,13 +918,44 @@ def cpu_baseline(cfg, stream, seg, flops):
                            oracle.to_f64(cp["v"], "bf16"), cfg.scale)
     t4 = time.perf_counter()
     step_s = t4 - t0
-    return {"value": round(flops / step_s / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": "one full step of the same workload (score, select, compact, float64 "
-                      "attention of all 665 queries x 32 heads)",
-            "stage_s": {"score": round(t1 - t0, 3), "select": round(t2 - t1, 3),
-                        "compact": round(t3 - t2, 3), "attend": round(t4 - t3, 3)},
-            "step_s": round(step_s, 3)}
+    res = {"value": round(flops / step_s / 1e12, 5), "unit": "TFLOP/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": "one full step of the same workload (score, select, compact, float64 "
+                     "attention of all 665 queries x 32 heads)",
+           "stage_s": {"score": round(t1 - t0, 3), "select": round(t2 - t1, 3),
+                       "compact": round(t3 - t2, 3), "attend": round(t4 - t3, 3)},
+           "step_s": round(step_s, 3)}
+    # The same oracle on one thread: score, select and compact as above, attention for the
+    # first KV head's group of query heads only (1/H_kv of the flops); the rate is scaled from
+    # that group's flops.
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover
+        return res
+    G = cfg.n_q_heads // cfg.n_kv_heads
+    with threadpool_limits(limits=1):
+        u0 = time.perf_counter()
+        sc = oracle.score_units(k, cfg.dtype, lay.unit_id, lay.modality, cfg.weights,
+                                lay.n_units)
+        _, keep, kept = oracle.select_units(sc["wsum"], sc["len"], sc["first"], sc["last"],
+                                            sc["flags"], cfg.budget, cfg.recent)
+        cp = oracle.compact_kv(k, v, lay.unit_id, lay.modality, lay.pos, keep, lay.n_units,
+                               bits(seg.k_chunk), bits(seg.v_chunk), lay.chunk_modality,
+                               lay.chunk_unit, cfg.budget + lay.chunk_len, cfg.page_size)
+        u1 = time.perf_counter()
+        oracle.chunk_attention(oracle.to_f64(bits(seg.q)[:, :G], "bf16"),
+                               oracle.to_f64(cp["k"][:, :1], "bf16"),
+                               oracle.to_f64(cp["v"][:, :1], "bf16"), cfg.scale)
+        u2 = time.perf_counter()
+    one_s = (u1 - u0) + (u2 - u1) * cfg.n_kv_heads
+    res["single_thread"] = {
+        "value": round(flops / one_s / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
+        "sample": f"score + select + compact of the step, then attention of query heads 0..{G - 1} "
+                  f"(KV head 0) timed and multiplied by {cfg.n_kv_heads}",
+        "stage_s": {"score_select_compact": round(u1 - u0, 3),
+                    "attend_one_kv_head": round(u2 - u1, 3)},
+        "step_s_estimated": round(one_s, 3)}
+    return res
 
 
 if __name__ == "__main__":
