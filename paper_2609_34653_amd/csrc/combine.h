@@ -11,7 +11,7 @@ namespace {
 
 // Merge split partials: out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, M = max_s m_s,
 // splits in order.
-// CH = splits loaded per step (4 for a few splits, 16 for many).
+// CH = splits loaded per step (4 for a few splits, 16 or 32 for many).
 template <int D, int CH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml,
@@ -79,8 +79,11 @@ hipError_t launch_combine(const float* part_o, const float* part_ml, int n_split
   if (n_split <= 4)
     hipLaunchKernelGGL((attn_combine_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, part_o,
                        part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
-  else
+  else if (n_split <= 16)
     hipLaunchKernelGGL((attn_combine_kernel<D, 16>), dim3(blocks), dim3(256), 0, stream, part_o,
+                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
+  else
+    hipLaunchKernelGGL((attn_combine_kernel<D, 32>), dim3(blocks), dim3(256), 0, stream, part_o,
                        part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
   return hipGetLastError();
 }

@@ -3,21 +3,30 @@
 // one token at a time reusing the cached states; OmniPage ablation -- decode attention time
 // over the native, OmniPage and eagerly compacted layouts).
 //
-// Bandwidth-bound: every (key, KV head) row is read once per call and serves all n_q * G query
-// vectors of its group, so there is no matrix work worth the matrix cores.
+// Bandwidth-bound: every (key, KV head) row is read once per call and serves all n_q * G <= 8
+// query vectors of its group.  The products still go to the matrix cores: on the vector ALUs the
+// per-key dot products, their cross-lane reductions and the P*V updates cost as much time as the
+// loads themselves, while a 16x16 MFMA block with the query vectors as columns (half of them
+// padding) costs almost nothing.
 //   grid      (key split, KV head, segment); the split count is chosen so that about 256
 //             eight-wave workgroups run (one per CU), and a combine kernel merges the partials in
 //             split order.
-//   lanes     a group of D/8 lanes covers one key's D dimensions (16 bytes per lane, a fully
-//             coalesced 2*D-byte read of the key's head slice); a wave covers 64/(D/8) keys per
-//             load, kUnroll loads per iteration, and loads the next iteration's rows before
-//             it processes the current ones.
-//   scores    each lane holds 8 dimensions of every query vector in float; a dot product is a
-//             reduction over the lane group.
-//   softmax   float throughout (the probabilities are not rounded): running maximum per query
-//             vector and lane group, rescaled once per kUnroll keys.
-//   merge     the lane groups of a wave merge by lane exchanges, then the waves through LDS;
-//             the result is the split's partial (or, with one split, the normalised output).
+//   waves     each wave owns 16 keys of every 128-key workgroup step and loads the next step's
+//             keys before it works on the current ones: the K operands straight from global
+//             memory into registers, the V rows by direct loads into a private double buffer in
+//             LDS.  No workgroup barrier is needed until the waves merge.
+//   products  S^T (16 keys x 16 columns) = K Q^T with v_mfma_f32_16x16x32_bf16 (lane l: key
+//             l%16, dims 8(l/16).. of each 32-dim slice, a 16-byte load); its output gives lane
+//             l column l%16 and keys 4(l/16)..+3, which is the P^T operand of
+//             O^T (16 dims x 16 columns) += V^T P^T with v_mfma_f32_16x16x16_bf16.  V^T comes
+//             from the LDS block through transposing reads.  Each probability enters twice, as
+//             its bf16 rounding and as the bf16 rounding of the remainder, so it carries about
+//             16 significant bits into the float accumulation.
+//   softmax   float; per column an optimistic reference that moves only when a block's sum
+//             would leave [0, 2^32) (as in the chunk attention), shared by the column's four
+//             lane groups.
+//   merge     the waves' (O, reference, sum) merge through LDS; the result is the split's
+//             partial (or, with one split, the normalised output).
 #include <algorithm>
 
 #include "common.h"
@@ -29,40 +38,71 @@ namespace {
 
 constexpr int kDecWaves = 8;
 constexpr int kDecThreads = kDecWaves * kWave;
-constexpr int kUnroll = 4;                 // keys per lane group per iteration
-constexpr int kDecTargetWGs = 256;       // one 8-wave workgroup per CU
-constexpr int kMaxQG = 8;                  // query vectors per KV head (n_q * G)
+constexpr int kKB = 16;                    // keys per wave per iteration (one 16x16 MFMA block)
+constexpr int kStep = kDecWaves * kKB;     // keys per workgroup iteration
+constexpr int kDecTargetWGs = 256;         // one eight-wave workgroup per CU
+constexpr int kMaxQG = 8;                  // query vectors per KV head (n_q * G), <= 16
 
-__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
-// Sum over each aligned group of N lanes (N = 8 or 16), result in every lane of the group, with
-// DPP lane permutations (no LDS): swap neighbours, swap pairs, mirror within 8 lanes (quad 0 <->
-// quad 1), mirror within 16 lanes (8-lane halves).
-template <int DPP>
-__device__ inline float dpp_f(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), DPP, 0xf, 0xf, false));
-}
-template <int N>
-__device__ inline float group_sum(float x) {
-  static_assert(N == 8 || N == 16, "group of 8 or 16 lanes");
-  x += dpp_f<0xB1>(x);    // quad_perm [1,0,3,2]
-  x += dpp_f<0x4E>(x);    // quad_perm [2,3,0,1]
-  x += dpp_f<0x141>(x);   // row_half_mirror
-  if constexpr (N == 16) x += dpp_f<0x140>(x);   // row_mirror
-  return x;
+__device__ inline uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<size_t>((const lds_void*)p));
 }
 
-template <int D, int QG>
+// 16-byte direct global -> LDS load: lane i reads base + voff_i and writes 16 bytes at LDS byte
+// address lds_base + 16 i (uniform base in SGPRs, per-lane 32-bit offset).  Inline assembly, so
+// that the compiler's wait insertion does not treat it as a pending LDS write; the issuing wave,
+// the only reader of the region it fills, waits for it with s_waitcnt vmcnt.  One wait state is
+// required between the M0 write and the load; this file's kernels have no other M0 user.
+__device__ inline void dma16(const void* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_base)
+               : "memory");
+}
+
+// Transposing 64-bit LDS read: within a 16-lane group, lane i receives element i%4 of the
+// 8-byte rows read by lanes i/4, 4+i/4, 8+i/4, 12+i/4.
+__device__ inline shortx4 ld_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) shortx4*)(p));
+}
+
+// 32-byte unit swizzle of a key's row in a wave's V block: the four keys one 16-lane group
+// reads (and the eight two groups read) land in distinct banks.
+template <int D>
+__device__ inline int vsw(int key) { return D == 128 ? (key & 7) : (key & 3); }
+
+// One (query token, query head) vector per column of 16x16 MFMA blocks, keys as rows:
+//   S^T (16 keys x 16 columns) = K (16 x d) Q^T with v_mfma_f32_16x16x32_bf16: the K operand
+//       is the key's 16-byte piece straight from global memory (lane l: key l%16, dims
+//       8(l/16).. of each 32-dim slice); lane l then holds column l%16, keys 4(l/16)..+3, which
+//       is exactly the P^T operand layout of the 16x16x16 product.
+//   O^T (16 dims x 16 columns) += V^T P^T with v_mfma_f32_16x16x16_bf16, once for the bf16
+//       rounding of each probability and once for its remainder, so the probabilities enter
+//       with about 16 significant bits; V^T comes from the wave's V block in LDS (direct
+//       loads) through transposing reads.
+// Each wave owns 16 keys of every 128-key workgroup step, prefetched one step ahead (K
+// operands in registers, V in a private double buffer), so no workgroup barrier is needed
+// until the waves merge.  Softmax reference per column: optimistic, as in the chunk attention.
+template <int D>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int nq,
     int Hq, int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_split, int32_t* __restrict__ status) {
-  constexpr int LPK = D / 8;               // lanes per key
-  constexpr int KPW = kWave / LPK;         // keys per wave load
-  constexpr int GROUPS = kDecWaves * KPW;  // lane groups per workgroup
-  constexpr int STEP = GROUPS * kUnroll;   // keys per workgroup iteration
+  constexpr int KC = D / 32;               // 32-dim slices (QK k-steps)
+  constexpr int DB = D / 16;               // 16-dim blocks of the output
+  constexpr int CHK = D / 8;               // 16-byte chunks per key row
+  constexpr int CALLS = kKB * CHK / kWave; // direct loads per lane per V block
+  constexpr int BLK = kKB * D;             // elements of one V block
+  constexpr float kSumLimit = 4294967296.f;
+  __shared__ __attribute__((aligned(1024))) uint16_t vbuf[kDecWaves][2][BLK];
+  __shared__ float sm[kDecWaves][16], sl[kDecWaves][16];
+
   const int split = blockIdx.x, g = blockIdx.y, seg = blockIdx.z;
   const int nctx = n_ctx_g[seg];
   if (nctx < nq || nctx > cap) {
@@ -75,138 +115,158 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   const int j1 = static_cast<int>(static_cast<long>(nctx) * (split + 1) / n_split);
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
-  const int wave = tid / kWave;
-  const int cl = lane % LPK;               // dims 8cl .. 8cl+7
-  const int grp = wave * KPW + lane / LPK; // lane group: one key per load
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int c16 = lane & 15, g4 = lane >> 4;
 
-  // Query vector qi = (token i = qi / G, head g*G + qi % G); unused slots stay zero.
-  float qv[QG][8];
-  int lim[QG];
+  // Q^T operand: column c16 = query vector (token c16 / G, head g*G + c16 % G); lane l holds
+  // dims 32kc + 8 g4 .. +7.  Columns past n_q*G stay zero.
+  const bool col_ok = c16 < nqg;
+  const int tok = col_ok ? c16 / G : 0;
+  const int lim = col_ok ? nctx - nq + tok : nctx - 1;   // keys <= lim are visible
+  bf16x8 qf[KC];
+  {
+    const uint16_t* qrow =
+        q + ((static_cast<size_t>(seg) * nq + tok) * Hq + g * G + (col_ok ? c16 % G : 0)) * D;
 #pragma unroll
-  for (int qi = 0; qi < QG; ++qi) {
-    const bool ok = qi < nqg;
-    const int i = ok ? qi / G : 0;
-    const int h = g * G + (ok ? qi % G : 0);
-    lim[qi] = ok ? nctx - nq + i : -1;     // keys <= lim are visible
-    const u32x4 w = ok ? *reinterpret_cast<const u32x4*>(
-                             q + ((static_cast<size_t>(seg) * nq + i) * Hq + h) * D + 8 * cl)
-                       : u32x4{0, 0, 0, 0};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      qv[qi][2 * e] = bf16_lo(w[e]);
-      qv[qi][2 * e + 1] = bf16_hi(w[e]);
+    for (int kc = 0; kc < KC; ++kc) {
+      const u32x4 w = col_ok ? *reinterpret_cast<const u32x4*>(qrow + 32 * kc + 8 * g4)
+                             : u32x4{0, 0, 0, 0};
+      qf[kc] = __builtin_bit_cast(bf16x8, w);
     }
-  }
-  float m[QG], l[QG], o[QG][8];
-#pragma unroll
-  for (int qi = 0; qi < QG; ++qi) {
-    m[qi] = -INFINITY;
-    l[qi] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[qi][e] = 0.f;
   }
   const size_t row_stride = static_cast<size_t>(Hkv) * D;
-  const uint16_t* kh = k + (static_cast<size_t>(seg) * cap * Hkv + g) * D + 8 * cl;
-  const uint16_t* vh = v + (static_cast<size_t>(seg) * cap * Hkv + g) * D + 8 * cl;
-
-  // Keys of iteration `base` for this lane group: base + u*GROUPS + grp; rows past j1 load row j0
-  // (in range, ignored).  The next iteration's rows are loaded before this one is processed.
-  constexpr bool kPrefetch = QG <= 4;     // keeps QG = 8 within 256 registers
-  u32x4 kw[kUnroll], vw[kUnroll], kn[kUnroll], vn[kUnroll];
-  auto load = [&](int base, u32x4 (&kd)[kUnroll], u32x4 (&vd)[kUnroll]) {
+  const uint16_t* kh = k + (static_cast<size_t>(seg) * cap * Hkv + g) * D;
+  const uint16_t* vh = v + (static_cast<size_t>(seg) * cap * Hkv + g) * D;
+  // V block loads: LDS chunk cq*64 + lane of the block holds key (cq*64 + lane) / CHK, stored
+  // at unit position ((that chunk) >> 1) ^ vsw(key); the lane fetches the global chunk that
+  // belongs there.
+  uint32_t voff[CALLS];
+  int vkey[CALLS];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int key = base + u * GROUPS + grp;
-      const size_t r = static_cast<size_t>(key < j1 ? key : j0) * row_stride;
-      kd[u] = *reinterpret_cast<const u32x4*>(kh + r);
-      vd[u] = *reinterpret_cast<const u32x4*>(vh + r);
+  for (int cq = 0; cq < CALLS; ++cq) {
+    const int lc = cq * kWave + lane;
+    const int key = lc / CHK, pc = lc % CHK;
+    vkey[cq] = key;
+    voff[cq] = 2u * static_cast<uint32_t>(8 * (2 * ((pc >> 1) ^ vsw<D>(key)) + (pc & 1)));
+  }
+  const uint32_t vlds = lds_addr(&vbuf[wave][0][0]);
+  // keys of iteration it for this wave: base(it) + [0, 16), base(it) = j0 + it*kStep + 16*wave;
+  // rows past j1 - 1 are clamped to it (read, then masked)
+  auto issue = [&](int it, int buf, bf16x8 (&ka)[KC]) {
+    const int kb0 = j0 + it * kStep + kKB * wave;
+    const int kr = min(kb0 + c16, j1 - 1);
+    const uint16_t* kp = kh + static_cast<size_t>(kr) * row_stride + 8 * g4;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc)
+      ka[kc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kp + 32 * kc));
+    const int r0 = min(kb0, j1 - 1);
+#pragma unroll
+    for (int cq = 0; cq < CALLS; ++cq) {
+      const int shift = min(kb0 + vkey[cq], j1 - 1) - r0;   // >= 0
+      dma16(vh + static_cast<size_t>(r0) * row_stride,
+            voff[cq] + 2u * static_cast<uint32_t>(shift * row_stride),
+            vlds + static_cast<uint32_t>((buf * BLK + cq * kWave * 8) * 2));
     }
   };
-  if (j0 < j1) load(j0, kw, vw);
-  for (int base = j0; base < j1; base += STEP) {
-    if (kPrefetch && base + STEP < j1) load(base + STEP, kn, vn);
-    int key[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) key[u] = base + u * GROUPS + grp;
-#pragma unroll
-    for (int qi = 0; qi < QG; ++qi) {
-      float s[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        float acc = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc = fmaf(qv[qi][2 * e], bf16_lo(kw[u][e]), acc);
-          acc = fmaf(qv[qi][2 * e + 1], bf16_hi(kw[u][e]), acc);
-        }
-        acc = group_sum<LPK>(acc);
-        s[u] = (key[u] < j1 && key[u] <= lim[qi]) ? acc * scale_log2 : -INFINITY;
-      }
-      float mx = s[0];
-#pragma unroll
-      for (int u = 1; u < kUnroll; ++u) mx = fmaxf(mx, s[u]);
-      const float m_new = fmaxf(m[qi], mx);
-      if (m_new == -INFINITY) continue;    // nothing visible yet for this query vector
-      const float alpha = __builtin_amdgcn_exp2f(m[qi] - m_new);
-      m[qi] = m_new;
-      float lsum = l[qi] * alpha;
-      float acc8[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc8[e] = o[qi][e] * alpha;
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const float p = __builtin_amdgcn_exp2f(s[u] - m_new);
-        lsum += p;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc8[2 * e] = fmaf(p, bf16_lo(vw[u][e]), acc8[2 * e]);
-          acc8[2 * e + 1] = fmaf(p, bf16_hi(vw[u][e]), acc8[2 * e + 1]);
-        }
-      }
-      l[qi] = lsum;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[qi][e] = acc8[e];
-    }
-    if (kPrefetch) {
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        kw[u] = kn[u];
-        vw[u] = vn[u];
-      }
-    } else if (base + STEP < j1) {
-      load(base + STEP, kw, vw);
-    }
-  }
 
-  // Merge the KPW lane groups of each wave (lanes LPK, 2 LPK, ... apart), then the waves.
+  floatx4 o[DB];
 #pragma unroll
-  for (int qi = 0; qi < QG; ++qi) {
+  for (int db = 0; db < DB; ++db) o[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const int n_it = (j1 - j0 + kStep - 1) / kStep;
+  bf16x8 kA[KC], kB[KC];
+  // V^T operand read: lane (g4, i) takes dims 16db + i of keys 4g4 .. 4g4+3; the lanes of its
+  // group read key 4g4 + (i >> 2), dims 16db + 4(i & 3) .. +3.
+  const int vrow = 4 * g4 + (c16 >> 2);
+  const int vsub = 4 * (c16 & 3);
+
+  auto step = [&](auto bpar, int it) {
+    constexpr int B = decltype(bpar)::value;
+    bf16x8(&ka)[KC] = B == 0 ? kA : kB;
+    bf16x8(&kn)[KC] = B == 0 ? kB : kA;
+    const bool more = it + 1 < n_it;
+    floatx4 s = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int off = LPK; off < kWave; off <<= 1) {
-      const float mo = __shfl_xor(m[qi], off, kWave);
-      const float lo = __shfl_xor(l[qi], off, kWave);
-      const float mn = fmaxf(m[qi], mo);
-      const float a = m[qi] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[qi] - mn);
-      const float b = mo == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
-      l[qi] = a * l[qi] + b * lo;
+    for (int kc = 0; kc < KC; ++kc)
+      s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kc], qf[kc], s, 0, 0, 0);
+    // the next iteration's loads go out once this one's K operands are consumed
+    if (more) issue(it + 1, 1 - B, kn);
+    const int kb0 = j0 + it * kStep + kKB * wave;
+    const int key0 = kb0 + 4 * g4;
+    if (kb0 + kKB > j1 || kb0 + kKB - 1 > nctx - nq) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[qi][e] = a * o[qi][e] + b * __shfl_xor(o[qi][e], off, kWave);
-      m[qi] = mn;
+      for (int i = 0; i < 4; ++i)
+        if (key0 + i >= j1 || key0 + i > lim) s[i] = -INFINITY;
     }
-  }
-  __shared__ float sm[kDecWaves][QG], sl[kDecWaves][QG];
-  __shared__ float so[kDecWaves][QG][D];
-  if (lane < LPK) {
+    float e[4];
 #pragma unroll
-    for (int qi = 0; qi < QG; ++qi) {
-      if (lane == 0) {
-        sm[wave][qi] = m[qi];
-        sl[wave][qi] = l[qi];
-      }
+    for (int i = 0; i < 4; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(s[i], scale_log2, -m_run));
+    float ls = (e[0] + e[1]) + (e[2] + e[3]);
+    if (__any(!(ls < kSumLimit))) {
+      // exact block maximum per column (its four lane groups), move the reference, rescale
+      float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float m_new = fmaxf(m_run, mx * scale_log2);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      l_run *= alpha;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) so[wave][qi][8 * cl + e] = o[qi][e];
+      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+      m_run = m_new;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(s[i], scale_log2, -m_use));
     }
+    // probabilities as bf16 plus bf16 remainder
+    shortx4 ph, pl;
+    float lsum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const __bf16 hi = static_cast<__bf16>(e[i]);
+      const __bf16 lo = static_cast<__bf16>(e[i] - static_cast<float>(hi));
+      ph[i] = __builtin_bit_cast(short, hi);
+      pl[i] = __builtin_bit_cast(short, lo);
+      lsum += static_cast<float>(hi) + static_cast<float>(lo);
+    }
+    l_run += lsum;
+    // this iteration's V block has landed (the next one's loads may still be in flight)
+    static_assert(CALLS + KC == 8 || CALLS + KC == 4, "vmcnt immediates below");
+    if (more) {
+      if constexpr (CALLS + KC == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    const uint16_t* vb = &vbuf[wave][B][0] + vrow * D + vsub;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const shortx4 vt = ld_tr(vb + 16 * (db ^ vsw<D>(vrow)));
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, ph, o[db], 0, 0, 0);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pl, o[db], 0, 0, 0);
+    }
+  };
+  if (n_it > 0) issue(0, 0, kA);
+  int it = 0;
+  for (; it + 1 < n_it; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    step(std::integral_constant<int, 1>{}, it + 1);
   }
+  if (it < n_it) step(std::integral_constant<int, 0>{}, it);
+
+  // merge the waves: per column the reference, the sum over the four lane groups, and O^T
+  const float l_col = l_run + __shfl_xor(l_run, 16, kWave) + __shfl_xor(l_run, 32, kWave) +
+                      __shfl_xor(l_run, 48, kWave);
+  __syncthreads();                         // every wave is done with its V blocks
+  float* so = reinterpret_cast<float*>(&vbuf[0][0][0]);   // [wave][16 columns][D]
+  static_assert(sizeof(vbuf) >= kDecWaves * 16 * D * sizeof(float), "merge buffer");
+  if (g4 == 0) {
+    sm[wave][c16] = m_run;
+    sl[wave][c16] = l_col;
+  }
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) so[(wave * 16 + c16) * D + 16 * db + 4 * g4 + i] = o[db][i];
   __syncthreads();
   for (int idx = tid; idx < nqg * D; idx += kDecThreads) {
     const int qi = idx / D, d = idx % D;
@@ -216,7 +276,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     if (M != -INFINITY) {
       for (int gr = 0; gr < kDecWaves; ++gr) {
         const float w = sm[gr][qi] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sm[gr][qi] - M);
-        num = fmaf(w, so[gr][qi][d], num);
+        num = fmaf(w, so[(gr * 16 + qi) * D + d], num);
         den = fmaf(w, sl[gr][qi], den);
       }
     }
@@ -233,14 +293,14 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   }
 }
 
-template <int D, int QG>
+template <int D>
 hipError_t launch_decode_t(const DecodeArgs& a, int n_split, hipStream_t stream) {
   const dim3 grid(n_split, a.n_kv_heads, a.n_seg);
   const size_t n_rows = static_cast<size_t>(a.n_seg) * a.n_q * a.n_q_heads;
   float* part_o = static_cast<float*>(a.workspace);
   float* part_ml = part_o ? part_o + static_cast<size_t>(n_split) * n_rows * D : nullptr;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  hipLaunchKernelGGL((decode_kernel<D, QG>), grid, dim3(kDecThreads), 0, stream,
+  hipLaunchKernelGGL((decode_kernel<D>), grid, dim3(kDecThreads), 0, stream,
                      static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                      static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
                      a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status);
@@ -248,15 +308,6 @@ hipError_t launch_decode_t(const DecodeArgs& a, int n_split, hipStream_t stream)
   if (e != hipSuccess || n_split == 1) return e;
   return launch_combine<D>(part_o, part_ml, n_split, n_rows, a.n_ctx, a.n_q, a.n_q_heads, a.cap,
                            a.out, stream);
-}
-
-template <int D>
-hipError_t launch_decode_d(const DecodeArgs& a, int n_split, hipStream_t stream) {
-  const int qg = a.n_q * (a.n_q_heads / a.n_kv_heads);
-  if (qg <= 1) return launch_decode_t<D, 1>(a, n_split, stream);
-  if (qg <= 2) return launch_decode_t<D, 2>(a, n_split, stream);
-  if (qg <= 4) return launch_decode_t<D, 4>(a, n_split, stream);
-  return launch_decode_t<D, kMaxQG>(a, n_split, stream);
 }
 
 }  // namespace
@@ -280,8 +331,8 @@ int decode_max_query_vectors() { return kMaxQG; }
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream) {
   const int s = decode_num_splits(a.n_seg, a.cap, a.n_kv_heads);
-  if (a.head_dim == 128) return launch_decode_d<128>(a, s, stream);
-  if (a.head_dim == 64) return launch_decode_d<64>(a, s, stream);
+  if (a.head_dim == 128) return launch_decode_t<128>(a, s, stream);
+  if (a.head_dim == 64) return launch_decode_t<64>(a, s, stream);
   return hipErrorInvalidValue;
 }
 
