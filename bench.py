@@ -32,19 +32,20 @@ CSRC = os.path.join(ROOT, "paper_2609_34653_amd", "csrc")
 
 # HBM traffic of one call of each stage on the default workload, from two rocprofv3 --pmc passes
 # over `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0 --no-ceilings
-# --copy-calibration-mb 1024` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch, summed over the stage's kernels).  Scaled by what the same
+# --no-other-configs --copy-calibration-mb 1024` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch,
+# summed over the stage's kernels).  Scaled by what the same
 # counters read for the calibration copy (1 GiB read + 1 GiB written by one elementwise kernel):
 # FETCH_SIZE reads 524,297 KiB for 1,048,576 KiB fetched (x2.000), WRITE_SIZE reads 1,048,576 KiB
 # (x1.000).  Each entry carries a hash of the sources of its kernels and is reported only while
 # they are unchanged (otherwise null: the counters describe other code).
 FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 COUNTER_TRAFFIC = {
-    "score": (("score.hip", "common.h"), "096c5fd963427f8e", 57081.4, 490.7),
+    "score": (("score.hip", "common.h"), "096c5fd963427f8e", 57080.8, 490.7),
     "select": (("select.hip", "common.h"), "0baf3f02762d4c67", 19.5, 3.0),
-    "compact": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34148.4, 68080.3),
-    "attend": (("attention.hip", "combine.h", "common.h"), "212a52447aff3e0c", 55381.1, 45074.8),
-    "compact_rope": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34177.5, 68026.7),
-    "decode": (("decode.hip", "combine.h", "common.h"), "25878bb4cb9068be", 34371.6, 536.0),
+    "compact": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34140.8, 68071.0),
+    "attend": (("attention.hip", "combine.h", "common.h"), "f9d0adb1db48cb97", 55361.6, 45074.8),
+    "compact_rope": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34177.5, 68026.8),
+    "decode": (("decode.hip", "combine.h", "common.h"), "13e3be08fc88d039", 34299.5, 536.0),
 }
 
 
