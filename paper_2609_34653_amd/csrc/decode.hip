@@ -257,16 +257,21 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   const float l_col = l_run + __shfl_xor(l_run, 16, kWave) + __shfl_xor(l_run, 32, kWave) +
                       __shfl_xor(l_run, 48, kWave);
   __syncthreads();                         // every wave is done with its V blocks
-  float* so = reinterpret_cast<float*>(&vbuf[0][0][0]);   // [wave][16 columns][D]
-  static_assert(sizeof(vbuf) >= kDecWaves * 16 * D * sizeof(float), "merge buffer");
+  // [wave][D][kMaxQG + 1 columns]: with the padding, the lanes of one store (8 columns x four
+  // lane groups) and the consecutive dims of one load fall in distinct banks
+  constexpr int SCOL = kMaxQG + 1;
+  float* so = reinterpret_cast<float*>(&vbuf[0][0][0]);
+  static_assert(sizeof(vbuf) >= kDecWaves * D * SCOL * sizeof(float), "merge buffer");
   if (g4 == 0) {
     sm[wave][c16] = m_run;
     sl[wave][c16] = l_col;
   }
+  if (c16 < kMaxQG) {
 #pragma unroll
-  for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) so[(wave * 16 + c16) * D + 16 * db + 4 * g4 + i] = o[db][i];
+      for (int i = 0; i < 4; ++i) so[(wave * D + 16 * db + 4 * g4 + i) * SCOL + c16] = o[db][i];
+  }
   __syncthreads();
   for (int idx = tid; idx < nqg * D; idx += kDecThreads) {
     const int qi = idx / D, d = idx % D;
@@ -276,7 +281,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     if (M != -INFINITY) {
       for (int gr = 0; gr < kDecWaves; ++gr) {
         const float w = sm[gr][qi] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sm[gr][qi] - M);
-        num = fmaf(w, so[(gr * 16 + qi) * D + d], num);
+        num = fmaf(w, so[(gr * D + d) * SCOL + qi], num);
         den = fmaf(w, sl[gr][qi], den);
       }
     }
