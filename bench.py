@@ -49,6 +49,27 @@ COUNTER_TRAFFIC = {
 }
 
 
+# Matrix-core busy fraction of the chunk attention kernel from rocprofv3 counters over
+# `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0 --no-other-configs`:
+# SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1,024 SIMDs) per dispatch (the MFMA-only
+# probe reads 0.968 with this normalisation); keyed by the kernel's sources like COUNTER_TRAFFIC.
+MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "f9d0adb1db48cb97", 0.516)
+
+
+def mfma_busy(config):
+    """Counter-measured MFMA busy fraction of attn_kernel, or None if not measured on this
+    code/config."""
+    import hashlib
+    srcs, digest, frac = MFMA_BUSY
+    if config != WORKLOAD:
+        return None
+    h = hashlib.sha256()
+    for f in srcs:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return frac if h.hexdigest()[:16] == digest else None
+
+
 def graph_time(fn, reps, dev, use_graph=True, replays=5):
     """GPU time of fn() over `reps` calls, captured in one HIP graph and replayed (the calls are
     too short for host-side launches to keep the GPU busy); if capture fails, or use_graph is
@@ -449,7 +470,8 @@ def main():
                      "timing": kernels["attend"]["timing"],
                      "achieved": round(attn_tflops, 3), "peak": BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
-                     "traffic": kernels["attend"]["traffic"]},
+                     "traffic": kernels["attend"]["traffic"],
+                     "mfma_busy_counter": mfma_busy(cfg.name)},
         "wall_s_timed_region": round(wall, 4),
     }
     if args.ceilings:
