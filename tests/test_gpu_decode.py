@@ -60,6 +60,8 @@ def oracle_decode(q, k, v, n, scale):
     ([3001], 3001, 1, 8, 1, 64),              # 8 query heads on one KV head, d = 64
     ([1500, 1499], 2000, 2, 8, 8, 64),        # no grouping, two tokens
     ([16948], 17049, 1, 32, 8, 128),          # the 80K-history pool after compaction
+    ([2500, 700], 2600, 2, 32, 8, 128),       # eight query vectors per KV head, d = 128
+    ([129], 129, 4, 8, 4, 64),                # four tokens (causal among them), eight vectors
 ])
 def test_decode_parity(n_ctx, cap, n_q, Hq, Hkv, d):
     q, k, v, out, status, scale = run_decode(n_ctx, cap, n_q, Hq, Hkv, d)
