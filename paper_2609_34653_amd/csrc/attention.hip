@@ -125,7 +125,7 @@ __device__ inline T& pick(T& a, T& b) {
 // SPAN = false: keys are the contiguous rows [0, n_ctx) of the compacted pool, the chunk last.
 // SPAN = true: keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span);
 // slot j is visible to query i iff 0 <= key_pos[j] <= q_pos0 + i; only the active tiles listed
-// by span_tiles_kernel are visited, and a tile is masked only if it holds an empty slot or a
+// by span_list_kernel are visited, and a tile is masked only if it holds an empty slot or a
 // position past the workgroup's first row.
 template <int D, bool SPAN>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status,
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ qpos0_g,
-    const int2* __restrict__ tile_info, const int32_t* __restrict__ tile_list,
+    const int4* __restrict__ tile_info, const int32_t* __restrict__ tile_list,
     const int32_t* __restrict__ n_active_g, int max_tiles) {
   using S = Smem<D>;
   // Tile buffers K0, K1, V0, V1 at fixed offsets (every access below names its buffer at
@@ -238,7 +238,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         *reinterpret_cast<u32x4*>(base + 8 * idx) = u32x4{0, 0, 0, 0};
   };
 
-  // SPAN: the a-th visited tile is tile_list[a]; its (largest position, has an empty slot).
+  // SPAN: the a-th visited tile is tile_list[a]; tile_info holds its (largest position, has an
+  // empty slot, occupancy bits 0-31, occupancy bits 32-63).
   const size_t tl_base = static_cast<size_t>(seg) * max_tiles;
   auto tile_of = [&](int a) -> int {
     if constexpr (SPAN) return tile_list[tl_base + a]; else return a;
@@ -305,23 +306,34 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       const int j0 = t * kKT;
       const bool has_next = t + 1 < t_end;
       __builtin_amdgcn_s_waitcnt(0);      // this wave's pieces of K(t+1) and V(t) have landed
+      // SPAN: t indexes the tile list.  The V rows of the tile's empty slots (their contents are
+      // arbitrary) are zeroed by the lanes that loaded them, before the barrier publishes the
+      // tile; a key is then masked by the tile's occupancy bits, or, in a tile holding a
+      // position past the workgroup's first row, by its published position.
+      int4 info = int4{0, 0, 0, 0};
+      if constexpr (SPAN) {
+        info = tile_info[tl_base + tile_of(t)];
+        if (info.y != 0) {
+          const uint64_t valid = static_cast<uint64_t>(static_cast<uint32_t>(info.z)) |
+                                 (static_cast<uint64_t>(static_cast<uint32_t>(info.w)) << 32);
+          uint16_t* vb = lds + (2 + B) * S::TILE_ELEMS;
+#pragma unroll
+          for (int cq = 0; cq < S::CALLS; ++cq) {
+            if (((valid >> krowl[cq]) & 1) == 0)
+              *reinterpret_cast<u32x4*>(vb + 8 * ((wave + kAttnWaves * cq) * kWave + lane)) =
+                  u32x4{0, 0, 0, 0};
+          }
+        }
+      }
       __syncthreads();                    // ... everyone's; iteration t-1 is finished
       bool masked;
+      bool causal = false;
       if constexpr (SPAN) {
-        // t indexes the tile list: publish this tile's key positions, zero the V rows of its
-        // empty slots (their contents are arbitrary), then mask per key.
-        const int2 info = tile_info[tl_base + tile_of(t)];
-        masked = info.y != 0 || info.x > full_lim;
-        if (masked) {
+        causal = info.x > full_lim;
+        masked = info.y != 0 || causal;
+        if (causal) {
           if (wave == 0) kpos_lds[lane] = kp_next;
           __syncthreads();
-          if (info.y != 0) {
-            uint16_t* vb = lds + (2 + B) * S::TILE_ELEMS;
-            for (int idx = tid; idx < kKT * S::CHUNKS; idx += kAttnThreads)
-              if (kpos_lds[idx / S::CHUNKS] < 0)
-                *reinterpret_cast<u32x4*>(vb + 8 * idx) = u32x4{0, 0, 0, 0};
-            __syncthreads();
-          }
         }
         if (t + 2 < t_end) issue(k_head, koff, tile_of(t + 2), B);
         if (has_next) {
@@ -340,15 +352,27 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       }
 
       if (masked) {
+        if (SPAN && !causal) {
+          // occupancy bits of this lane's keys 32st + 16h + i
+          const uint32_t half_bits[2] = {static_cast<uint32_t>(info.z) >> (16 * h),
+                                         static_cast<uint32_t>(info.w) >> (16 * h)};
 #pragma unroll
-        for (int st = 0; st < 2; ++st) {
+          for (int st = 0; st < 2; ++st) {
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            if constexpr (SPAN) {
-              const int kp = kpos_lds[32 * st + 16 * h + i];
-              if (kp < 0 || kp > lim) s_cur[st][i] = -INFINITY;
-            } else {
-              if (j0 + 32 * st + 16 * h + i > lim) s_cur[st][i] = -INFINITY;
+            for (int i = 0; i < 16; ++i)
+              if (((half_bits[st] >> i) & 1) == 0) s_cur[st][i] = -INFINITY;
+          }
+        } else {
+#pragma unroll
+          for (int st = 0; st < 2; ++st) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              if constexpr (SPAN) {
+                const int kp = kpos_lds[32 * st + 16 * h + i];
+                if (kp < 0 || kp > lim) s_cur[st][i] = -INFINITY;
+              } else {
+                if (j0 + 32 * st + 16 * h + i > lim) s_cur[st][i] = -INFINITY;
+              }
             }
           }
         }
@@ -485,15 +509,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
 
 // Active tiles of a span.  span_info_kernel: one wave per 64-slot tile of [0, span) (a grid of
 // workgroups) records the tile's largest key position, whether it holds an empty slot (or
-// slots past the span) and whether it is visited (it holds an entry, or every tile of the span
-// is visited).  span_list_kernel: one workgroup per
-// segment lists the tiles holding an entry, in order.
+// slots past the span), its 64 occupancy bits and whether it is visited (it holds an entry, or
+// every tile of the span is visited).  span_list_kernel: one workgroup per segment lists the
+// visited tiles, in order.
 constexpr int kSpanThreads = 1024;
 constexpr int kInfoThreads = 256;
 
 __global__ __launch_bounds__(kInfoThreads) void span_info_kernel(
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ span_g, int cap, int L,
-    int max_tiles, int skip_empty, int2* __restrict__ tile_info, uint8_t* __restrict__ act_g) {
+    int max_tiles, int skip_empty, int4* __restrict__ tile_info, uint8_t* __restrict__ act_g) {
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
   const int t = blockIdx.x * (kInfoThreads / kWave) + threadIdx.x / kWave;
@@ -508,7 +532,9 @@ __global__ __launch_bounds__(kInfoThreads) void span_info_kernel(
   for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off, kWave));
   if (lane == 0) {
     const size_t tb = static_cast<size_t>(seg) * max_tiles;
-    tile_info[tb + t] = make_int2(mx, valid != ~0ull ? 1 : 0);
+    tile_info[tb + t] = make_int4(mx, valid != ~0ull ? 1 : 0,
+                                  static_cast<int>(valid & 0xffffffffu),
+                                  static_cast<int>(valid >> 32));
     act_g[tb + t] = (valid != 0 || !skip_empty) ? 1 : 0;
   }
 }
@@ -553,8 +579,8 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
     uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
                    (n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
     const size_t nt = static_cast<size_t>(a.n_seg) * max_tiles;
-    int2* tile_info = reinterpret_cast<int2*>(tbl);
-    int32_t* tile_list = reinterpret_cast<int32_t*>(tbl + nt * sizeof(int2));
+    int4* tile_info = reinterpret_cast<int4*>(tbl);
+    int32_t* tile_list = reinterpret_cast<int32_t*>(tbl + nt * sizeof(int4));
     int32_t* n_active = tile_list + nt;
     uint8_t* act = reinterpret_cast<uint8_t*>(n_active + a.n_seg);
     const int per_block = kInfoThreads / kWave;
@@ -612,7 +638,7 @@ size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_head
                                  int n_kv_heads, int head_dim) {
   const size_t max_tiles = (static_cast<size_t>(cap) + kKT - 1) / kKT;
   return attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim) +
-         static_cast<size_t>(n_seg) * max_tiles * (sizeof(int2) + sizeof(int32_t) + 1) +
+         static_cast<size_t>(n_seg) * max_tiles * (sizeof(int4) + sizeof(int32_t) + 1) +
          static_cast<size_t>(n_seg) * sizeof(int32_t);
 }
 
