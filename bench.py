@@ -781,10 +781,23 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         # per-step latency: eager = score + select + compact + attention; native layouts =
         # eviction (+ packing) + placement + attention with tile skipping
         a = 4 if n == "eager" else 0
-        lat = np.array([ev[n][i][a].elapsed_time(ev[n][i][2]) for i in range(steps)])
+        per_step = lambda x, y: np.array([ev[n][i][x].elapsed_time(ev[n][i][y])  # noqa: E731
+                                          for i in range(steps)])
+        pct = lambda arr: {"p50": round(float(np.percentile(arr, 50)), 4),  # noqa: E731
+                           "p99": round(float(np.percentile(arr, 99)), 4)}
+        lat = per_step(a, 2)
         r["step_ms_p50"] = round(float(np.percentile(lat, 50)), 4)
         r["step_ms_p99"] = round(float(np.percentile(lat, 99)), 4)
         r["step_ms_max"] = round(float(lat.max()), 4)
+        # the same per call: eager score + select, compaction, attention; native maintenance
+        # (eviction, packing, placement), attention with and without tile skipping
+        if n == "eager":
+            r["per_call_ms"] = {"score_select": pct(per_step(4, 0)),
+                                "compact": pct(per_step(0, 1)), "attend": pct(per_step(1, 2))}
+        else:
+            r["per_call_ms"] = {"maintenance": pct(per_step(0, 1)),
+                                "attend_skip": pct(per_step(1, 2)),
+                                "attend_full_span": pct(per_step(2, 3))}
         if n == "eager":
             r["attend_ms_total"] = round(ms(1, 2), 3)
         else:

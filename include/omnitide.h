@@ -377,8 +377,9 @@ size_t omnitide_place_chunk_workspace_bytes(int n_seg, int cap);
  *   workspace  device scratch of omnitide_span_attn_workspace_bytes() bytes (always > 0).
  * skip_empty_tiles != 0: 64-slot tiles without an entry are skipped (kernels with tile
  * skipping); 0: every tile of the span is traversed, masked (kernels that traverse the physical
- * span).  Tiles whose entries are all visible to every query of a workgroup run unmasked.  With key_pos[j] = j for j < span and q_pos0 = span -
- * chunk_len this computes omnitide_chunk_attn with n_ctx = span (up to summation order).
+ * span).  Tiles whose entries are all visible to every query of a workgroup run unmasked.
+ * With key_pos[j] = j for j < span and q_pos0 = span - chunk_len this computes
+ * omnitide_chunk_attn with n_ctx = span (up to summation order).
  * Limits: as omnitide_chunk_attn, and cap <= 2,097,152.
  */
 int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_t* key_pos,
