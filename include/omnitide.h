@@ -117,9 +117,10 @@ int omnitide_score_units(const void* k, int dtype, int n_seg, int n_slots, int n
  *   unit_score   uint64 [n_seg][n_units]   floor(W_u / len_u), 0 for units without slots
  *   keep         uint8  [n_seg][n_units]   1 = unit retained whole
  *   kept_tokens  int32  [n_seg]            retained history tokens (<= budget)
- *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run or runs are out
- *                of unit order; OMNITIDE_E_BUDGET as above.  On either error the segment's
- *                keep is all 0 and kept_tokens 0.
+ *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run, runs are out
+ *                of unit order, or a score reaches 2^51 (omnitide_score_units' outputs stay
+ *                below 2^43); OMNITIDE_E_BUDGET as above.  On either error the segment's keep
+ *                is all 0 and kept_tokens 0.
  * Limits: 1 <= n_units <= 8192, budget_tokens >= 0, recent_tokens >= 0.  One workgroup per
  * segment; latency-bound.
  */

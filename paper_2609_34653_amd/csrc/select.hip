@@ -21,6 +21,22 @@ constexpr int kSelThreads = 1024;
 constexpr int kMaxUnits = OMNITIDE_MAX_UNITS;
 constexpr int kPer = kMaxUnits / kSelThreads;
 constexpr int kIdBits = 13;   // 2^13 = kMaxUnits
+// Scores below 2^51 fit the 64-bit ranking key (score << kIdBits | id) with one bit to spare.
+// omnitide_score_units never exceeds 2^43: a slot contributes at most 4,096 elements x 2^21 x
+// a weight of 2^10.
+constexpr int kScoreBits = 51;
+
+// floor(n / d) for d >= 1.  Below 2^53 the dividend is exact in double: the correctly rounded
+// quotient is at most one above the floor (when the true quotient lies just below an integer),
+// which the remainder's sign corrects.  Larger dividends take the integer division.
+__device__ inline uint64_t udiv64(uint64_t n, uint32_t d) {
+  if (n < (1ull << 53)) {
+    uint64_t q = static_cast<uint64_t>(static_cast<double>(n) / static_cast<double>(d));
+    if (static_cast<int64_t>(n - q * d) < 0) --q;
+    return q;
+  }
+  return n / d;
+}
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const uint64_t* __restrict__ wsum_g, const int32_t* __restrict__ len_g,
@@ -63,8 +79,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     if (!mine || ln[i] <= 0) ln[i] = 0;
     const bool live = ln[i] > 0;
     sys[i] = live && (fl[i] & 1u) != 0;
-    sc[i] = live ? ws[i] / static_cast<uint32_t>(ln[i]) : 0;
+    sc[i] = live ? udiv64(ws[i], static_cast<uint32_t>(ln[i])) : 0;
     bad |= live && (ls[i] - fs[i] + 1) != ln[i];
+    bad |= (sc[i] >> kScoreBits) != 0;          // the ranking key holds kScoreBits of score
     if (live) my_max_first = max(my_max_first, fs[i]);
     if (mine) {
       score_g[base + u] = sc[i];
@@ -186,11 +203,16 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 // wave-level scans (no workgroup barriers) and, instead of a full sort, an MSD radix select of
 // the cut.  The walk "rank order, stop at the first misfit" keeps exactly the candidates whose
 // key exceeds the first misfit's key; the misfit is found digit by digit: a histogram of
-// candidate lengths over the next 8 key bits (LDS atomics) and a scan in descending digit order
+// candidate lengths over the next key bits (LDS atomics) and a scan in descending digit order
 // locate the bucket where the running total first exceeds the cap; higher buckets are kept,
 // lower ones dropped, and the search continues inside that bucket until it holds one key.
+// Digits are 10 bits wide (1,024 buckets), so a 50-bit key takes five passes.
 constexpr int kSmallUnits = 512;
 constexpr int kSmallPer = kSmallUnits / kWave;
+constexpr int kDigitBits = 10;                       // radix-select digit
+constexpr int kBuckets = 1 << kDigitBits;
+constexpr int kBucketsPerLane = kBuckets / kWave;
+
 
 __device__ inline int wave_exclusive_sum(int v, int* total) {
   const int inc = wave_inclusive_scan(v);
@@ -204,7 +226,7 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
     const uint32_t* __restrict__ flags_g, int n_units, int budget, int recent,
     uint64_t* __restrict__ score_g, uint8_t* __restrict__ keep_g,
     int32_t* __restrict__ kept_tokens_g, int32_t* __restrict__ status) {
-  __shared__ int32_t hist[256];
+  __shared__ __attribute__((aligned(16))) int32_t hist[kBuckets];
   const int seg = blockIdx.x;
   const int lane = threadIdx.x;
   const int U = n_units;
@@ -233,8 +255,9 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
     if (u >= U || ln[i] <= 0) ln[i] = 0;
     const bool live = ln[i] > 0;
     sys[i] = live && (fl[i] & 1u) != 0;
-    const uint64_t sc = live ? ws[i] / static_cast<uint32_t>(ln[i]) : 0;
+    const uint64_t sc = live ? udiv64(ws[i], static_cast<uint32_t>(ln[i])) : 0;
     bad |= live && (ls[i] - fs[i] + 1) != ln[i];
+    bad |= (sc >> kScoreBits) != 0;
     if (live) my_max_first = max(my_max_first, fs[i]);
     if (u < U) score_g[base + u] = sc;
     key[i] = (sc << kIdBits) | static_cast<uint64_t>(u);
@@ -305,29 +328,38 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
   int taken = 0;                                   // tokens already kept by the search
   int hi = 64 - __builtin_clzll(kmax | 1);         // key bits in use
   while (hi > 0) {
-    const int lo = max(hi - 8, 0);
+    const int lo = max(hi - kDigitBits, 0);
     const uint64_t mask = (1ull << (hi - lo)) - 1;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) hist[lane + kWave * j] = 0;
+    for (int j = 0; j < kBucketsPerLane / 4; ++j)
+      *reinterpret_cast<int4*>(&hist[kBucketsPerLane * lane + 4 * j]) = make_int4(0, 0, 0, 0);
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i)
       if (state[i] == 1) atomicAdd(&hist[(key[i] >> lo) & mask], ln[i]);
     __syncthreads();
-    // descending digit order: lane owns digits 255-4*lane .. 252-4*lane
-    int hv[4], hsum = 0;
+    // descending digit order: lane owns digits kBuckets-1 - kBucketsPerLane*lane - j
+    int hv[kBucketsPerLane], hsum = 0;
+    {
+      const int top = kBuckets - kBucketsPerLane * (lane + 1);   // lowest digit of the lane
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      hv[j] = hist[255 - 4 * lane - j];
-      hsum += hv[j];
+      for (int j = 0; j < kBucketsPerLane / 4; ++j) {
+        const int4 w = *reinterpret_cast<const int4*>(&hist[top + 4 * j]);
+        hv[kBucketsPerLane - 1 - 4 * j] = w.x;
+        hv[kBucketsPerLane - 2 - 4 * j] = w.y;
+        hv[kBucketsPerLane - 3 - 4 * j] = w.z;
+        hv[kBucketsPerLane - 4 - 4 * j] = w.w;
+      }
+#pragma unroll
+      for (int j = 0; j < kBucketsPerLane; ++j) hsum += hv[j];
     }
     int tot;
     int acc = taken + wave_exclusive_sum(hsum, &tot);
     (void)tot;
     int cut = -1;                                  // first digit whose bucket overflows
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (cut < 0 && acc + hv[j] > cap_sel) cut = 255 - 4 * lane - j;
+    for (int j = 0; j < kBucketsPerLane; ++j) {
+      if (cut < 0 && acc + hv[j] > cap_sel) cut = kBuckets - 1 - kBucketsPerLane * lane - j;
       acc += hv[j];
     }
     const uint64_t cut_lanes = __ballot(cut >= 0);

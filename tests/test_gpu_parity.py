@@ -461,3 +461,60 @@ def test_select_random_instances_many_segments(U, tie_levels):
         assert np.array_equal(sc_h[si], score)
         assert np.array_equal(keep_h[si], keep), si
         assert int(kept_h[si]) == kept
+
+
+@pytest.mark.parametrize("U", [300, 1200])
+def test_select_scores_at_division_edges(U):
+    """Unit scores floor(W_u / len_u) where the quotient sits just below, at and just above an
+    integer, around 2^53 and far above it (both select paths), against the oracle."""
+    from paper_2609_34653_amd import omnitide as ot
+    rng = np.random.default_rng(U + 53)
+    lens = rng.integers(1, 3000, size=U)
+    first = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    last = first + lens - 1
+    kind = rng.integers(0, 4, size=U)
+    q = rng.integers(1, 1 << 40, size=U, dtype=np.int64)
+    wsum = np.where(kind == 0, q * lens + rng.integers(-1, 2, size=U),          # near multiples
+                    np.where(kind == 1, (1 << 53) + rng.integers(-3, 4, size=U),  # around 2^53
+                             np.where(kind == 2, rng.integers(1 << 53,
+                                                              np.maximum(lens << 50,
+                                                                         (1 << 53) + 1),
+                                                              dtype=np.int64),
+                                      rng.integers(0, 1 << 53, size=U, dtype=np.int64))))
+    wsum = np.maximum(wsum, 0).astype(np.int64)
+    flags = np.zeros(U, np.int64)
+    budget, recent = int(lens.sum() // 3), 2000
+    i32 = lambda a: dev(np.asarray(a, np.int32))   # noqa: E731
+    sc_d = torch.zeros(U, dtype=torch.int64, device="cuda")
+    keep_d = torch.zeros(U, dtype=torch.uint8, device="cuda")
+    kept_d = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stat = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ot.omnitide_select_units(dev(wsum), i32(lens), i32(first), i32(last), i32(flags), 1, U,
+                             budget, recent, sc_d, keep_d, kept_d, stat)
+    torch.cuda.synchronize()
+    assert int(host(stat)[0]) == 0
+    score, keep, kept = oracle.select_units(wsum, lens, first, last, flags, budget, recent)
+    assert np.array_equal(host(sc_d), score)
+    assert np.array_equal(host(keep_d), keep)
+    assert int(host(kept_d)[0]) == kept
+
+
+def test_select_score_out_of_key_range_reported():
+    """A score of 2^51 or more does not fit the ranking key: E_TAGS, nothing kept."""
+    from paper_2609_34653_amd import omnitide as ot
+    U = 40
+    lens = np.full(U, 10)
+    first = np.arange(U) * 10
+    last = first + 9
+    wsum = np.full(U, 1000, np.int64)
+    wsum[7] = 10 << 51
+    i32 = lambda a: dev(np.asarray(a, np.int32))   # noqa: E731
+    sc_d = torch.zeros(U, dtype=torch.int64, device="cuda")
+    keep_d = torch.ones(U, dtype=torch.uint8, device="cuda")
+    kept_d = torch.ones(1, dtype=torch.int32, device="cuda")
+    stat = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ot.omnitide_select_units(dev(wsum), i32(lens), i32(first), i32(last), i32(np.zeros(U)), 1, U,
+                             200, 30, sc_d, keep_d, kept_d, stat)
+    torch.cuda.synchronize()
+    assert int(host(stat)[0]) == ot.E_TAGS
+    assert not host(keep_d).any() and int(host(kept_d)[0]) == 0
