@@ -106,6 +106,15 @@ __device__ inline void dma16(const void* base, uint32_t voff, uint32_t lds_base)
 }
 
 // max(x over both 32-lane halves): v_permlane32_swap exchanges the halves without LDS.
+// This lane's index in its wave, recomputed (two instructions) at the point of use.  The span
+// paths index by lane only now and then; a fresh value there spares the register allocator a
+// long-lived copy, which it would otherwise spill and reload behind the tile prefetches.
+__device__ inline int lane_now() {
+  int r;   // volatile: not hoisted out of the loop (where it would be spilled again)
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(r));
+  return r;
+}
+
 __device__ inline float max_halves(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
                                                   false);
@@ -247,7 +256,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   // SPAN: wave 0 holds the positions of the next V tile's keys (one per lane, -1 past the span)
   int kp_next = -1;
   auto load_kpos = [&](int t) {
-    const int j = t * kKT + lane;
+    const int j = t * kKT + lane_now();
     kp_next = j < nctx ? key_pos[static_cast<size_t>(seg) * cap + j] : -1;
   };
 
@@ -320,7 +329,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
 #pragma unroll
           for (int cq = 0; cq < S::CALLS; ++cq) {
             if (((valid >> krowl[cq]) & 1) == 0)
-              *reinterpret_cast<u32x4*>(vb + 8 * ((wave + kAttnWaves * cq) * kWave + lane)) =
+              *reinterpret_cast<u32x4*>(vb + 8 * ((wave + kAttnWaves * cq) * kWave + lane_now())) =
                   u32x4{0, 0, 0, 0};
           }
         }
@@ -332,7 +341,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         causal = info.x > full_lim;
         masked = info.y != 0 || causal;
         if (causal) {
-          if (wave == 0) kpos_lds[lane] = kp_next;
+          if (wave == 0) kpos_lds[lane_now()] = kp_next;
           __syncthreads();
         }
         if (t + 2 < t_end) issue(k_head, koff, tile_of(t + 2), B);
