@@ -109,7 +109,7 @@ def test_modality_weight_ratio():
 
 def test_brute_force_tiny_config():
     """Per-element scalar loop (math.floor on Python floats) on a small slice of the 1.6K case."""
-    st = sg.make_stream(sg.CONFIGS[0])
+    st = sg.make_stream(sg.CONFIG_BY_NAME["tiny_1p6k_f32"])
     seg = st.segment(0)
     n = 200
     k = storage_np(seg.k_hist)[:n]

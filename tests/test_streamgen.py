@@ -48,13 +48,13 @@ def test_80k_frame_mix():
 
 
 def test_values_seeded_and_shaped():
-    cfg = sg.CONFIGS[1]
+    cfg = sg.CONFIG_BY_NAME["single_layer_8k"]
     a = sg.make_stream(cfg).segment(0)
     b = sg.make_stream(cfg).segment(0)
     assert a.k_hist.dtype == torch.bfloat16 and tuple(a.k_hist.shape) == (8192, 8, 128)
     assert tuple(a.q.shape) == (665, 32, 128) and tuple(a.v_chunk.shape) == (665, 8, 128)
     assert torch.equal(a.k_hist, b.k_hist) and torch.equal(a.q, b.q)
-    c = sg.make_stream(sg.CONFIGS[2])
+    c = sg.make_stream(sg.CONFIG_BY_NAME["hires_32k_36layer"])
     assert not torch.equal(c.segment(0).k_chunk, c.segment(1).k_chunk)
     x = a.k_hist.float()
     assert abs(x.mean().item()) < 0.3 and 0.9 < x.std().item() < 1.3
