@@ -357,6 +357,12 @@ def main():
         kernels[n]["us_host_launched"] = avg[j] * 1e3
     for k in ("score", "compact"):
         kernels[k]["frac_hbm"] = kernels[k]["GBps"] / HBM_PEAK_GBPS
+    # Minimum movement: kept history rows whose slot changes (the rest could stay in place), read
+    # and written once each for K and V -- the figure a selective migration would move.
+    src = st.src_of_dst[:kept].cpu().numpy()
+    moved = int(np.count_nonzero(src != np.arange(kept)))
+    kernels["compact"]["moved_rows"] = moved
+    kernels["compact"]["min_move_bytes"] = 2 * moved * 2 * H * d * elt
     kernels["attend"]["frac_mfma"] = attn_tflops / BF16_PEAK_TFLOPS
     for k in kernels:
         kernels[k]["traffic"] = counter_traffic(k, cfg.name)
