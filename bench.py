@@ -936,6 +936,18 @@ def other_configs(dev, steps, use_graph=True):
     return res
 
 
+def cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(cfg, stream, seg, flops):
     """The CPU oracle (exact integers + float64 attention) on one step of the same workload."""
     import oracle
@@ -967,7 +979,7 @@ def cpu_baseline(cfg, stream, seg, flops):
                      "attention of all 665 queries x 32 heads)",
            "stage_s": {"score": round(t1 - t0, 3), "select": round(t2 - t1, 3),
                        "compact": round(t3 - t2, 3), "attend": round(t4 - t3, 3)},
-           "step_s": round(step_s, 3)}
+           "step_s": round(step_s, 3), "cpu_model": cpu_model()}
     # The same oracle on one thread: score, select and compact as above, attention for the
     # first KV head's group of query heads only (1/H_kv of the flops); the rate is scaled from
     # that group's flops.
