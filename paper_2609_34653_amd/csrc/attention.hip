@@ -328,7 +328,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
           uint16_t* vb = lds + (2 + B) * S::TILE_ELEMS;
 #pragma unroll
           for (int cq = 0; cq < S::CALLS; ++cq) {
-            if (((valid >> krowl[cq]) & 1) == 0)
+            if (((valid >> (((wave + kAttnWaves * cq) * kWave + lane_now()) / S::CHUNKS)) & 1) == 0)
               *reinterpret_cast<u32x4*>(vb + 8 * ((wave + kAttnWaves * cq) * kWave + lane_now())) =
                   u32x4{0, 0, 0, 0};
           }
