@@ -391,7 +391,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       // of this tile, so the vector ALU works while the matrix core runs (a wave issues in
       // order).  In the last iteration the next-K buffer holds a stale tile; the scores
       // computed from it are discarded, which keeps the loop body branch-free.
+      // Each segment also rounds its completed pairs of probabilities into the P operand and
+      // adds them to the row sum (in the same pair order and chains as the rowsum below), so
+      // no vector work is left between the two MFMA phases.
+      static_assert(EPS % 2 == 0, "whole pairs per segment");
       float e[32];
+      bf16x8 pf[2][2];
+      const bf16x2 one2 = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+      float ls_run[2] = {0.f, 0.f};
       {
         s_nxt[0] = floatx16{};
         s_nxt[1] = floatx16{};
@@ -409,10 +416,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
             const int x = i * EPS + j;
             e[x] = __builtin_amdgcn_exp2f(fmaf(s_cur[x >> 4][x & 15], scale_log2, -m_use));
           }
+#pragma unroll
+          for (int j = 0; j < EPS; j += 2) {
+            const int x = i * EPS + j;
+            const __bf16 b0 = static_cast<__bf16>(e[x]), b1 = static_cast<__bf16>(e[x + 1]);
+            pf[x >> 4][(x >> 3) & 1][x & 7] = b0;
+            pf[x >> 4][(x >> 3) & 1][(x & 7) + 1] = b1;
+            const bf16x2 pr = {b0, b1};
+            ls_run[(x >> 1) & 1] =
+                __builtin_amdgcn_fdot2_f32_bf16(pr, one2, ls_run[(x >> 1) & 1], false);
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
-      bf16x8 pf[2][2];
       auto pack = [&]() {
 #pragma unroll
         for (int x = 0; x < 32; ++x) pf[x >> 4][(x >> 3) & 1][x & 7] = static_cast<__bf16>(e[x]);
@@ -420,7 +436,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       // Row sum of the rounded probabilities (exactly the weights the P*V product uses), two
       // bf16 pairs per instruction against (1, 1), in two chains.
       auto rowsum = [&]() {
-        const bf16x2 one2 = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
         float ls[2] = {0.f, 0.f};
 #pragma unroll
         for (int x = 0; x < 16; ++x) {
@@ -431,8 +446,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         }
         return ls[0] + ls[1];
       };
-      pack();
-      float lsum = rowsum();
+      float lsum = ls_run[0] + ls_run[1];
       if (__any(!(lsum < kSumLimit))) {
         // Slow path: exact tile maximum, move the reference, rescale, recompute the tile.
         float mx = -INFINITY;
