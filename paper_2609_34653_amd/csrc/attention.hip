@@ -472,22 +472,25 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
       l_run += lsum;
 
       // O^T += V^T P^T: the V^T operand (dims 32dt.., keys 32st+16h+8cc..+8) from two
-      // transposing reads of four keys each.
+      // transposing reads of four keys each, read three products ahead (the order pinned by
+      // the segment fences; the scheduler would otherwise move the reads next to their use).
+      constexpr int NPV = 4 * (D / 32);
+      auto vop = [&](int i) {
+        const int dt = i % (D / 32), cc = (i / (D / 32)) & 1, st = i / (2 * (D / 32));
+        const int unit = (2 * dt + gq) ^ vsl;
+        const uint16_t* vp = Vs + (32 * st + 16 * h + 8 * cc) * D + 16 * unit + v_lane_off;
+        const shortx4 lo = ld_tr(vp);
+        const shortx4 hi = ld_tr(vp + 4 * D);
+        return __builtin_bit_cast(bf16x8,
+                                  __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      };
+      bf16x8 va[4] = {vop(0), vop(1), vop(2), bf16x8{}};
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int cc = 0; cc < 2; ++cc) {
-#pragma unroll
-          for (int dt = 0; dt < D / 32; ++dt) {
-            const int unit = (2 * dt + gq) ^ vsl;
-            const uint16_t* vp = Vs + (32 * st + 16 * h + 8 * cc) * D + 16 * unit + v_lane_off;
-            const shortx4 lo = ld_tr(vp);
-            const shortx4 hi = ld_tr(vp + 4 * D);
-            const bf16x8 av = __builtin_bit_cast(
-                bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            o[dt] = mfma(av, pf[st][cc], o[dt]);
-          }
-        }
+      for (int i = 0; i < NPV; ++i) {
+        if (i + 3 < NPV) va[(i + 3) % 4] = vop(i + 3);
+        const int dt = i % (D / 32), cc = (i / (D / 32)) & 1, st = i / (2 * (D / 32));
+        o[dt] = mfma(va[i % 4], pf[st][cc], o[dt]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     };
     int t = t_begin;
