@@ -42,10 +42,10 @@ FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 COUNTER_TRAFFIC = {
     "score": (("score.hip", "common.h"), "096c5fd963427f8e", 57080.8, 490.7),
     "select": (("select.hip", "common.h"), "ed497466cc16c45f", 21.1, 3.0),
-    "compact": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34140.8, 68063.6),
-    "attend": (("attention.hip", "combine.h", "common.h"), "ecc4af619b0c9f8b", 54335.1, 43058.8),
+    "compact": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34140.8, 68074.5),
+    "attend": (("attention.hip", "combine.h", "common.h"), "0099f670a6691cbb", 54331.4, 43058.8),
     "compact_rope": (("compact.hip", "common.h"), "92c1892509b5a7e4", 34177.5, 68026.7),
-    "decode": (("decode.hip", "combine.h", "common.h"), "6b7db838cc5d8230", 34300.0, 536.0),
+    "decode": (("decode.hip", "combine.h", "common.h"), "055a8a55b6500f7b", 34353.5, 536.0),
 }
 
 
@@ -53,7 +53,7 @@ COUNTER_TRAFFIC = {
 # `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0 --no-other-configs`:
 # SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1,024 SIMDs) per dispatch (the MFMA-only
 # probe reads 0.97 with this normalisation); keyed by the kernel's sources like COUNTER_TRAFFIC.
-MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "ecc4af619b0c9f8b", 0.539)
+MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "0099f670a6691cbb", 0.55)
 
 
 def mfma_busy(config):

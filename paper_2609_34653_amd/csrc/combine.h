@@ -11,16 +11,17 @@ namespace {
 
 // Merge split partials: out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, M = max_s m_s,
 // splits in order.
-// CH = splits loaded per step (4 for a few splits, 16 or 32 for many).
-template <int D, int CH>
-__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
+// CH = splits loaded per step (4 for a few splits, 16 or 32 for many); BLOCK = threads per
+// workgroup.
+template <int D, int CH, int BLOCK = 256>
+__global__ __launch_bounds__(BLOCK) void attn_combine_kernel(const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml,
                                                            int n_split, size_t n_rows,
                                                            const int32_t* __restrict__ n_ctx_g,
                                                            int L, int Hq, int cap,
                                                            float* __restrict__ out) {
   constexpr int TPR = D / 4;                       // threads per row, 4 floats each
-  const size_t row = static_cast<size_t>(blockIdx.x) * (256 / TPR) + threadIdx.x / TPR;
+  const size_t row = static_cast<size_t>(blockIdx.x) * (BLOCK / TPR) + threadIdx.x / TPR;
   if (row >= n_rows) return;
   const int seg = static_cast<int>(row / (static_cast<size_t>(L) * Hq));
   const int nctx = n_ctx_g[seg];
@@ -83,8 +84,12 @@ hipError_t launch_combine(const float* part_o, const float* part_ml, int n_split
     hipLaunchKernelGGL((attn_combine_kernel<D, 16>), dim3(blocks), dim3(256), 0, stream, part_o,
                        part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
   else
-    hipLaunchKernelGGL((attn_combine_kernel<D, 32>), dim3(blocks), dim3(256), 0, stream, part_o,
-                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
+    // many splits and few rows (decode): two rows per 64-thread block, so that the loads of the
+    // partials spread over more CUs
+    hipLaunchKernelGGL((attn_combine_kernel<D, 32, 64>),
+                       dim3(static_cast<unsigned>((n_rows + 64 / (D / 4) - 1) / (64 / (D / 4)))),
+                       dim3(64), 0, stream, part_o, part_ml, n_split, n_rows, n_ctx, L, Hq, cap,
+                       out);
   return hipGetLastError();
 }
 
