@@ -23,6 +23,6 @@ from .omnipage import compact_kv, page_span, n_pages  # noqa: F401
 from .attention import chunk_attention, to_f64  # noqa: F401
 from .pipeline import stream_step  # noqa: F401
 from .rope import rope_thetas, pair_dims, shift_keys  # noqa: F401
-from .spans import plan_spans, unit_modality  # noqa: F401
+from .spans import plan_spans  # noqa: F401
 from .native import (evict_logical, place_chunk, span_of, active_pages,  # noqa: F401
                      packed_span, plan_suffix, pack_suffix, span_attention)

@@ -6,7 +6,7 @@ class OracleError(Exception):
 
 
 class TagError(OracleError):
-    """Malformed slot tags: unit id outside [-1, U), modality above 3, or a live unit whose
+    """Malformed slot tags: unit id outside [-1, U), modality above 4, or a live unit whose
     slots are not one contiguous run in temporal (slot) order."""
     code = -17
 

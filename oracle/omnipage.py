@@ -41,12 +41,14 @@ def page_span(n_ctx: int, page_size: int) -> int:
 
 def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
                k_chunk, v_chunk, chunk_modality, chunk_unit, cap_dst: int, page_size: int,
-               rope=None, keep_len=None):
+               rope=None, keep_len=None, keep_slot=None):
     """Order-preserving out-of-place packing of the kept units' rows, then the chunk.
 
     keep: per unit, nonzero = kept whole.  keep_len (instead of keep, which is then ignored):
     per unit, the number of its leading live slots (in slot order) that stay -- the span plan's
-    partially retained units.
+    partially retained units of one modality.  keep_slot (instead of both): per slot, nonzero =
+    the slot's entry stays -- the span plan's retained spans inside units; a unit survives if
+    any of its slots does.
 
     k_src/v_src: [n_slots, H_kv, d] (any dtype; rows are copied verbatim).
     Returns a dict: k, v ([n_ctx, H_kv, d]), unit_id, modality, pos, src_of_dst (per destination
@@ -64,12 +66,17 @@ def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
     L = len(chunk_modality)
 
     has_rows = np.zeros(n_units, bool)
-    has_rows[unit_id[unit_id >= 0]] = True
-    if keep_len is not None:
-        quota = np.asarray(keep_len, np.int64).copy()
+    if keep_slot is not None:
+        stay = (unit_id >= 0) & (np.asarray(keep_slot) != 0)
+        has_rows[unit_id[stay]] = True
+        kept_unit = has_rows
     else:
-        quota = np.where(np.asarray(keep) != 0, np.iinfo(np.int64).max, 0)
-    kept_unit = (quota > 0) & has_rows
+        has_rows[unit_id[unit_id >= 0]] = True
+        if keep_len is not None:
+            quota = np.asarray(keep_len, np.int64).copy()
+        else:
+            quota = np.where(np.asarray(keep) != 0, np.iinfo(np.int64).max, 0)
+        kept_unit = (quota > 0) & has_rows
     unit_remap = np.full(n_units, -1, np.int64)
     nxt = 0
     for u in range(n_units):
@@ -85,8 +92,12 @@ def compact_kv(k_src, v_src, unit_id, modality, pos, keep, n_units: int,
         u = unit_id[s]
         if u < 0:
             continue
-        if quota[u] > 0:
-            quota[u] -= 1
+        if keep_slot is not None:
+            stays = bool(stay[s])
+        else:
+            stays = quota[u] > 0
+            quota[u] -= 1 if stays else 0
+        if stays:
             rows.append(s)
             new_pos.append(int(pos[s]) - deleted)
         else:

@@ -26,6 +26,9 @@ Readings where the paper is silent (the paper's planner is metadata-only and pri
     ties go to the newer unit), kept in rank order while they fit into what is left of B; stop
     at the first that does not fit.
   * Units are whole: a unit is kept entirely or not at all.
+  * Structural markers (modality tag 4: a unit's start and end tokens and the open and close
+    tokens of its image and audio spans, as in the paper's unit grammar) are special tokens of
+    the language model's text vocabulary, so the score weighs them as text.
 """
 from __future__ import annotations
 
@@ -34,7 +37,10 @@ import numpy as np
 from .errors import BudgetError, TagError
 
 MOD_SYS = 0
-N_MODALITIES = 4
+MOD_TEXT = 3
+MOD_MARK = 4
+N_MODALITIES = 4          # weights: system, video, audio, text
+N_TAGS = 5                # modality tags: the four modalities and the structural marker
 Q_CLAMP = 32.0
 Q_SCALE = 65536.0
 
@@ -68,8 +74,13 @@ def weights_q88(weights) -> np.ndarray:
 def check_slot_tags(unit_id: np.ndarray, modality: np.ndarray, n_units: int) -> None:
     if np.any(unit_id < -1) or np.any(unit_id >= n_units):
         raise TagError("unit id out of range")
-    if np.any(modality >= N_MODALITIES):
+    if np.any(modality < 0) or np.any(modality >= N_TAGS):
         raise TagError("modality out of range")
+
+
+def weight_index(m: int) -> int:
+    """Weight slot of a modality tag: structural markers take the text weight."""
+    return MOD_TEXT if m == MOD_MARK else int(m)
 
 
 def score_units(k: np.ndarray, dtype: str, unit_id: np.ndarray, modality: np.ndarray,
@@ -100,7 +111,7 @@ def score_units(k: np.ndarray, dtype: str, unit_id: np.ndarray, modality: np.nda
         u = unit_id[s]
         if u < 0:
             continue
-        wsum[u] += wq[modality[s]] * a[s]
+        wsum[u] += wq[weight_index(modality[s])] * a[s]
         length[u] += 1
         first[u] = min(first[u], s)
         last[u] = max(last[u], s)

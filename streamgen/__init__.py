@@ -26,8 +26,9 @@ from typing import List, Optional, Tuple
 import numpy as np
 import torch
 
-MOD_SYS, MOD_VIDEO, MOD_AUDIO, MOD_TEXT = 0, 1, 2, 3
-MODALITY_NAMES = {MOD_SYS: "sys", MOD_VIDEO: "video", MOD_AUDIO: "audio", MOD_TEXT: "text"}
+MOD_SYS, MOD_VIDEO, MOD_AUDIO, MOD_TEXT, MOD_MARK = 0, 1, 2, 3, 4
+MODALITY_NAMES = {MOD_SYS: "sys", MOD_VIDEO: "video", MOD_AUDIO: "audio", MOD_TEXT: "text",
+                  MOD_MARK: "marker"}
 
 # Modality importance weights (video 1.0, audio 1.5, text 2.0; system tokens are protected,
 # their weight is irrelevant and set to 2.0).  Index = modality tag.
@@ -145,6 +146,55 @@ def stream_units(cfg: StreamConfig, rng: np.random.Generator):
     return units, chunk
 
 
+@dataclasses.dataclass(frozen=True)
+class MixedUnit:
+    """A unit given token by token: one modality tag per token (tag 4 = structural marker)."""
+    codes: Tuple[int, ...]
+
+
+def grammar_unit(n_video: int, n_audio: int, n_text: int) -> MixedUnit:
+    """A unit in the paper's grammar (Overview, key insight): a start marker, the image span
+    between its open and close markers, the audio span between its own markers, text, and an
+    end marker.  An empty image or audio span is left out with its markers."""
+    codes = [MOD_MARK]
+    if n_video:
+        codes += [MOD_MARK] + [MOD_VIDEO] * n_video + [MOD_MARK]
+    if n_audio:
+        codes += [MOD_MARK] + [MOD_AUDIO] * n_audio + [MOD_MARK]
+    codes += [MOD_TEXT] * n_text + [MOD_MARK]
+    return MixedUnit(tuple(codes))
+
+
+def unit_codes(unit) -> np.ndarray:
+    """Per-token modality tags of a unit given as (modality, length) or as a MixedUnit."""
+    if isinstance(unit, MixedUnit):
+        return np.asarray(unit.codes, np.uint8)
+    m, n = unit
+    return np.full(n, m, np.uint8)
+
+
+def grammar_stream_units(cfg: StreamConfig, rng: np.random.Generator):
+    """The history of ``cfg`` with each second's content as one grammar unit: the second's
+    frame (if any), its audio and the text turns that follow it inside the same unit.  The
+    chunk is one grammar unit too.  Same seeded structure draws as ``stream_units``."""
+    units, chunk = stream_units(cfg, rng)
+    out, cur = [], None
+    for m, n in units:
+        if m == MOD_TEXT and cur is not None:
+            cur[2] += n
+            continue
+        if m == MOD_VIDEO or cur is None or (m == MOD_AUDIO and cur[1]):
+            if cur is not None:
+                out.append(grammar_unit(*cur))
+            cur = [0, 0, 0]
+        cur[0 if m == MOD_VIDEO else 1 if m == MOD_AUDIO else 2] += n
+    if cur is not None:
+        out.append(grammar_unit(*cur))
+    nv = sum(n for m, n in chunk if m == MOD_VIDEO)
+    na = sum(n for m, n in chunk if m == MOD_AUDIO)
+    return out, [grammar_unit(nv, na, 0)]
+
+
 @dataclasses.dataclass
 class Layout:
     """Per-slot tags of a history pool: unit id (-1 = hole), modality, logical position."""
@@ -168,8 +218,10 @@ class Layout:
 
 
 def build_layout(units, chunk, evicted: Optional[set] = None) -> Layout:
+    """Units are (modality, length) pairs or MixedUnit token lists, in temporal order."""
     evicted = evicted or set()
-    n_slots = sum(n for _, n in units)
+    codes = [unit_codes(u) for u in units]
+    n_slots = sum(len(c) for c in codes)
     unit_id = np.empty(n_slots, np.int32)
     modality = np.empty(n_slots, np.uint8)
     pos = np.empty(n_slots, np.int32)
@@ -177,8 +229,9 @@ def build_layout(units, chunk, evicted: Optional[set] = None) -> Layout:
     s = 0
     live_id = 0
     live_pos = 0
-    for ui, (m, n) in enumerate(units):
-        modality[s:s + n] = m
+    for ui, c in enumerate(codes):
+        n = len(c)
+        modality[s:s + n] = c
         orig[s:s + n] = ui
         if ui in evicted:
             unit_id[s:s + n] = -1
@@ -189,8 +242,10 @@ def build_layout(units, chunk, evicted: Optional[set] = None) -> Layout:
             live_id += 1
             live_pos += n
         s += n
-    cmod = np.concatenate([np.full(n, m, np.uint8) for m, n in chunk])
-    cunit = np.concatenate([np.full(n, i, np.int32) for i, (_, n) in enumerate(chunk)])
+    ccodes = [unit_codes(u) for u in chunk]
+    cmod = np.concatenate([c for c in ccodes]) if ccodes else np.zeros(0, np.uint8)
+    cunit = (np.concatenate([np.full(len(c), i, np.int32) for i, c in enumerate(ccodes)])
+             if ccodes else np.zeros(0, np.int32))
     return Layout(unit_id, modality, pos, live_id, orig, len(units), cmod, cunit, len(chunk))
 
 
@@ -202,9 +257,10 @@ def choose_evicted(rng, units, frac: float, recent: int) -> set:
     tail = 0
     protected = set()
     for ui in range(len(units) - 1, -1, -1):
-        if tail + units[ui][1] > recent:
+        n = len(unit_codes(units[ui]))
+        if tail + n > recent:
             break
-        tail += units[ui][1]
+        tail += n
         protected.add(ui)
     pool = [ui for ui in range(len(units)) if ui not in protected]
     k = int(round(frac * len(units)))
@@ -262,9 +318,10 @@ class Stream:
         return draw_segment(self.cfg, self.layout, self.segment_seed(layer))
 
 
-def make_stream(cfg: StreamConfig) -> Stream:
+def make_stream(cfg: StreamConfig, grammar: bool = False) -> Stream:
+    """The workload's stream; ``grammar`` groups each second into one mixed grammar unit."""
     rng = np.random.default_rng(cfg.seed)
-    units, chunk = stream_units(cfg, rng)
+    units, chunk = (grammar_stream_units if grammar else stream_units)(cfg, rng)
     evicted = choose_evicted(rng, units, cfg.evict_frac, cfg.recent)
     return Stream(cfg, build_layout(units, chunk, evicted))
 
@@ -290,10 +347,33 @@ def custom_stream(units, chunk, *, n_q_heads=4, n_kv_heads=1, head_dim=64, dtype
 
 def random_units(rng: np.random.Generator, n_units: int, lo: int = 1, hi: int = 40,
                  sys_prefix: int = 0):
-    """Random mixed-modality unit list (tests)."""
+    """Random single-modality unit list (tests)."""
     units = []
     if sys_prefix:
         units.append((MOD_SYS, sys_prefix))
     for _ in range(n_units):
         units.append((int(rng.integers(1, 4)), int(rng.integers(lo, hi + 1))))
+    return units
+
+
+def random_mixed_units(rng: np.random.Generator, n_units: int, hi: int = 40,
+                       sys_prefix: int = 0):
+    """Random units of mixed modality (tests): grammar units with random span lengths (empty
+    spans included), units of one modality, and free token sequences with several spans of a
+    modality, with or without markers between them."""
+    units = []
+    if sys_prefix:
+        units.append((MOD_SYS, sys_prefix))
+    for _ in range(n_units):
+        kind = int(rng.integers(3))
+        if kind == 0:
+            units.append(grammar_unit(int(rng.integers(0, hi + 1)), int(rng.integers(0, hi // 2 + 1)),
+                                      int(rng.integers(0, hi // 2 + 1))))
+        elif kind == 1:
+            units.append((int(rng.integers(1, 4)), int(rng.integers(1, hi + 1))))
+        else:
+            codes = []
+            for _ in range(int(rng.integers(1, 6))):
+                codes += [int(rng.integers(1, 5))] * int(rng.integers(1, hi // 2 + 1))
+            units.append(MixedUnit(tuple(codes)))
     return units

@@ -97,14 +97,27 @@ def test_sign_and_permutation_invariance():
 
 
 def test_modality_weight_ratio():
-    # identical keys tagged video then audio then text: sums in ratio 256 : 384 : 512
+    # identical keys tagged video, audio, text, marker: sums in ratio 256 : 384 : 512 : 512
     rng = np.random.default_rng(3)
     row = rng.standard_normal((1, 2, 8)).astype(np.float32)
-    k = np.repeat(row, 3, axis=0)
-    sc = oracle.score_units(k, "f32", np.array([0, 1, 2], np.int32), np.array([1, 2, 3], np.uint8),
-                            sg.DEFAULT_WEIGHTS, 3)
+    k = np.repeat(row, 4, axis=0)
+    sc = oracle.score_units(k, "f32", np.array([0, 1, 2, 3], np.int32),
+                            np.array([1, 2, 3, 4], np.uint8), (1.0, 1.0, 1.5, 2.5), 4)
     w = sc["wsum"]
-    assert w[0] * 384 == w[1] * 256 and w[0] * 512 == w[2] * 256
+    assert w[0] * 384 == w[1] * 256 and w[0] * 640 == w[2] * 256 and w[3] == w[2]
+
+
+def test_mixed_unit_closed_form():
+    """One grammar unit (markers, 3 video, 2 audio, 1 text) of constant keys c = 0.75:
+    a_s = 16 * 49152 per slot, W = a_s * (6 markers * 512 + 3 * 256 + 2 * 384 + 512)."""
+    lay = sg.build_layout([sg.grammar_unit(3, 2, 1)], [])
+    n = lay.n_slots
+    assert n == 12 and (lay.modality == 4).sum() == 6
+    k = np.full((n, 2, 8), 0.75, np.float32)
+    sc = oracle.score_units(k, "f32", lay.unit_id, lay.modality, sg.DEFAULT_WEIGHTS, 1)
+    a = 16 * 49152
+    assert sc["wsum"].tolist() == [a * (6 * 512 + 3 * 256 + 2 * 384 + 512)]
+    assert sc["len"].tolist() == [12] and sc["flags"].tolist() == [0]
 
 
 def test_brute_force_tiny_config():
@@ -137,7 +150,7 @@ def test_tag_errors(bad):
     elif bad == "id_low":
         unit_id[0] = -2
     else:
-        mod[1] = 4
+        mod[1] = 5
     with pytest.raises(TagError):
         oracle.score_units(np.zeros((3, 1, 4), np.float32), "f32", unit_id, mod,
                            sg.DEFAULT_WEIGHTS, 2)
