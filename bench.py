@@ -408,16 +408,18 @@ def main():
                          "in_step": False}
     del pools
 
-    # Span plan (recent units whole; older units keep 256 video / 16 audio leading tokens; 1,024
-    # text tokens oldest first; trimmed toward the budget) and compaction of its kept prefixes,
-    # each timed on its own after the step loop on the same pool.
+    # Span plan (recent units whole; older units keep their markers, 256 leading tokens of each
+    # video span and 16 of each audio span, and 1,024 text tokens oldest first; trimmed toward
+    # the budget) and compaction of its kept slots, each timed on its own after the step loop
+    # on the same pool.
     sp = dict(low=cfg.budget, high=cfg.budget, recent=cfg.recent, sink_video=256, sink_audio=16,
               text_budget=1024)
     c = copies[0]
     st.score(c["k"], c["uid"], c["mod"])
     def plan_call(i):
-        st.plan_spans(copies[i % len(copies)]["mod"], sp["low"], sp["high"], sp["recent"],
-                      sp["sink_video"], sp["sink_audio"], sp["text_budget"])
+        c = copies[i % len(copies)]
+        st.plan_spans(c["uid"], c["mod"], sp["low"], sp["high"], sp["recent"], sp["sink_video"],
+                      sp["sink_audio"], sp["text_budget"])
     plan_us, plan_how = graph_time_us(plan_call, args.steps, dev, not args.no_graph)
     torch.cuda.synchronize()
     kept_sp = int(st.kept_tokens.item())
@@ -430,7 +432,8 @@ def main():
     status = int(st.d_status.item())
     if status != 0:
         raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
-    plan_bytes = lay.n_units * (4 * 4 + 1 + 4) + 4
+    # tags in (unit id, modality), the slot mask out, per-unit structure in, keep_len out
+    plan_bytes = lay.n_slots * (4 + 1 + 1) + lay.n_units * (4 * 4 + 4) + 4
     sbytes_c = compact_bytes(kept_sp, L, H, d, elt, st.cap_dst, lay.n_units)
     kernels["span_plan"] = {"us": round(plan_us, 4), "bytes": plan_bytes, "timing": plan_how,
                             "GBps": round(plan_bytes / (plan_us * 1e-6) / 1e9, 4),

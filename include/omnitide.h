@@ -7,10 +7,10 @@
  *   3. omnitide_compact_kv    order-preserving packing of the kept rows + chunk (OmniPage)
  *   4. omnitide_chunk_attn    GQA prefill attention of the chunk over [history || chunk]
  * plus omnitide_compact_kv_rope (compaction with rotary re-encoding of the moved keys),
- * omnitide_plan_spans + omnitide_compact_kv_spans (the span plan: recent units whole, sink
- * prefixes of older units, a shared text budget, oldest-first trimming, then compaction of the
- * kept prefixes) and omnitide_decode_attn (decode attention of the last few tokens over the
- * compacted pool); omnitide_evict_native, omnitide_pack_suffix, omnitide_place_chunk and
+ * omnitide_plan_spans + omnitide_compact_kv_spans (the span plan: recent units whole, boundary
+ * tokens and sink prefixes of the image and audio spans of older units, a shared text budget,
+ * oldest-first trimming, then compaction of the kept slots) and omnitide_decode_attn (decode
+ * attention of the last few tokens over the compacted pool); omnitide_evict_native, omnitide_pack_suffix, omnitide_place_chunk and
  * omnitide_span_attn keep the native (logical-only) layout with holes instead.
  *
  * Conventions shared by every entry point
@@ -32,9 +32,11 @@
  *
  * KV layout: K and V pools are [n_seg][n_slots][n_kv_heads][head_dim] (token-major: one slot's
  * keys for all KV heads form one contiguous row).  Tags are int32 unit id (-1 = empty slot),
- * uint8 modality (0 system, 1 video, 2 audio, 3 text) and int32 logical position per slot.
- * Units are numbered 0..n_units-1 in temporal order; each live unit occupies one contiguous run
- * of slots, and runs appear in unit order.
+ * uint8 modality (0 system, 1 video, 2 audio, 3 text, 4 structural marker: a unit's start and
+ * end tokens and the open and close tokens of its image and audio spans) and int32 logical
+ * position per slot.  Units are numbered 0..n_units-1 in temporal order; each live unit
+ * occupies one contiguous run of slots, and runs appear in unit order.  A unit may mix
+ * modalities (paper: Overview, the unit grammar).
  */
 #ifndef OMNITIDE_H
 #define OMNITIDE_H
@@ -65,7 +67,8 @@ enum { OMNITIDE_BF16 = 0, OMNITIDE_F32 = 1 };
 /* rotary dimension pairing for omnitide_compact_kv_rope */
 enum { OMNITIDE_ROPE_HALF = 0,          /* pairs (j, j + rope_dims/2) */
        OMNITIDE_ROPE_INTERLEAVED = 1 }; /* pairs (2j, 2j + 1) */
-enum { OMNITIDE_MOD_SYS = 0, OMNITIDE_MOD_VIDEO = 1, OMNITIDE_MOD_AUDIO = 2, OMNITIDE_MOD_TEXT = 3 };
+enum { OMNITIDE_MOD_SYS = 0, OMNITIDE_MOD_VIDEO = 1, OMNITIDE_MOD_AUDIO = 2, OMNITIDE_MOD_TEXT = 3,
+       OMNITIDE_MOD_MARK = 4 };
 
 /* Limits checked on the host. */
 #define OMNITIDE_MAX_UNITS 8192       /* units per segment */
@@ -79,19 +82,21 @@ enum { OMNITIDE_MOD_SYS = 0, OMNITIDE_MOD_VIDEO = 1, OMNITIDE_MOD_AUDIO = 2, OMN
  *   q(x)  = floor(min(|x|, 32) * 2^16)        (NaN and +-Inf count as 32)
  *   a_s   = sum of q over the n_kv_heads*head_dim key elements of slot s
  *   W_u   = sum over live slots s of unit u of w[modality(s)] * a_s, w in units of 1/256
+ *           (marker tokens take the text weight: they are special text-vocabulary tokens)
  * Exact integer arithmetic: the result does not depend on the order of summation.
  *
  *   k          [n_seg][n_slots][n_kv_heads][head_dim], dtype OMNITIDE_BF16 or OMNITIDE_F32
  *   unit_id    int32 [n_seg][n_slots]; -1 marks an empty slot
  *   modality   uint8 [n_seg][n_slots]
- *   weights    HOST float[4], weight per modality tag; each an exact multiple of 1/256 in (0, 4]
+ *   weights    HOST float[4]: system, video, audio, text; each an exact multiple of 1/256 in
+ *              (0, 4]
  *   outputs, [n_seg][n_units] each, fully overwritten:
  *     unit_wsum        uint64  W_u
  *     unit_len         int32   live slots of u
  *     unit_first_slot  int32   first slot of u (n_slots if u has none)
  *     unit_last_slot   int32   last slot of u (-1 if u has none)
  *     unit_flags       uint32  bit 0: u holds a system-modality token
- *   d_status   device: OMNITIDE_E_TAGS for a unit id outside [-1, n_units) or a modality > 3
+ *   d_status   device: OMNITIDE_E_TAGS for a unit id outside [-1, n_units) or a modality > 4
  *              (such a slot is then ignored).
  * Limits: n_seg >= 1, n_slots >= 0, 1 <= n_units <= 8192, head_dim in {64, 128},
  * n_kv_heads >= 1, n_kv_heads * head_dim <= 4096.
@@ -210,58 +215,69 @@ int omnitide_compact_kv_rope(const void* k_src, const void* v_src, int dtype, in
 size_t omnitide_compact_workspace_bytes(int n_seg, int n_units, int cap_dst);
 
 /*
- * omnitide_plan_spans -- span retention plan (paper: Structure-aware retention planning:
- * retention starts above the high watermark and trims toward the low watermark; the system
- * prefix is protected; recent units are kept in full; older units, oldest to newest, keep short
- * image and audio prefixes as sinks, with separate lengths per modality; text is kept oldest to
- * newest until a shared budget is used up; then units are dropped oldest first, partially
- * retained ones before complete ones, until the target is met or one unit remains).
- * Per segment, with len_u > 0 marking live units and class_u = modality[first slot of u]:
- *   sum len_u <= high_watermark  -> keep_len = len (nothing removed)
- *   otherwise keep_len_u =
- *     len_u                              if u holds a system token (flag bit 0; never dropped)
- *     len_u                              if u is recent: newest live non-system units walked
- *                                        newest to oldest while their total <= recent_tokens,
- *                                        stopping at the first misfit
- *     min(len_u, sink_video)             older video unit
- *     min(len_u, sink_audio)             older audio unit
- *     min(len_u, text_budget - T)        older text unit, T = older text tokens before u
- *                                        (clamped at 0: the budget is used up to the token)
+ * omnitide_plan_spans -- span retention plan (paper: Overview, the unit grammar; Structure-aware
+ * retention planning: retention starts above the high watermark and trims toward the low
+ * watermark; the system prefix is protected; recent units are kept in full; older units,
+ * oldest to newest, keep their boundary tokens and short prefixes of their image and audio
+ * spans as sinks, with separate lengths per modality; text is kept oldest to newest until a
+ * shared budget is used up; then units are dropped oldest first, partially retained ones
+ * before complete ones, until the target is met or one unit remains).
+ * Per segment, with len_u > 0 marking live units.  A span is a maximal run of consecutive
+ * slots of one unit with the same modality tag.
+ *   sum len_u <= high_watermark  -> every live slot stays (keep_len = len)
+ *   otherwise:
+ *     a unit holding a system token (flag bit 0) stays whole and is never dropped
+ *     recent units stay whole: newest live non-system units walked newest to oldest while their
+ *       total <= recent_tokens, stopping at the first misfit
+ *     an older unit keeps its marker tokens (tag 4), the first sink_video slots of each video
+ *       span, the first sink_audio slots of each audio span, and its first
+ *       clamp(text_budget - T, 0, text_u) text slots, T = text slots of older units before it
+ *       (the budget is used up to the token)
  *   then, while sum keep_len > low_watermark and more than one unit has keep_len > 0, the next
  *   unit of the drop order gets keep_len 0: partially retained units (0 < keep_len < len) by
  *   id, then complete non-system units by id.  The low watermark is a target, not a bound.
  *   Inputs: omnitide_score_units' unit_len, unit_first_slot, unit_last_slot, unit_flags
- *   ([n_seg][n_units]) and the slot modality tags [n_seg][n_slots].
- *   keep_len     int32 [n_seg][n_units]   leading tokens of each unit that stay
+ *   ([n_seg][n_units]) for the slot tags unit_id (int32) and modality (uint8) [n_seg][n_slots].
+ *   keep_len     int32 [n_seg][n_units]   kept slots of each unit (0: dropped, len: whole)
+ *   keep_slot    uint8 [n_seg][n_slots]   1: the slot's entry stays; 0: deleted or empty slot
  *   kept_tokens  int32 [n_seg]            sum of keep_len
+ *   workspace    device scratch of omnitide_plan_spans_workspace_bytes() bytes
  *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run inside
- *                [0, n_slots), runs are out of unit order, or a unit's first modality is > 3;
- *                the segment's keep_len is then all 0 and kept_tokens 0.
+ *                [0, n_slots), runs are out of unit order, or a unit holds a modality > 4;
+ *                the segment's keep_len and keep_slot are then all 0 and kept_tokens 0.
  * Limits: 1 <= n_units <= 8192, n_slots >= 0, 0 <= low_watermark <= high_watermark, and
- * recent_tokens, sink_video, sink_audio, text_budget >= 0.  One workgroup per segment.
+ * recent_tokens, sink_video, sink_audio, text_budget >= 0.  Three kernels: a census of each
+ * unit's spans (one wave per unit), the plan (one workgroup per segment), the slot mask.
  */
 int omnitide_plan_spans(const int32_t* unit_len, const int32_t* unit_first_slot,
                         const int32_t* unit_last_slot, const uint32_t* unit_flags,
-                        const uint8_t* modality, int n_seg, int n_slots, int n_units,
-                        int low_watermark, int high_watermark, int recent_tokens,
+                        const int32_t* unit_id, const uint8_t* modality, int n_seg, int n_slots,
+                        int n_units, int low_watermark, int high_watermark, int recent_tokens,
                         int sink_video, int sink_audio, int text_budget, int32_t* keep_len,
-                        int32_t* kept_tokens, int32_t* d_status, void* stream);
+                        uint8_t* keep_slot, int32_t* kept_tokens, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream);
+
+size_t omnitide_plan_spans_workspace_bytes(int n_seg, int n_slots, int n_units);
 
 /*
  * omnitide_compact_kv_spans -- compaction of a span plan (paper: Applying the retention plan --
  * unselected ranges are deleted, every retained token moves down by the deleted tokens before
  * it, a partially retained unit keeps its identity with its new length).  Same arguments,
  * outputs and errors as omnitide_compact_kv_rope with `keep` replaced by
- *   keep_len  int32 [n_seg][n_units]: unit u keeps its first min(max(keep_len_u, 0), len_u)
- *             live slots (omnitide_plan_spans' output); units with 0 are dropped and renumbered
- *             -1, the others keep their order and are renumbered densely.
+ *   keep_slot  uint8 [n_seg][n_slots_src]: a live slot stays iff its byte is non-zero
+ *              (omnitide_plan_spans' output; bytes of empty slots are ignored); a unit with no
+ *              remaining slot is dropped and renumbered -1, the others keep their order and are
+ *              renumbered densely.  Destination rows keep slot order; each moves down by the
+ *              deleted live slots before its source slot.
  * and rope_dims == 0 meaning no rotary re-encoding (keys copied verbatim, rope_base and
  * rope_style ignored); otherwise the rope arguments are as for omnitide_compact_kv_rope.
+ * d_status additionally reports OMNITIDE_E_TAGS for a live unit whose slot range
+ * (unit_first_slot, unit_len) leaves the pool; such a unit keeps nothing.
  */
 int omnitide_compact_kv_spans(const void* k_src, const void* v_src, int dtype, int n_seg,
                               int n_slots_src, int n_kv_heads, int head_dim, int page_size,
                               const int32_t* unit_id_src, const uint8_t* modality_src,
-                              const int32_t* pos_src, const int32_t* keep_len,
+                              const int32_t* pos_src, const uint8_t* keep_slot,
                               const int32_t* unit_len, const int32_t* unit_first_slot,
                               int n_units, const void* k_chunk, const void* v_chunk,
                               const uint8_t* chunk_modality, const int32_t* chunk_unit,

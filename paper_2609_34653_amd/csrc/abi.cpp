@@ -126,20 +126,25 @@ namespace {
 int compact_impl(const void* k_src, const void* v_src, int dtype, int n_seg, int n_slots_src,
                  int n_kv_heads, int head_dim, int page_size, const int32_t* unit_id_src,
                  const uint8_t* modality_src, const int32_t* pos_src, const uint8_t* keep,
-                 const int32_t* keep_len, const int32_t* unit_len,
-                 const int32_t* unit_first_slot, int n_units,
+                 const int32_t* keep_len, const uint8_t* keep_slot, bool use_mask,
+                 const int32_t* unit_len, const int32_t* unit_first_slot, int n_units,
                  const void* k_chunk, const void* v_chunk, const uint8_t* chunk_modality,
                  const int32_t* chunk_unit, int chunk_len, void* k_dst, void* v_dst, int cap_dst,
                  int32_t* unit_id_dst, uint8_t* modality_dst, int32_t* pos_dst,
                  int32_t* src_of_dst, int32_t* unit_remap, int32_t* n_ctx, int32_t* n_pages,
                  void* workspace, size_t workspace_bytes, bool rope, double rope_base,
                  int rope_dims, int rope_style, int32_t* d_status, void* stream) {
-  if (!all_set({keep != nullptr ? static_cast<const void*>(keep) : keep_len, unit_len,
-                unit_first_slot, k_dst, v_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
-                unit_remap, n_ctx, n_pages}))
+  // the plan: per-unit keep flags or kept prefixes, or (use_mask) a per-slot mask, which may
+  // be NULL only for a pool without slots
+  const void* plan = use_mask ? static_cast<const void*>(unit_len)
+                     : keep != nullptr ? static_cast<const void*>(keep)
+                                       : static_cast<const void*>(keep_len);
+  if (!all_set({plan, unit_len, unit_first_slot, k_dst, v_dst, unit_id_dst, modality_dst,
+                pos_dst, src_of_dst, unit_remap, n_ctx, n_pages}))
     return OMNITIDE_E_NULL;
   if (n_slots_src > 0 && !all_set({k_src, v_src, unit_id_src, modality_src, pos_src}))
     return OMNITIDE_E_NULL;
+  if (use_mask && n_slots_src > 0 && keep_slot == nullptr) return OMNITIDE_E_NULL;
   if (chunk_len > 0 && !all_set({k_chunk, v_chunk, chunk_modality, chunk_unit}))
     return OMNITIDE_E_NULL;
   const int eb = elt_bytes(dtype);
@@ -171,7 +176,7 @@ int compact_impl(const void* k_src, const void* v_src, int dtype, int n_seg, int
                  {workspace, need}, {d_status, 4}},
                 {{k_src, src_slots * row}, {v_src, src_slots * row}, {unit_id_src, src_slots * 4},
                  {modality_src, src_slots}, {pos_src, src_slots * 4}, {keep, units},
-                 {keep_len, units * 4},
+                 {keep_len, units * 4}, {keep_slot, src_slots},
                  {unit_len, units * 4}, {unit_first_slot, units * 4},
                  {k_chunk, chunk_rows * row}, {v_chunk, chunk_rows * row},
                  {chunk_modality, static_cast<size_t>(chunk_len)},
@@ -189,6 +194,8 @@ int compact_impl(const void* k_src, const void* v_src, int dtype, int n_seg, int
   a.pos_src = pos_src;
   a.keep = keep;
   a.keep_len = keep_len;
+  a.keep_slot = keep_slot;
+  a.use_mask = use_mask;
   a.unit_len = unit_len;
   a.unit_first = unit_first_slot;
   a.n_units = n_units;
@@ -231,8 +238,8 @@ int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_s
                         int32_t* n_ctx, int32_t* n_pages, void* workspace,
                         size_t workspace_bytes, int32_t* d_status, void* stream) {
   return compact_impl(k_src, v_src, dtype, n_seg, n_slots_src, n_kv_heads, head_dim, page_size,
-                      unit_id_src, modality_src, pos_src, keep, nullptr, unit_len,
-                      unit_first_slot,
+                      unit_id_src, modality_src, pos_src, keep, nullptr, nullptr, false,
+                      unit_len, unit_first_slot,
                       n_units, k_chunk, v_chunk, chunk_modality, chunk_unit, chunk_len, k_dst,
                       v_dst, cap_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
                       unit_remap, n_ctx, n_pages, workspace, workspace_bytes, false, 0.0, 0, 0,
@@ -253,8 +260,8 @@ int omnitide_compact_kv_rope(const void* k_src, const void* v_src, int dtype, in
                              double rope_base, int rope_dims, int rope_style,
                              int32_t* d_status, void* stream) {
   return compact_impl(k_src, v_src, dtype, n_seg, n_slots_src, n_kv_heads, head_dim, page_size,
-                      unit_id_src, modality_src, pos_src, keep, nullptr, unit_len,
-                      unit_first_slot,
+                      unit_id_src, modality_src, pos_src, keep, nullptr, nullptr, false,
+                      unit_len, unit_first_slot,
                       n_units, k_chunk, v_chunk, chunk_modality, chunk_unit, chunk_len, k_dst,
                       v_dst, cap_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
                       unit_remap, n_ctx, n_pages, workspace, workspace_bytes, true, rope_base,
@@ -264,7 +271,7 @@ int omnitide_compact_kv_rope(const void* k_src, const void* v_src, int dtype, in
 int omnitide_compact_kv_spans(const void* k_src, const void* v_src, int dtype, int n_seg,
                               int n_slots_src, int n_kv_heads, int head_dim, int page_size,
                               const int32_t* unit_id_src, const uint8_t* modality_src,
-                              const int32_t* pos_src, const int32_t* keep_len,
+                              const int32_t* pos_src, const uint8_t* keep_slot,
                               const int32_t* unit_len, const int32_t* unit_first_slot,
                               int n_units, const void* k_chunk, const void* v_chunk,
                               const uint8_t* chunk_modality, const int32_t* chunk_unit,
@@ -274,41 +281,51 @@ int omnitide_compact_kv_spans(const void* k_src, const void* v_src, int dtype, i
                               int32_t* n_pages, void* workspace, size_t workspace_bytes,
                               double rope_base, int rope_dims, int rope_style,
                               int32_t* d_status, void* stream) {
-  if (keep_len == nullptr) return OMNITIDE_E_NULL;
   return compact_impl(k_src, v_src, dtype, n_seg, n_slots_src, n_kv_heads, head_dim, page_size,
-                      unit_id_src, modality_src, pos_src, nullptr, keep_len, unit_len,
+                      unit_id_src, modality_src, pos_src, nullptr, nullptr, keep_slot, true,
+                      unit_len,
                       unit_first_slot, n_units, k_chunk, v_chunk, chunk_modality, chunk_unit,
                       chunk_len, k_dst, v_dst, cap_dst, unit_id_dst, modality_dst, pos_dst,
                       src_of_dst, unit_remap, n_ctx, n_pages, workspace, workspace_bytes,
                       rope_dims != 0, rope_base, rope_dims, rope_style, d_status, stream);
 }
 
+size_t omnitide_plan_spans_workspace_bytes(int n_seg, int n_slots, int n_units) {
+  if (n_seg < 1 || n_slots < 0 || n_units < 1) return 0;
+  return omnitide::span_plan_workspace_bytes(n_seg, n_slots, n_units);
+}
+
 int omnitide_plan_spans(const int32_t* unit_len, const int32_t* unit_first_slot,
                         const int32_t* unit_last_slot, const uint32_t* unit_flags,
-                        const uint8_t* modality, int n_seg, int n_slots, int n_units,
-                        int low_watermark, int high_watermark, int recent_tokens,
+                        const int32_t* unit_id, const uint8_t* modality, int n_seg, int n_slots,
+                        int n_units, int low_watermark, int high_watermark, int recent_tokens,
                         int sink_video, int sink_audio, int text_budget, int32_t* keep_len,
-                        int32_t* kept_tokens, int32_t* d_status, void* stream) {
+                        uint8_t* keep_slot, int32_t* kept_tokens, void* workspace,
+                        size_t workspace_bytes, int32_t* d_status, void* stream) {
   if (!all_set({unit_len, unit_first_slot, unit_last_slot, unit_flags, keep_len, kept_tokens}))
     return OMNITIDE_E_NULL;
-  if (n_slots > 0 && modality == nullptr) return OMNITIDE_E_NULL;
+  if (n_slots > 0 && !all_set({unit_id, modality, keep_slot})) return OMNITIDE_E_NULL;
   if (n_seg < 1 || n_seg > kMaxGridY || n_slots < 0 || n_units < 1 ||
       n_units > OMNITIDE_MAX_UNITS || low_watermark < 0 || high_watermark < low_watermark ||
       recent_tokens < 0 || sink_video < 0 || sink_audio < 0 || text_budget < 0 ||
       static_cast<long>(n_seg) * n_units > INT32_MAX ||
       static_cast<long>(n_seg) * n_slots > INT32_MAX)
     return OMNITIDE_E_SHAPE;
+  const size_t need = omnitide::span_plan_workspace_bytes(n_seg, n_slots, n_units);
+  if (workspace == nullptr || workspace_bytes < need) return OMNITIDE_E_WORKSPACE;
   const size_t units = static_cast<size_t>(n_seg) * n_units;
   const size_t slots = static_cast<size_t>(n_seg) * n_slots;
-  if (any_alias({{keep_len, units * 4}, {kept_tokens, n_seg * 4ull}, {d_status, 4}},
+  if (any_alias({{keep_len, units * 4}, {keep_slot, slots}, {kept_tokens, n_seg * 4ull},
+                 {workspace, need}, {d_status, 4}},
                 {{unit_len, units * 4}, {unit_first_slot, units * 4}, {unit_last_slot, units * 4},
-                 {unit_flags, units * 4}, {modality, slots}}))
+                 {unit_flags, units * 4}, {unit_id, slots * 4}, {modality, slots}}))
     return OMNITIDE_E_ALIAS;
   omnitide::SpanPlanArgs a;
   a.unit_len = unit_len;
   a.unit_first = unit_first_slot;
   a.unit_last = unit_last_slot;
   a.unit_flags = unit_flags;
+  a.unit_id = unit_id;
   a.modality = modality;
   a.n_seg = n_seg;
   a.n_slots = n_slots;
@@ -320,7 +337,9 @@ int omnitide_plan_spans(const int32_t* unit_len, const int32_t* unit_first_slot,
   a.sink_audio = sink_audio;
   a.text_budget = text_budget;
   a.keep_len = keep_len;
+  a.keep_slot = keep_slot;
   a.kept_tokens = kept_tokens;
+  a.workspace = workspace;
   a.d_status = d_status;
   return hip_status(omnitide::launch_plan_spans(a, static_cast<hipStream_t>(stream)));
 }

@@ -1,13 +1,17 @@
 // Eager, order-preserving, out-of-place compaction of the retained rows plus the chunk append.
-// A unit keeps its first k live tokens: k = len for a unit kept whole (keep flag), or the
-// span plan's kept-prefix length; a partially kept unit's deleted tail counts among the
-// deleted tokens before every later unit.
+// A unit keeps its first k live tokens: k = len for a unit kept whole (keep flag), or a
+// kept-prefix length; or it keeps the slots a per-slot mask marks (the span plan's retained
+// spans).  The deleted tokens of a partially kept unit count among the deleted tokens before
+// every later token.
 //
 // Plan: exclusive scans over units give each kept unit its destination offset, its rank (= new
 // unit id) and the number of deleted live tokens before it.  Up to 512 units every copy
 // workgroup builds this table in LDS itself (wave 0, wave scans), so the compaction is a single
 // kernel; beyond, a plan kernel (1024 threads) writes it to the workspace together with, for
 // every destination tile, the rank of the unit holding the tile's first row.
+// Mask: a count kernel (one wave per unit) gives each unit its kept count, the plan kernel
+// scans those, and a map kernel (one wave per unit, ballots over 64 slots at a time) writes
+// each kept slot's destination row, its tags and its position shift.
 // Copy: one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
 // source slots (binary search over the LDS table, or a short forward walk from the workspace
 // hint), tags are written, then every thread moves 16-byte vectors of the K and V rows.  Rows
@@ -32,7 +36,7 @@ struct RankRec {
 };
 
 struct WsLayout {
-  size_t rank_off, tile_off, meta_off, seg_bytes;
+  size_t rank_off, tile_off, meta_off, count_off, shift_off, seg_bytes;
 };
 
 __host__ __device__ inline WsLayout ws_layout(int n_units, int cap_dst) {
@@ -41,10 +45,14 @@ __host__ __device__ inline WsLayout ws_layout(int n_units, int cap_dst) {
   w.rank_off = 0;
   w.tile_off = (static_cast<size_t>(n_units) + 1) * sizeof(RankRec);
   w.meta_off = w.tile_off + ((n_tiles * 4 + 15) / 16) * 16;
-  w.seg_bytes = ((w.meta_off + 16 + 255) / 256) * 256;
+  w.count_off = w.meta_off + 16;                                  // mask: kept count per unit
+  w.shift_off = w.count_off + ((static_cast<size_t>(n_units) * 4 + 15) / 16) * 16;
+  w.seg_bytes = ((w.shift_off + static_cast<size_t>(cap_dst) * 4 + 255) / 256) * 256;
   return w;
 }
 
+// Kept tokens per unit come from keep (whole units), keep_len (prefixes) or, when both are
+// null, the mask count kernel's per-unit counts in the workspace.
 __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
     const uint8_t* __restrict__ keep_g, const int32_t* __restrict__ keep_len_g,
     const int32_t* __restrict__ len_g, const int32_t* __restrict__ first_g, int n_units,
@@ -63,6 +71,7 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
   RankRec* rank = reinterpret_cast<RankRec*>(wseg + L.rank_off);
   int32_t* tile_hint = reinterpret_cast<int32_t*>(wseg + L.tile_off);
   int32_t* meta = reinterpret_cast<int32_t*>(wseg + L.meta_off);
+  const int32_t* counts = reinterpret_cast<const int32_t*>(wseg + L.count_off);
 
   int kl[kPer], dl[kPer], fs[kPer];
   int my_k = 0, my_d = 0, my_n = 0;
@@ -72,8 +81,9 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
     kl[i] = dl[i] = fs[i] = 0;
     if (i < per && u < U) {
       const int n = max(len_g[base + u], 0);
-      kl[i] = keep_len_g != nullptr ? min(max(keep_len_g[base + u], 0), n)
-                                    : (keep_g[base + u] != 0 ? n : 0);
+      if (keep_len_g != nullptr) kl[i] = min(max(keep_len_g[base + u], 0), n);
+      else if (keep_g != nullptr) kl[i] = keep_g[base + u] != 0 ? n : 0;
+      else kl[i] = min(max(counts[u], 0), n);
       dl[i] = n - kl[i];
       fs[i] = first_g[base + u];
     }
@@ -93,7 +103,9 @@ __global__ __launch_bounds__(kPlanThreads) void compact_plan_kernel(
       if (kl[i] > 0) {
         rank[rk] = RankRec{off, fs[i], del, 0};
         remap_g[base + u] = rk;
-        for (int t = (off + kTile - 1) / kTile; t * kTile < off + kl[i]; ++t) tile_hint[t] = rk;
+        // hints only for tiles inside the destination (kept may exceed it: capacity error)
+        for (int t = (off + kTile - 1) / kTile; t * kTile < min(off + kl[i], cap_dst); ++t)
+          tile_hint[t] = rk;
         ++rk;
       } else {
         remap_g[base + u] = -1;
@@ -151,6 +163,7 @@ struct FusedPlanArgs {
   int32_t* n_ctx;
   int32_t* n_pages;
   int32_t* status;
+  bool mapped;       // history rows were resolved by the mask map kernel
 };
 
 __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_dst,
@@ -237,7 +250,8 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
                                    int32_t* __restrict__ pos_dst,
                                    int32_t* __restrict__ src_of_dst,
                                    const uint8_t* __restrict__ ws, int32_t* src_row,
-                                   int32_t* shift_row, const TilePlan<true>* plan = nullptr) {
+                                   int32_t* shift_row, const TilePlan<true>* plan = nullptr,
+                                   bool mapped = false) {
   const int tid = threadIdx.x;
   const int r0 = t * kTile;
   const size_t dst_tag = static_cast<size_t>(seg) * cap_dst;
@@ -257,7 +271,13 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
 
   if (tid < nrows) {
     const int r = r0 + tid;
-    if (r < kept) {
+    if (r < kept && mapped) {                     // the map kernel wrote the row's tags
+      const WsLayout L = ws_layout(n_units, cap_dst);
+      const int32_t* shift = reinterpret_cast<const int32_t*>(
+          ws + static_cast<size_t>(seg) * L.seg_bytes + L.shift_off);
+      src_row[tid] = src_of_dst[dst_tag + r];
+      if (shift_row) shift_row[tid] = shift[r];
+    } else if (r < kept) {
       int k;
       RankRec rec;
       if (plan != nullptr) {                      // largest kept rank k with roff[k] <= r
@@ -336,7 +356,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
   }
   const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
                                  pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, nullptr, pp);
+                                 src_of_dst, ws, src_row, nullptr, pp, fp.mapped);
   if (nrows == 0) return;
   const int r0 = t * kTile;
 
@@ -385,8 +405,8 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
 }
 
 FusedPlanArgs fused_args(const CompactArgs& a) {
-  return FusedPlanArgs{a.keep, a.keep_len, a.unit_len, a.unit_first, a.page_size,
-                       a.unit_remap, a.n_ctx, a.n_pages, a.d_status};
+  return FusedPlanArgs{a.keep,      a.keep_len, a.unit_len, a.unit_first, a.page_size,
+                       a.unit_remap, a.n_ctx,   a.n_pages,  a.d_status,   a.use_mask};
 }
 
 template <int VPT, bool FUSED>
@@ -449,7 +469,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
   }
   const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
                                  pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, shift_row, pp);
+                                 src_of_dst, ws, src_row, shift_row, pp, fp.mapped);
   if (nrows == 0) return;
   const int r0 = t * kTile;
   constexpr double kTwoPi = 6.283185307179586476925286766559;
@@ -580,6 +600,86 @@ hipError_t launch_copy_rope(const CompactArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+constexpr int kUnitWaves = 4;      // one wave per unit in the mask kernels
+
+__device__ inline bool unit_in_pool(int n, int f, int n_slots) {
+  return n > 0 && f >= 0 && f <= n_slots - n;
+}
+
+__global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_count_kernel(
+    const uint8_t* __restrict__ mask_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, int n_slots, int n_units, int cap_dst,
+    uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
+  const int seg = blockIdx.y;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
+  if (u >= n_units) return;
+  const WsLayout L = ws_layout(n_units, cap_dst);
+  int32_t* cnt = reinterpret_cast<int32_t*>(ws + static_cast<size_t>(seg) * L.seg_bytes +
+                                            L.count_off);
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  const int n = len_g[ub + u], f = first_g[ub + u];
+  uint32_t c = 0;
+  if (unit_in_pool(n, f, n_slots)) {
+    const uint8_t* m = mask_g + static_cast<size_t>(seg) * n_slots;
+    for (int s = f + lane; s < f + n; s += 4 * kWave) {
+      uint8_t b[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = s + j * kWave < f + n ? m[s + j * kWave] : 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) c += b[j] != 0 ? 1u : 0u;
+    }
+    c = wave_sum_u32(c);
+  } else if (n > 0 && lane == 0) {
+    set_status(status, OMNITIDE_E_TAGS);          // a unit outside the pool keeps nothing
+  }
+  if (lane == 0) cnt[u] = static_cast<int32_t>(c);
+}
+
+__global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
+    const uint8_t* __restrict__ mask_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, int n_slots, int n_units, int cap_dst,
+    const int32_t* __restrict__ remap_g, const int32_t* __restrict__ n_ctx_g,
+    int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, uint8_t* __restrict__ ws) {
+  const int seg = blockIdx.y;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
+  if (u >= n_units) return;
+  if (n_ctx_g[seg] == 0) return;                  // capacity error: no history row is written
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  const int rk = remap_g[ub + u];
+  if (rk < 0) return;                             // nothing kept (count 0 also for bad units)
+  const int n = len_g[ub + u], f = first_g[ub + u];
+  const WsLayout L = ws_layout(n_units, cap_dst);
+  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+  const RankRec rec = reinterpret_cast<const RankRec*>(wseg + L.rank_off)[rk];
+  int32_t* shift = reinterpret_cast<int32_t*>(wseg + L.shift_off);
+  const size_t sb = static_cast<size_t>(seg) * n_slots;
+  const size_t db = static_cast<size_t>(seg) * cap_dst;
+  const uint8_t* m = mask_g + sb;
+  int carry = 0;                                  // kept slots of the unit before the chunk
+  for (int c = 0; c < n; c += kWave) {
+    const int s = f + c + lane;
+    const bool keep = s < f + n && m[s] != 0;
+    const uint64_t bal = __ballot(keep);
+    const int within = carry + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                   static_cast<uint32_t>(bal >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u)));
+    if (keep) {
+      const int r = rec.off + within;
+      const int delb = rec.del + (s - f) - within;   // deleted live slots before s
+      src_of_dst[db + r] = s;
+      uid_dst[db + r] = rk;
+      mod_dst[db + r] = mod_src[sb + s];
+      pos_dst[db + r] = pos_src[sb + s] - delb;
+      shift[r] = -delb;
+    }
+    carry += __popcll(bal);
+  }
+}
+
 }  // namespace
 
 size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
@@ -605,13 +705,33 @@ hipError_t launch_copies(const CompactArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
+  uint8_t* ws = static_cast<uint8_t*>(a.workspace);
+  if (a.use_mask) {
+    // Per-slot mask: kept counts per unit, the unit plan over them, then the row map.
+    const dim3 ugrid((a.n_units + kUnitWaves - 1) / kUnitWaves, a.n_seg);
+    hipLaunchKernelGGL(compact_mask_count_kernel, ugrid, dim3(kUnitWaves * kWave), 0, stream,
+                       a.keep_slot, a.unit_len, a.unit_first, a.n_slots_src, a.n_units,
+                       a.cap_dst, ws, a.d_status);
+    const uint8_t* no_keep = nullptr;             // counts come from the workspace
+    const int32_t* no_keep_len = nullptr;
+    hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream,
+                       no_keep, no_keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len,
+                       a.cap_dst, a.page_size, a.unit_remap, a.n_ctx, a.n_pages, ws,
+                       a.d_status);
+    hipLaunchKernelGGL(compact_mask_map_kernel, ugrid, dim3(kUnitWaves * kWave), 0, stream,
+                       a.keep_slot, a.unit_len, a.unit_first, a.modality_src, a.pos_src,
+                       a.n_slots_src, a.n_units, a.cap_dst, a.unit_remap, a.n_ctx,
+                       a.unit_id_dst, a.modality_dst, a.pos_dst, a.src_of_dst, ws);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_copies<false>(a, stream);
+  }
   // Up to 512 units every copy workgroup plans for itself (one kernel); beyond, a plan kernel
   // writes the rank table and tile hints to the workspace first.
   if (a.n_units <= kSmallUnits) return launch_copies<true>(a, stream);
   hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream, a.keep,
                      a.keep_len, a.unit_len, a.unit_first, a.n_units, a.chunk_len, a.cap_dst,
-                     a.page_size, a.unit_remap, a.n_ctx, a.n_pages,
-                     static_cast<uint8_t*>(a.workspace), a.d_status);
+                     a.page_size, a.unit_remap, a.n_ctx, a.n_pages, ws, a.d_status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_copies<false>(a, stream);

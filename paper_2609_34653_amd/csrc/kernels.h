@@ -28,6 +28,8 @@ struct CompactArgs {
   const int32_t* pos_src;
   const uint8_t* keep;
   const int32_t* keep_len = nullptr;   // kept leading tokens per unit; replaces keep when set
+  const uint8_t* keep_slot = nullptr;  // per-slot keep mask, used when use_mask (replaces keep
+  bool use_mask = false;               // and keep_len; may be null only without slots)
   const int32_t* unit_len;
   const int32_t* unit_first;
   int n_units;
@@ -62,14 +64,25 @@ struct SpanPlanArgs {
   const int32_t* unit_first;
   const int32_t* unit_last;
   const uint32_t* unit_flags;
+  const int32_t* unit_id;
   const uint8_t* modality;
   int n_seg, n_slots, n_units;
   int low, high, recent, sink_video, sink_audio, text_budget;
   int32_t* keep_len;
+  uint8_t* keep_slot;
   int32_t* kept_tokens;
+  void* workspace;
   int32_t* d_status;
 };
 
+// Span-plan workspace per segment: a per-slot code, then three per-unit arrays.
+__host__ __device__ inline size_t span_ws_info_bytes(int n_slots) {
+  return (static_cast<size_t>(n_slots) * 4 + 255) / 256 * 256;
+}
+__host__ __device__ inline size_t span_ws_seg_bytes(int n_slots, int n_units) {
+  return span_ws_info_bytes(n_slots) + (static_cast<size_t>(n_units) * 12 + 255) / 256 * 256;
+}
+size_t span_plan_workspace_bytes(int n_seg, int n_slots, int n_units);
 hipError_t launch_plan_spans(const SpanPlanArgs& a, hipStream_t stream);
 
 // Native layout: logical eviction in place, ordered-suffix packing, chunk placement.

@@ -91,7 +91,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
     uid = unit_id[tag0 + lane];
     mod = modality[tag0 + lane];
   }
-  const bool bad = lane < nrows && (uid < -1 || uid >= n_units || mod > 3);
+  const bool bad = lane < nrows && (uid < -1 || uid >= n_units || mod > 4);
   if (bad) {
     set_status(status, OMNITIDE_E_TAGS);
     uid = -1;

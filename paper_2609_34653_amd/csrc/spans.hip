@@ -1,32 +1,153 @@
-// OmniPick span plan, one workgroup per segment (one wave up to 512 units, 1024 threads beyond).
+// OmniPick span plan in three kernels.
 //
-// Each thread owns up to 8 consecutive units.  Every step of the plan is a scan over units in
-// id (temporal) order, so the sequential walks of the planner become thresholds on prefix sums:
-//   recent    newest live non-system units whose suffix total (own tokens included) is at most
-//             R: lengths are positive, so the suffix grows monotonically and "stop at the first
-//             misfit" is the set {u : suffix(u) <= R}
-//   sinks     older video / audio units keep min(len, sink_video / sink_audio) leading tokens
-//   text      older text unit u keeps clamp(text_budget - (older text tokens before u), 0, len)
-//   trimming  drop order = partially retained units by id, then complete non-system units by
-//             id.  The i-th candidate is dropped iff, before it, the plan still exceeds the low
-//             watermark and more than one unit is retained.  Both quantities only decrease along
-//             the order, so each candidate decides from its exclusive prefix (tokens and count
-//             of earlier candidates) alone.
+// 1. Census (one wave per unit).  The wave walks its unit's slots 256 at a time (4 per lane) and
+//    finds where each span starts: at the unit's first slot and wherever the tag changes.  A
+//    running maximum of the start slots (wave scan plus a carry across chunks) gives every
+//    token its place in its span.  Each slot gets a code in the workspace: marker tokens and
+//    the first sink_video / sink_audio tokens of each video / audio span are sinks (kept while
+//    the unit is retained at all), text tokens get their rank among the unit's text tokens,
+//    everything else is dropped from a partially kept unit.  Per unit: sinks, text tokens.
+// 2. Plan (one workgroup per segment: one wave up to 512 units, 1024 threads beyond).  Each
+//    thread owns up to 8 consecutive units.  Every step of the plan is a scan over units in id
+//    (temporal) order, so the sequential walks of the planner become thresholds on prefix sums:
+//      recent    newest live non-system units whose suffix total (own tokens included) is at
+//                most R: lengths are positive, so the suffix grows monotonically and "stop at
+//                the first misfit" is the set {u : suffix(u) <= R}
+//      older     unit u keeps its sinks plus clamp(text_budget - T_u, 0, text_u) of its text
+//                tokens, T_u = text tokens of older units before u
+//      trimming  drop order = partially retained units by id, then complete non-system units
+//                by id.  The i-th candidate is dropped iff, before it, the plan still exceeds
+//                the low watermark and more than one unit is retained.  Both quantities only
+//                decrease along the order, so each candidate decides from its exclusive prefix
+//                (tokens and count of earlier candidates) alone.
+// 3. Mark (one thread per slot): the slot stays if its unit is kept whole, or its unit is kept
+//    in part and the slot is a sink or one of the unit's first text_keep text tokens.
 #include "common.h"
 #include "kernels.h"
 
 namespace omnitide {
+
+size_t span_plan_workspace_bytes(int n_seg, int n_slots, int n_units) {
+  return span_ws_seg_bytes(n_slots, n_units) * static_cast<size_t>(n_seg);
+}
+
 namespace {
 
 constexpr int kMaxPer = 8;
+constexpr int kCensusWaves = 4;
+constexpr int32_t kInfoSink = -1;   // marker, or inside the sink prefix of its span
+constexpr int32_t kInfoDrop = -2;   // any other non-text token
+
+struct SpanWs {
+  int32_t* info;        // [n_slots] per-slot code: kInfoSink, kInfoDrop or text rank in unit
+  int32_t* sinks;       // [U] sink tokens of the unit (-1: bad tag or slots outside the pool)
+  int32_t* text;        // [U] text tokens of the unit
+  int32_t* text_keep;   // [U] text tokens an older unit keeps
+};
+
+__device__ inline SpanWs span_ws(uint8_t* ws, int seg, int n_slots, int n_units) {
+  uint8_t* b = ws + span_ws_seg_bytes(n_slots, n_units) * static_cast<size_t>(seg);
+  const size_t info_bytes = span_ws_info_bytes(n_slots);
+  const size_t ub = static_cast<size_t>(n_units) * 4;
+  return SpanWs{reinterpret_cast<int32_t*>(b), reinterpret_cast<int32_t*>(b + info_bytes),
+                reinterpret_cast<int32_t*>(b + info_bytes + ub),
+                reinterpret_cast<int32_t*>(b + info_bytes + 2 * ub)};
+}
+
+__global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
+    const uint8_t* __restrict__ mod_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, int n_slots, int n_units, int sink_video,
+    int sink_audio, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
+  const int seg = blockIdx.y;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int u = blockIdx.x * kCensusWaves + threadIdx.x / kWave;
+  if (u >= n_units) return;
+  const SpanWs W = span_ws(ws, seg, n_slots, n_units);
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  const int n = len_g[ub + u];
+  const int f = first_g[ub + u];
+  if (n <= 0 || f < 0 || f > n_slots - n) {     // no slots, or not inside the pool (the plan
+    if (lane == 0) {                            // reports the latter as a tag error)
+      W.sinks[u] = n <= 0 ? 0 : -1;
+      W.text[u] = 0;
+    }
+    return;
+  }
+  const uint8_t* mod = mod_g + static_cast<size_t>(seg) * n_slots;
+  int carry_tag = -1;      // tag of the slot before the chunk (-1 at the unit's start)
+  int carry_start = f;     // first slot of the span that slot belongs to
+  int carry_text = 0;      // the unit's text tokens before the chunk
+  int sinks = 0;
+  bool bad = false;
+  for (int c = 0; c < n; c += 4 * kWave) {
+    const int s0 = f + c + 4 * lane;
+    int m[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) m[j] = s0 + j < f + n ? mod[s0 + j] : -1;
+    int prev = __shfl_up(m[3], 1, kWave);
+    if (lane == 0) prev = carry_tag;
+    int st[4], tr[4];
+    int run = -1, nt = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int pm = j == 0 ? prev : m[j - 1];
+      if (m[j] >= 0 && m[j] != pm) run = s0 + j;   // a span starts here
+      st[j] = run;
+      tr[j] = nt;                                  // text tokens of this lane before slot j
+      nt += m[j] == OMNITIDE_MOD_TEXT ? 1 : 0;
+    }
+    int inc = run;                                 // running maximum of span starts
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int o = __shfl_up(inc, off, kWave);
+      if (lane >= off) inc = max(inc, o);
+    }
+    int exc = __shfl_up(inc, 1, kWave);
+    if (lane == 0) exc = -1;
+    const int start_before = max(exc, carry_start);
+    int text_tot;
+    const int text_before = carry_text + [&] {
+      const int incl = wave_inclusive_scan(nt);
+      text_tot = __shfl(incl, kWave - 1, kWave);
+      return incl - nt;
+    }();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int s = s0 + j;
+      if (m[j] < 0) continue;
+      const int place = s - max(start_before, st[j]) + 1;   // 1-based place in its span
+      int32_t code = kInfoDrop;
+      if (m[j] == OMNITIDE_MOD_TEXT) {
+        code = text_before + tr[j];
+      } else if (m[j] == OMNITIDE_MOD_MARK ||
+                 (m[j] == OMNITIDE_MOD_VIDEO && place <= sink_video) ||
+                 (m[j] == OMNITIDE_MOD_AUDIO && place <= sink_audio)) {
+        code = kInfoSink;
+        ++sinks;
+      }
+      bad |= m[j] > OMNITIDE_MOD_MARK;
+      W.info[static_cast<size_t>(s)] = code;
+    }
+    carry_tag = __shfl(m[3], kWave - 1, kWave);
+    carry_start = max(carry_start, __shfl(inc, kWave - 1, kWave));
+    carry_text += text_tot;
+  }
+  const uint32_t tot = wave_sum_u32(static_cast<uint32_t>(sinks));
+  const bool any_bad = __any(bad);
+  if (lane == 0) {
+    W.sinks[u] = any_bad ? -1 : static_cast<int32_t>(tot);
+    W.text[u] = carry_text;
+    if (any_bad) set_status(status, OMNITIDE_E_TAGS);
+  }
+}
 
 template <int T>
 __global__ __launch_bounds__(T) void plan_spans_kernel(
     const int32_t* __restrict__ len_g, const int32_t* __restrict__ first_g,
-    const int32_t* __restrict__ last_g, const uint32_t* __restrict__ flags_g,
-    const uint8_t* __restrict__ mod_g, int n_slots, int n_units, int low, int high, int recent,
-    int sink_video, int sink_audio, int text_budget, int32_t* __restrict__ keep_len_g,
-    int32_t* __restrict__ kept_g, int32_t* __restrict__ status) {
+    const int32_t* __restrict__ last_g, const uint32_t* __restrict__ flags_g, int n_slots,
+    int n_units, int low, int high, int recent, int text_budget,
+    int32_t* __restrict__ keep_len_g, int32_t* __restrict__ kept_g, uint8_t* __restrict__ ws,
+    int32_t* __restrict__ status) {
   __shared__ int32_t scr[T / kWave + 1];
   const int seg = blockIdx.x;
   const int tid = threadIdx.x;
@@ -34,9 +155,9 @@ __global__ __launch_bounds__(T) void plan_spans_kernel(
   const int per = (U + T - 1) / T;
   const int u0 = tid * per;
   const size_t base = static_cast<size_t>(seg) * U;
-  const size_t sbase = static_cast<size_t>(seg) * n_slots;
+  const SpanWs W = span_ws(ws, seg, n_slots, n_units);
 
-  int ln[kMaxPer], fs[kMaxPer], ls[kMaxPer];
+  int ln[kMaxPer], fs[kMaxPer], ls[kMaxPer], sk[kMaxPer], tx[kMaxPer];
   uint32_t fl[kMaxPer];
 #pragma unroll
   for (int i = 0; i < kMaxPer; ++i) {        // all loads first: one memory round trip
@@ -45,18 +166,17 @@ __global__ __launch_bounds__(T) void plan_spans_kernel(
     fs[i] = first_g[base + u];
     ls[i] = last_g[base + u];
     fl[i] = flags_g[base + u];
+    sk[i] = W.sinks[u];
+    tx[i] = W.text[u];
   }
   bool bad = false;
   int my_max_first = -1;
-  int md[kMaxPer];
 #pragma unroll
   for (int i = 0; i < kMaxPer; ++i) {
     if (!(i < per && u0 + i < U) || ln[i] <= 0) ln[i] = 0;
     const bool live = ln[i] > 0;
-    const bool in_range = live && fs[i] >= 0 && fs[i] < n_slots;
-    bad |= live && (!in_range || ls[i] - fs[i] + 1 != ln[i]);
-    md[i] = in_range ? mod_g[sbase + fs[i]] : 0;
-    bad |= live && md[i] > OMNITIDE_MOD_TEXT;
+    const bool in_range = live && fs[i] >= 0 && fs[i] <= n_slots - ln[i];
+    bad |= live && (!in_range || ls[i] - fs[i] + 1 != ln[i] || sk[i] < 0);
     if (live) my_max_first = max(my_max_first, fs[i]);
   }
   // live units must appear in unit order
@@ -117,29 +237,26 @@ __global__ __launch_bounds__(T) void plan_spans_kernel(
       rec[i] = suffix <= recent;
     }
   }
-  // older units: sink prefixes and the shared text budget (oldest first)
+  // older units: their sinks, and text tokens under the shared budget (oldest first)
   int my_text = 0;
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i)
-    my_text += (ln[i] > 0 && !sys[i] && !rec[i] && md[i] == OMNITIDE_MOD_TEXT) ? ln[i] : 0;
+  for (int i = 0; i < kMaxPer; ++i) my_text += (ln[i] > 0 && !sys[i] && !rec[i]) ? tx[i] : 0;
   int text_total;
   int text_before = block_exclusive_scan(my_text, scr, &text_total);
   int my_kept = 0, my_part = 0, my_part_n = 0, my_comp = 0, my_comp_n = 0, my_ret = 0;
 #pragma unroll
   for (int i = 0; i < kMaxPer; ++i) {
-    int k = 0;
+    int k = 0, tk = 0;
     if (ln[i] > 0) {
       if (sys[i] || rec[i]) {
         k = ln[i];
-      } else if (md[i] == OMNITIDE_MOD_VIDEO) {
-        k = min(ln[i], sink_video);
-      } else if (md[i] == OMNITIDE_MOD_AUDIO) {
-        k = min(ln[i], sink_audio);
-      } else if (md[i] == OMNITIDE_MOD_TEXT) {
-        k = min(ln[i], max(text_budget - text_before, 0));
-        text_before += ln[i];
+      } else {
+        tk = min(tx[i], max(text_budget - text_before, 0));
+        k = sk[i] + tk;
+        text_before += tx[i];
       }
     }
+    if (i < per && u0 + i < U) W.text_keep[u0 + i] = tk;
     kl[i] = k;
     my_kept += k;
     my_ret += k > 0 ? 1 : 0;
@@ -183,17 +300,55 @@ __global__ __launch_bounds__(T) void plan_spans_kernel(
 
 }  // namespace
 
+constexpr int kMarkThreads = 256;
+
+__global__ __launch_bounds__(kMarkThreads) void span_mark_kernel(
+    const int32_t* __restrict__ uid_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ keep_len_g, int n_slots, int n_units, uint8_t* __restrict__ ws,
+    uint8_t* __restrict__ keep_slot_g) {
+  const int seg = blockIdx.y;
+  const int s = blockIdx.x * kMarkThreads + threadIdx.x;
+  if (s >= n_slots) return;
+  const size_t sb = static_cast<size_t>(seg) * n_slots;
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  const int u = uid_g[sb + s];
+  uint8_t out = 0;
+  if (u >= 0 && u < n_units) {
+    const int kl = keep_len_g[ub + u];
+    if (kl > 0) {
+      if (kl >= len_g[ub + u]) {
+        out = 1;
+      } else {
+        const SpanWs W = span_ws(ws, seg, n_slots, n_units);
+        const int32_t code = W.info[s];
+        out = (code == kInfoSink || (code >= 0 && code < W.text_keep[u])) ? 1 : 0;
+      }
+    }
+  }
+  keep_slot_g[sb + s] = out;
+}
+
 hipError_t launch_plan_spans(const SpanPlanArgs& a, hipStream_t stream) {
+  uint8_t* ws = static_cast<uint8_t*>(a.workspace);
+  const dim3 cgrid((a.n_units + kCensusWaves - 1) / kCensusWaves, a.n_seg);
+  hipLaunchKernelGGL(span_census_kernel, cgrid, dim3(kCensusWaves * kWave), 0, stream,
+                     a.modality, a.unit_len, a.unit_first, a.n_slots, a.n_units, a.sink_video,
+                     a.sink_audio, ws, a.d_status);
   if (a.n_units <= 64 * kMaxPer)
     hipLaunchKernelGGL(plan_spans_kernel<64>, dim3(a.n_seg), dim3(64), 0, stream, a.unit_len,
-                       a.unit_first, a.unit_last, a.unit_flags, a.modality, a.n_slots,
-                       a.n_units, a.low, a.high, a.recent, a.sink_video, a.sink_audio,
-                       a.text_budget, a.keep_len, a.kept_tokens, a.d_status);
+                       a.unit_first, a.unit_last, a.unit_flags, a.n_slots, a.n_units, a.low,
+                       a.high, a.recent, a.text_budget, a.keep_len, a.kept_tokens, ws,
+                       a.d_status);
   else
     hipLaunchKernelGGL(plan_spans_kernel<1024>, dim3(a.n_seg), dim3(1024), 0, stream, a.unit_len,
-                       a.unit_first, a.unit_last, a.unit_flags, a.modality, a.n_slots,
-                       a.n_units, a.low, a.high, a.recent, a.sink_video, a.sink_audio,
-                       a.text_budget, a.keep_len, a.kept_tokens, a.d_status);
+                       a.unit_first, a.unit_last, a.unit_flags, a.n_slots, a.n_units, a.low,
+                       a.high, a.recent, a.text_budget, a.keep_len, a.kept_tokens, ws,
+                       a.d_status);
+  if (a.n_slots > 0) {
+    const dim3 mgrid((a.n_slots + kMarkThreads - 1) / kMarkThreads, a.n_seg);
+    hipLaunchKernelGGL(span_mark_kernel, mgrid, dim3(kMarkThreads), 0, stream, a.unit_id,
+                       a.unit_len, a.keep_len, a.n_slots, a.n_units, ws, a.keep_slot);
+  }
   return hipGetLastError();
 }
 

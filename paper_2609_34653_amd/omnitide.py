@@ -27,7 +27,8 @@ BF16, F32 = 0, 1
 ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 
 EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
-           "omnitide_compact_kv_rope", "omnitide_plan_spans", "omnitide_compact_kv_spans",
+           "omnitide_compact_kv_rope", "omnitide_plan_spans",
+           "omnitide_plan_spans_workspace_bytes", "omnitide_compact_kv_spans",
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
            "omnitide_attn_workspace_bytes", "omnitide_span_attn", "omnitide_evict_native",
            "omnitide_evict_native_workspace_bytes", "omnitide_pack_suffix",
@@ -68,8 +69,10 @@ def lib() -> ctypes.CDLL:
         L.omnitide_compact_kv_rope.argtypes = (L.omnitide_compact_kv.argtypes[:-2] +
                                                [ctypes.c_double, _I, _I, _P, _P])
         L.omnitide_compact_kv_spans.argtypes = L.omnitide_compact_kv_rope.argtypes
-        L.omnitide_plan_spans.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I,
-                                          _I, _P, _P, _P, _P]
+        L.omnitide_plan_spans.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I,
+                                          _I, _I, _P, _P, _P, _P, _SZ, _P, _P]
+        L.omnitide_plan_spans_workspace_bytes.argtypes = [_I, _I, _I]
+        L.omnitide_plan_spans_workspace_bytes.restype = _SZ
         L.omnitide_compact_workspace_bytes.argtypes = [_I, _I, _I]
         L.omnitide_compact_workspace_bytes.restype = _SZ
         L.omnitide_chunk_attn.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
@@ -203,24 +206,33 @@ def omnitide_select_units(unit_wsum, unit_len, unit_first_slot, unit_last_slot, 
            "omnitide_select_units")
 
 
-def omnitide_plan_spans(unit_len, unit_first_slot, unit_last_slot, unit_flags, modality, n_seg,
-                        n_slots, n_units, low_watermark, high_watermark, recent_tokens,
-                        sink_video, sink_audio, text_budget, keep_len, kept_tokens,
-                        d_status=None, stream=None):
+def omnitide_plan_spans_workspace_bytes(n_seg, n_slots, n_units) -> int:
+    return int(lib().omnitide_plan_spans_workspace_bytes(n_seg, n_slots, n_units))
+
+
+def omnitide_plan_spans(unit_len, unit_first_slot, unit_last_slot, unit_flags, unit_id, modality,
+                        n_seg, n_slots, n_units, low_watermark, high_watermark, recent_tokens,
+                        sink_video, sink_audio, text_budget, keep_len, keep_slot, kept_tokens,
+                        workspace, d_status=None, stream=None):
     nu = n_seg * n_units
     for t, nm in ((unit_len, "unit_len"), (unit_first_slot, "unit_first_slot"),
                   (unit_last_slot, "unit_last_slot"), (unit_flags, "unit_flags"),
                   (keep_len, "keep_len")):
         _need(t, nm, I32, nu)
+    _need(unit_id, "unit_id", I32, n_seg * n_slots)
     _need(modality, "modality", U8, n_seg * n_slots)
+    _need(keep_slot, "keep_slot", U8, n_seg * n_slots)
     _need(kept_tokens, "kept_tokens", I32, n_seg)
+    _need(workspace, "workspace", U8)
     if d_status is not None:
         _need(d_status, "d_status", I32, 1)
     _check(lib().omnitide_plan_spans(_ptr(unit_len), _ptr(unit_first_slot), _ptr(unit_last_slot),
-                                     _ptr(unit_flags), _ptr(modality), n_seg, n_slots, n_units,
-                                     low_watermark, high_watermark, recent_tokens, sink_video,
-                                     sink_audio, text_budget, _ptr(keep_len), _ptr(kept_tokens),
-                                     _ptr(d_status), _stream(stream)),
+                                     _ptr(unit_flags), _ptr(unit_id), _ptr(modality), n_seg,
+                                     n_slots, n_units, low_watermark, high_watermark,
+                                     recent_tokens, sink_video, sink_audio, text_budget,
+                                     _ptr(keep_len), _ptr(keep_slot), _ptr(kept_tokens),
+                                     _ptr(workspace), workspace.numel(), _ptr(d_status),
+                                     _stream(stream)),
            "omnitide_plan_spans")
 
 
@@ -231,10 +243,10 @@ def omnitide_compact_workspace_bytes(n_seg, n_units, cap_dst) -> int:
 def _compact_call_args(k_src, v_src, page_size, unit_id_src, modality_src, pos_src, keep,
                        unit_len, unit_first_slot, n_units, k_chunk, v_chunk, chunk_modality,
                        chunk_unit, k_dst, v_dst, unit_id_dst, modality_dst, pos_dst, src_of_dst,
-                       unit_remap, n_ctx, n_pages, workspace, d_status, keep_dtype=U8):
+                       unit_remap, n_ctx, n_pages, workspace, d_status, per_slot=False):
     """Checked C arguments shared by the compaction entry points (all but the rotary arguments
-    and the stream).  `keep` is the uint8 keep flags, or (keep_dtype int32) the kept-prefix
-    lengths of the span plan."""
+    and the stream).  `keep` is the uint8 keep flags per unit, or (per_slot) the span plan's
+    uint8 keep mask per slot."""
     n_seg, n_slots, H, d = _pool_dims(k_src, "k_src")
     dt = (k_src.dtype,)
     _need(k_src, "k_src", (torch.bfloat16, torch.float32))
@@ -244,7 +256,7 @@ def _compact_call_args(k_src, v_src, page_size, unit_id_src, modality_src, pos_s
     _need(modality_src, "modality_src", U8, ns)
     _need(pos_src, "pos_src", I32, ns)
     nu = n_seg * n_units
-    _need(keep, "keep", keep_dtype, nu)
+    _need(keep, "keep_slot" if per_slot else "keep", U8, ns if per_slot else nu)
     _need(unit_len, "unit_len", I32, nu)
     _need(unit_first_slot, "unit_first_slot", I32, nu)
     L = 0 if chunk_modality is None else chunk_modality.numel()
@@ -307,16 +319,16 @@ def omnitide_compact_kv_rope(k_src, v_src, page_size, unit_id_src, modality_src,
 
 
 def omnitide_compact_kv_spans(k_src, v_src, page_size, unit_id_src, modality_src, pos_src,
-                              keep_len, unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
+                              keep_slot, unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
                               chunk_modality, chunk_unit, k_dst, v_dst, unit_id_dst,
                               modality_dst, pos_dst, src_of_dst, unit_remap, n_ctx, n_pages,
                               workspace, rope_base=0.0, rope_dims=0, rope_style=ROPE_HALF,
                               d_status=None, stream=None):
     args = _compact_call_args(k_src, v_src, page_size, unit_id_src, modality_src, pos_src,
-                              keep_len, unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
+                              keep_slot, unit_len, unit_first_slot, n_units, k_chunk, v_chunk,
                               chunk_modality, chunk_unit, k_dst, v_dst, unit_id_dst,
                               modality_dst, pos_dst, src_of_dst, unit_remap, n_ctx, n_pages,
-                              workspace, d_status, keep_dtype=I32)
+                              workspace, d_status, per_slot=True)
     _check(lib().omnitide_compact_kv_spans(*args, float(rope_base), int(rope_dims),
                                            int(rope_style), _ptr(d_status), _stream(stream)),
            "omnitide_compact_kv_spans")

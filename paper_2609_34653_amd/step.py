@@ -42,6 +42,10 @@ class StreamStep:
         self.unit_score = torch.zeros(nu, dtype=torch.int64, device=dev)
         self.keep = torch.zeros(nu, dtype=torch.uint8, device=dev)
         self.keep_len = torch.zeros(nu, **i32)
+        self.keep_slot = torch.zeros(n_seg * n_slots, dtype=torch.uint8, device=dev)
+        self.span_ws = torch.zeros(max(1, ot.omnitide_plan_spans_workspace_bytes(n_seg, n_slots,
+                                                                                 n_units)),
+                                   dtype=torch.uint8, device=dev)
         self.kept_tokens = torch.zeros(n_seg, **i32)
         cap = self.cap_dst
         self.k_dst = torch.zeros(n_seg, cap, n_kv_heads, head_dim, dtype=kv_dtype, device=dev)
@@ -74,22 +78,24 @@ class StreamStep:
                                  self.recent, self.unit_score, self.keep, self.kept_tokens,
                                  self.d_status, stream)
 
-    def plan_spans(self, modality, low, high, recent, sink_video, sink_audio, text_budget,
-                   stream=None):
-        """Span plan (recent units whole, sink prefixes, text budget, trimming) into keep_len;
-        kept_tokens receives its total."""
+    def plan_spans(self, unit_id, modality, low, high, recent, sink_video, sink_audio,
+                   text_budget, stream=None):
+        """Span plan (recent units whole, boundary tokens and span sinks, text budget,
+        trimming) into keep_len (per unit) and keep_slot (per slot); kept_tokens receives its
+        total."""
         ot.omnitide_plan_spans(self.unit_len, self.unit_first, self.unit_last, self.unit_flags,
-                               modality, self.n_seg, self.n_slots, self.n_units, low, high,
-                               recent, sink_video, sink_audio, text_budget, self.keep_len,
-                               self.kept_tokens, self.d_status, stream)
+                               unit_id, modality, self.n_seg, self.n_slots, self.n_units, low,
+                               high, recent, sink_video, sink_audio, text_budget, self.keep_len,
+                               self.keep_slot, self.kept_tokens, self.span_ws, self.d_status,
+                               stream)
 
     def compact_spans(self, k_hist, v_hist, unit_id, modality, pos, k_chunk, v_chunk,
-                      chunk_modality, chunk_unit, stream=None, keep_len=None, rope=None):
-        """Compaction of the span plan's kept prefixes; rope as in ``compact``."""
+                      chunk_modality, chunk_unit, stream=None, keep_slot=None, rope=None):
+        """Compaction of the span plan's kept slots; rope as in ``compact``."""
         base, dims, style = rope if rope is not None else (0.0, 0, ot.ROPE_HALF)
         ot.omnitide_compact_kv_spans(
             k_hist, v_hist, self.page_size, unit_id, modality, pos,
-            self.keep_len if keep_len is None else keep_len, self.unit_len, self.unit_first,
+            self.keep_slot if keep_slot is None else keep_slot, self.unit_len, self.unit_first,
             self.n_units, k_chunk, v_chunk, chunk_modality, chunk_unit, self.k_dst, self.v_dst,
             self.unit_id_dst, self.modality_dst, self.pos_dst, self.src_of_dst,
             self.unit_remap, self.n_ctx, self.n_pages, self.compact_ws, base, dims, style,

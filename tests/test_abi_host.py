@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -149,17 +149,30 @@ def test_compact_rope_validation(L):
 
 
 def plan_spans(L, **kw):
-    a = dict(ln=fake(0), fs=fake(1), ls=fake(2), fl=fake(3), mod=fake(4), n_seg=1, n_slots=1000,
-             U=10, low=100, high=120, R=10, sv=4, sa=2, tb=16, kl=fake(5), kt=fake(6), st=fake(7))
+    a = dict(ln=fake(0), fs=fake(1), ls=fake(2), fl=fake(3), uid=fake(8), mod=fake(4), n_seg=1,
+             n_slots=1000, U=10, low=100, high=120, R=10, sv=4, sa=2, tb=16, kl=fake(5),
+             ks=fake(9), kt=fake(6), ws=fake(10),
+             wsb=ot.omnitide_plan_spans_workspace_bytes(1, 1000, 10), st=fake(7))
     a.update(kw)
-    return L.omnitide_plan_spans(a["ln"], a["fs"], a["ls"], a["fl"], a["mod"], a["n_seg"],
-                                 a["n_slots"], a["U"], a["low"], a["high"], a["R"], a["sv"],
-                                 a["sa"], a["tb"], a["kl"], a["kt"], a["st"], None)
+    return L.omnitide_plan_spans(a["ln"], a["fs"], a["ls"], a["fl"], a["uid"], a["mod"],
+                                 a["n_seg"], a["n_slots"], a["U"], a["low"], a["high"], a["R"],
+                                 a["sv"], a["sa"], a["tb"], a["kl"], a["ks"], a["kt"], a["ws"],
+                                 a["wsb"], a["st"], None)
 
 
 def test_plan_spans_validation(L):
     assert plan_spans(L, kl=None) == ot.E_NULL
     assert plan_spans(L, mod=None) == ot.E_NULL
+    assert plan_spans(L, uid=None) == ot.E_NULL
+    assert plan_spans(L, ks=None) == ot.E_NULL
+    assert plan_spans(L, ws=None) == ot.E_WORKSPACE
+    assert plan_spans(L, wsb=ot.omnitide_plan_spans_workspace_bytes(1, 1000, 10) - 1) == \
+        ot.E_WORKSPACE
+    assert ot.omnitide_plan_spans_workspace_bytes(1, 1000, 10) >= 1000 * 4 + 10 * 12
+    assert ot.omnitide_plan_spans_workspace_bytes(3, 1000, 10) == \
+        3 * ot.omnitide_plan_spans_workspace_bytes(1, 1000, 10)
+    assert plan_spans(L, ks=P(fake(8).value + 100)) == ot.E_ALIAS   # mask over the unit ids
+    assert plan_spans(L, ws=P(fake(6).value)) == ot.E_ALIAS         # workspace over an output
     assert plan_spans(L, high=99) == ot.E_SHAPE          # high watermark below the low one
     assert plan_spans(L, low=-1) == ot.E_SHAPE
     for k in ("R", "sv", "sa", "tb"):
@@ -173,13 +186,13 @@ def test_plan_spans_validation(L):
 
 def compact_spans(L, base=0.0, rdims=0, style=0, **kw):
     a = dict(ks=fake(0), vs=fake(1), dtype=0, n_seg=1, n=1000, H=8, d=128, P=64, uid=fake(2),
-             mod=fake(3), pos=fake(4), kl=fake(5), ln=fake(6), fs=fake(7), U=10, kc=fake(8),
+             mod=fake(3), pos=fake(4), ks_=fake(5), ln=fake(6), fs=fake(7), U=10, kc=fake(8),
              vc=fake(9), cm=fake(10), cu=fake(11), Lc=16, kd=fake(12), vd=fake(13), cap=600,
              uidd=fake(14), modd=fake(15), posd=fake(16), src=fake(17), rm=fake(18), nctx=fake(19),
              npg=fake(20), ws=None, wsb=1 << 20, st=fake(22))
     a.update(kw)
     return L.omnitide_compact_kv_spans(a["ks"], a["vs"], a["dtype"], a["n_seg"], a["n"], a["H"],
-                                       a["d"], a["P"], a["uid"], a["mod"], a["pos"], a["kl"],
+                                       a["d"], a["P"], a["uid"], a["mod"], a["pos"], a["ks_"],
                                        a["ln"], a["fs"], a["U"], a["kc"], a["vc"], a["cm"],
                                        a["cu"], a["Lc"], a["kd"], a["vd"], a["cap"], a["uidd"],
                                        a["modd"], a["posd"], a["src"], a["rm"], a["nctx"],
@@ -190,11 +203,12 @@ def compact_spans(L, base=0.0, rdims=0, style=0, **kw):
 def test_compact_spans_validation(L):
     assert compact_spans(L) == ot.E_WORKSPACE           # valid: only the workspace is missing
     assert compact_spans(L, base=1e6, rdims=128) == ot.E_WORKSPACE
-    assert compact_spans(L, kl=None) == ot.E_NULL
+    assert compact_spans(L, ks_=None) == ot.E_NULL
+    assert compact_spans(L, ks_=None, n=0) == ot.E_WORKSPACE  # no slots: the mask may be NULL
     assert compact_spans(L, rdims=-2) == ot.E_SHAPE
     assert compact_spans(L, base=1.0, rdims=64) == ot.E_SHAPE
     assert compact_spans(L, cap=15) == ot.E_CAPACITY
-    assert compact_spans(L, ws=fake(21), kd=P(fake(5).value + 16)) == ot.E_ALIAS   # over keep_len
+    assert compact_spans(L, ws=fake(21), kd=P(fake(5).value + 999)) == ot.E_ALIAS  # over the mask
 
 
 def test_compact_validation(L):
