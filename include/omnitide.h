@@ -58,6 +58,8 @@ enum {
   OMNITIDE_E_WORKSPACE = -6,  /* workspace pointer NULL or smaller than required */
   OMNITIDE_E_ALIAS = -7,      /* an output overlaps an input it must not overlap */
   OMNITIDE_E_HIP = -8,        /* a HIP launch failed */
+  OMNITIDE_E_SCRATCH = -9,    /* the call needs more scratch than the fixed array holds
+                                 (omnitide_chunk_attn_noalloc) */
   OMNITIDE_E_BUDGET = -16,    /* device: protected (system) tokens exceed the budget */
   OMNITIDE_E_TAGS = -17       /* device: malformed tags (id or modality out of range, a unit
                                  not one contiguous run, runs out of unit order) */
@@ -312,6 +314,28 @@ int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32
 
 size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                      int n_kv_heads, int head_dim);
+
+/*
+ * omnitide_chunk_attn_noalloc -- omnitide_chunk_attn for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels, with the split-KV partials in a fixed array inside the library instead of
+ * a caller workspace.  Same arguments, results and errors as omnitide_chunk_attn without
+ * workspace / workspace_bytes; the output is bitwise equal to omnitide_chunk_attn's.
+ *   - The array holds OMNITIDE_NOALLOC_SCRATCH_BYTES bytes per device (allocated when the
+ *     library's code is loaded on a device, kept until the process ends).  A shape whose
+ *     omnitide_attn_workspace_bytes() exceeds it returns OMNITIDE_E_SCRATCH (host check,
+ *     nothing enqueued); the 80K-history call (665 queries, 32/8 heads, d 128) needs ~33 MB.
+ *   - No allocation or free of any kind.  The array's device address is looked up once per
+ *     device (hipGetSymbolAddress, on the first call that runs on that device) and cached.
+ *   - Every call on one device shares that device's array: calls that overlap in time on one
+ *     device (different streams without ordering between them) race on it and give undefined
+ *     results.  Calls ordered on one stream are safe; no call expects the array zeroed.
+ */
+#define OMNITIDE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int omnitide_chunk_attn_noalloc(const void* q, const void* k, const void* v,
+                                const int32_t* n_ctx, int n_seg, int cap, int chunk_len,
+                                int n_q_heads, int n_kv_heads, int head_dim, float scale,
+                                float* out, int32_t* d_status, void* stream);
 
 /*
  * Native (logical-only) layout: the retained entries stay in their slots after eviction, the

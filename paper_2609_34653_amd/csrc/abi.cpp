@@ -359,7 +359,7 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
               const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int chunk_len,
               int n_q_heads, int n_kv_heads, int head_dim, float scale, float* out,
               void* workspace, size_t workspace_bytes, int32_t* d_status, void* stream,
-              bool skip_empty = true) {
+              bool skip_empty = true, bool noalloc = false) {
   const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
   if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
@@ -375,10 +375,15 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
                                                  head_dim)
            : omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
                                             head_dim);
-  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return OMNITIDE_E_WORKSPACE;
+  if (noalloc) {
+    if (need > OMNITIDE_NOALLOC_SCRATCH_BYTES) return OMNITIDE_E_SCRATCH;
+  } else if (need > 0 && (workspace == nullptr || workspace_bytes < need)) {
+    return OMNITIDE_E_WORKSPACE;
+  }
   const size_t qrows = static_cast<size_t>(n_seg) * chunk_len * n_q_heads;
   const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * 2;
-  if (any_alias({{out, qrows * head_dim * 4}, {workspace, need}, {d_status, 4}},
+  if (any_alias({{out, qrows * head_dim * 4}, {noalloc ? nullptr : workspace, need},
+                 {d_status, 4}},
                 {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull},
                  {key_pos, static_cast<size_t>(n_seg) * cap * 4}, {q_pos0, n_seg * 4ull}}))
     return OMNITIDE_E_ALIAS;
@@ -400,6 +405,7 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
   a.key_pos = key_pos;
   a.q_pos0 = q_pos0;
   a.skip_empty = skip_empty;
+  if (noalloc) return hip_status(omnitide::launch_attn_noalloc(a, static_cast<hipStream_t>(stream)));
   return hip_status(omnitide::launch_attn(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -411,6 +417,14 @@ int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32
                         size_t workspace_bytes, int32_t* d_status, void* stream) {
   return attn_impl(q, k, v, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len, n_q_heads,
                    n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream);
+}
+
+int omnitide_chunk_attn_noalloc(const void* q, const void* k, const void* v,
+                                const int32_t* n_ctx, int n_seg, int cap, int chunk_len,
+                                int n_q_heads, int n_kv_heads, int head_dim, float scale,
+                                float* out, int32_t* d_status, void* stream) {
+  return attn_impl(q, k, v, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len, n_q_heads,
+                   n_kv_heads, head_dim, scale, out, nullptr, 0, d_status, stream, true, true);
 }
 
 size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
@@ -635,6 +649,7 @@ const char* omnitide_status_string(int code) {
     case OMNITIDE_E_WORKSPACE: return "workspace missing or too small";
     case OMNITIDE_E_ALIAS: return "an output overlaps an input or another output";
     case OMNITIDE_E_HIP: return "HIP kernel launch failed";
+    case OMNITIDE_E_SCRATCH: return "the call needs more scratch than the library's fixed array";
     case OMNITIDE_E_BUDGET: return "protected tokens exceed the retention budget";
     case OMNITIDE_E_TAGS: return "malformed unit/modality tags";
     default: return "unknown status";

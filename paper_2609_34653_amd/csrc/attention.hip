@@ -25,6 +25,8 @@
 //            dealt round-robin over 8 XCDs), so their K/V re-reads hit that XCD's L2.
 #include <algorithm>
 
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 #include "combine.h"
@@ -676,6 +678,59 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
   if (a.head_dim == 128) return launch_attn_t<128>(a, s, stream);
   if (a.head_dim == 64) return launch_attn_t<64>(a, s, stream);
   return hipErrorInvalidValue;
+}
+
+// Fixed scratch of omnitide_chunk_attn_noalloc: the split-KV partials live in this array, one
+// copy per device, held until the process ends.  Host code never passes the array's name to a
+// kernel (on the host it is only a stand-in for the symbol): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and is cached here.
+static __device__ __align__(256) uint8_t scratch[OMNITIDE_NOALLOC_SCRATCH_BYTES];
+// Splits times row-tile workgroups never exceed kTargetWGs and a row tile holds kRowsWG rows, so
+// the partials need at most kTargetWGs * kRowsWG * (128 + 2) floats: every valid shape fits.
+static_assert(static_cast<size_t>(kTargetWGs) * kRowsWG * (128 + 2) * sizeof(float) <=
+                  OMNITIDE_NOALLOC_SCRATCH_BYTES,
+              "the split heuristic can exceed the fixed scratch");
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(hipStream_t stream, void** ptr) {
+  int dev = -1;
+  hipError_t e = stream != nullptr ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t r = hipSetDevice(cur);
+      if (e == hipSuccess) e = r;
+    }
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_attn_noalloc(const AttnArgs& a, hipStream_t stream) {
+  AttnArgs b = a;
+  b.workspace = nullptr;
+  if (attn_workspace_bytes(a.n_seg, a.cap, a.chunk_len, a.n_q_heads, a.n_kv_heads,
+                           a.head_dim) > 0) {
+    const hipError_t e = noalloc_scratch(stream, &b.workspace);
+    if (e != hipSuccess) return e;
+  }
+  return launch_attn(b, stream);
 }
 
 }  // namespace omnitide

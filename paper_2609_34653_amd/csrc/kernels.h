@@ -160,6 +160,9 @@ int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_h
 size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
                             int head_dim);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
+// launch_attn with the split-KV partials in the library's fixed per-device scratch array (no
+// allocation; the caller has checked attn_workspace_bytes <= OMNITIDE_NOALLOC_SCRATCH_BYTES).
+hipError_t launch_attn_noalloc(const AttnArgs& a, hipStream_t stream);
 size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                  int n_kv_heads, int head_dim);
 int span_attn_max_cap();

@@ -20,8 +20,9 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libomnitide.so")
 
-OK, E_NULL, E_SHAPE, E_DTYPE, E_WEIGHT, E_CAPACITY, E_WORKSPACE, E_ALIAS, E_HIP = \
-    0, -1, -2, -3, -4, -5, -6, -7, -8
+OK, E_NULL, E_SHAPE, E_DTYPE, E_WEIGHT, E_CAPACITY, E_WORKSPACE, E_ALIAS, E_HIP, E_SCRATCH = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8, -9
+NOALLOC_SCRATCH_BYTES = 64 << 20
 E_BUDGET, E_TAGS = -16, -17
 BF16, F32 = 0, 1
 ROPE_HALF, ROPE_INTERLEAVED = 0, 1
@@ -30,6 +31,7 @@ EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv
            "omnitide_compact_kv_rope", "omnitide_plan_spans",
            "omnitide_plan_spans_workspace_bytes", "omnitide_compact_kv_spans",
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
+           "omnitide_chunk_attn_noalloc",
            "omnitide_attn_workspace_bytes", "omnitide_span_attn", "omnitide_evict_native",
            "omnitide_evict_native_workspace_bytes", "omnitide_pack_suffix",
            "omnitide_pack_suffix_workspace_bytes", "omnitide_place_chunk",
@@ -77,6 +79,8 @@ def lib() -> ctypes.CDLL:
         L.omnitide_compact_workspace_bytes.restype = _SZ
         L.omnitide_chunk_attn.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                           ctypes.c_float, _P, _P, _SZ, _P, _P]
+        L.omnitide_chunk_attn_noalloc.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
+                                                  ctypes.c_float, _P, _P, _P]
         L.omnitide_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_attn_workspace_bytes.restype = _SZ
         L.omnitide_span_attn.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
@@ -103,7 +107,8 @@ def lib() -> ctypes.CDLL:
         L.omnitide_version.restype = ctypes.c_char_p
         for name in ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv",
                      "omnitide_compact_kv_rope", "omnitide_compact_kv_spans",
-                     "omnitide_plan_spans", "omnitide_chunk_attn", "omnitide_span_attn",
+                     "omnitide_plan_spans", "omnitide_chunk_attn",
+                     "omnitide_chunk_attn_noalloc", "omnitide_span_attn",
                      "omnitide_evict_native", "omnitide_pack_suffix", "omnitide_place_chunk",
                      "omnitide_decode_attn"):
             getattr(L, name).restype = _I
@@ -361,6 +366,27 @@ def omnitide_chunk_attn(q, k, v, n_ctx, scale, out, workspace=None, d_status=Non
                                      0 if workspace is None else workspace.numel(),
                                      _ptr(d_status), _stream(stream)), "omnitide_chunk_attn")
 
+
+def omnitide_chunk_attn_noalloc(q, k, v, n_ctx, scale, out, d_status=None, stream=None):
+    """omnitide_chunk_attn with the library's fixed scratch (allocates nothing)."""
+    if q.dim() == 3:
+        n_seg, (L, Hq, d) = 1, q.shape
+    else:
+        n_seg, L, Hq, d = q.shape
+    ds, cap, Hkv, dd = _pool_dims(k, "k")
+    if ds != n_seg or dd != d:
+        raise ValueError("k shape does not match q")
+    _need(q, "q", (torch.bfloat16,))
+    _need(k, "k", (torch.bfloat16,))
+    _need(v, "v", (torch.bfloat16,), k.numel())
+    _need(n_ctx, "n_ctx", I32, n_seg)
+    _need(out, "out", (torch.float32,), q.numel())
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_chunk_attn_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(n_ctx), n_seg, cap,
+                                             L, Hq, Hkv, d, float(scale), _ptr(out),
+                                             _ptr(d_status), _stream(stream)),
+           "omnitide_chunk_attn_noalloc")
 
 def omnitide_span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
                                        head_dim) -> int:

@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 22
+    assert len(names) == 23
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -245,6 +245,44 @@ def test_attention_validation(L):
     assert need > 0 and attn(L, wsb=need - 1) == ot.E_WORKSPACE
     # split count: 21 row tiles x 8 KV heads -> 3 splits on the 80K-history shape
     assert need == 3 * 665 * 32 * 130 * 4
+
+
+def attn_noalloc(L, **kw):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), nctx=fake(3), n_seg=1, cap=17049, Lc=665, Hq=32,
+             Hkv=8, d=128, scale=0.0884, out=fake(4), st=fake(6))
+    a.update(kw)
+    return L.omnitide_chunk_attn_noalloc(a["q"], a["k"], a["v"], a["nctx"], a["n_seg"], a["cap"],
+                                         a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"],
+                                         a["out"], a["st"], None)
+
+
+def test_attention_noalloc_validation(L):
+    """The same host checks as the workspace entry point (nothing launched here)."""
+    assert attn_noalloc(L, q=None) == ot.E_NULL
+    assert attn_noalloc(L, out=None) == ot.E_NULL
+    assert attn_noalloc(L, Hq=30) == ot.E_SHAPE
+    assert attn_noalloc(L, d=80) == ot.E_SHAPE
+    assert attn_noalloc(L, scale=float("nan")) == ot.E_SHAPE
+    assert attn_noalloc(L, cap=100) == ot.E_CAPACITY
+    assert attn_noalloc(L, out=fake(1)) == ot.E_ALIAS
+    assert attn_noalloc(L, st=P(fake(4).value + 8)) == ot.E_ALIAS
+    assert "scratch" in ot.status_string(ot.E_SCRATCH)
+
+
+def test_noalloc_scratch_covers_every_shape():
+    """Splits times row-tile workgroups stay within 512, so the partials of any shape fit the
+    fixed 64 MiB array (the E_SCRATCH check is a guard, not a reachable limit today)."""
+    worst = 0
+    for n_seg in (1, 2, 3, 8, 36):
+        for Lc in (1, 32, 89, 128, 665, 1000, 2329, 8192):
+            for Hq, Hkv in ((4, 1), (8, 8), (32, 8), (64, 4), (128, 1)):
+                for d in (64, 128):
+                    for cap in (Lc, 4096, 17049, 131072):
+                        if cap < Lc:
+                            continue
+                        worst = max(worst, ot.omnitide_attn_workspace_bytes(n_seg, cap, Lc, Hq,
+                                                                            Hkv, d))
+    assert 0 < worst <= 512 * 128 * 130 * 4 <= ot.NOALLOC_SCRATCH_BYTES
 
 
 def span_attn(L, **kw):
