@@ -669,9 +669,11 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     eager path's score + select decide each step's plan; the native pools apply the same keep
     flags (their unit ids and positions coincide with the eager pool's).  Attention over a
     native pool runs twice per step: skipping empty 64-slot tiles, and traversing the whole
-    span (as kernels without tile skipping do).  Attention and maintenance are timed with events
-    around their launches (the per-step latency percentiles come from the same events); spans
-    and active pages are recorded per step."""
+    span (as kernels without tile skipping do).  Each step then decodes the chunk's last token
+    over each layout (the eager pool's rows [0, n_ctx); a native pool's span, with and without
+    tile skipping), as the decode half of the paper's layout ablation.  Attention, decode and
+    maintenance are timed with events around their launches (the per-step latency percentiles
+    come from the same events); spans and active pages are recorded per step."""
     from paper_2609_34653_amd.step import StreamStep
     cfg = sg.CONFIG_BY_NAME["stream_loop_64x665"]
     stream = sg.make_stream(cfg)
@@ -722,12 +724,21 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
                        device=dev)
     ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap_n, L, Hq, H, d),
                        dtype=torch.uint8, device=dev)
+    ws_d = torch.zeros(max(1, ot.omnitide_decode_workspace_bytes(1, cap_e, 1, Hq, H, d)),
+                       dtype=torch.uint8, device=dev)
+    ws_ds = torch.zeros(ot.omnitide_decode_span_workspace_bytes(1, cap_n, 1, Hq, H, d),
+                        dtype=torch.uint8, device=dev)
+    dec_e = torch.zeros(1, 1, Hq, d, device=dev)
+    for pl in pools.values():
+        pl["dec"] = torch.zeros(1, 1, Hq, d, device=dev)
+        pl["qpos"] = torch.zeros(1, **i32)
     names = ["eager"] + list(pools)
-    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(steps)]
           for n in names}
     spans = {n: torch.zeros(steps, **i32) for n in names}
     active = {n: torch.zeros(steps, **i32) for n in names}
     diff = torch.zeros(len(pools), device=dev)
+    diff_dec = torch.zeros(len(pools), device=dev)
     s = torch.cuda.current_stream()
     d_status = st_first.d_status
     for i in range(steps):
@@ -744,6 +755,10 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         e[1].record(s)
         st.attend(c["q"], cfg.scale)
         e[2].record(s)
+        qd = c["q"][:, L - 1:L]                      # the chunk's last token decodes
+        ot.omnitide_decode_attn(qd, st.k_dst, st.v_dst, st.n_ctx, cfg.scale, dec_e, ws_d,
+                                d_status)
+        e[5].record(s)
         spans["eager"][i:i + 1].copy_(st.n_ctx)
         active["eager"][i:i + 1].copy_((st.n_ctx + page - 1) // page)
         for j, (n, pl) in enumerate(pools.items()):
@@ -768,6 +783,17 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
             ot.omnitide_span_attn(c["q"], pl["k"], pl["v"], pl["pos"], pl["span"], pl["kept"],
                                   cfg.scale, pl["out"], ws_a, d_status, skip_empty_tiles=False)
             e[3].record(s)
+            torch.add(pl["kept"], L - 1, out=pl["qpos"])   # position of the decoding token
+            e[5].record(s)
+            ot.omnitide_decode_span_attn(qd, pl["k"], pl["v"], pl["pos"], pl["span"],
+                                         pl["qpos"], cfg.scale, pl["dec"], ws_ds, d_status,
+                                         skip_empty_tiles=True)
+            e[6].record(s)
+            ot.omnitide_decode_span_attn(qd, pl["k"], pl["v"], pl["pos"], pl["span"],
+                                         pl["qpos"], cfg.scale, pl["dec"], ws_ds, d_status,
+                                         skip_empty_tiles=False)
+            e[7].record(s)
+            diff_dec[j] = torch.maximum(diff_dec[j], (pl["dec"] - dec_e).abs().max())
             spans[n][i:i + 1].copy_(pl["span"])
             occ = (pl["uid"] >= 0).view(-1, page).any(dim=1)
             active[n][i:i + 1].copy_(occ.sum().view(1).to(torch.int32))
@@ -779,7 +805,8 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     if status != 0:
         raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
     res = {"steps": steps, "page_size": page,
-           "max_abs_diff_vs_eager": round(float(diff.max().item()), 6)}
+           "max_abs_diff_vs_eager": round(float(diff.max().item()), 6),
+           "decode_max_abs_diff_vs_eager": round(float(diff_dec.max().item()), 8)}
     for n in names:
         ms = lambda a, b: sum(ev[n][i][a].elapsed_time(ev[n][i][b]) for i in range(steps))  # noqa
         sp = spans[n].cpu().numpy()
@@ -802,16 +829,22 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         # (eviction, packing, placement), attention with and without tile skipping
         if n == "eager":
             r["per_call_ms"] = {"score_select": pct(per_step(4, 0)),
-                                "compact": pct(per_step(0, 1)), "attend": pct(per_step(1, 2))}
+                                "compact": pct(per_step(0, 1)), "attend": pct(per_step(1, 2)),
+                                "decode": pct(per_step(2, 5))}
         else:
             r["per_call_ms"] = {"maintenance": pct(per_step(0, 1)),
                                 "attend_skip": pct(per_step(1, 2)),
-                                "attend_full_span": pct(per_step(2, 3))}
+                                "attend_full_span": pct(per_step(2, 3)),
+                                "decode_skip": pct(per_step(5, 6)),
+                                "decode_full_span": pct(per_step(6, 7))}
         if n == "eager":
             r["attend_ms_total"] = round(ms(1, 2), 3)
+            r["decode_ms_total"] = round(ms(2, 5), 3)
         else:
             r["attend_skip_ms_total"] = round(ms(1, 2), 3)
             r["attend_full_span_ms_total"] = round(ms(2, 3), 3)
+            r["decode_skip_ms_total"] = round(ms(5, 6), 3)
+            r["decode_full_span_ms_total"] = round(ms(6, 7), 3)
             if pools[n]["min_pages"] > 0:
                 r["min_pages"] = pools[n]["min_pages"]
                 r["moved_rows_total"] = int(pools[n]["moved_sum"].item())
@@ -822,9 +855,13 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         for mode in ("skip", "full_span"):
             res[n][f"attend_{mode}_reduction_vs_native"] = round(
                 1 - res[n][f"attend_{mode}_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
+            res[n][f"decode_{mode}_reduction_vs_native"] = round(
+                1 - res[n][f"decode_{mode}_ms_total"] / nat[f"decode_{mode}_ms_total"], 4)
     for mode in ("skip", "full_span"):
         res["eager"][f"attend_reduction_vs_native_{mode}"] = round(
             1 - res["eager"]["attend_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
+        res["eager"][f"decode_reduction_vs_native_{mode}"] = round(
+            1 - res["eager"]["decode_ms_total"] / nat[f"decode_{mode}_ms_total"], 4)
     return res
 
 

@@ -61,8 +61,9 @@ enum {
   OMNITIDE_E_SCRATCH = -9,    /* the call needs more scratch than the fixed array holds
                                  (omnitide_chunk_attn_noalloc) */
   OMNITIDE_E_BUDGET = -16,    /* device: protected (system) tokens exceed the budget */
-  OMNITIDE_E_TAGS = -17       /* device: malformed tags (id or modality out of range, a unit
+  OMNITIDE_E_TAGS = -17,      /* device: malformed tags (id or modality out of range, a unit
                                  not one contiguous run, runs out of unit order) */
+  OMNITIDE_E_RANGE = -18      /* device: a unit score of 2^51 or more (select's ranking key) */
 };
 
 enum { OMNITIDE_BF16 = 0, OMNITIDE_F32 = 1 };
@@ -124,10 +125,11 @@ int omnitide_score_units(const void* k, int dtype, int n_seg, int n_slots, int n
  *   unit_score   uint64 [n_seg][n_units]   floor(W_u / len_u), 0 for units without slots
  *   keep         uint8  [n_seg][n_units]   1 = unit retained whole
  *   kept_tokens  int32  [n_seg]            retained history tokens (<= budget)
- *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run, runs are out
- *                of unit order, or a score reaches 2^51 (omnitide_score_units' outputs stay
- *                below 2^43); OMNITIDE_E_BUDGET as above.  On either error the segment's keep
- *                is all 0 and kept_tokens 0.
+ *   d_status     OMNITIDE_E_TAGS if a live unit is not one contiguous slot run or runs are
+ *                out of unit order; OMNITIDE_E_RANGE if a score reaches 2^51 (the ranking key
+ *                holds 51 bits of score; omnitide_score_units' outputs stay below 2^43);
+ *                OMNITIDE_E_BUDGET as above (first match in this order).  On any error the
+ *                segment's keep is all 0 and kept_tokens 0.
  * Limits: 1 <= n_units <= 8192, budget_tokens >= 0, recent_tokens >= 0.  One workgroup per
  * segment; latency-bound.
  */
@@ -458,6 +460,34 @@ int omnitide_decode_attn(const void* q, const void* k, const void* v, const int3
 
 size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,
                                        int n_kv_heads, int head_dim);
+
+/*
+ * omnitide_decode_span_attn -- decode attention over a pool with holes (paper: OmniPage
+ * ablation, decode attention time over the native and OmniPage layouts; Fragmentation after
+ * logical eviction: attention is presented the physical span).  For query token i in [0, n_q)
+ * and query head h:
+ *   out[i][h] = sum_j softmax_j(scale * <q[i][h], k[j][g]>) v[j][g],  g = h / (n_q_heads/n_kv_heads)
+ *   over slots j < span[seg] with 0 <= key_pos[j] <= q_pos0[seg] + i.
+ *   key_pos, span, q_pos0: as omnitide_span_attn (the query tokens' own keys are in the pool at
+ *            positions q_pos0 + i); n_q <= span <= cap, else OMNITIDE_E_CAPACITY on the device
+ *            and that segment's output is not written.  The K/V bytes of empty slots are never
+ *            used (they may hold anything, NaN included).
+ *   skip_empty_tiles != 0: 64-slot tiles without an entry are not read; 0: every tile of the
+ *            span is read and masked (a kernel presented the physical span).
+ *   q, k, v, out, scale, arithmetic and limits: as omnitide_decode_attn; cap <= 2,097,152.
+ *   workspace  device scratch of omnitide_decode_span_workspace_bytes() bytes (always > 0).
+ * With key_pos[j] = j for j < span and q_pos0 = span - n_q this computes omnitide_decode_attn
+ * with n_ctx = span (up to summation order).
+ */
+int omnitide_decode_span_attn(const void* q, const void* k, const void* v,
+                              const int32_t* key_pos, const int32_t* span,
+                              const int32_t* q_pos0, int n_seg, int cap, int n_q,
+                              int n_q_heads, int n_kv_heads, int head_dim, float scale,
+                              int skip_empty_tiles, float* out, void* workspace,
+                              size_t workspace_bytes, int32_t* d_status, void* stream);
+
+size_t omnitide_decode_span_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,
+                                            int n_kv_heads, int head_dim);
 
 /* Static description of a status code. */
 const char* omnitide_status_string(int code);

@@ -601,24 +601,33 @@ size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_head
   return omnitide::decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim);
 }
 
-int omnitide_decode_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
-                         int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
-                         int head_dim, float scale, float* out, void* workspace,
-                         size_t workspace_bytes, int32_t* d_status, void* stream) {
+namespace {
+
+// Decode attention over contiguous rows (key_pos == nullptr) or over a span with holes.
+int decode_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int n_q,
+                int n_q_heads, int n_kv_heads, int head_dim, float scale, bool skip_empty,
+                float* out, void* workspace, size_t workspace_bytes, int32_t* d_status,
+                void* stream) {
+  const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
+  if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
   if (n_seg < 1 || n_seg > kMaxGridY || n_q < 1 || n_kv_heads < 1 ||
       n_q_heads < n_kv_heads || n_q_heads % n_kv_heads != 0 || n_kv_heads > kMaxGridY ||
       !(head_dim == 64 || head_dim == 128) || !std::isfinite(scale) ||
       static_cast<long>(n_q) * (n_q_heads / n_kv_heads) > omnitide::decode_max_query_vectors())
     return OMNITIDE_E_SHAPE;
-  if (cap < n_q) return OMNITIDE_E_CAPACITY;
+  if (cap < n_q || (span && cap > omnitide::span_attn_max_cap())) return OMNITIDE_E_CAPACITY;
   const size_t need =
-      omnitide::decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim);
+      span ? omnitide::decode_span_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                                                   head_dim)
+           : omnitide::decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return OMNITIDE_E_WORKSPACE;
   const size_t qrows = static_cast<size_t>(n_seg) * n_q * n_q_heads;
   const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * 2;
   if (any_alias({{out, qrows * head_dim * 4}, {workspace, need}, {d_status, 4}},
-                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull}}))
+                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull},
+                 {key_pos, static_cast<size_t>(n_seg) * cap * 4}, {q_pos0, n_seg * 4ull}}))
     return OMNITIDE_E_ALIAS;
   DecodeArgs a;
   a.q = q;
@@ -635,7 +644,41 @@ int omnitide_decode_attn(const void* q, const void* k, const void* v, const int3
   a.out = out;
   a.workspace = need > 0 ? workspace : nullptr;
   a.d_status = d_status;
+  a.key_pos = key_pos;
+  a.q_pos0 = q_pos0;
+  a.skip_empty = skip_empty;
   return hip_status(omnitide::launch_decode(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+int omnitide_decode_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+                         int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
+                         int head_dim, float scale, float* out, void* workspace,
+                         size_t workspace_bytes, int32_t* d_status, void* stream) {
+  return decode_impl(q, k, v, n_ctx, nullptr, nullptr, n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                     head_dim, scale, true, out, workspace, workspace_bytes, d_status, stream);
+}
+
+size_t omnitide_decode_span_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,
+                                            int n_kv_heads, int head_dim) {
+  if (n_seg < 1 || cap < 1 || n_q < 1 || n_kv_heads < 1 || n_q_heads < n_kv_heads ||
+      n_q_heads % n_kv_heads != 0 || !(head_dim == 64 || head_dim == 128))
+    return 0;
+  return omnitide::decode_span_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                                               head_dim);
+}
+
+int omnitide_decode_span_attn(const void* q, const void* k, const void* v,
+                              const int32_t* key_pos, const int32_t* span,
+                              const int32_t* q_pos0, int n_seg, int cap, int n_q,
+                              int n_q_heads, int n_kv_heads, int head_dim, float scale,
+                              int skip_empty_tiles, float* out, void* workspace,
+                              size_t workspace_bytes, int32_t* d_status, void* stream) {
+  if (key_pos == nullptr || q_pos0 == nullptr) return OMNITIDE_E_NULL;
+  return decode_impl(q, k, v, span, key_pos, q_pos0, n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                     head_dim, scale, skip_empty_tiles != 0, out, workspace, workspace_bytes,
+                     d_status, stream);
 }
 
 const char* omnitide_status_string(int code) {
@@ -652,6 +695,7 @@ const char* omnitide_status_string(int code) {
     case OMNITIDE_E_SCRATCH: return "the call needs more scratch than the library's fixed array";
     case OMNITIDE_E_BUDGET: return "protected tokens exceed the retention budget";
     case OMNITIDE_E_TAGS: return "malformed unit/modality tags";
+    case OMNITIDE_E_RANGE: return "a unit score is outside the range the selection ranks (2^51)";
     default: return "unknown status";
   }
 }

@@ -592,6 +592,43 @@ __global__ __launch_bounds__(kSpanThreads) void span_list_kernel(
   if (tid == 0) n_active_g[seg] = running;
 }
 
+}  // namespace
+
+// Tables of n_seg segments: int4 info, int32 list, int32 counts, then the byte flags (the
+// caller places buf on a 256-byte boundary).
+SpanTiles span_tiles_at(void* buf, int n_seg, int cap) {
+  const size_t nt = static_cast<size_t>(n_seg) * ((cap + kKT - 1) / kKT);
+  uint8_t* b = static_cast<uint8_t*>(buf);
+  SpanTiles T;
+  T.info = reinterpret_cast<int4*>(b);
+  T.list = reinterpret_cast<int32_t*>(b + nt * sizeof(int4));
+  T.n_active = T.list + nt;
+  T.act = reinterpret_cast<uint8_t*>(T.n_active + n_seg);
+  return T;
+}
+
+size_t span_tiles_bytes(int n_seg, int cap) {
+  const size_t nt = static_cast<size_t>(n_seg) * ((cap + kKT - 1) / kKT);
+  return nt * (sizeof(int4) + sizeof(int32_t) + 1) + static_cast<size_t>(n_seg) * sizeof(int32_t);
+}
+
+hipError_t launch_span_tiles(const int32_t* key_pos, const int32_t* span, int n_seg, int cap,
+                             int min_span, bool skip_empty, void* buf, hipStream_t stream) {
+  const int max_tiles = (cap + kKT - 1) / kKT;
+  const SpanTiles T = span_tiles_at(buf, n_seg, cap);
+  const int per_block = kInfoThreads / kWave;
+  hipLaunchKernelGGL(span_info_kernel, dim3((max_tiles + per_block - 1) / per_block, n_seg),
+                     dim3(kInfoThreads), 0, stream, key_pos, span, cap, min_span, max_tiles,
+                     skip_empty ? 1 : 0, T.info, T.act);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(span_list_kernel, dim3(n_seg), dim3(kSpanThreads), 0, stream, T.act, span,
+                     cap, min_span, max_tiles, T.list, T.n_active);
+  return hipGetLastError();
+}
+
+namespace {
+
 template <int D>
 hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
   const int G = a.n_q_heads / a.n_kv_heads;
@@ -605,21 +642,13 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
     // span mode: tile table after the partials
     const int max_tiles = (a.cap + kKT - 1) / kKT;
     uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
-                   (n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
-    const size_t nt = static_cast<size_t>(a.n_seg) * max_tiles;
-    int4* tile_info = reinterpret_cast<int4*>(tbl);
-    int32_t* tile_list = reinterpret_cast<int32_t*>(tbl + nt * sizeof(int4));
-    int32_t* n_active = tile_list + nt;
-    uint8_t* act = reinterpret_cast<uint8_t*>(n_active + a.n_seg);
-    const int per_block = kInfoThreads / kWave;
-    hipLaunchKernelGGL(span_info_kernel, dim3((max_tiles + per_block - 1) / per_block, a.n_seg),
-                       dim3(kInfoThreads), 0, stream, a.key_pos, a.n_ctx, a.cap, a.chunk_len,
-                       max_tiles, a.skip_empty ? 1 : 0, tile_info, act);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(span_list_kernel, dim3(a.n_seg), dim3(kSpanThreads), 0, stream, act,
-                       a.n_ctx, a.cap, a.chunk_len, max_tiles, tile_list, n_active);
-    e = hipGetLastError();
+                   align256(n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
+    const SpanTiles T = span_tiles_at(tbl, a.n_seg, a.cap);
+    int4* tile_info = T.info;
+    int32_t* tile_list = T.list;
+    int32_t* n_active = T.n_active;
+    hipError_t e = launch_span_tiles(a.key_pos, a.n_ctx, a.n_seg, a.cap, a.chunk_len,
+                                     a.skip_empty, tbl, stream);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((attn_kernel<D, true>), grid, dim3(kAttnThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
@@ -664,10 +693,8 @@ size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, in
 
 size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                  int n_kv_heads, int head_dim) {
-  const size_t max_tiles = (static_cast<size_t>(cap) + kKT - 1) / kKT;
-  return attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim) +
-         static_cast<size_t>(n_seg) * max_tiles * (sizeof(int4) + sizeof(int32_t) + 1) +
-         static_cast<size_t>(n_seg) * sizeof(int32_t);
+  return align256(attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim)) +
+         span_tiles_bytes(n_seg, cap);
 }
 
 int span_attn_max_cap() { return 32768 * kKT; }

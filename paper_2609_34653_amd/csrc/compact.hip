@@ -10,8 +10,9 @@
 // kernel; beyond, a plan kernel (1024 threads) writes it to the workspace together with, for
 // every destination tile, the rank of the unit holding the tile's first row.
 // Mask: a count kernel (one wave per unit) gives each unit its kept count, the plan kernel
-// scans those, and a map kernel (one wave per unit, ballots over 64 slots at a time) writes
-// each kept slot's destination row, its tags and its position shift.
+// scans those, and a map kernel (one wave per unit, 16 consecutive slots per lane, an in-lane
+// count plus one wave scan per 1,024 slots) writes each kept slot's destination row, its tags
+// and its position shift.
 // Copy: one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
 // source slots (binary search over the LDS table, or a short forward walk from the workspace
 // hint), tags are written, then every thread moves 16-byte vectors of the K and V rows.  Rows
@@ -606,6 +607,8 @@ __device__ inline bool unit_in_pool(int n, int f, int n_slots) {
   return n > 0 && f >= 0 && f <= n_slots - n;
 }
 
+constexpr int kUnitPer = 16;       // consecutive slots per lane in one step of a unit walk
+
 __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_count_kernel(
     const uint8_t* __restrict__ mask_g, const int32_t* __restrict__ len_g,
     const int32_t* __restrict__ first_g, int n_slots, int n_units, int cap_dst,
@@ -622,12 +625,12 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_count_kernel(
   uint32_t c = 0;
   if (unit_in_pool(n, f, n_slots)) {
     const uint8_t* m = mask_g + static_cast<size_t>(seg) * n_slots;
-    for (int s = f + lane; s < f + n; s += 4 * kWave) {
-      uint8_t b[4];
+    for (int s0 = f + kUnitPer * lane; s0 < f + n; s0 += kUnitPer * kWave) {
+      uint8_t b[kUnitPer];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = s + j * kWave < f + n ? m[s + j * kWave] : 0;
+      for (int j = 0; j < kUnitPer; ++j) b[j] = s0 + j < f + n ? m[s0 + j] : 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) c += b[j] != 0 ? 1u : 0u;
+      for (int j = 0; j < kUnitPer; ++j) c += b[j] != 0 ? 1u : 0u;
     }
     c = wave_sum_u32(c);
   } else if (n > 0 && lane == 0) {
@@ -643,6 +646,7 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
     const int32_t* __restrict__ remap_g, const int32_t* __restrict__ n_ctx_g,
     int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
     int32_t* __restrict__ src_of_dst, uint8_t* __restrict__ ws) {
+  constexpr int P = kUnitPer;
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
   const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
@@ -659,24 +663,32 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
   const size_t sb = static_cast<size_t>(seg) * n_slots;
   const size_t db = static_cast<size_t>(seg) * cap_dst;
   const uint8_t* m = mask_g + sb;
-  int carry = 0;                                  // kept slots of the unit before the chunk
-  for (int c = 0; c < n; c += kWave) {
-    const int s = f + c + lane;
-    const bool keep = s < f + n && m[s] != 0;
-    const uint64_t bal = __ballot(keep);
-    const int within = carry + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                                   static_cast<uint32_t>(bal >> 32),
-                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(bal), 0u)));
-    if (keep) {
-      const int r = rec.off + within;
-      const int delb = rec.del + (s - f) - within;   // deleted live slots before s
-      src_of_dst[db + r] = s;
-      uid_dst[db + r] = rk;
-      mod_dst[db + r] = mod_src[sb + s];
-      pos_dst[db + r] = pos_src[sb + s] - delb;
-      shift[r] = -delb;
+  int carry = 0;                                  // kept slots of the unit before the step
+  for (int c = 0; c < n; c += P * kWave) {
+    const int s0 = f + c + P * lane;
+    bool keep[P];
+    int nk = 0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) keep[j] = s0 + j < f + n && m[s0 + j] != 0;
+#pragma unroll
+    for (int j = 0; j < P; ++j) nk += keep[j] ? 1 : 0;
+    const int incl = wave_inclusive_scan(nk);
+    int within = carry + incl - nk;               // kept slots of the unit before s0
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      if (keep[j]) {
+        const int s = s0 + j;
+        const int r = rec.off + within;
+        const int delb = rec.del + (s - f) - within;   // deleted live slots before s
+        src_of_dst[db + r] = s;
+        uid_dst[db + r] = rk;
+        mod_dst[db + r] = mod_src[sb + s];
+        pos_dst[db + r] = pos_src[sb + s] - delb;
+        shift[r] = -delb;
+        ++within;
+      }
     }
-    carry += __popcll(bal);
+    carry += __shfl(incl, kWave - 1, kWave);
   }
 }
 

@@ -39,6 +39,7 @@ namespace {
 constexpr int kDecWaves = 8;
 constexpr int kDecThreads = kDecWaves * kWave;
 constexpr int kKB = 16;                    // keys per wave per iteration (one 16x16 MFMA block)
+constexpr int kKT = 64;                    // slots per tile of a span's tile list
 constexpr int kStep = kDecWaves * kKB;     // keys per workgroup iteration
 constexpr int kDecTargetWGs = 256;         // one eight-wave workgroup per CU
 constexpr int kMaxQG = 8;                  // query vectors per KV head (n_q * G), <= 16
@@ -88,12 +89,20 @@ __device__ inline int vsw(int key) { return D == 128 ? (key & 7) : (key & 3); }
 // Each wave owns 16 keys of every 128-key workgroup step, prefetched one step ahead (K
 // operands in registers, V in a private double buffer), so no workgroup barrier is needed
 // until the waves merge.  Softmax reference per column: optimistic, as in the chunk attention.
-template <int D>
+// SPAN = false: keys are the contiguous rows [0, n_ctx) of the compacted pool.
+// SPAN = true: keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span); a
+// step covers two 64-slot tiles of the span's tile list (four waves each), slot j is visible
+// to query token i iff 0 <= key_pos[j] <= q_pos0 + i, and the V rows of empty slots are zeroed
+// in the wave's LDS block before use (their bytes may be anything, NaN included).
+template <int D, bool SPAN>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int nq,
     int Hq, int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
-    float* __restrict__ part_ml, int n_split, int32_t* __restrict__ status) {
+    float* __restrict__ part_ml, int n_split, int32_t* __restrict__ status,
+    const int32_t* __restrict__ key_pos, const int32_t* __restrict__ qpos0_g,
+    const int32_t* __restrict__ tile_list, const int32_t* __restrict__ n_active_g,
+    int max_tiles) {
   constexpr int KC = D / 32;               // 32-dim slices (QK k-steps)
   constexpr int DB = D / 16;               // 16-dim blocks of the output
   constexpr int CHK = D / 8;               // 16-byte chunks per key row
@@ -111,8 +120,13 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   }
   const int G = Hq / Hkv;
   const int nqg = nq * G;
-  const int j0 = static_cast<int>(static_cast<long>(nctx) * split / n_split);
-  const int j1 = static_cast<int>(static_cast<long>(nctx) * (split + 1) / n_split);
+  // contiguous: keys [j0, j1); SPAN: steps [j0, j1) of the tile list (two tiles per step)
+  const int n_units_all = SPAN ? (n_active_g[seg] + 1) / 2 : nctx;
+  const int j0 = static_cast<int>(static_cast<long>(n_units_all) * split / n_split);
+  const int j1 = static_cast<int>(static_cast<long>(n_units_all) * (split + 1) / n_split);
+  const int n_act = SPAN ? n_active_g[seg] : 0;
+  const size_t tl_base = static_cast<size_t>(seg) * max_tiles;
+  const int32_t* kpos = SPAN ? key_pos + static_cast<size_t>(seg) * cap : nullptr;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -122,7 +136,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   // dims 32kc + 8 g4 .. +7.  Columns past n_q*G stay zero.
   const bool col_ok = c16 < nqg;
   const int tok = col_ok ? c16 / G : 0;
-  const int lim = col_ok ? nctx - nq + tok : nctx - 1;   // keys <= lim are visible
+  // keys (contiguous: rows; SPAN: positions) <= lim are visible
+  const int lim = SPAN ? qpos0_g[seg] + tok : (col_ok ? nctx - nq + tok : nctx - 1);
   bf16x8 qf[KC];
   {
     const uint16_t* qrow =
@@ -150,19 +165,40 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     voff[cq] = 2u * static_cast<uint32_t>(8 * (2 * ((pc >> 1) ^ vsw<D>(key)) + (pc & 1)));
   }
   const uint32_t vlds = lds_addr(&vbuf[wave][0][0]);
-  // keys of iteration it for this wave: base(it) + [0, 16), base(it) = j0 + it*kStep + 16*wave;
-  // rows past j1 - 1 are clamped to it (read, then masked)
-  auto issue = [&](int it, int buf, bf16x8 (&ka)[KC]) {
-    const int kb0 = j0 + it * kStep + kKB * wave;
-    const int kr = min(kb0 + c16, j1 - 1);
-    const uint16_t* kp = kh + static_cast<size_t>(kr) * row_stride + 8 * g4;
+  // keys of iteration it for this wave: base(it) + [0, 16).  Contiguous: base(it) = j0 +
+  // it*kStep + 16*wave, rows past j1 - 1 clamped to it (read, then masked).  SPAN: base(it) =
+  // 64*tile + 16*(wave % 4) with tile the list entry 2*(j0 + it) + wave / 4, rows past the span
+  // clamped to its last slot; a wave past the list reads the span's first rows and masks them.
+  // Every load is issued unconditionally, so the vmcnt waits below count exactly.
+  auto block_base = [&](int it, bool& blk_ok) {
+    if constexpr (SPAN) {
+      const int a = 2 * (j0 + it) + (wave >> 2);
+      blk_ok = a < n_act;
+      return blk_ok ? kKT * tile_list[tl_base + a] + kKB * (wave & 3) : 0;
+    } else {
+      blk_ok = true;
+      return j0 + it * kStep + kKB * wave;
+    }
+  };
+  const int row_end = SPAN ? nctx : j1;      // rows >= row_end are clamped
+  auto issue = [&](int it, int buf, bf16x8 (&ka)[KC], int (&kp)[5]) {
+    bool blk_ok;
+    const int kb0 = block_base(it, blk_ok);
+    const int kr = min(kb0 + c16, row_end - 1);
+    const uint16_t* kp_ = kh + static_cast<size_t>(kr) * row_stride + 8 * g4;
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc)
-      ka[kc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kp + 32 * kc));
-    const int r0 = min(kb0, j1 - 1);
+      ka[kc] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kp_ + 32 * kc));
+    if constexpr (SPAN) {
+      // positions of keys 4 g4 .. +3 (for the mask) and of key c16 (for the V zeroing)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kp[i] = kpos[min(kb0 + 4 * g4 + i, row_end - 1)];
+      kp[4] = kpos[kr];
+    }
+    const int r0 = min(kb0, row_end - 1);
 #pragma unroll
     for (int cq = 0; cq < CALLS; ++cq) {
-      const int shift = min(kb0 + vkey[cq], j1 - 1) - r0;   // >= 0
+      const int shift = min(kb0 + vkey[cq], row_end - 1) - r0;   // >= 0
       dma16(vh + static_cast<size_t>(r0) * row_stride,
             voff[cq] + 2u * static_cast<uint32_t>(shift * row_stride),
             vlds + static_cast<uint32_t>((buf * BLK + cq * kWave * 8) * 2));
@@ -173,8 +209,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
 #pragma unroll
   for (int db = 0; db < DB; ++db) o[db] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  const int n_it = (j1 - j0 + kStep - 1) / kStep;
+  const int n_it = SPAN ? j1 - j0 : (j1 - j0 + kStep - 1) / kStep;
   bf16x8 kA[KC], kB[KC];
+  int pA[5] = {-1, -1, -1, -1, -1}, pB[5] = {-1, -1, -1, -1, -1};
   // V^T operand read: lane (g4, i) takes dims 16db + i of keys 4g4 .. 4g4+3; the lanes of its
   // group read key 4g4 + (i >> 2), dims 16db + 4(i & 3) .. +3.
   const int vrow = 4 * g4 + (c16 >> 2);
@@ -184,16 +221,24 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     constexpr int B = decltype(bpar)::value;
     bf16x8(&ka)[KC] = B == 0 ? kA : kB;
     bf16x8(&kn)[KC] = B == 0 ? kB : kA;
+    const int(&pc)[5] = B == 0 ? pA : pB;
+    int(&pn)[5] = B == 0 ? pB : pA;
     const bool more = it + 1 < n_it;
     floatx4 s = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc)
       s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kc], qf[kc], s, 0, 0, 0);
+    const int(&kpc)[5] = pc;   // positions of this iteration's keys (SPAN)
     // the next iteration's loads go out once this one's K operands are consumed
-    if (more) issue(it + 1, 1 - B, kn);
-    const int kb0 = j0 + it * kStep + kKB * wave;
+    if (more) issue(it + 1, 1 - B, kn, pn);
+    bool blk_ok;
+    const int kb0 = block_base(it, blk_ok);
     const int key0 = kb0 + 4 * g4;
-    if (kb0 + kKB > j1 || kb0 + kKB - 1 > nctx - nq) {
+    if constexpr (SPAN) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (!blk_ok || key0 + i >= nctx || kpc[i] < 0 || kpc[i] > lim) s[i] = -INFINITY;
+    } else if (kb0 + kKB > j1 || kb0 + kKB - 1 > nctx - nq) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         if (key0 + i >= j1 || key0 + i > lim) s[i] = -INFINITY;
@@ -229,13 +274,27 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
       lsum += static_cast<float>(hi) + static_cast<float>(lo);
     }
     l_run += lsum;
-    // this iteration's V block has landed (the next one's loads may still be in flight)
-    static_assert(CALLS + KC == 8 || CALLS + KC == 4, "vmcnt immediates below");
+    // this iteration's V block has landed (the next one's loads may still be in flight: KC K
+    // loads, in SPAN mode 5 position loads, CALLS direct loads)
+    constexpr int NEXT = CALLS + KC + (SPAN ? 5 : 0);
+    static_assert(NEXT == 8 || NEXT == 4 || NEXT == 13 || NEXT == 9, "vmcnt immediates below");
     if (more) {
-      if constexpr (CALLS + KC == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+      if constexpr (NEXT == 13) asm volatile("s_waitcnt vmcnt(13)" ::: "memory");
+      else if constexpr (NEXT == 9) asm volatile("s_waitcnt vmcnt(9)" ::: "memory");
+      else if constexpr (NEXT == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
       else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
     } else {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    if constexpr (SPAN) {
+      // V rows of empty slots (and of a wave past the list) are zeroed by the four lanes of
+      // their key, a quarter of the row each; the wave's own LDS reads below follow in order
+      if (!blk_ok || kpc[4] < 0) {
+        u32x4* row = reinterpret_cast<u32x4*>(&vbuf[wave][B][0] + c16 * D);
+#pragma unroll
+        for (int x = 0; x < CHK / 4; ++x) row[(CHK / 4) * g4 + x] = u32x4{0, 0, 0, 0};
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
     const uint16_t* vb = &vbuf[wave][B][0] + vrow * D + vsub;
 #pragma unroll
@@ -245,7 +304,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
       o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pl, o[db], 0, 0, 0);
     }
   };
-  if (n_it > 0) issue(0, 0, kA);
+  if (n_it > 0) issue(0, 0, kA, pA);
   int it = 0;
   for (; it + 1 < n_it; it += 2) {
     step(std::integral_constant<int, 0>{}, it);
@@ -302,13 +361,29 @@ template <int D>
 hipError_t launch_decode_t(const DecodeArgs& a, int n_split, hipStream_t stream) {
   const dim3 grid(n_split, a.n_kv_heads, a.n_seg);
   const size_t n_rows = static_cast<size_t>(a.n_seg) * a.n_q * a.n_q_heads;
-  float* part_o = static_cast<float*>(a.workspace);
+  float* part_o = n_split > 1 ? static_cast<float*>(a.workspace) : nullptr;
   float* part_ml = part_o ? part_o + static_cast<size_t>(n_split) * n_rows * D : nullptr;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  hipLaunchKernelGGL((decode_kernel<D>), grid, dim3(kDecThreads), 0, stream,
-                     static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
-                     static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
-                     a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status);
+  if (a.key_pos != nullptr) {
+    // span mode: the tile tables after the partials
+    uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
+                   align256(n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
+    hipError_t e = launch_span_tiles(a.key_pos, a.n_ctx, a.n_seg, a.cap, a.n_q, a.skip_empty,
+                                     tbl, stream);
+    if (e != hipSuccess) return e;
+    const SpanTiles T = span_tiles_at(tbl, a.n_seg, a.cap);
+    hipLaunchKernelGGL((decode_kernel<D, true>), grid, dim3(kDecThreads), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                       static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
+                       a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status,
+                       a.key_pos, a.q_pos0, T.list, T.n_active, (a.cap + kKT - 1) / kKT);
+  } else {
+    hipLaunchKernelGGL((decode_kernel<D, false>), grid, dim3(kDecThreads), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                       static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
+                       a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status,
+                       nullptr, nullptr, nullptr, nullptr, 0);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_split == 1) return e;
   return launch_combine<D>(part_o, part_ml, n_split, n_rows, a.n_ctx, a.n_q, a.n_q_heads, a.cap,
@@ -330,6 +405,12 @@ size_t decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_
   if (s == 1) return 0;
   const size_t rows = static_cast<size_t>(n_seg) * n_q * n_q_heads;
   return static_cast<size_t>(s) * rows * (static_cast<size_t>(head_dim) + 2) * sizeof(float);
+}
+
+size_t decode_span_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
+                                   int head_dim) {
+  return align256(decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim)) +
+         span_tiles_bytes(n_seg, cap);
 }
 
 int decode_max_query_vectors() { return kMaxQG; }

@@ -157,6 +157,21 @@ struct AttnArgs {
 
 int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
                     int head_dim);
+
+// Active 64-slot tiles of a span (a pool with holes), shared by the span chunk attention and the
+// span decode: per tile its largest position, an empty-slot flag and 64 occupancy bits; the
+// list of visited tiles (every tile of [0, span), or only tiles holding an entry) and its
+// length per segment.  Segments whose span is outside [min_span, cap] get no tiles.
+struct SpanTiles {
+  int4* info;          // [n_seg][max_tiles]
+  int32_t* list;       // [n_seg][max_tiles]
+  int32_t* n_active;   // [n_seg]
+  uint8_t* act;        // [n_seg][max_tiles]
+};
+SpanTiles span_tiles_at(void* buf, int n_seg, int cap);
+size_t span_tiles_bytes(int n_seg, int cap);
+hipError_t launch_span_tiles(const int32_t* key_pos, const int32_t* span, int n_seg, int cap,
+                             int min_span, bool skip_empty, void* buf, hipStream_t stream);
 size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
                             int head_dim);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
@@ -177,11 +192,17 @@ struct DecodeArgs {
   float* out;
   void* workspace;
   int32_t* d_status;
+  // span mode (keys = the slots [0, span) of a pool with holes; n_ctx holds the span):
+  const int32_t* key_pos = nullptr;   // [n_seg][cap] logical position, -1 = empty slot
+  const int32_t* q_pos0 = nullptr;    // [n_seg] logical position of query token 0
+  bool skip_empty = true;             // visit only 64-slot tiles holding an entry
 };
 
 int decode_num_splits(int n_seg, int cap, int n_kv_heads);
 size_t decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
                               int head_dim);
+size_t decode_span_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
+                                   int head_dim);
 int decode_max_query_vectors();
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   int ln[kPer], fs[kPer], ls[kPer];
   bool sys[kPer];
   uint64_t sc[kPer];
-  bool bad = false;
+  bool bad = false, big = false;
   int my_max_first = -1;
   uint32_t fl[kPer];
   uint64_t ws[kPer];
@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     sys[i] = live && (fl[i] & 1u) != 0;
     sc[i] = live ? udiv64(ws[i], static_cast<uint32_t>(ln[i])) : 0;
     bad |= live && (ls[i] - fs[i] + 1) != ln[i];
-    bad |= (sc[i] >> kScoreBits) != 0;          // the ranking key holds kScoreBits of score
+    big |= (sc[i] >> kScoreBits) != 0;          // the ranking key holds kScoreBits of score
     if (live) my_max_first = max(my_max_first, fs[i]);
     if (mine) {
       score_g[base + u] = sc[i];
@@ -100,17 +100,20 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     }
   }
   const int n_bad = block_sum(bad ? 1 : 0, scr_i);
+  const int n_big = block_sum(big ? 1 : 0, scr_i);
 
   int my_sys = 0;
 #pragma unroll
   for (int i = 0; i < kPer; ++i) my_sys += sys[i] ? ln[i] : 0;
   const int t_sys = block_sum(my_sys, scr_i);
 
-  if (n_bad > 0 || t_sys > budget) {
+  if (n_bad > 0 || n_big > 0 || t_sys > budget) {
     for (int u = tid; u < U; u += kSelThreads) keep_g[base + u] = 0;
     if (tid == 0) {
       kept_tokens_g[seg] = 0;
-      set_status(status, n_bad > 0 ? OMNITIDE_E_TAGS : OMNITIDE_E_BUDGET);
+      set_status(status, n_bad > 0   ? OMNITIDE_E_TAGS
+                         : n_big > 0 ? OMNITIDE_E_RANGE
+                                     : OMNITIDE_E_BUDGET);
     }
     return;
   }
@@ -247,7 +250,7 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
   }
   bool sys[kSmallPer];
   uint64_t key[kSmallPer];
-  bool bad = false;
+  bool bad = false, big = false;
   int my_max_first = -1;
 #pragma unroll
   for (int i = 0; i < kSmallPer; ++i) {
@@ -257,7 +260,7 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
     sys[i] = live && (fl[i] & 1u) != 0;
     const uint64_t sc = live ? udiv64(ws[i], static_cast<uint32_t>(ln[i])) : 0;
     bad |= live && (ls[i] - fs[i] + 1) != ln[i];
-    bad |= (sc >> kScoreBits) != 0;
+    big |= (sc >> kScoreBits) != 0;
     if (live) my_max_first = max(my_max_first, fs[i]);
     if (u < U) score_g[base + u] = sc;
     key[i] = (sc << kIdBits) | static_cast<uint64_t>(u);
@@ -287,13 +290,16 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
   wave_exclusive_sum(my_sys, &t_sys);
   const int elig_before = wave_exclusive_sum(my_elig, &elig_total);
   const bool any_bad = __any(bad);
-  if (any_bad || t_sys > budget) {
+  const bool any_big = __any(big);
+  if (any_bad || any_big || t_sys > budget) {
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i)
       if (u0 + i < U) keep_g[base + u0 + i] = 0;
     if (lane == 0) {
       kept_tokens_g[seg] = 0;
-      set_status(status, any_bad ? OMNITIDE_E_TAGS : OMNITIDE_E_BUDGET);
+      set_status(status, any_bad   ? OMNITIDE_E_TAGS
+                         : any_big ? OMNITIDE_E_RANGE
+                                   : OMNITIDE_E_BUDGET);
     }
     return;
   }

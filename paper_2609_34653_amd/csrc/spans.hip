@@ -1,6 +1,6 @@
 // OmniPick span plan in three kernels.
 //
-// 1. Census (one wave per unit).  The wave walks its unit's slots 256 at a time (4 per lane) and
+// 1. Census (one wave per unit).  The wave walks its unit's slots 1024 at a time (16 per lane) and
 //    finds where each span starts: at the unit's first slot and wherever the tag changes.  A
 //    running maximum of the start slots (wave scan plus a carry across chunks) gives every
 //    token its place in its span.  Each slot gets a code in the workspace: marker tokens and
@@ -54,10 +54,13 @@ __device__ inline SpanWs span_ws(uint8_t* ws, int seg, int n_slots, int n_units)
                 reinterpret_cast<int32_t*>(b + info_bytes + 2 * ub)};
 }
 
+constexpr int kCensusPer = 16;          // consecutive slots per lane in one census step
+
 __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
     const uint8_t* __restrict__ mod_g, const int32_t* __restrict__ len_g,
     const int32_t* __restrict__ first_g, int n_slots, int n_units, int sink_video,
     int sink_audio, uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
+  constexpr int P = kCensusPer;
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
   const int u = blockIdx.x * kCensusWaves + threadIdx.x / kWave;
@@ -74,26 +77,23 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
     return;
   }
   const uint8_t* mod = mod_g + static_cast<size_t>(seg) * n_slots;
-  int carry_tag = -1;      // tag of the slot before the chunk (-1 at the unit's start)
+  int carry_tag = -1;      // tag of the slot before the step (-1 at the unit's start)
   int carry_start = f;     // first slot of the span that slot belongs to
-  int carry_text = 0;      // the unit's text tokens before the chunk
+  int carry_text = 0;      // the unit's text tokens before the step
   int sinks = 0;
   bool bad = false;
-  for (int c = 0; c < n; c += 4 * kWave) {
-    const int s0 = f + c + 4 * lane;
-    int m[4];
+  for (int c = 0; c < n; c += P * kWave) {
+    const int s0 = f + c + P * lane;
+    int m[P];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) m[j] = s0 + j < f + n ? mod[s0 + j] : -1;
-    int prev = __shfl_up(m[3], 1, kWave);
+    for (int j = 0; j < P; ++j) m[j] = s0 + j < f + n ? mod[s0 + j] : -1;   // loads first
+    int prev = __shfl_up(m[P - 1], 1, kWave);
     if (lane == 0) prev = carry_tag;
-    int st[4], tr[4];
     int run = -1, nt = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < P; ++j) {
       const int pm = j == 0 ? prev : m[j - 1];
       if (m[j] >= 0 && m[j] != pm) run = s0 + j;   // a span starts here
-      st[j] = run;
-      tr[j] = nt;                                  // text tokens of this lane before slot j
       nt += m[j] == OMNITIDE_MOD_TEXT ? 1 : 0;
     }
     int inc = run;                                 // running maximum of span starts
@@ -104,31 +104,32 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
     }
     int exc = __shfl_up(inc, 1, kWave);
     if (lane == 0) exc = -1;
-    const int start_before = max(exc, carry_start);
-    int text_tot;
-    const int text_before = carry_text + [&] {
-      const int incl = wave_inclusive_scan(nt);
-      text_tot = __shfl(incl, kWave - 1, kWave);
-      return incl - nt;
-    }();
+    int start = max(exc, carry_start);             // span start of the slot before s0
+    const int incl = wave_inclusive_scan(nt);
+    const int text_tot = __shfl(incl, kWave - 1, kWave);
+    int text_rank = carry_text + incl - nt;        // the unit's text tokens before s0
+    int pm = prev;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < P; ++j) {
       const int s = s0 + j;
-      if (m[j] < 0) continue;
-      const int place = s - max(start_before, st[j]) + 1;   // 1-based place in its span
-      int32_t code = kInfoDrop;
-      if (m[j] == OMNITIDE_MOD_TEXT) {
-        code = text_before + tr[j];
-      } else if (m[j] == OMNITIDE_MOD_MARK ||
-                 (m[j] == OMNITIDE_MOD_VIDEO && place <= sink_video) ||
-                 (m[j] == OMNITIDE_MOD_AUDIO && place <= sink_audio)) {
-        code = kInfoSink;
-        ++sinks;
+      if (m[j] >= 0) {
+        if (m[j] != pm) start = s;
+        const int place = s - start + 1;           // 1-based place in its span
+        int32_t code = kInfoDrop;
+        if (m[j] == OMNITIDE_MOD_TEXT) {
+          code = text_rank++;
+        } else if (m[j] == OMNITIDE_MOD_MARK ||
+                   (m[j] == OMNITIDE_MOD_VIDEO && place <= sink_video) ||
+                   (m[j] == OMNITIDE_MOD_AUDIO && place <= sink_audio)) {
+          code = kInfoSink;
+          ++sinks;
+        }
+        bad |= m[j] > OMNITIDE_MOD_MARK;
+        W.info[static_cast<size_t>(s)] = code;
       }
-      bad |= m[j] > OMNITIDE_MOD_MARK;
-      W.info[static_cast<size_t>(s)] = code;
+      pm = m[j];
     }
-    carry_tag = __shfl(m[3], kWave - 1, kWave);
+    carry_tag = __shfl(m[P - 1], kWave - 1, kWave);
     carry_start = max(carry_start, __shfl(inc, kWave - 1, kWave));
     carry_text += text_tot;
   }

@@ -23,7 +23,7 @@ LIB_PATH = os.path.join(_PKG, "libomnitide.so")
 OK, E_NULL, E_SHAPE, E_DTYPE, E_WEIGHT, E_CAPACITY, E_WORKSPACE, E_ALIAS, E_HIP, E_SCRATCH = \
     0, -1, -2, -3, -4, -5, -6, -7, -8, -9
 NOALLOC_SCRATCH_BYTES = 64 << 20
-E_BUDGET, E_TAGS = -16, -17
+E_BUDGET, E_TAGS, E_RANGE = -16, -17, -18
 BF16, F32 = 0, 1
 ROPE_HALF, ROPE_INTERLEAVED = 0, 1
 
@@ -37,7 +37,8 @@ EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv
            "omnitide_pack_suffix_workspace_bytes", "omnitide_place_chunk",
            "omnitide_place_chunk_workspace_bytes",
            "omnitide_span_attn_workspace_bytes", "omnitide_decode_attn",
-           "omnitide_decode_workspace_bytes", "omnitide_status_string", "omnitide_version")
+           "omnitide_decode_workspace_bytes", "omnitide_decode_span_attn",
+           "omnitide_decode_span_workspace_bytes", "omnitide_status_string", "omnitide_version")
 
 
 class OmnitideError(RuntimeError):
@@ -102,6 +103,9 @@ def lib() -> ctypes.CDLL:
         L.omnitide_decode_attn.argtypes = L.omnitide_chunk_attn.argtypes
         L.omnitide_decode_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_decode_workspace_bytes.restype = _SZ
+        L.omnitide_decode_span_attn.argtypes = L.omnitide_span_attn.argtypes
+        L.omnitide_decode_span_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
+        L.omnitide_decode_span_workspace_bytes.restype = _SZ
         L.omnitide_status_string.argtypes = [_I]
         L.omnitide_status_string.restype = ctypes.c_char_p
         L.omnitide_version.restype = ctypes.c_char_p
@@ -110,7 +114,7 @@ def lib() -> ctypes.CDLL:
                      "omnitide_plan_spans", "omnitide_chunk_attn",
                      "omnitide_chunk_attn_noalloc", "omnitide_span_attn",
                      "omnitide_evict_native", "omnitide_pack_suffix", "omnitide_place_chunk",
-                     "omnitide_decode_attn"):
+                     "omnitide_decode_attn", "omnitide_decode_span_attn"):
             getattr(L, name).restype = _I
         _lib = L
     return _lib
@@ -420,6 +424,41 @@ def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_
                                     1 if skip_empty_tiles else 0, _ptr(out), _ptr(workspace),
                                     workspace.numel(),
                                     _ptr(d_status), _stream(stream)), "omnitide_span_attn")
+
+
+def omnitide_decode_span_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                                         head_dim) -> int:
+    return int(lib().omnitide_decode_span_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
+                                                          head_dim))
+
+
+def omnitide_decode_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace,
+                              d_status=None, stream=None, skip_empty_tiles=True):
+    """Decode attention of n_q tokens over a pool with holes: q [n_seg, n_q, Hq, d] bf16;
+    k/v [n_seg, cap, Hkv, d] bf16; key_pos int32 [n_seg * cap] (-1 = empty slot); span, q_pos0
+    int32 [n_seg] (device); out float32 like q."""
+    if q.dim() == 3:
+        n_seg, (nq, Hq, d) = 1, q.shape
+    else:
+        n_seg, nq, Hq, d = q.shape
+    ds, cap, Hkv, dd = _pool_dims(k, "k")
+    if ds != n_seg or dd != d:
+        raise ValueError("k shape does not match q")
+    _need(q, "q", (torch.bfloat16,))
+    _need(k, "k", (torch.bfloat16,))
+    _need(v, "v", (torch.bfloat16,), k.numel())
+    _need(key_pos, "key_pos", I32, n_seg * cap)
+    _need(span, "span", I32, n_seg)
+    _need(q_pos0, "q_pos0", I32, n_seg)
+    _need(out, "out", (torch.float32,), q.numel())
+    _need(workspace, "workspace", U8)
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_decode_span_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(key_pos), _ptr(span),
+                                           _ptr(q_pos0), n_seg, cap, nq, Hq, Hkv, d,
+                                           float(scale), 1 if skip_empty_tiles else 0, _ptr(out),
+                                           _ptr(workspace), workspace.numel(), _ptr(d_status),
+                                           _stream(stream)), "omnitide_decode_span_attn")
 
 
 def omnitide_evict_native_workspace_bytes(n_seg, n_units) -> int:

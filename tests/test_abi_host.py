@@ -25,7 +25,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol(L):
     names = header_functions()
-    assert len(names) == 23
+    assert len(names) == 25
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(ot.EXPORTS)
@@ -37,12 +37,15 @@ def test_header_codes_match_binding():
     assert codes["OK"] == ot.OK and codes["E_TAGS"] == ot.E_TAGS
     assert codes["E_BUDGET"] == ot.E_BUDGET and codes["E_CAPACITY"] == ot.E_CAPACITY
     assert codes["E_ALIAS"] == ot.E_ALIAS and codes["E_WORKSPACE"] == ot.E_WORKSPACE
+    assert codes["E_RANGE"] == ot.E_RANGE and codes["E_SCRATCH"] == ot.E_SCRATCH
+    assert len(set(codes.values())) == len(codes)
 
 
 def test_status_strings_and_version():
     assert ot.status_string(0) == "ok"
     assert "budget" in ot.status_string(-16)
     assert "tags" in ot.status_string(-17)
+    assert "2^51" in ot.status_string(ot.E_RANGE)
     assert ot.status_string(12345) == "unknown status"
     assert "gfx950" in ot.version()
 

@@ -535,22 +535,27 @@ def test_select_scores_at_division_edges(U):
     assert int(host(kept_d)[0]) == kept
 
 
-def test_select_score_out_of_key_range_reported():
-    """A score of 2^51 or more does not fit the ranking key: E_TAGS, nothing kept."""
+@pytest.mark.parametrize("U", [40, 600])
+def test_select_score_out_of_key_range_reported(U):
+    """A score of 2^51 or more does not fit the ranking key: E_RANGE, nothing kept (both
+    kernel shapes); a broken unit structure in the same call reports E_TAGS first."""
     from paper_2609_34653_amd import omnitide as ot
-    U = 40
     lens = np.full(U, 10)
     first = np.arange(U) * 10
     last = first + 9
     wsum = np.full(U, 1000, np.int64)
     wsum[7] = 10 << 51
     i32 = lambda a: dev(np.asarray(a, np.int32))   # noqa: E731
-    sc_d = torch.zeros(U, dtype=torch.int64, device="cuda")
-    keep_d = torch.ones(U, dtype=torch.uint8, device="cuda")
-    kept_d = torch.ones(1, dtype=torch.int32, device="cuda")
-    stat = torch.zeros(1, dtype=torch.int32, device="cuda")
-    ot.omnitide_select_units(dev(wsum), i32(lens), i32(first), i32(last), i32(np.zeros(U)), 1, U,
-                             200, 30, sc_d, keep_d, kept_d, stat)
-    torch.cuda.synchronize()
-    assert int(host(stat)[0]) == ot.E_TAGS
-    assert not host(keep_d).any() and int(host(kept_d)[0]) == 0
+    for broken, code in ((False, ot.E_RANGE), (True, ot.E_TAGS)):
+        lst = last.copy()
+        if broken:
+            lst[3] += 1
+        sc_d = torch.zeros(U, dtype=torch.int64, device="cuda")
+        keep_d = torch.ones(U, dtype=torch.uint8, device="cuda")
+        kept_d = torch.ones(1, dtype=torch.int32, device="cuda")
+        stat = torch.zeros(1, dtype=torch.int32, device="cuda")
+        ot.omnitide_select_units(dev(wsum), i32(lens), i32(first), i32(lst), i32(np.zeros(U)), 1,
+                                 U, 200, 30, sc_d, keep_d, kept_d, stat)
+        torch.cuda.synchronize()
+        assert int(host(stat)[0]) == code
+        assert not host(keep_d).any() and int(host(kept_d)[0]) == 0

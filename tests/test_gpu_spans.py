@@ -122,8 +122,8 @@ def test_plan_parity_random(U, seed, mixed):
 
 
 def test_plan_long_spans():
-    """Spans longer than one 256-slot census step, with sinks ending on, before and after step
-    boundaries and text ranks carried across steps."""
+    """Spans longer than one census step (1,024 slots), with sinks ending on, before and after
+    step boundaries and text ranks carried across steps."""
     rng = np.random.default_rng(14)
     units = [sg.grammar_unit(2304, 25, 600), sg.MixedUnit(tuple([1] * 255 + [2] * 2 + [1] * 300)),
              sg.grammar_unit(640, 25, 0), sg.MixedUnit(tuple([3] * 700 + [4] + [3] * 90)),
@@ -134,7 +134,8 @@ def test_plan_long_spans():
     length = np.bincount(uid, minlength=U)
     first = np.array([np.nonzero(uid == u)[0][0] for u in range(U)])
     sc = dict(len=length, first=first, last=first + length - 1, flags=np.zeros(U, np.int64))
-    for sv, sa, tb in ((255, 1, 650), (256, 2, 0), (257, 0, 10 ** 6), (1, 0, 255), (0, 0, 256)):
+    for sv, sa, tb in ((255, 1, 650), (256, 2, 0), (257, 0, 10 ** 6), (1, 0, 255), (0, 0, 256),
+                       (1021, 3, 1023), (1022, 1, 1025), (1023, 0, 700), (2047, 2, 1500)):
         low = int(rng.integers(0, 2000))
         p = dict(high=low, low=low, recent=0, sv=sv, sa=sa, tb=tb)
         want, wmask, wkept = oracle_plan(sc, lay.modality, p)
