@@ -558,7 +558,10 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
     slots, then the chunk) and eager compaction (the step's own compact + attend).  Each
     maintenance call is timed from its layout's state before it: `reps` repetitions of
     [restore the tags from a snapshot, call] in one captured graph, minus the same graph without
-    the call; attention is `reps` calls over the final layout."""
+    the call; attention is `reps` calls over the final layout.  `evict_rope_us` is the eviction
+    with the rotary adjustment of the keys that stay (base 1e6, 128 dims, split halves; on a copy
+    of the keys), the native counterpart of the eager path's rotary compaction
+    (kernels.compact_rope)."""
     cap = lay.n_slots + L
     pad = cap - lay.n_slots
     i32 = dict(dtype=torch.int32, device=dev)
@@ -574,6 +577,9 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
     kept, nku, span, slot, cut, moved = (torch.zeros(1, **i32) for _ in range(6))
     ws_e = torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, lay.n_units),
                        dtype=torch.uint8, device=dev)
+    ws_er = torch.zeros(ot.omnitide_evict_native_rope_workspace_bytes(1, lay.n_units, cap),
+                        dtype=torch.uint8, device=dev)
+    k_rope = k.clone()
     ws_p = torch.zeros(ot.omnitide_pack_suffix_workspace_bytes(0, 1, cap, H, d),
                        dtype=torch.uint8, device=dev)
     ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap, L, Hq, H, d),
@@ -589,6 +595,11 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
     def evict():
         ot.omnitide_evict_native(uid, pos, 1, lay.n_units, st.unit_len, remap, kept, nku, span,
                                  ws_e, keep=st.keep, d_status=st.d_status)
+
+    def evict_rope():
+        ot.omnitide_evict_native_rope(uid, pos, k_rope, 1, lay.n_units, st.unit_len, remap, kept,
+                                      nku, span, ws_er, 1.0e6, 128, ot.ROPE_HALF, keep=st.keep,
+                                      d_status=st.d_status)
 
     def pack():
         ot.omnitide_pack_suffix(k, v, 256, 1, uid, mod, pos, span, cut, moved, ws_p)
@@ -643,6 +654,8 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
         span_final = span.clone()
         span.copy_(torch.zeros_like(span))
         r["evict_us"], _ = staged(tags0, evict)
+        span.copy_(torch.zeros_like(span))
+        r["evict_rope_us"], _ = staged(tags0, evict_rope)
         span.copy_(span_ev)
         if packed:
             r["pack_us"], _ = staged(snap_ev, pack)

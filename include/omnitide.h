@@ -366,6 +366,30 @@ int omnitide_evict_native(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
 size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units);
 
 /*
+ * omnitide_evict_native_rope -- omnitide_evict_native plus the rotary adjustment of the cached
+ * keys that stay in place (paper: Applying the retention plan -- a retained token's position
+ * drops by the deleted tokens before it and its cached key is re-rotated to match).  Same
+ * arguments, outputs and errors as omnitide_evict_native, and:
+ *   k       [n_seg][cap][n_kv_heads][head_dim] of `dtype` (OMNITIDE_BF16 or OMNITIDE_F32),
+ *           rotary-encoded at the entries' old positions, updated in place: every kept slot
+ *           whose position changes by shift (< 0) has each pair (x, y) of its first rope_dims
+ *           dimensions per head turned by shift * theta_j (as omnitide_compact_kv_rope, same
+ *           precision); the rows of other slots and dimensions >= rope_dims keep their bits.
+ *   rope_base, rope_dims, rope_style  as omnitide_compact_kv_rope (OMNITIDE_E_SHAPE if invalid)
+ *   workspace  omnitide_evict_native_rope_workspace_bytes() bytes (the unit table and one
+ *           shift per slot).
+ * The V pool is not touched (values carry no position).
+ */
+int omnitide_evict_native_rope(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
+                               const uint8_t* keep, const int32_t* keep_len,
+                               const int32_t* unit_len, int n_units, void* k, int dtype,
+                               int n_kv_heads, int head_dim, double rope_base, int rope_dims,
+                               int rope_style, int32_t* unit_remap, int32_t* kept_tokens,
+                               int32_t* n_kept_units, int32_t* span, void* workspace,
+                               size_t workspace_bytes, int32_t* d_status, void* stream);
+size_t omnitide_evict_native_rope_workspace_bytes(int n_seg, int n_units, int cap);
+
+/*
  * omnitide_pack_suffix -- ordered-suffix migration in place (paper: scanning back from the end
  * of the cache, the suffix whose packing shortens the page-rounded span by at least a threshold
  * of pages is packed, order kept, everything before it untouched; no qualifying suffix, no

@@ -38,13 +38,20 @@ import numpy as np
 from .errors import CapacityError
 
 
-def evict_logical(unit_id, pos, keep_len, n_units: int):
+def evict_logical(unit_id, pos, keep_len, n_units: int, k=None, rope=None):
     """Logical eviction in place (returns new arrays).
 
     unit_id, pos: per-slot tags (-1 = empty).  keep_len: per unit, leading tokens (in position
     order) that stay.  Returns dict(unit_id, pos, unit_remap, kept, n_kept_units).
+
+    rope: optional dict(base, dims, style, dtype) with k ([cap, H_kv, d] storage values, encoded
+    at the old positions): the result then also holds "k_f64", the keys as float64 with every
+    kept slot re-rotated by its position change (new - old position, rope.shift_keys); other
+    slots are unchanged (the paper: the runtime adjusts the cached keys to the shifted
+    positions, while the entries stay in their slots).
     """
     unit_id = np.asarray(unit_id, np.int64).copy()
+    pos_in = pos
     pos = np.asarray(pos, np.int64).copy()
     quota = np.asarray(keep_len, np.int64).copy()
     live = np.nonzero(unit_id >= 0)[0]
@@ -73,8 +80,16 @@ def evict_logical(unit_id, pos, keep_len, n_units: int):
         else:
             unit_id[s] = -1
             pos[s] = -1
-    return {"unit_id": unit_id, "pos": pos, "unit_remap": remap, "kept": len(new_pos),
-            "n_kept_units": nxt}
+    out = {"unit_id": unit_id, "pos": pos, "unit_remap": remap, "kept": len(new_pos),
+           "n_kept_units": nxt}
+    if rope is not None:
+        from .omnipick import to_f64
+        from .rope import shift_keys
+        old = np.asarray(pos_in, np.int64)
+        shift = np.where(unit_id >= 0, pos - old, 0)
+        out["k_f64"] = shift_keys(to_f64(k, rope["dtype"]), shift, rope["base"], rope["dims"],
+                                  rope["style"])
+    return out
 
 
 def place_chunk(unit_id, chunk_len: int, cap: int) -> int:

@@ -452,25 +452,39 @@ size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units) {
   return omnitide::evict_workspace_bytes(n_seg, n_units);
 }
 
-int omnitide_evict_native(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
-                          const uint8_t* keep, const int32_t* keep_len, const int32_t* unit_len,
-                          int n_units, int32_t* unit_remap, int32_t* kept_tokens,
-                          int32_t* n_kept_units, int32_t* span, void* workspace,
-                          size_t workspace_bytes, int32_t* d_status, void* stream) {
+namespace {
+
+int evict_impl(int n_seg, int cap, int32_t* unit_id, int32_t* pos, const uint8_t* keep,
+               const int32_t* keep_len, const int32_t* unit_len, int n_units, void* k, int dtype,
+               int n_kv_heads, int head_dim, bool rope, double rope_base, int rope_dims,
+               int rope_style, int32_t* unit_remap, int32_t* kept_tokens, int32_t* n_kept_units,
+               int32_t* span, void* workspace, size_t workspace_bytes, int32_t* d_status,
+               void* stream) {
   if (!all_set({unit_len, unit_remap, kept_tokens, n_kept_units, span}) ||
       (keep == nullptr && keep_len == nullptr))
     return OMNITIDE_E_NULL;
   if (cap > 0 && !all_set({unit_id, pos})) return OMNITIDE_E_NULL;
+  if (rope && cap > 0 && k == nullptr) return OMNITIDE_E_NULL;
+  const int eb = rope ? elt_bytes(dtype) : 2;
+  if (eb == 0) return OMNITIDE_E_DTYPE;
+  if (rope && (!row_ok(n_kv_heads, head_dim) ||
+               !(rope_style == OMNITIDE_ROPE_HALF || rope_style == OMNITIDE_ROPE_INTERLEAVED) ||
+               rope_dims < 2 || rope_dims % 2 != 0 || rope_dims > head_dim ||
+               (rope_style == OMNITIDE_ROPE_HALF && (rope_dims / 2) % (16 / eb) != 0) ||
+               !(std::isfinite(rope_base) && rope_base > 1.0)))
+    return OMNITIDE_E_SHAPE;
   if (n_seg < 1 || n_seg > kMaxGridY || cap < 0 || cap > omnitide::native_max_cap() ||
       n_units < 1 || n_units > OMNITIDE_MAX_UNITS)
     return OMNITIDE_E_SHAPE;
-  const size_t need = omnitide::evict_workspace_bytes(n_seg, n_units);
+  const size_t need = rope ? omnitide::evict_rope_workspace_bytes(n_seg, n_units, cap)
+                           : omnitide::evict_workspace_bytes(n_seg, n_units);
   if (workspace == nullptr || workspace_bytes < need) return OMNITIDE_E_WORKSPACE;
   const size_t slots = static_cast<size_t>(n_seg) * cap;
   const size_t units = static_cast<size_t>(n_seg) * n_units;
+  const size_t kbytes = rope ? slots * n_kv_heads * head_dim * eb : 0;
   if (any_alias({{unit_id, slots * 4}, {pos, slots * 4}, {unit_remap, units * 4},
                  {kept_tokens, n_seg * 4ull}, {n_kept_units, n_seg * 4ull}, {span, n_seg * 4ull},
-                 {workspace, need}, {d_status, 4}},
+                 {workspace, need}, {d_status, 4}, {k, kbytes}},
                 {{keep, keep_len ? 0 : units}, {keep_len, units * 4}, {unit_len, units * 4}}))
     return OMNITIDE_E_ALIAS;
   omnitide::EvictArgs a;
@@ -488,7 +502,45 @@ int omnitide_evict_native(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
   a.span = span;
   a.workspace = workspace;
   a.d_status = d_status;
+  if (rope) {
+    a.k = k;
+    a.dtype = dtype;
+    a.n_kv_heads = n_kv_heads;
+    a.head_dim = head_dim;
+    a.rope_base = rope_base;
+    a.rope_dims = rope_dims;
+    a.rope_half = rope_style == OMNITIDE_ROPE_HALF;
+  }
   return hip_status(omnitide::launch_evict(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+int omnitide_evict_native(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
+                          const uint8_t* keep, const int32_t* keep_len, const int32_t* unit_len,
+                          int n_units, int32_t* unit_remap, int32_t* kept_tokens,
+                          int32_t* n_kept_units, int32_t* span, void* workspace,
+                          size_t workspace_bytes, int32_t* d_status, void* stream) {
+  return evict_impl(n_seg, cap, unit_id, pos, keep, keep_len, unit_len, n_units, nullptr, 0, 0, 0,
+                    false, 0.0, 0, 0, unit_remap, kept_tokens, n_kept_units, span, workspace,
+                    workspace_bytes, d_status, stream);
+}
+
+size_t omnitide_evict_native_rope_workspace_bytes(int n_seg, int n_units, int cap) {
+  if (n_seg < 1 || n_units < 1 || cap < 0) return 0;
+  return omnitide::evict_rope_workspace_bytes(n_seg, n_units, cap);
+}
+
+int omnitide_evict_native_rope(int n_seg, int cap, int32_t* unit_id, int32_t* pos,
+                               const uint8_t* keep, const int32_t* keep_len,
+                               const int32_t* unit_len, int n_units, void* k, int dtype,
+                               int n_kv_heads, int head_dim, double rope_base, int rope_dims,
+                               int rope_style, int32_t* unit_remap, int32_t* kept_tokens,
+                               int32_t* n_kept_units, int32_t* span, void* workspace,
+                               size_t workspace_bytes, int32_t* d_status, void* stream) {
+  return evict_impl(n_seg, cap, unit_id, pos, keep, keep_len, unit_len, n_units, k, dtype,
+                    n_kv_heads, head_dim, true, rope_base, rope_dims, rope_style, unit_remap,
+                    kept_tokens, n_kept_units, span, workspace, workspace_bytes, d_status, stream);
 }
 
 size_t omnitide_pack_suffix_workspace_bytes(int dtype, int n_seg, int cap, int n_kv_heads,

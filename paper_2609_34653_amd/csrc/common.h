@@ -32,6 +32,18 @@ __device__ inline uint32_t wave_sum_u32(uint32_t v) {
   return v;
 }
 
+// Byte arrays walked in 16-byte aligned blocks (absolute addresses): a block that holds a byte
+// of the array is read whole, and its bytes outside the caller's range are ignored.  An aligned
+// block never crosses a page, so the block of a valid byte is always mapped.
+__device__ inline uintptr_t block16_floor(const uint8_t* p) {
+  return reinterpret_cast<uintptr_t>(p) & ~static_cast<uintptr_t>(15);
+}
+__device__ inline void load_block16(uintptr_t addr, uint8_t (&b)[16]) {
+  const u32x4 w = *reinterpret_cast<const u32x4*>(addr);
+#pragma unroll
+  for (int j = 0; j < 16; ++j) b[j] = static_cast<uint8_t>(w[j >> 2] >> (8 * (j & 3)));
+}
+
 template <typename T>
 __device__ inline T readlane(T v, int lane) {
   return static_cast<T>(__builtin_amdgcn_readlane(static_cast<int>(v), lane));

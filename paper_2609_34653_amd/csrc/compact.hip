@@ -10,9 +10,9 @@
 // kernel; beyond, a plan kernel (1024 threads) writes it to the workspace together with, for
 // every destination tile, the rank of the unit holding the tile's first row.
 // Mask: a count kernel (one wave per unit) gives each unit its kept count, the plan kernel
-// scans those, and a map kernel (one wave per unit, 16 consecutive slots per lane, an in-lane
-// count plus one wave scan per 1,024 slots) writes each kept slot's destination row, its tags
-// and its position shift.
+// scans those, and a map kernel (one wave per unit, one aligned 16-byte block of the mask per
+// lane, an in-lane count plus one wave scan per 1,024 slots) writes each kept slot's
+// destination row, its tags and its position shift.
 // Copy: one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
 // source slots (binary search over the LDS table, or a short forward walk from the workspace
 // hint), tags are written, then every thread moves 16-byte vectors of the K and V rows.  Rows
@@ -435,46 +435,19 @@ hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
 // type (round to nearest even).  One workgroup per 16-row destination tile; the tile's cos/sin
 // table (rows x rot_dims/2) is built in LDS once and shared by all heads.
 constexpr int kMaxHalfRot = 64;     // rot_dims <= head_dim <= 128
+constexpr double kTwoPi = 6.283185307179586476925286766559;
 
-template <int EB, bool HALF, bool FUSED>
-__global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
-    const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
-    int n_kv_heads, int head_dim, const uint8_t* __restrict__ mod_src,
-    const int32_t* __restrict__ pos_src, const uint8_t* __restrict__ k_chunk,
-    const uint8_t* __restrict__ v_chunk, const uint8_t* __restrict__ chunk_mod,
-    const int32_t* __restrict__ chunk_unit, int chunk_len, uint8_t* __restrict__ k_dst,
-    uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
-    uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
-    int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
-    const uint8_t* __restrict__ ws, double rope_base, int rot_dims, FusedPlanArgs fp) {
-  constexpr int EPC = 16 / EB;                    // elements per 16-byte chunk
-  __shared__ int32_t src_row[kTile];
-  __shared__ int32_t shift_row[kTile];
-  __shared__ double theta[kMaxHalfRot];
-  __shared__ float2 cs[kTile][kMaxHalfRot];
-  __shared__ TilePlan<FUSED> plan;
-  const int seg = blockIdx.y;
-  const int t = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int half = rot_dims / 2;
-  if (tid < half) theta[tid] = pow(rope_base, -2.0 * tid / rot_dims);
-  int nctx;
-  const TilePlan<true>* pp = nullptr;
-  if constexpr (FUSED) {
-    plan_in_lds(seg, n_units, chunk_len, cap_dst, fp, plan);
-    nctx = plan.kept + chunk_len;
-    if (nctx > cap_dst) nctx = 0;
-    pp = &plan;
-  } else {
-    nctx = n_ctx_g[seg];
-  }
-  const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
-                                 pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, shift_row, pp, fp.mapped);
-  if (nrows == 0) return;
-  const int r0 = t * kTile;
-  constexpr double kTwoPi = 6.283185307179586476925286766559;
-  for (int idx = tid; idx < nrows * half; idx += kCopyThreads) {
+// theta_j = base^(-2j / rot_dims) for j < rot_dims / 2, into LDS.
+__device__ inline void rope_thetas(double* theta, double rope_base, int rot_dims) {
+  if (static_cast<int>(threadIdx.x) < rot_dims / 2)
+    theta[threadIdx.x] = pow(rope_base, -2.0 * static_cast<int>(threadIdx.x) / rot_dims);
+}
+
+// cos / sin of shift * theta_j for each of the tile's rows: the angle reduced modulo 2 pi in
+// double precision, then a float sine and cosine (rows with shift 0: exactly (1, 0)).
+__device__ inline void rope_table(int nrows, int half, const int32_t* shift_row,
+                                  const double* theta, float2 (*cs)[kMaxHalfRot]) {
+  for (int idx = threadIdx.x; idx < nrows * half; idx += kCopyThreads) {
     const int row = idx / half, j = idx % half;
     const int sh = shift_row[row];
     float c = 1.f, sn = 0.f;
@@ -485,29 +458,21 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     }
     cs[row][j] = make_float2(c, sn);
   }
-  __syncthreads();
+}
 
-  const int row_bytes = n_kv_heads * head_dim * EB;
-  const int row_vecs = row_bytes / 16;
-  const size_t src_base = static_cast<size_t>(seg) * n_slots;
-  const size_t chunk_base = static_cast<size_t>(seg) * chunk_len;
-  const size_t dst_base = static_cast<size_t>(seg) * cap_dst;
-  auto row_src = [&](const uint8_t* pool, const uint8_t* chunk, int row) {
-    const int s = src_row[row];
-    return s >= 0 ? pool + (src_base + s) * row_bytes
-                  : chunk + (chunk_base + (-1 - s)) * row_bytes;
-  };
-  // V rows: verbatim.
-  for (int f = tid; f < nrows * row_vecs; f += kCopyThreads) {
-    const int row = f / row_vecs, vec = f % row_vecs;
-    const u32x4 x = __builtin_nontemporal_load(
-        reinterpret_cast<const u32x4*>(row_src(v_src, v_chunk, row)) + vec);
-    __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(v_dst + (dst_base + r0 + row) *
-                                                            row_bytes) + vec);
-  }
-  // K rows: work items per head.  HALF: item i < rot_dims/(2 EPC) is the chunk pair (i, i +
-  // rot_dims/(2 EPC)); the remaining items are the unrotated chunks past rot_dims.  Otherwise
-  // every chunk is one item whose dimension pairs below rot_dims rotate.
+// K rows of a tile: row r is read through src(r) and written through dst(r) (byte pointers to
+// the row); each pair (x, y) of its first rot_dims dimensions per head turns by the row's
+// angle, (x cos - y sin, x sin + y cos) in float, rounded to the storage type.  IN_PLACE
+// (src == dst): rows with shift 0 and dimensions past rot_dims are left alone; otherwise they
+// are copied bit for bit.  HALF: work item i < rot_dims/(2 EPC) of a head is the chunk pair
+// (i, i + rot_dims/(2 EPC)), the remaining items the chunks past rot_dims; else every chunk is
+// one item whose dimension pairs below rot_dims turn.
+template <int EB, bool HALF, bool IN_PLACE, class SrcF, class DstF>
+__device__ inline void rope_rows(int nrows, int n_kv_heads, int head_dim, int rot_dims,
+                                 const int32_t* shift_row, const float2 (*cs)[kMaxHalfRot],
+                                 SrcF src_of, DstF dst_of) {
+  constexpr int EPC = 16 / EB;                    // elements per 16-byte chunk
+  const int half = rot_dims / 2;
   const int chunks = head_dim / EPC;
   const int pair_items = HALF ? half / EPC : 0;
   const int items = HALF ? pair_items + (head_dim - rot_dims) / EPC : chunks;
@@ -533,16 +498,15 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     }
     return v;
   };
-  for (int w = tid; w < nrows * n_kv_heads * items; w += kCopyThreads) {
+  for (int w = threadIdx.x; w < nrows * n_kv_heads * items; w += kCopyThreads) {
     const int row = w / (n_kv_heads * items);
     const int rem = w % (n_kv_heads * items);
     const int hd = rem / items, it = rem % items;
-    const u32x4* src = reinterpret_cast<const u32x4*>(row_src(k_src, k_chunk, row)) +
-                       hd * chunks;
-    u32x4* dst = reinterpret_cast<u32x4*>(k_dst + (dst_base + r0 + row) * row_bytes) +
-                 hd * chunks;
+    const bool moved = shift_row[row] != 0;        // unmoved rows keep their bits
+    if (IN_PLACE && !moved) continue;
+    const u32x4* src = reinterpret_cast<const u32x4*>(src_of(row)) + hd * chunks;
+    u32x4* dst = reinterpret_cast<u32x4*>(dst_of(row)) + hd * chunks;
     const float2* tab = cs[row];
-    const bool moved = shift_row[row] != 0;        // unmoved rows are copied bit for bit
     if (HALF && it < pair_items) {
       const int ca = it, cb = it + pair_items;
       u32x4 va = __builtin_nontemporal_load(src + ca), vb = __builtin_nontemporal_load(src + cb);
@@ -564,8 +528,10 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
       __builtin_nontemporal_store(vb, dst + cb);
     } else {
       const int c = HALF ? 2 * pair_items + (it - pair_items) : it;
+      const bool turns = !HALF && moved && c * EPC < rot_dims;
+      if (IN_PLACE && !turns) continue;            // nothing in this chunk changes
       u32x4 v = __builtin_nontemporal_load(src + c);
-      if (!HALF && moved && c * EPC < rot_dims) {
+      if (turns) {
         float f[EPC];
         unpack(v, f);
 #pragma unroll
@@ -583,6 +549,100 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
       __builtin_nontemporal_store(v, dst + c);
     }
   }
+}
+
+// Copy with rotary re-encoding of the moved keys (paper: Applying the retention plan -- the
+// position of each retained token drops by the deleted tokens before it, and the cached keys
+// are re-rotated by that shift).  V rows, chunk rows and unshifted rows are copied unchanged.
+// One workgroup per 16-row destination tile; the tile's cos/sin table (rows x rot_dims/2) is
+// built in LDS once and shared by all heads.
+template <int EB, bool HALF, bool FUSED>
+__global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
+    const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
+    int n_kv_heads, int head_dim, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, const uint8_t* __restrict__ k_chunk,
+    const uint8_t* __restrict__ v_chunk, const uint8_t* __restrict__ chunk_mod,
+    const int32_t* __restrict__ chunk_unit, int chunk_len, uint8_t* __restrict__ k_dst,
+    uint8_t* __restrict__ v_dst, int cap_dst, int n_units, int32_t* __restrict__ uid_dst,
+    uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
+    const uint8_t* __restrict__ ws, double rope_base, int rot_dims, FusedPlanArgs fp) {
+  __shared__ int32_t src_row[kTile];
+  __shared__ int32_t shift_row[kTile];
+  __shared__ double theta[kMaxHalfRot];
+  __shared__ float2 cs[kTile][kMaxHalfRot];
+  __shared__ TilePlan<FUSED> plan;
+  const int seg = blockIdx.y;
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x;
+  rope_thetas(theta, rope_base, rot_dims);
+  int nctx;
+  const TilePlan<true>* pp = nullptr;
+  if constexpr (FUSED) {
+    plan_in_lds(seg, n_units, chunk_len, cap_dst, fp, plan);
+    nctx = plan.kept + chunk_len;
+    if (nctx > cap_dst) nctx = 0;
+    pp = &plan;
+  } else {
+    nctx = n_ctx_g[seg];
+  }
+  const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
+                                 pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
+                                 src_of_dst, ws, src_row, shift_row, pp, fp.mapped);
+  if (nrows == 0) return;
+  const int r0 = t * kTile;
+  rope_table(nrows, rot_dims / 2, shift_row, theta, cs);
+  __syncthreads();
+
+  const int row_bytes = n_kv_heads * head_dim * EB;
+  const int row_vecs = row_bytes / 16;
+  const size_t src_base = static_cast<size_t>(seg) * n_slots;
+  const size_t chunk_base = static_cast<size_t>(seg) * chunk_len;
+  const size_t dst_base = static_cast<size_t>(seg) * cap_dst;
+  auto row_src = [&](const uint8_t* pool, const uint8_t* chunk, int row) {
+    const int s = src_row[row];
+    return s >= 0 ? pool + (src_base + s) * row_bytes
+                  : chunk + (chunk_base + (-1 - s)) * row_bytes;
+  };
+  // V rows: verbatim.
+  for (int f = tid; f < nrows * row_vecs; f += kCopyThreads) {
+    const int row = f / row_vecs, vec = f % row_vecs;
+    const u32x4 x = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x4*>(row_src(v_src, v_chunk, row)) + vec);
+    __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(v_dst + (dst_base + r0 + row) *
+                                                            row_bytes) + vec);
+  }
+  rope_rows<EB, HALF, false>(
+      nrows, n_kv_heads, head_dim, rot_dims, shift_row, cs,
+      [&](int row) { return row_src(k_src, k_chunk, row); },
+      [&](int row) { return k_dst + (dst_base + r0 + row) * row_bytes; });
+}
+
+// In-place rotary adjustment of the keys that stay in their slots while their position shifts
+// (native eviction): one workgroup per 16-slot tile of the pool; shift_g holds each slot's
+// position change (0: empty, evicted or unmoved; such rows are not touched).
+template <int EB, bool HALF>
+__global__ __launch_bounds__(kCopyThreads) void rope_in_place_kernel(
+    uint8_t* __restrict__ k, int cap, int n_kv_heads, int head_dim,
+    const int32_t* __restrict__ shift_g, double rope_base, int rot_dims) {
+  __shared__ int32_t shift_row[kTile];
+  __shared__ double theta[kMaxHalfRot];
+  __shared__ float2 cs[kTile][kMaxHalfRot];
+  const int seg = blockIdx.y;
+  const int r0 = blockIdx.x * kTile;
+  const int nrows = min(kTile, cap - r0);
+  const int tid = threadIdx.x;
+  const int sh = tid < nrows ? shift_g[static_cast<size_t>(seg) * cap + r0 + tid] : 0;
+  if (tid < kTile) shift_row[tid] = sh;
+  rope_thetas(theta, rope_base, rot_dims);
+  if (__syncthreads_or(sh != 0) == 0) return;     // nothing in this tile moves
+  rope_table(nrows, rot_dims / 2, shift_row, theta, cs);
+  __syncthreads();
+  const size_t row_bytes = static_cast<size_t>(n_kv_heads) * head_dim * EB;
+  uint8_t* base = k + (static_cast<size_t>(seg) * cap + r0) * row_bytes;
+  auto row_at = [&](int row) { return base + row * row_bytes; };
+  rope_rows<EB, HALF, true>(nrows, n_kv_heads, head_dim, rot_dims, shift_row, cs, row_at,
+                            row_at);
 }
 
 template <int EB, bool HALF, bool FUSED>
@@ -625,12 +685,14 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_count_kernel(
   uint32_t c = 0;
   if (unit_in_pool(n, f, n_slots)) {
     const uint8_t* m = mask_g + static_cast<size_t>(seg) * n_slots;
-    for (int s0 = f + kUnitPer * lane; s0 < f + n; s0 += kUnitPer * kWave) {
-      uint8_t b[kUnitPer];
+    const uintptr_t end = reinterpret_cast<uintptr_t>(m + f + n);
+    for (uintptr_t blk = block16_floor(m + f) + kUnitPer * static_cast<uintptr_t>(lane);
+         blk < end; blk += kUnitPer * kWave) {
+      const int s0 = static_cast<int>(static_cast<intptr_t>(blk) - reinterpret_cast<intptr_t>(m));
+      uint8_t b[16];
+      load_block16(blk, b);
 #pragma unroll
-      for (int j = 0; j < kUnitPer; ++j) b[j] = s0 + j < f + n ? m[s0 + j] : 0;
-#pragma unroll
-      for (int j = 0; j < kUnitPer; ++j) c += b[j] != 0 ? 1u : 0u;
+      for (int j = 0; j < kUnitPer; ++j) c += (s0 + j >= f && s0 + j < f + n && b[j] != 0);
     }
     c = wave_sum_u32(c);
   } else if (n > 0 && lane == 0) {
@@ -663,13 +725,19 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
   const size_t sb = static_cast<size_t>(seg) * n_slots;
   const size_t db = static_cast<size_t>(seg) * cap_dst;
   const uint8_t* m = mask_g + sb;
+  const uintptr_t end = reinterpret_cast<uintptr_t>(m + f + n);
   int carry = 0;                                  // kept slots of the unit before the step
-  for (int c = 0; c < n; c += P * kWave) {
-    const int s0 = f + c + P * lane;
+  for (uintptr_t c = block16_floor(m + f); c < end; c += P * kWave) {
+    const uintptr_t blk = c + P * static_cast<uintptr_t>(lane);
+    const int s0 = static_cast<int>(static_cast<intptr_t>(blk) - reinterpret_cast<intptr_t>(m));
     bool keep[P];
     int nk = 0;
+    {
+      uint8_t b[16] = {};
+      if (blk < end) load_block16(blk, b);
 #pragma unroll
-    for (int j = 0; j < P; ++j) keep[j] = s0 + j < f + n && m[s0 + j] != 0;
+      for (int j = 0; j < P; ++j) keep[j] = s0 + j >= f && s0 + j < f + n && b[j] != 0;
+    }
 #pragma unroll
     for (int j = 0; j < P; ++j) nk += keep[j] ? 1 : 0;
     const int incl = wave_inclusive_scan(nk);
@@ -693,6 +761,23 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
 }
 
 }  // namespace
+
+hipError_t launch_rope_in_place(void* k, int dtype, int n_seg, int cap, int n_kv_heads,
+                                int head_dim, const int32_t* shift, double rope_base,
+                                int rope_dims, bool rope_half, hipStream_t stream) {
+  const dim3 grid((cap + kTile - 1) / kTile, n_seg);
+  uint8_t* kp = static_cast<uint8_t*>(k);
+#define OMNITIDE_ROPE_IP(EB, HALF)                                                          \
+  hipLaunchKernelGGL((rope_in_place_kernel<EB, HALF>), grid, dim3(kCopyThreads), 0, stream, \
+                     kp, cap, n_kv_heads, head_dim, shift, rope_base, rope_dims)
+  if (dtype == OMNITIDE_BF16) {
+    if (rope_half) OMNITIDE_ROPE_IP(2, true); else OMNITIDE_ROPE_IP(2, false);
+  } else {
+    if (rope_half) OMNITIDE_ROPE_IP(4, true); else OMNITIDE_ROPE_IP(4, false);
+  }
+#undef OMNITIDE_ROPE_IP
+  return hipGetLastError();
+}
 
 size_t compact_workspace_bytes(int n_seg, int n_units, int cap_dst) {
   return ws_layout(n_units, cap_dst).seg_bytes * static_cast<size_t>(n_seg);

@@ -99,6 +99,12 @@ struct EvictArgs {
   int32_t* span;
   void* workspace;
   int32_t* d_status;
+  // rotary adjustment of the keys that stay (off when rope_dims == 0)
+  void* k = nullptr;
+  int dtype = 0, n_kv_heads = 0, head_dim = 0;
+  double rope_base = 0.0;
+  int rope_dims = 0;
+  bool rope_half = true;
 };
 struct SuffixArgs {
   int n_seg, cap, row_bytes, page_size, min_pages;
@@ -133,6 +139,11 @@ struct PlaceArgs {
 int native_max_cap();
 size_t place_workspace_bytes(int n_seg, int cap);
 size_t evict_workspace_bytes(int n_seg, int n_units);
+size_t evict_rope_workspace_bytes(int n_seg, int n_units, int cap);
+// Keys of the slots whose position changes (shift != 0) re-rotated in place by that change.
+hipError_t launch_rope_in_place(void* k, int dtype, int n_seg, int cap, int n_kv_heads,
+                                int head_dim, const int32_t* shift, double rope_base,
+                                int rope_dims, bool rope_half, hipStream_t stream);
 size_t suffix_workspace_bytes(int n_seg, int cap, int row_bytes);
 hipError_t launch_evict(const EvictArgs& a, hipStream_t stream);
 hipError_t launch_pack_suffix(const SuffixArgs& a, hipStream_t stream);

@@ -127,10 +127,12 @@ __device__ inline void load_bitmap(const uint32_t* __restrict__ bits_g, uint32_t
   }
   __syncthreads();
 }
+// shift_g (optional, [n_seg][cap]): each slot's position change (0 for slots that are empty,
+// evicted or keep their position), for the rotary adjustment of the keys that stay.
 __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
     int32_t* __restrict__ uid_g, int32_t* __restrict__ pos_g, int cap, int n_units,
     const UnitRec* __restrict__ table, const int32_t* __restrict__ len_g,
-    int32_t* __restrict__ span_g, int32_t* __restrict__ status) {
+    int32_t* __restrict__ span_g, int32_t* __restrict__ shift_g, int32_t* __restrict__ status) {
   const int seg = blockIdx.y;
   const int s = blockIdx.x * kCopyThreads + threadIdx.x;
   const size_t sb = static_cast<size_t>(seg) * cap;
@@ -138,6 +140,7 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
   int end = 0;                                    // slot + 1 if this slot stays occupied
   if (s < cap) {
     const int u = uid_g[sb + s];
+    int shift = 0;
     if (u >= 0) {
       bool bad = u >= n_units;
       if (!bad) {
@@ -148,6 +151,7 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
         if (!bad && r < rec.kl) {
           uid_g[sb + s] = rec.rank;
           pos_g[sb + s] = p - rec.del;
+          shift = -rec.del;
           end = s + 1;
         } else if (!bad) {
           uid_g[sb + s] = -1;
@@ -156,6 +160,7 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
       }
       if (bad) set_status(status, OMNITIDE_E_TAGS);
     }
+    if (shift_g != nullptr) shift_g[sb + s] = shift;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) end = max(end, __shfl_xor(end, off, kWave));
@@ -402,6 +407,11 @@ size_t evict_workspace_bytes(int n_seg, int n_units) {
   return static_cast<size_t>(n_seg) * n_units * sizeof(UnitRec);
 }
 
+size_t evict_rope_workspace_bytes(int n_seg, int n_units, int cap) {
+  return align256(evict_workspace_bytes(n_seg, n_units)) +
+         static_cast<size_t>(n_seg) * cap * sizeof(int32_t);
+}
+
 hipError_t launch_evict(const EvictArgs& a, hipStream_t stream) {
   UnitRec* table = static_cast<UnitRec*>(a.workspace);
   hipLaunchKernelGGL(evict_plan_kernel, dim3(a.n_seg), dim3(kNatThreads), 0, stream, a.keep,
@@ -409,10 +419,19 @@ hipError_t launch_evict(const EvictArgs& a, hipStream_t stream) {
                      a.n_kept_units, a.span);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.cap == 0) return hipSuccess;
+  // with rotary adjustment: the slots' shifts go to the workspace after the unit table
+  int32_t* shift = a.rope_dims > 0 ? reinterpret_cast<int32_t*>(
+                                         static_cast<uint8_t*>(a.workspace) +
+                                         align256(evict_workspace_bytes(a.n_seg, a.n_units)))
+                                   : nullptr;
   const dim3 grid((a.cap + kCopyThreads - 1) / kCopyThreads, a.n_seg);
   hipLaunchKernelGGL(evict_apply_kernel, grid, dim3(kCopyThreads), 0, stream, a.unit_id, a.pos,
-                     a.cap, a.n_units, table, a.unit_len, a.span, a.d_status);
-  return hipGetLastError();
+                     a.cap, a.n_units, table, a.unit_len, a.span, shift, a.d_status);
+  e = hipGetLastError();
+  if (e != hipSuccess || shift == nullptr) return e;
+  return launch_rope_in_place(a.k, a.dtype, a.n_seg, a.cap, a.n_kv_heads, a.head_dim, shift,
+                              a.rope_base, a.rope_dims, a.rope_half, stream);
 }
 
 static size_t bitmap_bytes(int n_seg, int cap) {

@@ -1,6 +1,7 @@
 // OmniPick span plan in three kernels.
 //
-// 1. Census (one wave per unit).  The wave walks its unit's slots 1024 at a time (16 per lane) and
+// 1. Census (one wave per unit).  The wave walks its unit's slots 1024 at a time (one aligned
+//    16-byte block of tags per lane) and
 //    finds where each span starts: at the unit's first slot and wherever the tag changes.  A
 //    running maximum of the start slots (wave scan plus a carry across chunks) gives every
 //    token its place in its span.  Each slot gets a code in the workspace: marker tokens and
@@ -76,17 +77,26 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
     }
     return;
   }
-  const uint8_t* mod = mod_g + static_cast<size_t>(seg) * n_slots;
+  // aligned 16-slot blocks of the segment's tag bytes (slot s at seg_tags + s)
+  const uint8_t* seg_tags = mod_g + static_cast<size_t>(seg) * n_slots;
+  const uintptr_t blk0 = block16_floor(seg_tags + f);
+  const uintptr_t end = reinterpret_cast<uintptr_t>(seg_tags + f + n);
   int carry_tag = -1;      // tag of the slot before the step (-1 at the unit's start)
   int carry_start = f;     // first slot of the span that slot belongs to
   int carry_text = 0;      // the unit's text tokens before the step
   int sinks = 0;
   bool bad = false;
-  for (int c = 0; c < n; c += P * kWave) {
-    const int s0 = f + c + P * lane;
+  for (uintptr_t c = blk0; c < end; c += P * kWave) {
+    const uintptr_t b = c + P * static_cast<uintptr_t>(lane);   // this lane's block
+    const int s0 = static_cast<int>(static_cast<intptr_t>(b) -
+                                    reinterpret_cast<intptr_t>(seg_tags));
     int m[P];
+    {
+      uint8_t raw[16] = {};
+      if (b < end) load_block16(b, raw);
 #pragma unroll
-    for (int j = 0; j < P; ++j) m[j] = s0 + j < f + n ? mod[s0 + j] : -1;   // loads first
+      for (int j = 0; j < P; ++j) m[j] = (s0 + j >= f && s0 + j < f + n) ? raw[j] : -1;
+    }
     int prev = __shfl_up(m[P - 1], 1, kWave);
     if (lane == 0) prev = carry_tag;
     int run = -1, nt = 0;

@@ -33,7 +33,8 @@ EXPORTS = ("omnitide_score_units", "omnitide_select_units", "omnitide_compact_kv
            "omnitide_compact_workspace_bytes", "omnitide_chunk_attn",
            "omnitide_chunk_attn_noalloc",
            "omnitide_attn_workspace_bytes", "omnitide_span_attn", "omnitide_evict_native",
-           "omnitide_evict_native_workspace_bytes", "omnitide_pack_suffix",
+           "omnitide_evict_native_workspace_bytes", "omnitide_evict_native_rope",
+           "omnitide_evict_native_rope_workspace_bytes", "omnitide_pack_suffix",
            "omnitide_pack_suffix_workspace_bytes", "omnitide_place_chunk",
            "omnitide_place_chunk_workspace_bytes",
            "omnitide_span_attn_workspace_bytes", "omnitide_decode_attn",
@@ -92,6 +93,11 @@ def lib() -> ctypes.CDLL:
                                             _SZ, _P, _P]
         L.omnitide_evict_native_workspace_bytes.argtypes = [_I, _I]
         L.omnitide_evict_native_workspace_bytes.restype = _SZ
+        L.omnitide_evict_native_rope.argtypes = [_I, _I, _P, _P, _P, _P, _P, _I, _P, _I, _I, _I,
+                                                 ctypes.c_double, _I, _I, _P, _P, _P, _P, _P,
+                                                 _SZ, _P, _P]
+        L.omnitide_evict_native_rope_workspace_bytes.argtypes = [_I, _I, _I]
+        L.omnitide_evict_native_rope_workspace_bytes.restype = _SZ
         L.omnitide_pack_suffix.argtypes = [_P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P,
                                            _P, _P, _P, _SZ, _P]
         L.omnitide_pack_suffix_workspace_bytes.argtypes = [_I, _I, _I, _I, _I]
@@ -113,7 +119,8 @@ def lib() -> ctypes.CDLL:
                      "omnitide_compact_kv_rope", "omnitide_compact_kv_spans",
                      "omnitide_plan_spans", "omnitide_chunk_attn",
                      "omnitide_chunk_attn_noalloc", "omnitide_span_attn",
-                     "omnitide_evict_native", "omnitide_pack_suffix", "omnitide_place_chunk",
+                     "omnitide_evict_native", "omnitide_evict_native_rope",
+                     "omnitide_pack_suffix", "omnitide_place_chunk",
                      "omnitide_decode_attn", "omnitide_decode_span_attn"):
             getattr(L, name).restype = _I
         _lib = L
@@ -491,6 +498,45 @@ def omnitide_evict_native(unit_id, pos, n_seg, n_units, unit_len, unit_remap, ke
                                        _ptr(workspace), workspace.numel(), _ptr(d_status),
                                        _stream(stream)), "omnitide_evict_native")
 
+
+
+def omnitide_evict_native_rope_workspace_bytes(n_seg, n_units, cap) -> int:
+    return int(lib().omnitide_evict_native_rope_workspace_bytes(n_seg, n_units, cap))
+
+
+def omnitide_evict_native_rope(unit_id, pos, k, n_seg, n_units, unit_len, unit_remap,
+                               kept_tokens, n_kept_units, span, workspace, rope_base, rope_dims,
+                               rope_style=ROPE_HALF, keep=None, keep_len=None, d_status=None,
+                               stream=None):
+    """Logical eviction in place plus the rotary adjustment, in place, of the keys k
+    ([n_seg, cap, H, d] bf16 or float32) whose positions shift."""
+    cap = unit_id.numel() // n_seg
+    nu = n_seg * n_units
+    ds, kcap, H, d = _pool_dims(k, "k")
+    if ds != n_seg or kcap != cap:
+        raise ValueError("k shape does not match the tags")
+    _need(k, "k", (torch.bfloat16, torch.float32))
+    _need(unit_id, "unit_id", I32, n_seg * cap)
+    _need(pos, "pos", I32, n_seg * cap)
+    if keep_len is not None:
+        _need(keep_len, "keep_len", I32, nu)
+    else:
+        _need(keep, "keep", U8, nu)
+    for t, nm in ((unit_len, "unit_len"), (unit_remap, "unit_remap")):
+        _need(t, nm, I32, nu)
+    for t, nm in ((kept_tokens, "kept_tokens"), (n_kept_units, "n_kept_units"), (span, "span")):
+        _need(t, nm, I32, n_seg)
+    _need(workspace, "workspace", U8)
+    if d_status is not None:
+        _need(d_status, "d_status", I32, 1)
+    _check(lib().omnitide_evict_native_rope(n_seg, cap, _ptr(unit_id), _ptr(pos),
+                                            _ptr(keep) if keep_len is None else None,
+                                            _ptr(keep_len), _ptr(unit_len), n_units, _ptr(k),
+                                            _kv_dtype(k), H, d, float(rope_base), int(rope_dims),
+                                            int(rope_style), _ptr(unit_remap), _ptr(kept_tokens),
+                                            _ptr(n_kept_units), _ptr(span), _ptr(workspace),
+                                            workspace.numel(), _ptr(d_status), _stream(stream)),
+           "omnitide_evict_native_rope")
 
 def omnitide_pack_suffix_workspace_bytes(dtype, n_seg, cap, n_kv_heads, head_dim) -> int:
     return int(lib().omnitide_pack_suffix_workspace_bytes(dtype, n_seg, cap, n_kv_heads,

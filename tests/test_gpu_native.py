@@ -428,3 +428,83 @@ def test_native_kernels_several_segments():
         want_k[s0:s0 + L] = storage_np(seg.k_chunk)
         assert np.array_equal(storage_np(k[si]), want_k)
         assert int(host(span)[si]) == oracle.span_of(want_uid)
+
+
+@pytest.mark.parametrize("cfg_name,plan,rope", [
+    ("history_80k", "whole", (1.0e6, 128, 0)),          # the benchmark's rotary setting
+    ("single_layer_8k", "prefix", (10000.0, 64, 0)),    # arbitrary kept prefixes, partial width
+    ("tiny_1p6k_f32", "prefix", (10000.0, 32, 1)),      # float32 keys, interleaved pairs
+])
+def test_evict_native_rope_parity(cfg_name, plan, rope):
+    """Eviction with the rotary adjustment: tags bit-exact, the keys of kept slots whose position
+    shifts re-rotated in place within the rotary bound (half a storage ulp plus 2^-21 of the
+    pair's length), every other key byte and all of V unchanged."""
+    from paper_2609_34653_amd import omnitide as ot
+    from tests.test_gpu_rope import pair_norm, ulp
+    cfg, lay, seg, g, h = native_state(cfg_name, plan=plan, seed_keep=31)
+    cap = len(h["uid"])
+    style = ("half", "interleaved")[rope[2]]
+    ws = torch.zeros(ot.omnitide_evict_native_rope_workspace_bytes(1, lay.n_units, cap),
+                     dtype=torch.uint8, device="cuda")
+    ot.omnitide_evict_native_rope(g["uid"], g["pos"], g["k"], 1, lay.n_units, g["len"],
+                                  g["remap"], g["kept"], g["nku"], g["span"], ws, rope[0],
+                                  rope[1], rope[2], keep_len=g["keep_len"], d_status=g["st"])
+    torch.cuda.synchronize()
+    assert int(host(g["st"])[0]) == 0
+    kl = np.minimum(np.maximum(h["keep_len"], 0), h["sc"]["len"])
+    ev = oracle.evict_logical(h["uid"], h["pos"], kl, lay.n_units, k=h["k"],
+                              rope=dict(base=rope[0], dims=rope[1], style=style, dtype=cfg.dtype))
+    assert np.array_equal(host(g["uid"]), ev["unit_id"])
+    assert np.array_equal(host(g["pos"]), ev["pos"])
+    assert int(host(g["kept"])[0]) == ev["kept"]
+    kd = storage_np(g["k"][0])
+    moved = (ev["unit_id"] >= 0) & (ev["pos"] != h["pos"])
+    assert moved.sum() > 1000 or cfg_name == "tiny_1p6k_f32" and moved.sum() > 100
+    assert np.array_equal(kd[~moved], h["k"][~moved])             # untouched rows: same bytes
+    assert np.array_equal(storage_np(g["v"][0]), h["v"])           # values carry no position
+    R = rope[1]
+    assert np.array_equal(kd[moved][..., R:], h["k"][moved][..., R:])
+    got = oracle.to_f64(kd[moved], cfg.dtype)[..., :R]
+    want = ev["k_f64"][moved][..., :R]
+    src = oracle.to_f64(h["k"][moved], cfg.dtype)
+    bound = 0.5 * ulp(want, cfg.dtype) + 2.0 ** -21 * pair_norm(src, R, style)[..., :R]
+    assert np.all(np.abs(got - want) <= bound)
+
+
+def test_evict_native_rope_then_span_attention_equals_compaction():
+    """On the 80K history: eviction with the rotary adjustment followed by attention over the
+    span gives what rotary compaction followed by chunk attention gives (same keys at the same
+    logical positions)."""
+    from paper_2609_34653_amd import omnitide as ot
+    from tests.test_gpu_parity import make_step, gpu_inputs
+    cfg, lay, seg, g, h = native_state("history_80k")
+    cap = len(h["uid"])
+    L = lay.chunk_len
+    rope = (1.0e6, 128, 0)
+    ws = torch.zeros(ot.omnitide_evict_native_rope_workspace_bytes(1, lay.n_units, cap),
+                     dtype=torch.uint8, device="cuda")
+    ot.omnitide_evict_native_rope(g["uid"], g["pos"], g["k"], 1, lay.n_units, g["len"],
+                                  g["remap"], g["kept"], g["nku"], g["span"], ws, *rope,
+                                  keep=g["keep"], d_status=g["st"])
+    ot.omnitide_place_chunk(g["k"], g["v"], g["uid"], g["mod"], g["pos"],
+                            seg.k_chunk.cuda()[None].contiguous(),
+                            seg.v_chunk.cuda()[None].contiguous(), dev(lay.chunk_modality),
+                            dev(lay.chunk_unit), g["kept"], g["nku"], i32([0]), g["span"],
+                            place_ws(cap), d_status=g["st"])
+    nb = ot.omnitide_span_attn_workspace_bytes(1, cap, L, cfg.n_q_heads, cfg.n_kv_heads,
+                                               cfg.head_dim)
+    out_n = torch.zeros(1, L, cfg.n_q_heads, cfg.head_dim, device="cuda")
+    ot.omnitide_span_attn(seg.q.cuda()[None].contiguous(), g["k"], g["v"], g["pos"], g["span"],
+                          g["kept"], cfg.scale, out_n,
+                          torch.zeros(nb, dtype=torch.uint8, device="cuda"), g["st"])
+    st = make_step(cfg, lay)
+    inp = gpu_inputs(lay, [seg])
+    st.score(inp["k_hist"], inp["unit_id"], inp["modality"])
+    st.select()
+    st.compact(inp["k_hist"], inp["v_hist"], inp["unit_id"], inp["modality"], inp["pos"],
+               inp["k_chunk"], inp["v_chunk"], inp["chunk_modality"], inp["chunk_unit"],
+               rope=rope)
+    st.attend(inp["q"], cfg.scale)
+    torch.cuda.synchronize()
+    assert int(host(g["st"])[0]) == 0 and int(host(st.d_status)[0]) == 0
+    assert np.abs(host(out_n) - host(st.out)).max() <= 2e-3

@@ -309,10 +309,11 @@ def test_span_step_with_rope(cfg_name, rope):
     check_span_segment(cfg, lay, seg, st, 0, p, rope=rope)
 
 
-@pytest.mark.parametrize("n_units_extra", [0, 600])
-def test_compaction_of_arbitrary_masks(n_units_extra):
+@pytest.mark.parametrize("n_units_extra,shift", [(0, 0), (600, 0), (0, 5)])
+def test_compaction_of_arbitrary_masks(n_units_extra, shift):
     """Any per-slot mask (bytes of empty slots set too, values other than 1) against the oracle;
-    with 600 extra slotless unit ids the compaction plans through the workspace."""
+    with 600 extra slotless unit ids the compaction plans through the workspace; the mask may
+    start at an odd address."""
     cfg = sg.CONFIG_BY_NAME["single_layer_8k"]
     stream = sg.make_stream(cfg, grammar=True)
     lay, seg = stream.layout, stream.segment(0)
@@ -325,9 +326,12 @@ def test_compaction_of_arbitrary_masks(n_units_extra):
     st = make_step(cfg, lay, cap_dst=lay.n_slots + lay.chunk_len, n_units=U)
     g = gpu_inputs(lay, [seg])
     st.score(g["k_hist"], g["unit_id"], g["modality"])
+    raw = torch.zeros(len(mask) + 32, dtype=torch.uint8, device="cuda")
+    mask_d = raw[shift:shift + len(mask)]
+    mask_d.copy_(dev(mask))
     st.compact_spans(g["k_hist"], g["v_hist"], g["unit_id"], g["modality"], g["pos"],
                      g["k_chunk"], g["v_chunk"], g["chunk_modality"], g["chunk_unit"],
-                     keep_slot=dev(mask))
+                     keep_slot=mask_d)
     torch.cuda.synchronize()
     assert int(host(st.d_status)[0]) == 0
     cp = oracle.compact_kv(storage_np(seg.k_hist), storage_np(seg.v_hist), lay.unit_id,
@@ -378,3 +382,34 @@ def test_whole_units_match_the_keep_flag_compaction():
     torch.cuda.synchronize()
     for k, v in ref.items():
         assert torch.equal(getattr(st, k), v), k
+
+
+@pytest.mark.parametrize("shift", [1, 7, 15])
+def test_byte_arrays_at_unaligned_addresses(shift):
+    """The tag and mask bytes are walked in 16-byte aligned blocks of absolute addresses: the
+    plan and the mask compaction give the same result for arrays starting at odd addresses."""
+    from paper_2609_34653_amd import omnitide as ot
+    rng = np.random.default_rng(40 + shift)
+    sc, modality = random_layout(rng, 300, hole_p=0.3)
+    n = len(modality)
+    p = dict(high=600, low=500, recent=150, sv=5, sa=2, tb=30)
+    want, wmask, wkept = oracle_plan(sc, modality, p)
+    raw = torch.zeros(n + 64, dtype=torch.uint8, device="cuda")
+    mod_odd = raw[shift:shift + n]
+    mod_odd.copy_(dev(np.asarray(modality, np.uint8)))
+    assert mod_odd.data_ptr() % 16 == shift % 16
+    U = len(sc["len"])
+    kl = torch.full((U,), -7, dtype=torch.int32, device="cuda")
+    ks_raw = torch.full((n + 64,), 7, dtype=torch.uint8, device="cuda")
+    ks = ks_raw[shift:shift + n]
+    kt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.zeros(ot.omnitide_plan_spans_workspace_bytes(1, n, U), dtype=torch.uint8,
+                     device="cuda")
+    ot.omnitide_plan_spans(i32(sc["len"]), i32(sc["first"]), i32(sc["last"]), i32(sc["flags"]),
+                           i32(sc["unit_id"]), mod_odd, 1, n, U, p["low"], p["high"],
+                           p["recent"], p["sv"], p["sa"], p["tb"], kl, ks, kt, ws, st)
+    torch.cuda.synchronize()
+    assert int(host(st)[0]) == 0
+    assert np.array_equal(host(kl), want) and np.array_equal(host(ks), wmask)
+    assert int(host(kt)[0]) == wkept

@@ -91,6 +91,33 @@ def test_eviction_then_packing_equals_compaction():
         assert np.array_equal(ev["unit_remap"], cp["unit_remap"])
 
 
+def test_eviction_rotary_adjustment_equals_compaction():
+    """Keys re-rotated at logical eviction (entries in place) equal, row for row, the keys the
+    compaction re-encodes for the same plan; evicted and empty slots keep their keys, and a
+    unit kept at its old positions (nothing deleted before it) is not rotated."""
+    rng = np.random.default_rng(22)
+    for trial in range(40):
+        U = int(rng.integers(1, 15))
+        uid, pos = random_native_pool(rng, U)
+        length = np.bincount(uid[uid >= 0], minlength=U)
+        kl = rng.integers(0, length + 2)
+        n = len(uid)
+        k = rng.standard_normal((n, 2, 8)).astype(np.float32)
+        rope = dict(base=10000.0, dims=8 if trial % 2 else 4,
+                    style="half" if trial % 3 else "interleaved", dtype="f32")
+        cp = oracle.compact_kv(k, k, uid, np.ones(n, np.uint8), pos, None, U,
+                               np.zeros((0, 2, 8), np.float32), np.zeros((0, 2, 8), np.float32),
+                               np.zeros(0, np.uint8), np.zeros(0, np.int64), n, 64, keep_len=kl,
+                               rope=rope)
+        ev = oracle.evict_logical(uid, pos, kl, U, k=k, rope=rope)
+        kept_slots = np.nonzero(ev["unit_id"] >= 0)[0]          # slot order = position order
+        assert np.array_equal(ev["k_f64"][kept_slots], cp["k_f64"][:cp["kept"]])
+        rest = np.setdiff1d(np.arange(n), kept_slots)
+        assert np.array_equal(ev["k_f64"][rest], k[rest].astype(np.float64))
+        same = kept_slots[ev["pos"][kept_slots] == pos[kept_slots]]
+        assert np.array_equal(ev["k_f64"][same], k[same].astype(np.float64))
+
+
 def test_suffix_cut_by_exhaustive_packing():
     """The cut equals the largest c whose actual packing (span measured after moving the rows)
     saves the threshold -- not via the closed-form packed span."""
