@@ -299,30 +299,37 @@ int omnitide_compact_kv_spans(const void* k_src, const void* v_src, int dtype, i
  * [0, n_ctx)).  For query position i in [0, chunk_len) and query head h:
  *   out[i][h] = sum_j softmax_j(scale * <q[i][h], k[j][g]>) v[j][g],  g = h / (n_q_heads/n_kv_heads)
  *   over keys j <= n_ctx - chunk_len + i (causal, anchored bottom-right).
- *   q      bf16 [n_seg][chunk_len][n_q_heads][head_dim]
- *   k, v   bf16 [n_seg][cap][n_kv_heads][head_dim]: the pools written by omnitide_compact_kv
- *          (the chunk's own keys are the last chunk_len rows before n_ctx)
+ *   q      [n_seg][chunk_len][n_q_heads][head_dim] of `dtype`
+ *   k, v   [n_seg][cap][n_kv_heads][head_dim] of `dtype`: the pools written by
+ *          omnitide_compact_kv (the chunk's own keys are the last chunk_len rows before n_ctx)
+ *   dtype  OMNITIDE_BF16, or OMNITIDE_F32: q, k and v are then rounded to bf16 (nearest even)
+ *          into the workspace first (all cap rows of k and v), and the bf16 kernels run on
+ *          the copies
  *   n_ctx  int32 [n_seg], device: rows in use; chunk_len <= n_ctx <= cap is required (device
  *          check: OMNITIDE_E_CAPACITY, the segment's output is then not written)
- *   out    float32 [n_seg][chunk_len][n_q_heads][head_dim]
- *   workspace  device scratch of omnitide_attn_workspace_bytes() bytes (split-KV partials)
+ *   out    [n_seg][chunk_len][n_q_heads][head_dim] of `out_dtype`: OMNITIDE_F32, or
+ *          OMNITIDE_BF16 (the float result rounded to nearest even)
+ *   workspace  device scratch of omnitide_attn_workspace_bytes(dtype, ...) bytes (split-KV
+ *          partials, and the bf16 copies for float32 inputs; may be NULL when that is 0)
  * Numerics: bf16 inputs, bf16 matrix-core products with fp32 accumulation, fp32 softmax.
  * Limits: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0; chunk_len >= 1; cap >= chunk_len.
  */
-int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
-                        int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
-                        int head_dim, float scale, float* out, void* workspace,
-                        size_t workspace_bytes, int32_t* d_status, void* stream);
+int omnitide_chunk_attn(const void* q, const void* k, const void* v, int dtype,
+                        const int32_t* n_ctx, int n_seg, int cap, int chunk_len, int n_q_heads,
+                        int n_kv_heads, int head_dim, float scale, void* out, int out_dtype,
+                        void* workspace, size_t workspace_bytes, int32_t* d_status,
+                        void* stream);
 
-size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
-                                     int n_kv_heads, int head_dim);
+size_t omnitide_attn_workspace_bytes(int dtype, int n_seg, int cap, int chunk_len,
+                                     int n_q_heads, int n_kv_heads, int head_dim);
 
 /*
  * omnitide_chunk_attn_noalloc -- omnitide_chunk_attn for callers that cannot allocate device
  * memory (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
  * the same kernels, with the split-KV partials in a fixed array inside the library instead of
- * a caller workspace.  Same arguments, results and errors as omnitide_chunk_attn without
- * workspace / workspace_bytes; the output is bitwise equal to omnitide_chunk_attn's.
+ * a caller workspace.  Same arguments, results and errors as omnitide_chunk_attn with bf16
+ * inputs (no dtype argument) and without workspace / workspace_bytes; the output is bitwise
+ * equal to omnitide_chunk_attn's.
  *   - The array holds OMNITIDE_NOALLOC_SCRATCH_BYTES bytes per device (allocated when the
  *     library's code is loaded on a device, kept until the process ends).  A shape whose
  *     omnitide_attn_workspace_bytes() exceeds it returns OMNITIDE_E_SCRATCH (host check,
@@ -337,7 +344,7 @@ size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_
 int omnitide_chunk_attn_noalloc(const void* q, const void* k, const void* v,
                                 const int32_t* n_ctx, int n_seg, int cap, int chunk_len,
                                 int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                                float* out, int32_t* d_status, void* stream);
+                                void* out, int out_dtype, int32_t* d_status, void* stream);
 
 /*
  * Native (logical-only) layout: the retained entries stay in their slots after eviction, the
@@ -441,6 +448,7 @@ size_t omnitide_place_chunk_workspace_bytes(int n_seg, int cap);
  *   q_pos0   int32 [n_seg], device: logical position of chunk query 0
  *   q, k, v, out, scale: as omnitide_chunk_attn.  The K/V bytes of empty slots are never used
  *   (they may hold anything, NaN included).
+ *   q, k, v are bf16 and out float32 (OMNITIDE_E_DTYPE is not used here).
  *   workspace  device scratch of omnitide_span_attn_workspace_bytes() bytes (always > 0).
  * skip_empty_tiles != 0: 64-slot tiles without an entry are skipped (kernels with tile
  * skipping); 0: every tile of the span is traversed, masked (kernels that traverse the physical

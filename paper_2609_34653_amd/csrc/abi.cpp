@@ -344,25 +344,36 @@ int omnitide_plan_spans(const int32_t* unit_len, const int32_t* unit_first_slot,
   return hip_status(omnitide::launch_plan_spans(a, static_cast<hipStream_t>(stream)));
 }
 
-size_t omnitide_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
-                                     int n_kv_heads, int head_dim) {
-  if (n_seg < 1 || cap < 1 || chunk_len < 1 || n_kv_heads < 1 || n_q_heads < n_kv_heads ||
-      n_q_heads % n_kv_heads != 0 || !(head_dim == 64 || head_dim == 128))
+size_t omnitide_attn_workspace_bytes(int dtype, int n_seg, int cap, int chunk_len,
+                                     int n_q_heads, int n_kv_heads, int head_dim) {
+  if (elt_bytes(dtype) == 0 || n_seg < 1 || cap < 1 || chunk_len < 1 || n_kv_heads < 1 ||
+      n_q_heads < n_kv_heads || n_q_heads % n_kv_heads != 0 ||
+      !(head_dim == 64 || head_dim == 128))
     return 0;
-  return omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
+  const size_t part =
+      omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
+  if (dtype == OMNITIDE_BF16) return part;
+  return omnitide::align256(part) +
+         omnitide::attn_cast_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim);
 }
 
 namespace {
 
 // Chunk attention over contiguous rows (key_pos == nullptr) or over a span with holes.
-int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
+// dtype: of q, k, v (float32 only for contiguous rows: cast to bf16 in the workspace);
+// out_dtype: of out (bf16 only for contiguous rows).
+int attn_impl(const void* q, const void* k, const void* v, int dtype, const int32_t* n_ctx,
               const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int chunk_len,
-              int n_q_heads, int n_kv_heads, int head_dim, float scale, float* out,
-              void* workspace, size_t workspace_bytes, int32_t* d_status, void* stream,
-              bool skip_empty = true, bool noalloc = false) {
+              int n_q_heads, int n_kv_heads, int head_dim, float scale, void* out,
+              int out_dtype, void* workspace, size_t workspace_bytes, int32_t* d_status,
+              void* stream, bool skip_empty = true, bool noalloc = false) {
   const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
   if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
+  const int eb = elt_bytes(dtype), ob = elt_bytes(out_dtype);
+  if (eb == 0 || ob == 0 || ((span || noalloc) && (dtype != OMNITIDE_BF16)) ||
+      (span && out_dtype != OMNITIDE_F32))
+    return OMNITIDE_E_DTYPE;
   if (n_seg < 1 || n_seg > kMaxGridY || chunk_len < 1 || n_kv_heads < 1 ||
       n_q_heads < n_kv_heads || n_q_heads % n_kv_heads != 0 ||
       !(head_dim == 64 || head_dim == 128) || !std::isfinite(scale) ||
@@ -370,21 +381,24 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
     return OMNITIDE_E_SHAPE;
   if (cap < chunk_len || (span && cap > omnitide::span_attn_max_cap()))
     return OMNITIDE_E_CAPACITY;
-  const size_t need =
+  size_t need =
       span ? omnitide::span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
                                                  head_dim)
            : omnitide::attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
                                             head_dim);
+  if (dtype == OMNITIDE_F32)
+    need = omnitide::align256(need) + omnitide::attn_cast_bytes(n_seg, cap, chunk_len,
+                                                                n_q_heads, n_kv_heads, head_dim);
   if (noalloc) {
     if (need > OMNITIDE_NOALLOC_SCRATCH_BYTES) return OMNITIDE_E_SCRATCH;
   } else if (need > 0 && (workspace == nullptr || workspace_bytes < need)) {
     return OMNITIDE_E_WORKSPACE;
   }
   const size_t qrows = static_cast<size_t>(n_seg) * chunk_len * n_q_heads;
-  const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * 2;
-  if (any_alias({{out, qrows * head_dim * 4}, {noalloc ? nullptr : workspace, need},
+  const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim * eb;
+  if (any_alias({{out, qrows * head_dim * ob}, {noalloc ? nullptr : workspace, need},
                  {d_status, 4}},
-                {{q, qrows * head_dim * 2}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull},
+                {{q, qrows * head_dim * eb}, {k, kv}, {v, kv}, {n_ctx, n_seg * 4ull},
                  {key_pos, static_cast<size_t>(n_seg) * cap * 4}, {q_pos0, n_seg * 4ull}}))
     return OMNITIDE_E_ALIAS;
   AttnArgs a;
@@ -400,6 +414,8 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
   a.head_dim = head_dim;
   a.scale = scale;
   a.out = out;
+  a.out_bf16 = out_dtype == OMNITIDE_BF16;
+  a.in_f32 = dtype == OMNITIDE_F32;
   a.workspace = need > 0 ? workspace : nullptr;
   a.d_status = d_status;
   a.key_pos = key_pos;
@@ -411,20 +427,23 @@ int attn_impl(const void* q, const void* k, const void* v, const int32_t* n_ctx,
 
 }  // namespace
 
-int omnitide_chunk_attn(const void* q, const void* k, const void* v, const int32_t* n_ctx,
-                        int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
-                        int head_dim, float scale, float* out, void* workspace,
-                        size_t workspace_bytes, int32_t* d_status, void* stream) {
-  return attn_impl(q, k, v, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len, n_q_heads,
-                   n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream);
+int omnitide_chunk_attn(const void* q, const void* k, const void* v, int dtype,
+                        const int32_t* n_ctx, int n_seg, int cap, int chunk_len, int n_q_heads,
+                        int n_kv_heads, int head_dim, float scale, void* out, int out_dtype,
+                        void* workspace, size_t workspace_bytes, int32_t* d_status,
+                        void* stream) {
+  return attn_impl(q, k, v, dtype, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len, n_q_heads,
+                   n_kv_heads, head_dim, scale, out, out_dtype, workspace, workspace_bytes,
+                   d_status, stream);
 }
 
 int omnitide_chunk_attn_noalloc(const void* q, const void* k, const void* v,
                                 const int32_t* n_ctx, int n_seg, int cap, int chunk_len,
                                 int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                                float* out, int32_t* d_status, void* stream) {
-  return attn_impl(q, k, v, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len, n_q_heads,
-                   n_kv_heads, head_dim, scale, out, nullptr, 0, d_status, stream, true, true);
+                                void* out, int out_dtype, int32_t* d_status, void* stream) {
+  return attn_impl(q, k, v, OMNITIDE_BF16, n_ctx, nullptr, nullptr, n_seg, cap, chunk_len,
+                   n_q_heads, n_kv_heads, head_dim, scale, out, out_dtype, nullptr, 0, d_status,
+                   stream, true, true);
 }
 
 size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
@@ -442,9 +461,9 @@ int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_
                        int skip_empty_tiles, float* out, void* workspace,
                        size_t workspace_bytes, int32_t* d_status, void* stream) {
   if (key_pos == nullptr || q_pos0 == nullptr) return OMNITIDE_E_NULL;
-  return attn_impl(q, k, v, span, key_pos, q_pos0, n_seg, cap, chunk_len, n_q_heads,
-                   n_kv_heads, head_dim, scale, out, workspace, workspace_bytes, d_status, stream,
-                   skip_empty_tiles != 0);
+  return attn_impl(q, k, v, OMNITIDE_BF16, span, key_pos, q_pos0, n_seg, cap, chunk_len,
+                   n_q_heads, n_kv_heads, head_dim, scale, out, OMNITIDE_F32, workspace,
+                   workspace_bytes, d_status, stream, skip_empty_tiles != 0);
 }
 
 size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units) {

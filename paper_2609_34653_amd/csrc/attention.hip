@@ -142,8 +142,9 @@ template <int D, bool SPAN>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int L, int Hq,
-    int Hkv, float scale_log2, float* __restrict__ out, float* __restrict__ part_o,
-    float* __restrict__ part_ml, int n_mt, int n_split, int32_t* __restrict__ status,
+    int Hkv, float scale_log2, void* __restrict__ out, bool out_bf16,
+    float* __restrict__ part_o, float* __restrict__ part_ml, int n_mt, int n_split,
+    int32_t* __restrict__ status,
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ qpos0_g,
     const int4* __restrict__ tile_info, const int32_t* __restrict__ tile_list,
     const int32_t* __restrict__ n_active_g, int max_tiles) {
@@ -508,15 +509,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   const size_t orow = (static_cast<size_t>(seg) * L + p) * Hq + head;
   if (n_split == 1) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    float* dst = out + orow * D;
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        float4 val = make_float4(o[dt][4 * qd] * inv, o[dt][4 * qd + 1] * inv,
-                                 o[dt][4 * qd + 2] * inv, o[dt][4 * qd + 3] * inv);
-        *reinterpret_cast<float4*>(dst + 32 * dt + 8 * qd + 4 * h) = val;
-      }
+      for (int qd = 0; qd < 4; ++qd)
+        store_out4(out, orow * D + 32 * dt + 8 * qd + 4 * h, out_bf16, o[dt][4 * qd] * inv,
+                   o[dt][4 * qd + 1] * inv, o[dt][4 * qd + 2] * inv, o[dt][4 * qd + 3] * inv);
     }
   } else {
     const size_t n_rows_all = static_cast<size_t>(gridDim.y) * L * Hq;
@@ -653,20 +651,20 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
     hipLaunchKernelGGL((attn_kernel<D, true>), grid, dim3(kAttnThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
-                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_mt,
-                       n_split, a.d_status, a.key_pos, a.q_pos0, tile_info, tile_list, n_active,
-                       max_tiles);
+                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, a.out_bf16, part_o, part_ml,
+                       n_mt, n_split, a.d_status, a.key_pos, a.q_pos0, tile_info, tile_list,
+                       n_active, max_tiles);
   } else {
     hipLaunchKernelGGL((attn_kernel<D, false>), grid, dim3(kAttnThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
-                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_mt,
-                       n_split, a.d_status, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
+                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, a.out_bf16, part_o, part_ml,
+                       n_mt, n_split, a.d_status, nullptr, nullptr, nullptr, nullptr, nullptr, 0);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_split == 1) return e;
   return launch_combine<D>(part_o, part_ml, n_split, n_rows, a.n_ctx, a.chunk_len, a.n_q_heads,
-                           a.cap, a.out, stream);
+                           a.cap, a.out, stream, a.out_bf16);
 }
 
 }  // namespace
@@ -699,11 +697,65 @@ size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_head
 
 int span_attn_max_cap() { return 32768 * kKT; }
 
+namespace {
+
+// float32 -> bf16 (round to nearest even), four values per thread; n is a multiple of 4.
+__global__ __launch_bounds__(256) void cast_bf16_kernel(const float4* __restrict__ src,
+                                                        uint2* __restrict__ dst, size_t n4) {
+  for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n4;
+       i += static_cast<size_t>(gridDim.x) * 256) {
+    const float4 x = src[i];
+    const __bf16 b[4] = {static_cast<__bf16>(x.x), static_cast<__bf16>(x.y),
+                         static_cast<__bf16>(x.z), static_cast<__bf16>(x.w)};
+    dst[i] = make_uint2(static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b[0])) |
+                            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b[1])) << 16),
+                        static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b[2])) |
+                            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b[3])) << 16));
+  }
+}
+
+hipError_t cast_bf16(const void* src, void* dst, size_t n, hipStream_t stream) {
+  const size_t n4 = n / 4;
+  const unsigned blocks = static_cast<unsigned>(std::min<size_t>((n4 + 255) / 256, 4096));
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(cast_bf16_kernel, dim3(blocks), dim3(256), 0, stream,
+                     static_cast<const float4*>(src), static_cast<uint2*>(dst), n4);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t attn_cast_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                       int head_dim) {
+  const size_t q = static_cast<size_t>(n_seg) * chunk_len * n_q_heads * head_dim;
+  const size_t kv = static_cast<size_t>(n_seg) * cap * n_kv_heads * head_dim;
+  return align256(q * 2) + 2 * align256(kv * 2);
+}
+
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
   const int s = attn_num_splits(a.n_seg, a.cap, a.chunk_len, a.n_q_heads, a.n_kv_heads,
                                 a.head_dim);
-  if (a.head_dim == 128) return launch_attn_t<128>(a, s, stream);
-  if (a.head_dim == 64) return launch_attn_t<64>(a, s, stream);
+  AttnArgs b = a;
+  if (a.in_f32) {
+    // bf16 copies of q, k and v after the partials
+    uint8_t* w = static_cast<uint8_t*>(a.workspace) +
+                 align256(attn_workspace_bytes(a.n_seg, a.cap, a.chunk_len, a.n_q_heads,
+                                               a.n_kv_heads, a.head_dim));
+    const size_t nq = static_cast<size_t>(a.n_seg) * a.chunk_len * a.n_q_heads * a.head_dim;
+    const size_t nkv = static_cast<size_t>(a.n_seg) * a.cap * a.n_kv_heads * a.head_dim;
+    void* q16 = w;
+    void* k16 = w + align256(nq * 2);
+    void* v16 = w + align256(nq * 2) + align256(nkv * 2);
+    hipError_t e = cast_bf16(a.q, q16, nq, stream);
+    if (e == hipSuccess) e = cast_bf16(a.k, k16, nkv, stream);
+    if (e == hipSuccess) e = cast_bf16(a.v, v16, nkv, stream);
+    if (e != hipSuccess) return e;
+    b.q = q16;
+    b.k = k16;
+    b.v = v16;
+  }
+  if (a.head_dim == 128) return launch_attn_t<128>(b, s, stream);
+  if (a.head_dim == 64) return launch_attn_t<64>(b, s, stream);
   return hipErrorInvalidValue;
 }
 

@@ -9,6 +9,19 @@
 namespace omnitide {
 namespace {
 
+// Stores four consecutive output values as float32, or rounded to bf16 (nearest even).
+__device__ inline void store_out4(void* out, size_t idx, bool out_bf16, float a, float b, float c,
+                                  float d) {
+  if (out_bf16) {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    const bf16x4 v = {static_cast<__bf16>(a), static_cast<__bf16>(b), static_cast<__bf16>(c),
+                      static_cast<__bf16>(d)};
+    *reinterpret_cast<bf16x4*>(static_cast<__bf16*>(out) + idx) = v;
+  } else {
+    *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = make_float4(a, b, c, d);
+  }
+}
+
 // Merge split partials: out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, M = max_s m_s,
 // splits in order.
 // CH = splits loaded per step (4 for a few splits, 16 or 32 for many); BLOCK = threads per
@@ -19,7 +32,8 @@ __global__ __launch_bounds__(BLOCK) void attn_combine_kernel(const float* __rest
                                                            int n_split, size_t n_rows,
                                                            const int32_t* __restrict__ n_ctx_g,
                                                            int L, int Hq, int cap,
-                                                           float* __restrict__ out) {
+                                                           void* __restrict__ out,
+                                                           bool out_bf16) {
   constexpr int TPR = D / 4;                       // threads per row, 4 floats each
   const size_t row = static_cast<size_t>(blockIdx.x) * (BLOCK / TPR) + threadIdx.x / TPR;
   if (row >= n_rows) return;
@@ -66,30 +80,30 @@ __global__ __launch_bounds__(BLOCK) void attn_combine_kernel(const float* __rest
     M = Mn;
   }
   const float inv = den > 0.f ? 1.f / den : 0.f;
-  *reinterpret_cast<float4*>(out + row * D + 4 * d4) =
-      make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
+  store_out4(out, row * D + 4 * d4, out_bf16, num.x * inv, num.y * inv, num.z * inv,
+             num.w * inv);
 }
 
 // Launch the combine for n_rows rows.
 template <int D>
 hipError_t launch_combine(const float* part_o, const float* part_ml, int n_split, size_t n_rows,
-                          const int32_t* n_ctx, int L, int Hq, int cap, float* out,
-                          hipStream_t stream) {
+                          const int32_t* n_ctx, int L, int Hq, int cap, void* out,
+                          hipStream_t stream, bool out_bf16 = false) {
   constexpr int rows_per_block = 256 / (D / 4);
   const unsigned blocks = static_cast<unsigned>((n_rows + rows_per_block - 1) / rows_per_block);
   if (n_split <= 4)
     hipLaunchKernelGGL((attn_combine_kernel<D, 4>), dim3(blocks), dim3(256), 0, stream, part_o,
-                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
+                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out, out_bf16);
   else if (n_split <= 16)
     hipLaunchKernelGGL((attn_combine_kernel<D, 16>), dim3(blocks), dim3(256), 0, stream, part_o,
-                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out);
+                       part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out, out_bf16);
   else
     // many splits and few rows (decode): two rows per 64-thread block, so that the loads of the
     // partials spread over more CUs
     hipLaunchKernelGGL((attn_combine_kernel<D, 32, 64>),
                        dim3(static_cast<unsigned>((n_rows + 64 / (D / 4) - 1) / (64 / (D / 4)))),
                        dim3(64), 0, stream, part_o, part_ml, n_split, n_rows, n_ctx, L, Hq, cap,
-                       out);
+                       out, out_bf16);
   return hipGetLastError();
 }
 

@@ -13,8 +13,6 @@ constexpr int kWave = 64;
 // Native 16-byte vector (usable with the nontemporal load/store builtins).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__host__ __device__ inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
-
 // First error wins: only a zero status word is overwritten.
 __device__ inline void set_status(int32_t* status, int32_t code) {
   if (status != nullptr) atomicCAS(status, 0, code);

@@ -7,6 +7,9 @@
 
 namespace omnitide {
 
+// Byte counts rounded up to the 256-byte boundaries workspaces place their arrays on.
+__host__ __device__ inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
 hipError_t launch_score(const void* k, int dtype, int n_seg, int n_slots, int row_elems,
                         const int32_t* unit_id, const uint8_t* modality, const uint32_t wq[4],
                         int n_units, uint64_t* unit_wsum, int32_t* unit_len, int32_t* unit_first,
@@ -157,7 +160,9 @@ struct AttnArgs {
   const int32_t* n_ctx;
   int n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim;
   float scale;
-  float* out;
+  void* out;
+  bool out_bf16 = false;              // out is bf16 (rounded to nearest even), else float32
+  bool in_f32 = false;                // q, k, v are float32: cast to bf16 in the workspace
   void* workspace;
   int32_t* d_status;
   // span mode (keys = the slots [0, span) of a pool with holes; n_ctx holds the span):
@@ -185,6 +190,9 @@ hipError_t launch_span_tiles(const int32_t* key_pos, const int32_t* span, int n_
                              int min_span, bool skip_empty, void* buf, hipStream_t stream);
 size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
                             int head_dim);
+// bf16 copies of float32 q, k, v (placed after the 256-aligned partials)
+size_t attn_cast_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,
+                       int head_dim);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream);
 // launch_attn with the split-KV partials in the library's fixed per-device scratch array (no
 // allocation; the caller has checked attn_workspace_bytes <= OMNITIDE_NOALLOC_SCRATCH_BYTES).

@@ -79,11 +79,11 @@ def lib() -> ctypes.CDLL:
         L.omnitide_plan_spans_workspace_bytes.restype = _SZ
         L.omnitide_compact_workspace_bytes.argtypes = [_I, _I, _I]
         L.omnitide_compact_workspace_bytes.restype = _SZ
-        L.omnitide_chunk_attn.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
-                                          ctypes.c_float, _P, _P, _SZ, _P, _P]
+        L.omnitide_chunk_attn.argtypes = [_P, _P, _P, _I, _P, _I, _I, _I, _I, _I, _I,
+                                          ctypes.c_float, _P, _I, _P, _SZ, _P, _P]
         L.omnitide_chunk_attn_noalloc.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
-                                                  ctypes.c_float, _P, _P, _P]
-        L.omnitide_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
+                                                  ctypes.c_float, _P, _I, _P, _P]
+        L.omnitide_attn_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, _I]
         L.omnitide_attn_workspace_bytes.restype = _SZ
         L.omnitide_span_attn.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                          ctypes.c_float, _I, _P, _P, _SZ, _P, _P]
@@ -106,7 +106,8 @@ def lib() -> ctypes.CDLL:
                                            _P, _I, _P, _P, _P, _P, _P, _SZ, _P, _P]
         L.omnitide_place_chunk_workspace_bytes.argtypes = [_I, _I]
         L.omnitide_place_chunk_workspace_bytes.restype = _SZ
-        L.omnitide_decode_attn.argtypes = L.omnitide_chunk_attn.argtypes
+        L.omnitide_decode_attn.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
+                                           ctypes.c_float, _P, _P, _SZ, _P, _P]
         L.omnitide_decode_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I]
         L.omnitide_decode_workspace_bytes.restype = _SZ
         L.omnitide_decode_span_attn.argtypes = L.omnitide_span_attn.argtypes
@@ -350,12 +351,14 @@ def omnitide_compact_kv_spans(k_src, v_src, page_size, unit_id_src, modality_src
            "omnitide_compact_kv_spans")
 
 
-def omnitide_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim) -> int:
-    return int(lib().omnitide_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
-                                                   head_dim))
+def omnitide_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim,
+                                  dtype=BF16) -> int:
+    return int(lib().omnitide_attn_workspace_bytes(dtype, n_seg, cap, chunk_len, n_q_heads,
+                                                   n_kv_heads, head_dim))
 
 
 def omnitide_chunk_attn(q, k, v, n_ctx, scale, out, workspace=None, d_status=None, stream=None):
+    """q/k/v bf16 or float32 (all the same); out float32 or bf16 (its dtype selects)."""
     if q.dim() == 3:
         n_seg, (L, Hq, d) = 1, q.shape
     else:
@@ -363,17 +366,18 @@ def omnitide_chunk_attn(q, k, v, n_ctx, scale, out, workspace=None, d_status=Non
     ds, cap, Hkv, dd = _pool_dims(k, "k")
     if ds != n_seg or dd != d:
         raise ValueError("k shape does not match q")
-    _need(q, "q", (torch.bfloat16,))
-    _need(k, "k", (torch.bfloat16,))
-    _need(v, "v", (torch.bfloat16,), k.numel())
+    _need(q, "q", (torch.bfloat16, torch.float32))
+    _need(k, "k", (q.dtype,))
+    _need(v, "v", (q.dtype,), k.numel())
     _need(n_ctx, "n_ctx", I32, n_seg)
-    _need(out, "out", (torch.float32,), q.numel())
+    _need(out, "out", (torch.float32, torch.bfloat16), q.numel())
     if workspace is not None:
         _need(workspace, "workspace", U8)
     if d_status is not None:
         _need(d_status, "d_status", I32, 1)
-    _check(lib().omnitide_chunk_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(n_ctx), n_seg, cap, L, Hq,
-                                     Hkv, d, float(scale), _ptr(out), _ptr(workspace),
+    _check(lib().omnitide_chunk_attn(_ptr(q), _ptr(k), _ptr(v), _kv_dtype(q), _ptr(n_ctx), n_seg,
+                                     cap, L, Hq, Hkv, d, float(scale), _ptr(out), _kv_dtype(out),
+                                     _ptr(workspace),
                                      0 if workspace is None else workspace.numel(),
                                      _ptr(d_status), _stream(stream)), "omnitide_chunk_attn")
 
@@ -391,12 +395,12 @@ def omnitide_chunk_attn_noalloc(q, k, v, n_ctx, scale, out, d_status=None, strea
     _need(k, "k", (torch.bfloat16,))
     _need(v, "v", (torch.bfloat16,), k.numel())
     _need(n_ctx, "n_ctx", I32, n_seg)
-    _need(out, "out", (torch.float32,), q.numel())
+    _need(out, "out", (torch.float32, torch.bfloat16), q.numel())
     if d_status is not None:
         _need(d_status, "d_status", I32, 1)
     _check(lib().omnitide_chunk_attn_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(n_ctx), n_seg, cap,
                                              L, Hq, Hkv, d, float(scale), _ptr(out),
-                                             _ptr(d_status), _stream(stream)),
+                                             _kv_dtype(out), _ptr(d_status), _stream(stream)),
            "omnitide_chunk_attn_noalloc")
 
 def omnitide_span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,

@@ -59,8 +59,9 @@ class StreamStep:
         self.n_pages = torch.zeros(n_seg, **i32)
         self.compact_ws = torch.zeros(max(1, ot.omnitide_compact_workspace_bytes(n_seg, n_units, cap)),
                                       dtype=torch.uint8, device=dev)
-        aw = ot.omnitide_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
-                                              head_dim)
+        aw = ot.omnitide_attn_workspace_bytes(
+            n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim,
+            dtype=ot.F32 if kv_dtype == torch.float32 else ot.BF16)
         self.attn_ws = torch.zeros(aw, dtype=torch.uint8, device=dev) if aw else None
         self.out = torch.zeros(n_seg, chunk_len, n_q_heads, head_dim, dtype=torch.float32,
                                device=dev)

@@ -227,12 +227,13 @@ def test_compact_validation(L):
 
 
 def attn(L, **kw):
-    a = dict(q=fake(0), k=fake(1), v=fake(2), nctx=fake(3), n_seg=1, cap=17049, Lc=665, Hq=32,
-             Hkv=8, d=128, scale=0.0884, out=fake(4), ws=fake(5), wsb=1 << 30, st=fake(6))
+    a = dict(q=fake(0), k=fake(1), v=fake(2), dt=0, nctx=fake(3), n_seg=1, cap=17049, Lc=665,
+             Hq=32, Hkv=8, d=128, scale=0.0884, out=fake(4), odt=1, ws=fake(5), wsb=1 << 30,
+             st=fake(6))
     a.update(kw)
-    return L.omnitide_chunk_attn(a["q"], a["k"], a["v"], a["nctx"], a["n_seg"], a["cap"], a["Lc"],
-                                 a["Hq"], a["Hkv"], a["d"], a["scale"], a["out"], a["ws"],
-                                 a["wsb"], a["st"], None)
+    return L.omnitide_chunk_attn(a["q"], a["k"], a["v"], a["dt"], a["nctx"], a["n_seg"],
+                                 a["cap"], a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"],
+                                 a["out"], a["odt"], a["ws"], a["wsb"], a["st"], None)
 
 
 def test_attention_validation(L):
@@ -244,10 +245,18 @@ def test_attention_validation(L):
     assert attn(L, cap=100) == ot.E_CAPACITY
     assert attn(L, ws=None) == ot.E_WORKSPACE
     assert attn(L, out=fake(1)) == ot.E_ALIAS
+    assert attn(L, dt=2) == ot.E_DTYPE and attn(L, odt=5) == ot.E_DTYPE
     need = ot.omnitide_attn_workspace_bytes(1, 17049, 665, 32, 8, 128)
     assert need > 0 and attn(L, wsb=need - 1) == ot.E_WORKSPACE
     # split count: 21 row tiles x 8 KV heads -> 3 splits on the 80K-history shape
     assert need == 3 * 665 * 32 * 130 * 4
+    # float32 inputs: the bf16 copies of q, k and v follow the partials
+    need32 = ot.omnitide_attn_workspace_bytes(1, 17049, 665, 32, 8, 128, dtype=ot.F32)
+    copies = 665 * 32 * 128 * 2 + 2 * 17049 * 8 * 128 * 2
+    assert copies <= need32 - need <= copies + 4 * 256
+    assert attn(L, dt=1, wsb=need32 - 1) == ot.E_WORKSPACE
+    # a float32 output (4 bytes an element) ending inside q aliases it
+    assert attn(L, out=P(fake(0).value - 665 * 32 * 128 * 3)) == ot.E_ALIAS
 
 
 def attn_noalloc(L, **kw):
@@ -256,7 +265,7 @@ def attn_noalloc(L, **kw):
     a.update(kw)
     return L.omnitide_chunk_attn_noalloc(a["q"], a["k"], a["v"], a["nctx"], a["n_seg"], a["cap"],
                                          a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"],
-                                         a["out"], a["st"], None)
+                                         a["out"], a.get("odt", 1), a["st"], None)
 
 
 def test_attention_noalloc_validation(L):

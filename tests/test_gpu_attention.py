@@ -95,3 +95,47 @@ def test_chunk_attention_rising_scores_move_the_reference():
     out, status = run_attn(bf16(q)[None], bf16(k)[None], bf16(v)[None], [n], scale)
     assert status == 0
     check(out[0], bf16(q), bf16(k), bf16(v), n, scale)
+
+
+def run_attn_dtypes(q, k, v, n_ctx, scale, out_dtype):
+    """Like run_attn, with q/k/v of any storage dtype (host tensors) and the output dtype."""
+    from paper_2609_34653_amd import omnitide as ot
+    n_seg, L, Hq, d = q.shape
+    cap, Hkv = k.shape[1], k.shape[2]
+    dt = ot.F32 if q.dtype == torch.float32 else ot.BF16
+    out = torch.full((n_seg, L, Hq, d), float("nan"), dtype=out_dtype, device="cuda")
+    nb = ot.omnitide_attn_workspace_bytes(n_seg, cap, L, Hq, Hkv, d, dtype=dt)
+    ws = torch.full((max(nb, 1),), 0xFF, dtype=torch.uint8, device="cuda")
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ot.omnitide_chunk_attn(q.cuda(), k.cuda(), v.cuda(),
+                           torch.tensor(n_ctx, dtype=torch.int32, device="cuda"), scale, out, ws,
+                           st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    return out.cpu()
+
+
+@pytest.mark.parametrize("n_ctx,cap,L,Hq,Hkv,d", [
+    ([17048], 17100, 665, 32, 8, 128),        # the 80K-history shape: three splits, combine
+    ([700, 300], 800, 37, 8, 2, 64),          # two segments, one split
+])
+def test_output_and_input_dtypes(n_ctx, cap, L, Hq, Hkv, d):
+    """bf16 output: the float32 result rounded to nearest even, bit for bit (single-split and
+    combine paths).  float32 inputs: rounded to bf16 inside the library, so the output equals the
+    call on bf16 copies rounded the same way (torch's cast), bit for bit."""
+    rng = np.random.default_rng(77)
+    n_seg = len(n_ctx)
+    q32 = torch.from_numpy(rng.standard_normal((n_seg, L, Hq, d)).astype(np.float32))
+    k32 = torch.from_numpy(rng.standard_normal((n_seg, cap, Hkv, d)).astype(np.float32))
+    v32 = torch.from_numpy(rng.standard_normal((n_seg, cap, Hkv, d)).astype(np.float32))
+    q, k, v = (t.to(torch.bfloat16) for t in (q32, k32, v32))
+    scale = d ** -0.5
+    ref = run_attn_dtypes(q, k, v, n_ctx, scale, torch.float32)
+    for i, n in enumerate(n_ctx):
+        check(ref[i].numpy(), q[i], k[i], v[i], n, scale)
+    ob = run_attn_dtypes(q, k, v, n_ctx, scale, torch.bfloat16)
+    assert torch.equal(ob.view(torch.int16), ref.to(torch.bfloat16).view(torch.int16))
+    of = run_attn_dtypes(q32, k32, v32, n_ctx, scale, torch.float32)
+    assert torch.equal(of, ref)
+    ofb = run_attn_dtypes(q32, k32, v32, n_ctx, scale, torch.bfloat16)
+    assert torch.equal(ofb.view(torch.int16), ob.view(torch.int16))

@@ -66,12 +66,8 @@ def run_gpu(cfg, st, inp, attend=True, sync=True):
     st.select()
     st.compact(inp["k_hist"], inp["v_hist"], inp["unit_id"], inp["modality"], inp["pos"],
                inp["k_chunk"], inp["v_chunk"], inp["chunk_modality"], inp["chunk_unit"])
-    if attend:
-        if cfg.dtype == "bf16":
-            st.attend(inp["q"], cfg.scale)
-        else:   # float32 pools: attention runs on round-to-nearest-even bf16 copies
-            st.attend(inp["q"].to(torch.bfloat16), cfg.scale, k=st.k_dst.to(torch.bfloat16),
-                      v=st.v_dst.to(torch.bfloat16))
+    if attend:   # float32 pools: the library rounds q, k, v to bf16 (nearest even) itself
+        st.attend(inp["q"], cfg.scale)
     if sync:
         torch.cuda.synchronize()
 
