@@ -487,6 +487,8 @@ def main():
         result["measured_ceilings"] = measured_ceilings(dev)
         c = result["measured_ceilings"]
         result["roofline"]["frac_of_measured_mfma"] = round(attn_tflops / c["mfma_bf16_tflops"], 4)
+        result["roofline"]["frac_of_measured_mfma_randn"] = round(
+            attn_tflops / c["mfma_bf16_randn_8w_tflops"], 4)
         for k in ("score", "compact"):
             kernels[k]["frac_of_measured_copy"] = round(kernels[k]["GBps"] / 1e3 /
                                                         c["copy_tbps"], 4)
@@ -546,8 +548,30 @@ def measured_ceilings(dev):
     cyc, ticks = (int(x) for x in clocks.cpu())
     out["mfma_bf16_tflops"] = round(n_wg * 4 * iters * 4 * 32768 / probe_s / 1e12, 1)
     out["sclk_ghz_under_mfma"] = round(cyc / (ticks / 100e6) / 1e9, 3) if ticks else None
+    # The same with N(0,1) operands rounded to bf16 (the attention inputs' statistics): the
+    # matrix cores draw more power on such bits and the clock drops.  Run at 1,024 workgroups
+    # (16 waves per CU) and at 512 (8 per CU, the chunk attention's occupancy).
+    probe.omnitide_probe_mfma_ops.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    gen = torch.Generator(device=dev).manual_seed(1)
+    ops = torch.randn(64 * 8 * 64 * 8, generator=gen, device=dev).to(torch.bfloat16)
+    for wg, key in ((1024, "mfma_bf16_randn_tflops"), (512, "mfma_bf16_randn_8w_tflops")):
+        it_ops = iters // 2
+
+        def run_ops():
+            if probe.omnitide_probe_mfma_ops(wg, it_ops, ctypes.c_void_p(ops.data_ptr()),
+                                             ctypes.c_void_p(sink.data_ptr()),
+                                             ctypes.c_void_p(clocks.data_ptr()), stream) != 0:
+                raise RuntimeError("probe launch failed")
+        ops_s = best(run_ops, 3)
+        out[key] = round(wg * 4 * it_ops * 8 * 32768 / ops_s / 1e12, 1)
+        if wg == 1024:
+            cyc, ticks = (int(x) for x in clocks.cpu())
+            out["sclk_ghz_under_mfma_randn"] = (round(cyc / (ticks / 100e6) / 1e9, 3)
+                                                if ticks else None)
     out["method"] += ("; an MFMA-only probe (1,024 x 4 waves x 20,000 x 4 independent "
-                      "32x32x16 bf16 MFMAs) with the shader clock of its first wave")
+                      "32x32x16 bf16 MFMAs) with the shader clock of its first wave, and the "
+                      "same with N(0,1) bf16 operands at 1,024 and 512 workgroups")
     return out
 
 

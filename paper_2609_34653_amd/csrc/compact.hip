@@ -15,9 +15,10 @@
 // destination row, its tags and its position shift.
 // Copy: one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
 // source slots (binary search over the LDS table, or a short forward walk from the workspace
-// hint), tags are written, then every thread moves 16-byte vectors of the K and V rows.  Rows
-// are whole 2 KB (bf16, 8 heads x 128) runs, so reads and writes are fully coalesced; source and
-// destination never alias, so a single pass is safe (no scratch round trip).
+// hint), then every thread moves 16-byte vectors of the K and V rows, and the rows' tags are
+// written while the first rows are in flight.  Rows are whole 2 KB (bf16, 8 heads x 128) runs,
+// so reads and writes are fully coalesced; source and destination never alias, so a single
+// pass is safe (no scratch round trip).
 #include "common.h"
 #include "kernels.h"
 
@@ -237,13 +238,17 @@ __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_
   __syncthreads();
 }
 
-// Writes the tags of destination tile t and resolves its rows: src_row[i] is the source slot of
-// row r0 + i, or -1 - c for chunk row c; shift_row[i] (if given) is the row's position change
-// (minus the deleted live slots before it; 0 for chunk rows).  Rows [n_ctx, cap_dst) become empty
-// slots, so the destination is a complete pool.  Returns the tile's row count (0: nothing to
-// copy).  Ends with a workgroup barrier.
-__device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int chunk_len,
-                                   int cap_dst, int n_units, const uint8_t* __restrict__ mod_src,
+// Writes the tags of destination rows [r0, r0 + span) (span <= threads) and resolves them:
+// src_row[i] is the source slot of row r0 + i, or -1 - c for chunk row c; shift_row[i] (if
+// given) is the row's position change (minus the deleted live slots before it; 0 for chunk
+// rows).  Rows [n_ctx, cap_dst) become empty slots, so the destination is a complete pool.
+// Returns the number of rows to copy (0: none).  Ends with a workgroup barrier.
+// With rank_row (and shift_row) given, the tags of the history and chunk rows are left to
+// tile_tags: rank_row[i] receives the row's new unit id (history) or the kept unit count
+// (chunk), so the caller can issue its row copies first and the tag reads overlap them.
+__device__ inline int resolve_rows(int seg, int r0, int span, int nctx, int n_slots,
+                                   int chunk_len, int cap_dst, int n_units,
+                                   const uint8_t* __restrict__ mod_src,
                                    const int32_t* __restrict__ pos_src,
                                    const uint8_t* __restrict__ chunk_mod,
                                    const int32_t* __restrict__ chunk_unit,
@@ -251,14 +256,13 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
                                    int32_t* __restrict__ pos_dst,
                                    int32_t* __restrict__ src_of_dst,
                                    const uint8_t* __restrict__ ws, int32_t* src_row,
-                                   int32_t* shift_row, const TilePlan<true>* plan = nullptr,
-                                   bool mapped = false) {
+                                   int32_t* shift_row, const TilePlan<true>* plan, bool mapped,
+                                   int32_t* rank_row) {
   const int tid = threadIdx.x;
-  const int r0 = t * kTile;
   const size_t dst_tag = static_cast<size_t>(seg) * cap_dst;
   {
     const int r = r0 + tid;
-    if (tid < kTile && r >= nctx && r < cap_dst) {
+    if (tid < span && r >= nctx && r < cap_dst) {
       uid_dst[dst_tag + r] = -1;
       mod_dst[dst_tag + r] = 0;
       pos_dst[dst_tag + r] = -1;
@@ -266,7 +270,7 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
     }
   }
   if (r0 >= nctx) return 0;
-  const int nrows = min(kTile, nctx - r0);
+  const int nrows = min(span, nctx - r0);
   const int kept = nctx - chunk_len;
   const size_t src_tag = static_cast<size_t>(seg) * n_slots;
 
@@ -294,15 +298,19 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
         const uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
         const RankRec* rank = reinterpret_cast<const RankRec*>(wseg + L.rank_off);
         const int32_t* tile_hint = reinterpret_cast<const int32_t*>(wseg + L.tile_off);
-        k = tile_hint[t];
+        k = tile_hint[r / kTile];
         while (rank[k + 1].off <= r) ++k;
         rec = rank[k];
       }
       const int s = rec.first + (r - rec.off);
-      uid_dst[dst_tag + r] = k;
-      mod_dst[dst_tag + r] = mod_src[src_tag + s];
-      pos_dst[dst_tag + r] = pos_src[src_tag + s] - rec.del;
-      src_of_dst[dst_tag + r] = s;
+      if (rank_row) {
+        rank_row[tid] = k;
+      } else {
+        uid_dst[dst_tag + r] = k;
+        mod_dst[dst_tag + r] = mod_src[src_tag + s];
+        pos_dst[dst_tag + r] = pos_src[src_tag + s] - rec.del;
+        src_of_dst[dst_tag + r] = s;
+      }
       src_row[tid] = s;
       if (shift_row) shift_row[tid] = -rec.del;
     } else {
@@ -316,10 +324,14 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
             ws + static_cast<size_t>(seg) * L.seg_bytes + L.meta_off);
         n_kept_units = meta[1];
       }
-      uid_dst[dst_tag + r] = n_kept_units + chunk_unit[i];
-      mod_dst[dst_tag + r] = chunk_mod[i];
-      pos_dst[dst_tag + r] = kept + i;
-      src_of_dst[dst_tag + r] = -1;
+      if (rank_row) {
+        rank_row[tid] = n_kept_units;
+      } else {
+        uid_dst[dst_tag + r] = n_kept_units + chunk_unit[i];
+        mod_dst[dst_tag + r] = chunk_mod[i];
+        pos_dst[dst_tag + r] = kept + i;
+        src_of_dst[dst_tag + r] = -1;
+      }
       src_row[tid] = -1 - i;
       if (shift_row) shift_row[tid] = 0;
     }
@@ -328,7 +340,128 @@ __device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int ch
   return nrows;
 }
 
-template <int VPT, bool FUSED>
+// resolve_rows over destination tile t (kTile rows).
+__device__ inline int resolve_tile(int seg, int t, int nctx, int n_slots, int chunk_len,
+                                   int cap_dst, int n_units, const uint8_t* __restrict__ mod_src,
+                                   const int32_t* __restrict__ pos_src,
+                                   const uint8_t* __restrict__ chunk_mod,
+                                   const int32_t* __restrict__ chunk_unit,
+                                   int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst,
+                                   int32_t* __restrict__ pos_dst,
+                                   int32_t* __restrict__ src_of_dst,
+                                   const uint8_t* __restrict__ ws, int32_t* src_row,
+                                   int32_t* shift_row, const TilePlan<true>* plan = nullptr,
+                                   bool mapped = false, int32_t* rank_row = nullptr) {
+  return resolve_rows(seg, t * kTile, kTile, nctx, n_slots, chunk_len, cap_dst, n_units,
+                      mod_src, pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
+                      src_of_dst, ws, src_row, shift_row, plan, mapped, rank_row);
+}
+
+// The tag writes resolve_rows leaves to its caller when given rank_row: the history rows
+// among destination rows [r0, r0 + nrows) (unless the mask map kernel wrote them) and the chunk
+// rows.  One thread per row.
+__device__ inline void tile_tags(int seg, int r0, int nrows, int nctx, int n_slots,
+                                 int chunk_len, int cap_dst, const uint8_t* __restrict__ mod_src,
+                                 const int32_t* __restrict__ pos_src,
+                                 const uint8_t* __restrict__ chunk_mod,
+                                 const int32_t* __restrict__ chunk_unit,
+                                 int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst,
+                                 int32_t* __restrict__ pos_dst, int32_t* __restrict__ src_of_dst,
+                                 const int32_t* src_row, const int32_t* shift_row,
+                                 const int32_t* rank_row, bool mapped) {
+  const int tid = threadIdx.x;
+  if (tid >= nrows) return;
+  const int r = r0 + tid;
+  const int kept = nctx - chunk_len;
+  const size_t d = static_cast<size_t>(seg) * cap_dst + r;
+  if (r < kept) {
+    if (mapped) return;
+    const int s = src_row[tid];
+    const size_t st = static_cast<size_t>(seg) * n_slots + s;
+    uid_dst[d] = rank_row[tid];
+    mod_dst[d] = mod_src[st];
+    pos_dst[d] = pos_src[st] + shift_row[tid];
+    src_of_dst[d] = s;
+  } else {
+    const int i = r - kept;
+    uid_dst[d] = rank_row[tid] + chunk_unit[i];    // the chunk's tags are shared by segments
+    mod_dst[d] = chunk_mod[i];
+    pos_dst[d] = kept + i;
+    src_of_dst[d] = -1;
+  }
+}
+
+// The rows one copy workgroup moves: destination rows dst_row0 + [0, nrows), source slot (or
+// chunk row) src_row[i]; per row a K run then a V run of row_vecs 16-byte vectors.
+struct CopyRows {
+  const uint8_t* k_src;
+  const uint8_t* v_src;
+  const uint8_t* k_chunk;
+  const uint8_t* v_chunk;
+  uint8_t* k_dst;
+  uint8_t* v_dst;
+  const int32_t* src_row;
+  int row_bytes, row_vecs, vecs2;
+  size_t src_base, chunk_base, dst_row0;
+  int nrows;
+};
+
+// Loads rows [rb, rb + RB) into buf: thread tid takes vectors tid + 256 v of each row.
+template <int RB, int VPT>
+__device__ __forceinline__ void copy_load(const CopyRows& c, int rb, u32x4 (&buf)[RB][VPT]) {
+  const int tid = threadIdx.x;
+  // members into locals first: a select between two members' addresses would keep the struct
+  // in memory
+  const uint8_t *const ks = c.k_src, *const vs = c.v_src, *const kc = c.k_chunk,
+                       *const vc = c.v_chunk;
+#pragma unroll
+  for (int j = 0; j < RB; ++j) {
+    const int row = rb + j;
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const int f = tid + kCopyThreads * v;
+      buf[j][v] = u32x4{0, 0, 0, 0};
+      if (row < c.nrows && f < c.vecs2) {
+        const int s = c.src_row[row];
+        const bool is_v = f >= c.row_vecs;
+        const int vec = is_v ? f - c.row_vecs : f;
+        const uint8_t* src;
+        if (s >= 0)
+          src = (is_v ? vs : ks) + (c.src_base + s) * c.row_bytes;
+        else
+          src = (is_v ? vc : kc) + (c.chunk_base + (-1 - s)) * c.row_bytes;
+        buf[j][v] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + vec);
+      }
+    }
+  }
+}
+
+template <int RB, int VPT>
+__device__ __forceinline__ void copy_store(const CopyRows& c, int rb,
+                                           const u32x4 (&buf)[RB][VPT]) {
+  const int tid = threadIdx.x;
+  uint8_t *const kd = c.k_dst, *const vd = c.v_dst;
+#pragma unroll
+  for (int j = 0; j < RB; ++j) {
+    const int row = rb + j;
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const int f = tid + kCopyThreads * v;
+      if (row < c.nrows && f < c.vecs2) {
+        const bool is_v = f >= c.row_vecs;
+        const int vec = is_v ? f - c.row_vecs : f;
+        uint8_t* dst = (is_v ? vd : kd) + (c.dst_row0 + row) * c.row_bytes;
+        __builtin_nontemporal_store(buf[j][v], reinterpret_cast<u32x4*>(dst) + vec);
+      }
+    }
+  }
+}
+
+// Copy: one workgroup per TPW consecutive destination tiles.  Its rows are resolved at once;
+// then batches of RB rows (RB x VPT x 4 KB of K and V) are software-pipelined through two
+// register buffers, the loads of batch b+1 in flight while batch b is stored; the rows' tags
+// are written while the first batch is in flight.
+template <int VPT, bool FUSED, int TPW>
 __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
     const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
     int row_bytes, const uint8_t* __restrict__ mod_src,
@@ -339,11 +472,13 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
     uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
     int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
     const uint8_t* __restrict__ ws, FusedPlanArgs fp) {
-  constexpr int RB = VPT >= 16 ? 1 : 16 / VPT;
-  __shared__ int32_t src_row[kTile];
+  constexpr int RB = VPT >= 16 ? 1 : 16 / VPT;     // rows per batch
+  constexpr int SPAN = TPW * kTile;
+  static_assert(SPAN <= kCopyThreads, "one resolving thread per row");
+  __shared__ int32_t src_row[SPAN], shift_row[SPAN], rank_row[SPAN];
   __shared__ TilePlan<FUSED> plan;
   const int seg = blockIdx.y;
-  const int t = blockIdx.x;
+  const int r0 = blockIdx.x * SPAN;
   const int tid = threadIdx.x;
   int nctx;
   const TilePlan<true>* pp = nullptr;
@@ -355,52 +490,30 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_kernel(
   } else {
     nctx = n_ctx_g[seg];
   }
-  const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
-                                 pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, nullptr, pp, fp.mapped);
+  const int nrows = resolve_rows(seg, r0, SPAN, nctx, n_slots, chunk_len, cap_dst, n_units,
+                                 mod_src, pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst,
+                                 pos_dst, src_of_dst, ws, src_row, shift_row, pp, fp.mapped,
+                                 rank_row);
   if (nrows == 0) return;
-  const int r0 = t * kTile;
 
   const int row_vecs = row_bytes / 16;
   const int vecs2 = 2 * row_vecs;       // K row then V row
   const size_t src_base = static_cast<size_t>(seg) * n_slots;
   const size_t chunk_base = static_cast<size_t>(seg) * chunk_len;
   const size_t dst_base = static_cast<size_t>(seg) * cap_dst;
-  for (int rb = 0; rb < nrows; rb += RB) {
-    u32x4 buf[RB][VPT];
-#pragma unroll
-    for (int j = 0; j < RB; ++j) {
-      const int row = rb + j;
-#pragma unroll
-      for (int v = 0; v < VPT; ++v) {
-        const int f = tid + kCopyThreads * v;
-        buf[j][v] = u32x4{0, 0, 0, 0};
-        if (row < nrows && f < vecs2) {
-          const int s = src_row[row];
-          const bool is_v = f >= row_vecs;
-          const int vec = is_v ? f - row_vecs : f;
-          const uint8_t* src;
-          if (s >= 0)
-            src = (is_v ? v_src : k_src) + (src_base + s) * row_bytes;
-          else
-            src = (is_v ? v_chunk : k_chunk) + (chunk_base + (-1 - s)) * row_bytes;
-          buf[j][v] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + vec);
-        }
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < RB; ++j) {
-      const int row = rb + j;
-#pragma unroll
-      for (int v = 0; v < VPT; ++v) {
-        const int f = tid + kCopyThreads * v;
-        if (row < nrows && f < vecs2) {
-          const bool is_v = f >= row_vecs;
-          const int vec = is_v ? f - row_vecs : f;
-          uint8_t* dst = (is_v ? v_dst : k_dst) + (dst_base + r0 + row) * row_bytes;
-          __builtin_nontemporal_store(buf[j][v], reinterpret_cast<u32x4*>(dst) + vec);
-        }
-      }
+  const CopyRows cr{k_src, v_src, k_chunk, v_chunk, k_dst, v_dst, src_row, row_bytes,
+                    row_vecs, vecs2, src_base, chunk_base, dst_base + r0, nrows};
+  u32x4 bA[RB][VPT], bB[RB][VPT];
+  copy_load<RB, VPT>(cr, 0, bA);
+  tile_tags(seg, r0, nrows, nctx, n_slots, chunk_len, cap_dst, mod_src, pos_src, chunk_mod,
+            chunk_unit, uid_dst, mod_dst, pos_dst, src_of_dst, src_row, shift_row, rank_row,
+            fp.mapped);
+  for (int rb = 0; rb < nrows; rb += 2 * RB) {
+    if (rb + RB < nrows) copy_load<RB, VPT>(cr, rb + RB, bB);
+    copy_store<RB, VPT>(cr, rb, bA);
+    if (rb + RB < nrows) {
+      if (rb + 2 * RB < nrows) copy_load<RB, VPT>(cr, rb + 2 * RB, bA);
+      copy_store<RB, VPT>(cr, rb + RB, bB);
     }
   }
 }
@@ -410,10 +523,17 @@ FusedPlanArgs fused_args(const CompactArgs& a) {
                        a.unit_remap, a.n_ctx,   a.n_pages,  a.d_status,   a.use_mask};
 }
 
+// Destination tiles per copy workgroup.  One: every workgroup of the grid is resident at once
+// and the grid's reads and writes overlap across workgroups; two or four tiles per workgroup,
+// pipelined, measured 7% and 25% slower on the 80K history.
+constexpr int kCopyTiles = 1;
+
 template <int VPT, bool FUSED>
 hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
-  const dim3 grid((a.cap_dst + kTile - 1) / kTile, a.n_seg);
-  hipLaunchKernelGGL((compact_copy_kernel<VPT, FUSED>), grid, dim3(kCopyThreads), 0, stream,
+  constexpr int span = kCopyTiles * kTile;
+  const dim3 grid((a.cap_dst + span - 1) / span, a.n_seg);
+  hipLaunchKernelGGL((compact_copy_kernel<VPT, FUSED, kCopyTiles>), grid, dim3(kCopyThreads), 0,
+                     stream,
                      static_cast<const uint8_t*>(a.k_src), static_cast<const uint8_t*>(a.v_src),
                      a.n_slots_src, a.row_bytes, a.modality_src, a.pos_src,
                      static_cast<const uint8_t*>(a.k_chunk), static_cast<const uint8_t*>(a.v_chunk),
@@ -569,6 +689,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     const uint8_t* __restrict__ ws, double rope_base, int rot_dims, FusedPlanArgs fp) {
   __shared__ int32_t src_row[kTile];
   __shared__ int32_t shift_row[kTile];
+  __shared__ int32_t rank_row[kTile];
   __shared__ double theta[kMaxHalfRot];
   __shared__ float2 cs[kTile][kMaxHalfRot];
   __shared__ TilePlan<FUSED> plan;
@@ -588,7 +709,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
   }
   const int nrows = resolve_tile(seg, t, nctx, n_slots, chunk_len, cap_dst, n_units, mod_src,
                                  pos_src, chunk_mod, chunk_unit, uid_dst, mod_dst, pos_dst,
-                                 src_of_dst, ws, src_row, shift_row, pp, fp.mapped);
+                                 src_of_dst, ws, src_row, shift_row, pp, fp.mapped, rank_row);
   if (nrows == 0) return;
   const int r0 = t * kTile;
   rope_table(nrows, rot_dims / 2, shift_row, theta, cs);
@@ -612,6 +733,9 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(v_dst + (dst_base + r0 + row) *
                                                             row_bytes) + vec);
   }
+  tile_tags(seg, r0, nrows, nctx, n_slots, chunk_len, cap_dst, mod_src, pos_src, chunk_mod,
+            chunk_unit, uid_dst, mod_dst, pos_dst, src_of_dst, src_row, shift_row, rank_row,
+            fp.mapped);
   rope_rows<EB, HALF, false>(
       nrows, n_kv_heads, head_dim, rot_dims, shift_row, cs,
       [&](int row) { return row_src(k_src, k_chunk, row); },
