@@ -184,9 +184,10 @@ int omnitide_compact_kv(const void* k_src, const void* v_src, int dtype, int n_s
 
 /*
  * omnitide_compact_kv_rope -- omnitide_compact_kv plus the rotary re-encoding of the moved keys
- * (paper: Applying the retention plan -- a retained token's position drops by the number of
- * deleted tokens before it, and the runtime applies the matching RoPE adjustment to the cached
- * keys).  Same arguments, outputs and errors as omnitide_compact_kv, except:
+ * (paper: section 5.2, Applying the retention plan).  Compaction lowers a kept token's position
+ * by the deleted tokens before it; its cached key, rotated for the old position, is turned by
+ * that (negative) shift so that it reads as rotated for the new one.  Same arguments, outputs
+ * and errors as omnitide_compact_kv, except:
  *   k_dst   history row r (source slot s) holds K[s] with each pair (x, y) of its first
  *           rope_dims dimensions (per head) turned by shift * theta_j:
  *           (x cos - y sin, x sin + y cos), shift = pos_dst[r] - pos_src[s] (<= 0, minus the

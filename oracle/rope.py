@@ -2,9 +2,9 @@
 
 Test infrastructure: used only by tests, the smoke check and the CPU baseline.
 
-Paper passage followed (Applying the retention plan): deleting ranges shifts every retained
-token's logical position down by the number of deleted tokens before it, and the runtime
-applies the matching RoPE adjustment to the cached keys.
+Paper passage followed (section 5.2, Applying the retention plan): after a deletion a kept
+token's logical position is lower by the deleted tokens before it, so its cached key, rotated
+for the old position, is turned by that shift to read as rotated for the new one.
 
 Readings where the paper is silent (its model's attention uses standard rotary embeddings):
   * A key stored after rotation at position p is moved to position p + shift by rotating each

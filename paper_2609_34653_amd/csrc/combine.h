@@ -38,8 +38,9 @@ __global__ __launch_bounds__(BLOCK) void attn_combine_kernel(const float* __rest
   const size_t row = static_cast<size_t>(blockIdx.x) * (BLOCK / TPR) + threadIdx.x / TPR;
   if (row >= n_rows) return;
   const int seg = static_cast<int>(row / (static_cast<size_t>(L) * Hq));
+  // the segment's validity is checked only before the store, so that its load and the
+  // partials' loads are in flight together (the partial buffers exist either way)
   const int nctx = n_ctx_g[seg];
-  if (nctx < L || nctx > cap) return;
   const int d4 = threadIdx.x % TPR;
   // One pass in fixed split order, kChunk splits at a time with all their loads in flight; the
   // running (M, num, den) is rescaled to each chunk's new maximum.
@@ -79,6 +80,7 @@ __global__ __launch_bounds__(BLOCK) void attn_combine_kernel(const float* __rest
     }
     M = Mn;
   }
+  if (nctx < L || nctx > cap) return;
   const float inv = den > 0.f ? 1.f / den : 0.f;
   store_out4(out, row * D + 4 * d4, out_bf16, num.x * inv, num.y * inv, num.z * inv,
              num.w * inv);

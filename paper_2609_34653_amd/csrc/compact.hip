@@ -544,9 +544,9 @@ hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Copy with rotary re-encoding of the moved keys (paper: Applying the retention plan -- the
-// position of each retained token drops by the deleted tokens before it and the cached keys get
-// the matching RoPE adjustment).  A history row whose position changes by `shift` has each pair
+// Copy with rotary re-encoding of the moved keys (paper: section 5.2, Applying the retention
+// plan): a kept key rotated for its old position is turned by its position shift (the deleted
+// tokens before it, negated).  A history row whose position changes by `shift` has each pair
 // (x, y) of its first rot_dims key dimensions turned by shift * theta_j, theta_j =
 // base^(-2j/rot_dims): (x cos - y sin, x sin + y cos).  Pairs are (j, j + rot_dims/2) (HALF) or
 // (2j, 2j+1).  V rows, chunk rows and unshifted rows are copied unchanged.
