@@ -152,6 +152,7 @@ struct TilePlan<true> {
   int32_t roff[kSmallUnits + 1];   // destination offset of each kept rank (+ sentinel)
   int32_t rfirst[kSmallUnits];     // first source slot of each kept rank
   int32_t rdel[kSmallUnits];       // deleted live tokens before each kept rank
+  int32_t rank_of[kSmallUnits];    // kept rank of each unit, -1 if it keeps nothing
   int32_t kept, n_kept;
 };
 
@@ -166,6 +167,7 @@ struct FusedPlanArgs {
   int32_t* n_pages;
   int32_t* status;
   bool mapped;       // history rows were resolved by the mask map kernel
+  const int32_t* counts = nullptr;   // kept count per unit (mask path), else keep / keep_len
 };
 
 __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_dst,
@@ -182,8 +184,9 @@ __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_
       const int u = min(u0 + i, U - 1);
       nl[i] = f.len[base + u];
       fs[i] = f.first[base + u];
-      kq[i] = f.keep_len != nullptr ? f.keep_len[base + u]
-                                    : (f.keep[base + u] != 0 ? INT32_MAX : 0);
+      kq[i] = f.counts != nullptr     ? f.counts[u]
+              : f.keep_len != nullptr ? f.keep_len[base + u]
+                                      : (f.keep[base + u] != 0 ? INT32_MAX : 0);
     }
     int kl[kSmallPer], dl[kSmallPer];
     int my_k = 0, my_d = 0, my_n = 0;
@@ -209,10 +212,12 @@ __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_
           P.roff[rk] = off;
           P.rfirst[rk] = fs[i];
           P.rdel[rk] = del;
+          P.rank_of[u] = rk;
           if (writer) f.remap[base + u] = rk;
           ++rk;
-        } else if (writer) {
-          f.remap[base + u] = -1;
+        } else {
+          P.rank_of[u] = -1;
+          if (writer) f.remap[base + u] = -1;
         }
       }
       off += kl[i];
@@ -884,6 +889,75 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
   }
 }
 
+// Up to kSmallUnits units: the plan over the count kernel's per-unit counts is built in LDS by
+// every map workgroup (wave 0, as in the fused copy), so no plan kernel runs; workgroup 0 also
+// writes unit_remap, n_ctx, n_pages, the kept totals and the capacity status.  Then one wave per
+// unit maps its kept slots as compact_mask_map_kernel does.
+__global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_fused_kernel(
+    const uint8_t* __restrict__ mask_g, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, int n_slots, int n_units, int chunk_len, int cap_dst,
+    int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, uint8_t* __restrict__ ws, FusedPlanArgs fp) {
+  constexpr int P = kUnitPer;
+  __shared__ TilePlan<true> plan;
+  const int seg = blockIdx.y;
+  const WsLayout L = ws_layout(n_units, cap_dst);
+  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+  fp.counts = reinterpret_cast<const int32_t*>(wseg + L.count_off);
+  plan_in_lds(seg, n_units, chunk_len, cap_dst, fp, plan);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    int32_t* meta = reinterpret_cast<int32_t*>(wseg + L.meta_off);
+    meta[0] = plan.kept;
+    meta[1] = plan.n_kept;
+  }
+  if (plan.kept + chunk_len > cap_dst) return;    // capacity error: no history row is written
+  const int lane = threadIdx.x & (kWave - 1);
+  const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
+  if (u >= n_units) return;
+  const int rk = plan.rank_of[u];
+  if (rk < 0) return;                             // nothing kept (count 0 also for bad units)
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  const int n = fp.len[ub + u], f = fp.first[ub + u];
+  const int rec_off = plan.roff[rk], rec_del = plan.rdel[rk];
+  int32_t* shift = reinterpret_cast<int32_t*>(wseg + L.shift_off);
+  const size_t sb = static_cast<size_t>(seg) * n_slots;
+  const size_t db = static_cast<size_t>(seg) * cap_dst;
+  const uint8_t* m = mask_g + sb;
+  const uintptr_t end = reinterpret_cast<uintptr_t>(m + f + n);
+  int carry = 0;                                  // kept slots of the unit before the step
+  for (uintptr_t c = block16_floor(m + f); c < end; c += P * kWave) {
+    const uintptr_t blk = c + P * static_cast<uintptr_t>(lane);
+    const int s0 = static_cast<int>(static_cast<intptr_t>(blk) - reinterpret_cast<intptr_t>(m));
+    bool keep[P];
+    int nk = 0;
+    {
+      uint8_t b[16] = {};
+      if (blk < end) load_block16(blk, b);
+#pragma unroll
+      for (int j = 0; j < P; ++j) keep[j] = s0 + j >= f && s0 + j < f + n && b[j] != 0;
+    }
+#pragma unroll
+    for (int j = 0; j < P; ++j) nk += keep[j] ? 1 : 0;
+    const int incl = wave_inclusive_scan(nk);
+    int within = carry + incl - nk;               // kept slots of the unit before s0
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      if (keep[j]) {
+        const int s = s0 + j;
+        const int r = rec_off + within;
+        const int delb = rec_del + (s - f) - within;   // deleted live slots before s
+        src_of_dst[db + r] = s;
+        uid_dst[db + r] = rk;
+        mod_dst[db + r] = mod_src[sb + s];
+        pos_dst[db + r] = pos_src[sb + s] - delb;
+        shift[r] = -delb;
+        ++within;
+      }
+    }
+    carry += __shfl(incl, kWave - 1, kWave);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_rope_in_place(void* k, int dtype, int n_seg, int cap, int n_kv_heads,
@@ -933,6 +1007,16 @@ hipError_t launch_compact(const CompactArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(compact_mask_count_kernel, ugrid, dim3(kUnitWaves * kWave), 0, stream,
                        a.keep_slot, a.unit_len, a.unit_first, a.n_slots_src, a.n_units,
                        a.cap_dst, ws, a.d_status);
+    if (a.n_units <= kSmallUnits) {
+      // the map workgroups plan for themselves
+      hipLaunchKernelGGL(compact_mask_map_fused_kernel, ugrid, dim3(kUnitWaves * kWave), 0,
+                         stream, a.keep_slot, a.modality_src, a.pos_src, a.n_slots_src,
+                         a.n_units, a.chunk_len, a.cap_dst, a.unit_id_dst, a.modality_dst,
+                         a.pos_dst, a.src_of_dst, ws, fused_args(a));
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      return launch_copies<false>(a, stream);
+    }
     const uint8_t* no_keep = nullptr;             // counts come from the workspace
     const int32_t* no_keep_len = nullptr;
     hipLaunchKernelGGL(compact_plan_kernel, dim3(a.n_seg), dim3(kPlanThreads), 0, stream,
