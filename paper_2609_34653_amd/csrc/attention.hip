@@ -553,9 +553,7 @@ __global__ __launch_bounds__(kInfoThreads) void span_info_kernel(
   const int j = t * kKT + lane;
   const int p = j < span ? key_pos[static_cast<size_t>(seg) * cap + j] : -1;
   const uint64_t valid = __ballot(p >= 0);
-  int mx = p;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off, kWave));
+  const int mx = wave_max_i32(p);
   if (lane == 0) {
     const size_t tb = static_cast<size_t>(seg) * max_tiles;
     tile_info[tb + t] = make_int4(mx, valid != ~0ull ? 1 : 0,

@@ -24,10 +24,54 @@ __device__ inline uint64_t wave_sum_u64(uint64_t v) {
   return v;
 }
 
+// Lane moves by data-parallel primitives (DPP, register to register, no LDS round trip):
+// row_shr:n shifts within each 16-lane row, row_bcast:15 / :31 hand lane 15 (31) to the next
+// row(s).  Lanes without a source, and rows outside ROW_MASK, receive `fill`.  Every lane of the
+// wave must be active.
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+constexpr int kDppWaveShr1 = 0x138;     // lane i receives lane i - 1 (lane 0: fill)
+
+template <int CTRL, int ROW_MASK>
+__device__ inline int dpp_move(int fill, int v) {
+  return __builtin_amdgcn_update_dpp(fill, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+// Inclusive scans of a 32-bit value over the wave's lanes: within rows by four row shifts,
+// then across rows by the two broadcasts.
+__device__ inline int wave_scan_add_i32(int x) {
+  x += dpp_move<kDppRowShr1, 0xf>(0, x);
+  x += dpp_move<kDppRowShr2, 0xf>(0, x);
+  x += dpp_move<kDppRowShr4, 0xf>(0, x);
+  x += dpp_move<kDppRowShr8, 0xf>(0, x);
+  x += dpp_move<kDppRowBcast15, 0xa>(0, x);
+  x += dpp_move<kDppRowBcast31, 0xc>(0, x);
+  return x;
+}
+__device__ inline int wave_scan_max_i32(int x, int lo) {
+  x = max(x, dpp_move<kDppRowShr1, 0xf>(lo, x));
+  x = max(x, dpp_move<kDppRowShr2, 0xf>(lo, x));
+  x = max(x, dpp_move<kDppRowShr4, 0xf>(lo, x));
+  x = max(x, dpp_move<kDppRowShr8, 0xf>(lo, x));
+  x = max(x, dpp_move<kDppRowBcast15, 0xa>(lo, x));
+  x = max(x, dpp_move<kDppRowBcast31, 0xc>(lo, x));
+  return x;
+}
+
+// Maximum over the wave, the same in every lane.
+__device__ inline int wave_max_i32(int v) {
+  return __builtin_amdgcn_readlane(wave_scan_max_i32(v, INT32_MIN), kWave - 1);
+}
+
+// Exclusive running maximum over the wave's lanes (lane 0: lo).
+__device__ inline int wave_exclusive_max_i32(int v, int lo) {
+  return dpp_move<kDppWaveShr1, 0xf>(lo, wave_scan_max_i32(v, lo));
+}
+
+// Sum over the wave, the same in every lane.
 __device__ inline uint32_t wave_sum_u32(uint32_t v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
+  return static_cast<uint32_t>(
+      __builtin_amdgcn_readlane(wave_scan_add_i32(static_cast<int>(v)), kWave - 1));
 }
 
 // Byte arrays walked in 16-byte aligned blocks (absolute addresses): a block that holds a byte
@@ -53,22 +97,32 @@ __device__ inline T readlane(T v, int lane) {
 
 template <typename T>
 __device__ inline T wave_inclusive_scan(T v) {
-  const int lane = threadIdx.x & (kWave - 1);
+  if constexpr (sizeof(T) == 4) {
+    // 32-bit integers wrap the same in either signedness
+    return static_cast<T>(wave_scan_add_i32(static_cast<int>(v)));
+  } else {
+    const int lane = threadIdx.x & (kWave - 1);
 #pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    T o = __shfl_up(v, off, kWave);
-    if (lane >= off) v += o;
+    for (int off = 1; off < kWave; off <<= 1) {
+      T o = __shfl_up(v, off, kWave);
+      if (lane >= off) v += o;
+    }
+    return v;
   }
-  return v;
 }
 
 // Returns the exclusive prefix of v over threads in thread order; *total gets the grand total.
+// A one-wave workgroup scans in registers only (no LDS, no barrier).
 template <typename T>
 __device__ inline T block_exclusive_scan(T v, T* scratch, T* total) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int n_waves = (blockDim.x + kWave - 1) / kWave;
   T inc = wave_inclusive_scan(v);
+  if (n_waves == 1) {
+    *total = __shfl(inc, kWave - 1, kWave);
+    return inc - v;
+  }
   __syncthreads();
   if (lane == kWave - 1) scratch[wave] = inc;
   __syncthreads();
@@ -99,13 +153,21 @@ __device__ inline T block_exclusive_max(T v, T lo, T* scratch, T* total) {
   const int wave = threadIdx.x / kWave;
   const int n_waves = (blockDim.x + kWave - 1) / kWave;
   T inc = v;
+  if constexpr (sizeof(T) == 4) {
+    inc = static_cast<T>(wave_scan_max_i32(static_cast<int>(v), static_cast<int>(lo)));
+  } else {
 #pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    T o = __shfl_up(inc, off, kWave);
-    if (lane >= off) inc = max(inc, o);
+    for (int off = 1; off < kWave; off <<= 1) {
+      T o = __shfl_up(inc, off, kWave);
+      if (lane >= off) inc = max(inc, o);
+    }
   }
   T exc = __shfl_up(inc, 1, kWave);
   if (lane == 0) exc = lo;
+  if (n_waves == 1) {
+    *total = __shfl(inc, kWave - 1, kWave);
+    return exc;
+  }
   __syncthreads();
   if (lane == kWave - 1) scratch[wave] = inc;
   __syncthreads();

@@ -162,8 +162,7 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
     }
     if (shift_g != nullptr) shift_g[sb + s] = shift;
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) end = max(end, __shfl_xor(end, off, kWave));
+  end = wave_max_i32(end);
   if ((threadIdx.x & (kWave - 1)) == 0 && end > 0) atomicMax(span_g + seg, end);
 }
 

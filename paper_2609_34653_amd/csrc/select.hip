@@ -266,13 +266,7 @@ __global__ __launch_bounds__(kWave) void select_small_kernel(
     key[i] = (sc << kIdBits) | static_cast<uint64_t>(u);
   }
   // unit order: every live unit's first slot exceeds all earlier live units' first slots
-  int run = my_max_first;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_up(run, off, kWave);
-    if (lane >= off) run = max(run, o);
-  }
-  run = lane == 0 ? -1 : __shfl_up(run, 1, kWave);
+  int run = wave_exclusive_max_i32(my_max_first, -1);
 #pragma unroll
   for (int i = 0; i < kSmallPer; ++i) {
     if (ln[i] > 0) {

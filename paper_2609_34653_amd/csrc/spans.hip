@@ -106,14 +106,9 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
       if (m[j] >= 0 && m[j] != pm) run = s0 + j;   // a span starts here
       nt += m[j] == OMNITIDE_MOD_TEXT ? 1 : 0;
     }
-    int inc = run;                                 // running maximum of span starts
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int o = __shfl_up(inc, off, kWave);
-      if (lane >= off) inc = max(inc, o);
-    }
-    int exc = __shfl_up(inc, 1, kWave);
-    if (lane == 0) exc = -1;
+    // running maximum of span starts, and over the lanes before this one
+    const int inc = wave_scan_max_i32(run, -1);
+    const int exc = dpp_move<kDppWaveShr1, 0xf>(-1, inc);
     int start = max(exc, carry_start);             // span start of the slot before s0
     const int incl = wave_inclusive_scan(nt);
     const int text_tot = __shfl(incl, kWave - 1, kWave);
