@@ -18,11 +18,6 @@ __device__ inline void set_status(int32_t* status, int32_t code) {
   if (status != nullptr) atomicCAS(status, 0, code);
 }
 
-__device__ inline uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-  return v;
-}
 
 // Lane moves by data-parallel primitives (DPP, register to register, no LDS round trip):
 // row_shr:n shifts within each 16-lane row, row_bcast:15 / :31 hand lane 15 (31) to the next
@@ -66,6 +61,26 @@ __device__ inline int wave_max_i32(int v) {
 // Exclusive running maximum over the wave's lanes (lane 0: lo).
 __device__ inline int wave_exclusive_max_i32(int v, int lo) {
   return dpp_move<kDppWaveShr1, 0xf>(lo, wave_scan_max_i32(v, lo));
+}
+
+// Sum of a 64-bit value over the wave (modulo 2^64), the same in every lane: the inclusive
+// scan of wave_scan_add_i32 with both halves moved by DPP and a 64-bit add per step.
+template <int CTRL, int ROW_MASK>
+__device__ inline uint64_t dpp_move_u64(uint64_t v) {
+  const int lo = dpp_move<CTRL, ROW_MASK>(0, static_cast<int>(static_cast<uint32_t>(v)));
+  const int hi = dpp_move<CTRL, ROW_MASK>(0, static_cast<int>(static_cast<uint32_t>(v >> 32)));
+  return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+}
+__device__ inline uint64_t wave_sum_u64(uint64_t v) {
+  v += dpp_move_u64<kDppRowShr1, 0xf>(v);
+  v += dpp_move_u64<kDppRowShr2, 0xf>(v);
+  v += dpp_move_u64<kDppRowShr4, 0xf>(v);
+  v += dpp_move_u64<kDppRowShr8, 0xf>(v);
+  v += dpp_move_u64<kDppRowBcast15, 0xa>(v);
+  v += dpp_move_u64<kDppRowBcast31, 0xc>(v);
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), 63);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), 63);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 // Sum over the wave, the same in every lane.

@@ -29,6 +29,10 @@ constexpr int kPlanThreads = 1024;
 constexpr int kPer = OMNITIDE_MAX_UNITS / kPlanThreads;
 constexpr int kTile = 16;           // destination rows per copy workgroup
 constexpr int kCopyThreads = 256;
+// Buffer resource word 3 for raw (unformatted) data on this chip, and a byte offset past any
+// buffer (accesses there read zero and write nothing).
+constexpr int kBufFlags = 0x00020000;
+constexpr int kOutOfBuf = 0x7ffffff0;
 
 struct RankRec {
   int32_t off;     // destination row of the unit's first token
@@ -149,9 +153,11 @@ template <bool FUSED>
 struct TilePlan {};
 template <>
 struct TilePlan<true> {
+  // by kept rank; entry kSmallUnits is a sink for the writes of units that keep nothing (roff
+  // then takes the sentinel, written last)
   int32_t roff[kSmallUnits + 1];   // destination offset of each kept rank (+ sentinel)
-  int32_t rfirst[kSmallUnits];     // first source slot of each kept rank
-  int32_t rdel[kSmallUnits];       // deleted live tokens before each kept rank
+  int32_t rfirst[kSmallUnits + 1]; // first source slot of each kept rank
+  int32_t rdel[kSmallUnits + 1];   // deleted live tokens before each kept rank
   int32_t rank_of[kSmallUnits];    // kept rank of each unit, -1 if it keeps nothing
   int32_t kept, n_kept;
 };
@@ -204,22 +210,23 @@ __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_
     int del = wave_excl(my_d, &dropped);
     int rk = wave_excl(my_n, &n_kept);
     (void)dropped;
+    // branch-free: a unit that keeps nothing writes to the sink entry (units past U have
+    // kl = 0); unit_remap through a buffer whose writes past U are dropped
+    const __amdgpu_buffer_rsrc_t r_remap =
+        __builtin_amdgcn_make_buffer_rsrc(f.remap + base, 0, 4 * U, kBufFlags);
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i) {
       const int u = u0 + i;
-      if (u < U) {
-        if (kl[i] > 0) {
-          P.roff[rk] = off;
-          P.rfirst[rk] = fs[i];
-          P.rdel[rk] = del;
-          P.rank_of[u] = rk;
-          if (writer) f.remap[base + u] = rk;
-          ++rk;
-        } else {
-          P.rank_of[u] = -1;
-          if (writer) f.remap[base + u] = -1;
-        }
-      }
+      const bool kk = kl[i] > 0;
+      const int at = kk ? rk : kSmallUnits;
+      P.roff[at] = off;
+      P.rfirst[at] = fs[i];
+      P.rdel[at] = del;
+      P.rank_of[u] = kk ? rk : -1;
+      if (writer)
+        __builtin_amdgcn_raw_buffer_store_b32(kk ? rk : -1, r_remap, u < U ? 4 * u : kOutOfBuf,
+                                              0, 0);
+      rk += kk ? 1 : 0;
       off += kl[i];
       del += dl[i];
     }
@@ -804,7 +811,7 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_count_kernel(
     uint8_t* __restrict__ ws, int32_t* __restrict__ status) {
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
-  const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
+  const int u = blockIdx.x * kUnitWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (u >= n_units) return;
   const WsLayout L = ws_layout(n_units, cap_dst);
   int32_t* cnt = reinterpret_cast<int32_t*>(ws + static_cast<size_t>(seg) * L.seg_bytes +
@@ -830,30 +837,35 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_count_kernel(
   if (lane == 0) cnt[u] = static_cast<int32_t>(c);
 }
 
-__global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
-    const uint8_t* __restrict__ mask_g, const int32_t* __restrict__ len_g,
-    const int32_t* __restrict__ first_g, const uint8_t* __restrict__ mod_src,
-    const int32_t* __restrict__ pos_src, int n_slots, int n_units, int cap_dst,
-    const int32_t* __restrict__ remap_g, const int32_t* __restrict__ n_ctx_g,
-    int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
-    int32_t* __restrict__ src_of_dst, uint8_t* __restrict__ ws) {
+// One wave maps the kept slots of one unit (slots [f, f + n), mask m of the segment): kept slot
+// number `within` of the unit goes to destination row rec_off + within with the unit's new id
+// rk, and its position drops by the deleted live slots before it (rec_del plus those of the
+// unit).  The wave walks aligned 16-slot blocks, 16 per lane per step, with one wave scan of
+// the kept counts per step.  Branch-free per slot: the tag reads and writes of slots that are
+// not kept use an offset past their buffer, which the hardware turns into a zero read and a
+// dropped write.
+__device__ inline void map_unit_slots(const uint8_t* m, int f, int n, int rk, int rec_off,
+                                      int rec_del, int lane, int seg, int n_slots, int cap_dst,
+                                      const uint8_t* mod_src, const int32_t* pos_src,
+                                      int32_t* uid_dst, uint8_t* mod_dst, int32_t* pos_dst,
+                                      int32_t* src_of_dst, int32_t* shift) {
   constexpr int P = kUnitPer;
-  const int seg = blockIdx.y;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
-  if (u >= n_units) return;
-  if (n_ctx_g[seg] == 0) return;                  // capacity error: no history row is written
-  const size_t ub = static_cast<size_t>(seg) * n_units;
-  const int rk = remap_g[ub + u];
-  if (rk < 0) return;                             // nothing kept (count 0 also for bad units)
-  const int n = len_g[ub + u], f = first_g[ub + u];
-  const WsLayout L = ws_layout(n_units, cap_dst);
-  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
-  const RankRec rec = reinterpret_cast<const RankRec*>(wseg + L.rank_off)[rk];
-  int32_t* shift = reinterpret_cast<int32_t*>(wseg + L.shift_off);
   const size_t sb = static_cast<size_t>(seg) * n_slots;
   const size_t db = static_cast<size_t>(seg) * cap_dst;
-  const uint8_t* m = mask_g + sb;
+  const __amdgpu_buffer_rsrc_t r_mod_s =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(mod_src + sb), 0, n_slots, kBufFlags);
+  const __amdgpu_buffer_rsrc_t r_pos_s = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(pos_src + sb), 0, 4 * n_slots, kBufFlags);
+  const __amdgpu_buffer_rsrc_t r_src =
+      __builtin_amdgcn_make_buffer_rsrc(src_of_dst + db, 0, 4 * cap_dst, kBufFlags);
+  const __amdgpu_buffer_rsrc_t r_uid =
+      __builtin_amdgcn_make_buffer_rsrc(uid_dst + db, 0, 4 * cap_dst, kBufFlags);
+  const __amdgpu_buffer_rsrc_t r_mod =
+      __builtin_amdgcn_make_buffer_rsrc(mod_dst + db, 0, cap_dst, kBufFlags);
+  const __amdgpu_buffer_rsrc_t r_pos =
+      __builtin_amdgcn_make_buffer_rsrc(pos_dst + db, 0, 4 * cap_dst, kBufFlags);
+  const __amdgpu_buffer_rsrc_t r_shift =
+      __builtin_amdgcn_make_buffer_rsrc(shift, 0, 4 * cap_dst, kBufFlags);
   const uintptr_t end = reinterpret_cast<uintptr_t>(m + f + n);
   int carry = 0;                                  // kept slots of the unit before the step
   for (uintptr_t c = block16_floor(m + f); c < end; c += P * kWave) {
@@ -865,7 +877,7 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
       uint8_t b[16] = {};
       if (blk < end) load_block16(blk, b);
 #pragma unroll
-      for (int j = 0; j < P; ++j) keep[j] = s0 + j >= f && s0 + j < f + n && b[j] != 0;
+      for (int j = 0; j < P; ++j) keep[j] = (s0 + j >= f) & (s0 + j < f + n) & (b[j] != 0);
     }
 #pragma unroll
     for (int j = 0; j < P; ++j) nk += keep[j] ? 1 : 0;
@@ -873,20 +885,47 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
     int within = carry + incl - nk;               // kept slots of the unit before s0
 #pragma unroll
     for (int j = 0; j < P; ++j) {
-      if (keep[j]) {
-        const int s = s0 + j;
-        const int r = rec.off + within;
-        const int delb = rec.del + (s - f) - within;   // deleted live slots before s
-        src_of_dst[db + r] = s;
-        uid_dst[db + r] = rk;
-        mod_dst[db + r] = mod_src[sb + s];
-        pos_dst[db + r] = pos_src[sb + s] - delb;
-        shift[r] = -delb;
-        ++within;
-      }
+      const int s = s0 + j;
+      const int r = rec_off + within;
+      const int delb = rec_del + (s - f) - within;   // deleted live slots before s
+      const int so = keep[j] ? s : kOutOfBuf / 4;    // source slot, or past the buffers
+      const int ro = keep[j] ? r : kOutOfBuf / 4;    // destination row, or past the buffers
+      const int mod = __builtin_amdgcn_raw_buffer_load_b8(r_mod_s, so, 0, 0);
+      const int pos = __builtin_amdgcn_raw_buffer_load_b32(r_pos_s, 4 * so, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(s, r_src, 4 * ro, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(rk, r_uid, 4 * ro, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b8(static_cast<uint8_t>(mod), r_mod, ro, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(pos - delb, r_pos, 4 * ro, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(-delb, r_shift, 4 * ro, 0, 0);
+      within += keep[j] ? 1 : 0;
     }
     carry += __shfl(incl, kWave - 1, kWave);
   }
+}
+
+__global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_kernel(
+    const uint8_t* __restrict__ mask_g, const int32_t* __restrict__ len_g,
+    const int32_t* __restrict__ first_g, const uint8_t* __restrict__ mod_src,
+    const int32_t* __restrict__ pos_src, int n_slots, int n_units, int cap_dst,
+    const int32_t* __restrict__ remap_g, const int32_t* __restrict__ n_ctx_g,
+    int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
+    int32_t* __restrict__ src_of_dst, uint8_t* __restrict__ ws) {
+  const int seg = blockIdx.y;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int u = blockIdx.x * kUnitWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (u >= n_units) return;
+  if (n_ctx_g[seg] == 0) return;                  // capacity error: no history row is written
+  const size_t ub = static_cast<size_t>(seg) * n_units;
+  const int rk = remap_g[ub + u];
+  if (rk < 0) return;                             // nothing kept (count 0 also for bad units)
+  const int n = len_g[ub + u], f = first_g[ub + u];
+  const WsLayout L = ws_layout(n_units, cap_dst);
+  uint8_t* wseg = ws + static_cast<size_t>(seg) * L.seg_bytes;
+  const RankRec rec = reinterpret_cast<const RankRec*>(wseg + L.rank_off)[rk];
+  int32_t* shift = reinterpret_cast<int32_t*>(wseg + L.shift_off);
+  const size_t sb = static_cast<size_t>(seg) * n_slots;
+  map_unit_slots(mask_g + sb, f, n, rk, rec.off, rec.del, lane, seg, n_slots, cap_dst, mod_src,
+                 pos_src, uid_dst, mod_dst, pos_dst, src_of_dst, shift);
 }
 
 // Up to kSmallUnits units: the plan over the count kernel's per-unit counts is built in LDS by
@@ -898,7 +937,6 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_fused_ker
     const int32_t* __restrict__ pos_src, int n_slots, int n_units, int chunk_len, int cap_dst,
     int32_t* __restrict__ uid_dst, uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
     int32_t* __restrict__ src_of_dst, uint8_t* __restrict__ ws, FusedPlanArgs fp) {
-  constexpr int P = kUnitPer;
   __shared__ TilePlan<true> plan;
   const int seg = blockIdx.y;
   const WsLayout L = ws_layout(n_units, cap_dst);
@@ -912,7 +950,7 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_fused_ker
   }
   if (plan.kept + chunk_len > cap_dst) return;    // capacity error: no history row is written
   const int lane = threadIdx.x & (kWave - 1);
-  const int u = blockIdx.x * kUnitWaves + threadIdx.x / kWave;
+  const int u = blockIdx.x * kUnitWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (u >= n_units) return;
   const int rk = plan.rank_of[u];
   if (rk < 0) return;                             // nothing kept (count 0 also for bad units)
@@ -921,41 +959,8 @@ __global__ __launch_bounds__(kUnitWaves * kWave) void compact_mask_map_fused_ker
   const int rec_off = plan.roff[rk], rec_del = plan.rdel[rk];
   int32_t* shift = reinterpret_cast<int32_t*>(wseg + L.shift_off);
   const size_t sb = static_cast<size_t>(seg) * n_slots;
-  const size_t db = static_cast<size_t>(seg) * cap_dst;
-  const uint8_t* m = mask_g + sb;
-  const uintptr_t end = reinterpret_cast<uintptr_t>(m + f + n);
-  int carry = 0;                                  // kept slots of the unit before the step
-  for (uintptr_t c = block16_floor(m + f); c < end; c += P * kWave) {
-    const uintptr_t blk = c + P * static_cast<uintptr_t>(lane);
-    const int s0 = static_cast<int>(static_cast<intptr_t>(blk) - reinterpret_cast<intptr_t>(m));
-    bool keep[P];
-    int nk = 0;
-    {
-      uint8_t b[16] = {};
-      if (blk < end) load_block16(blk, b);
-#pragma unroll
-      for (int j = 0; j < P; ++j) keep[j] = s0 + j >= f && s0 + j < f + n && b[j] != 0;
-    }
-#pragma unroll
-    for (int j = 0; j < P; ++j) nk += keep[j] ? 1 : 0;
-    const int incl = wave_inclusive_scan(nk);
-    int within = carry + incl - nk;               // kept slots of the unit before s0
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      if (keep[j]) {
-        const int s = s0 + j;
-        const int r = rec_off + within;
-        const int delb = rec_del + (s - f) - within;   // deleted live slots before s
-        src_of_dst[db + r] = s;
-        uid_dst[db + r] = rk;
-        mod_dst[db + r] = mod_src[sb + s];
-        pos_dst[db + r] = pos_src[sb + s] - delb;
-        shift[r] = -delb;
-        ++within;
-      }
-    }
-    carry += __shfl(incl, kWave - 1, kWave);
-  }
+  map_unit_slots(mask_g + sb, f, n, rk, rec_off, rec_del, lane, seg, n_slots, cap_dst, mod_src,
+                 pos_src, uid_dst, mod_dst, pos_dst, src_of_dst, shift);
 }
 
 }  // namespace

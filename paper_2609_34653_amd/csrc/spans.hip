@@ -56,6 +56,10 @@ __device__ inline SpanWs span_ws(uint8_t* ws, int seg, int n_slots, int n_units)
 }
 
 constexpr int kCensusPer = 16;          // consecutive slots per lane in one census step
+// Buffer resource word 3 for raw (unformatted) 32-bit data on this chip, and a byte offset past
+// any buffer (accesses there read zero and write nothing).
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kOutOfBuffer = 0x7fffffff;
 
 __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
     const uint8_t* __restrict__ mod_g, const int32_t* __restrict__ len_g,
@@ -64,7 +68,7 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
   constexpr int P = kCensusPer;
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
-  const int u = blockIdx.x * kCensusWaves + threadIdx.x / kWave;
+  const int u = blockIdx.x * kCensusWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (u >= n_units) return;
   const SpanWs W = span_ws(ws, seg, n_slots, n_units);
   const size_t ub = static_cast<size_t>(seg) * n_units;
@@ -81,6 +85,8 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
   const uint8_t* seg_tags = mod_g + static_cast<size_t>(seg) * n_slots;
   const uintptr_t blk0 = block16_floor(seg_tags + f);
   const uintptr_t end = reinterpret_cast<uintptr_t>(seg_tags + f + n);
+  const __amdgpu_buffer_rsrc_t info_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(W.info, 0, 4 * n_slots, kBufferFlags);
   int carry_tag = -1;      // tag of the slot before the step (-1 at the unit's start)
   int carry_start = f;     // first slot of the span that slot belongs to
   int carry_text = 0;      // the unit's text tokens before the step
@@ -95,7 +101,7 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
       uint8_t raw[16] = {};
       if (b < end) load_block16(b, raw);
 #pragma unroll
-      for (int j = 0; j < P; ++j) m[j] = (s0 + j >= f && s0 + j < f + n) ? raw[j] : -1;
+      for (int j = 0; j < P; ++j) m[j] = ((s0 + j >= f) & (s0 + j < f + n)) ? raw[j] : -1;
     }
     int prev = __shfl_up(m[P - 1], 1, kWave);
     if (lane == 0) prev = carry_tag;
@@ -113,25 +119,25 @@ __global__ __launch_bounds__(kCensusWaves * kWave) void span_census_kernel(
     const int incl = wave_inclusive_scan(nt);
     const int text_tot = __shfl(incl, kWave - 1, kWave);
     int text_rank = carry_text + incl - nt;        // the unit's text tokens before s0
+    // Branch-free per slot (selects instead of divergent branches); the code of a slot outside
+    // the unit goes to an offset past the buffer, which the hardware drops.
     int pm = prev;
 #pragma unroll
     for (int j = 0; j < P; ++j) {
       const int s = s0 + j;
-      if (m[j] >= 0) {
-        if (m[j] != pm) start = s;
-        const int place = s - start + 1;           // 1-based place in its span
-        int32_t code = kInfoDrop;
-        if (m[j] == OMNITIDE_MOD_TEXT) {
-          code = text_rank++;
-        } else if (m[j] == OMNITIDE_MOD_MARK ||
-                   (m[j] == OMNITIDE_MOD_VIDEO && place <= sink_video) ||
-                   (m[j] == OMNITIDE_MOD_AUDIO && place <= sink_audio)) {
-          code = kInfoSink;
-          ++sinks;
-        }
-        bad |= m[j] > OMNITIDE_MOD_MARK;
-        W.info[static_cast<size_t>(s)] = code;
-      }
+      // (bitwise & and | on the conditions: no short-circuit branches)
+      const bool live = m[j] >= 0;
+      start = (live & (m[j] != pm)) ? s : start;
+      const int place = s - start + 1;             // 1-based place in its span
+      const bool text = m[j] == OMNITIDE_MOD_TEXT;
+      const bool sink = (m[j] == OMNITIDE_MOD_MARK) |
+                        ((m[j] == OMNITIDE_MOD_VIDEO) & (place <= sink_video)) |
+                        ((m[j] == OMNITIDE_MOD_AUDIO) & (place <= sink_audio));
+      const int32_t code = text ? text_rank : (sink ? kInfoSink : kInfoDrop);
+      text_rank += (live & text) ? 1 : 0;
+      sinks += (live & !text & sink) ? 1 : 0;
+      bad |= live & (m[j] > OMNITIDE_MOD_MARK);
+      __builtin_amdgcn_raw_buffer_store_b32(code, info_rsrc, live ? 4 * s : kOutOfBuffer, 0, 0);
       pm = m[j];
     }
     carry_tag = __shfl(m[P - 1], kWave - 1, kWave);
