@@ -185,21 +185,31 @@ __device__ inline void plan_in_lds(int seg, int n_units, int chunk_len, int cap_
     const int u0 = lane * kSmallPer;
     const size_t base = static_cast<size_t>(seg) * U;
     int nl[kSmallPer], fs[kSmallPer], kq[kSmallPer];
+    // all loads first, straight-line (the source of the kept counts is chosen once): one
+    // memory round trip; keep flags become counts after every load is issued
 #pragma unroll
-    for (int i = 0; i < kSmallPer; ++i) {        // all loads first: one memory round trip
+    for (int i = 0; i < kSmallPer; ++i) {
       const int u = min(u0 + i, U - 1);
       nl[i] = f.len[base + u];
       fs[i] = f.first[base + u];
-      kq[i] = f.counts != nullptr     ? f.counts[u]
-              : f.keep_len != nullptr ? f.keep_len[base + u]
-                                      : (f.keep[base + u] != 0 ? INT32_MAX : 0);
+    }
+    const bool flags = f.counts == nullptr && f.keep_len == nullptr;
+    if (f.counts != nullptr) {
+#pragma unroll
+      for (int i = 0; i < kSmallPer; ++i) kq[i] = f.counts[min(u0 + i, U - 1)];
+    } else if (f.keep_len != nullptr) {
+#pragma unroll
+      for (int i = 0; i < kSmallPer; ++i) kq[i] = f.keep_len[base + min(u0 + i, U - 1)];
+    } else {
+#pragma unroll
+      for (int i = 0; i < kSmallPer; ++i) kq[i] = f.keep[base + min(u0 + i, U - 1)];
     }
     int kl[kSmallPer], dl[kSmallPer];
     int my_k = 0, my_d = 0, my_n = 0;
 #pragma unroll
     for (int i = 0; i < kSmallPer; ++i) {
       const int n = (u0 + i < U) ? max(nl[i], 0) : 0;
-      kl[i] = min(max(kq[i], 0), n);
+      kl[i] = flags ? (kq[i] != 0 ? n : 0) : min(max(kq[i], 0), n);
       dl[i] = n - kl[i];
       my_k += kl[i];
       my_d += dl[i];
