@@ -166,6 +166,20 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
   if ((threadIdx.x & (kWave - 1)) == 0 && end > 0) atomicMax(span_g + seg, end);
 }
 
+// Position of set bit number n (0-based) of x; x has more than n set bits.
+__device__ inline int nth_set_bit(uint32_t x, int n) {
+  int pos = 0;
+#pragma unroll
+  for (int width = 16; width >= 1; width >>= 1) {
+    const int c = __popc((x >> pos) & ((1u << width) - 1u));
+    if (n >= c) {
+      n -= c;
+      pos += width;
+    }
+  }
+  return pos;
+}
+
 __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
     const uint32_t* __restrict__ bits_g, int cap, int page_size, int min_pages,
     int32_t* __restrict__ list, int32_t* __restrict__ meta, int32_t* __restrict__ span_g,
@@ -196,16 +210,24 @@ __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
   // thread's slots (the packed span never decreases with c).
   const long limit = static_cast<long>(pages_now - min_pages) * page_size;
   (void)last_before;
+  // Per word: with e entries before slot 32w, slot 32w + j has packed span
+  // (32w + total - e) + z(j), z(j) = empty slots of the word below j (non-decreasing), so the
+  // largest qualifying j is the position of zero number K = limit - (32w + total - e) (or the
+  // word's last slot below the span when it has at most K zeros below it).
   int best = -1;
   if (limit >= 0) {
-    int live_lt = live_before;                      // entries before slot s
+    int live_lt = live_before;                      // entries before slot 32 w
     for (int w = w0; w < w1 && 32 * w < span; ++w) {
       const uint32_t word = bits[w];
-      for (int j = 0; j < 32 && 32 * w + j < span; ++j) {
-        const int s = 32 * w + j;
-        if (s + (total - live_lt) <= limit) best = s;
-        live_lt += (word >> j) & 1u;
+      const int jmax = min(31, span - 1 - 32 * w);  // slots of the word below the span
+      const long K = limit - (32L * w + total - live_lt);
+      if (K >= 0) {
+        const uint32_t valid = jmax == 31 ? ~0u : ((1u << (jmax + 1)) - 1u);
+        const uint32_t zeros = ~word & valid;
+        const int nz_below_max = __popc(zeros & ((1u << jmax) - 1u) & valid);
+        best = 32 * w + (K >= nz_below_max ? jmax : nth_set_bit(zeros, static_cast<int>(K)));
       }
+      live_lt += __popc(word);
     }
   }
   int c;
@@ -338,6 +360,18 @@ __global__ __launch_bounds__(kNatThreads) void place_plan_kernel(
   for (int w = w0; w < w1 && cand < 0; ++w) {
     const uint32_t word = bits[w];
     const int end = min(32 * w + 32, cap);          // slots of this word: [32 w, end)
+    if (chunk_len >= 32) {
+      // A run of chunk_len >= 32 empty slots that ends inside this word ends before the
+      // word's first occupied slot: O(1) per word.
+      const int s = max(32 * w, last + chunk_len);  // first slot ending a long enough run
+      const int first_set = word ? 32 * w + __ffs(word) - 1 : end;
+      if (s < min(first_set, end)) {
+        cand = s - chunk_len + 1;
+        break;
+      }
+      if (word) last = 32 * w + 31 - __clz(word);
+      continue;
+    }
     if (word == 0u) {                               // all empty: the run only grows
       if (last + chunk_len < end) cand = last + 1;
       continue;
