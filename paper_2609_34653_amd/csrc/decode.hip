@@ -316,9 +316,11 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   const float l_col = l_run + __shfl_xor(l_run, 16, kWave) + __shfl_xor(l_run, 32, kWave) +
                       __shfl_xor(l_run, 48, kWave);
   __syncthreads();                         // every wave is done with its V blocks
-  // [wave][D][kMaxQG + 1 columns]: with the padding, the lanes of one store (8 columns x four
-  // lane groups) and the consecutive dims of one load fall in distinct banks
-  constexpr int SCOL = kMaxQG + 1;
+  // [wave][D][SCOL]: the LDS serves 32 lanes a cycle from 32 four-byte banks.  A store covers
+  // 8 columns x lane groups (0, 1) in one half-wave and (2, 3) in the other, i.e. banks
+  // c + 4 g SCOL; a load covers 32 consecutive dims of one column, banks d SCOL.  SCOL = 11
+  // (odd, 4 SCOL = 12 mod 32) keeps both within distinct banks.
+  constexpr int SCOL = kMaxQG + 3;
   float* so = reinterpret_cast<float*>(&vbuf[0][0][0]);
   static_assert(sizeof(vbuf) >= kDecWaves * D * SCOL * sizeof(float), "merge buffer");
   if (g4 == 0) {
