@@ -89,6 +89,20 @@ __device__ inline uint32_t wave_sum_u32(uint32_t v) {
       __builtin_amdgcn_readlane(wave_scan_add_i32(static_cast<int>(v)), kWave - 1));
 }
 
+// Position of set bit number n (0-based) of x; x has more than n set bits.
+__device__ inline int nth_set_bit(uint32_t x, int n) {
+  int pos = 0;
+#pragma unroll
+  for (int width = 16; width >= 1; width >>= 1) {
+    const int c = __popc((x >> pos) & ((1u << width) - 1u));
+    if (n >= c) {
+      n -= c;
+      pos += width;
+    }
+  }
+  return pos;
+}
+
 // Byte arrays walked in 16-byte aligned blocks (absolute addresses): a block that holds a byte
 // of the array is read whole, and its bytes outside the caller's range are ignored.  An aligned
 // block never crosses a page, so the block of a valid byte is always mapped.

@@ -574,130 +574,167 @@ hipError_t launch_copy(const CompactArgs& a, hipStream_t stream) {
 // (2j, 2j+1).  V rows, chunk rows and unshifted rows are copied unchanged.
 // Angles: theta_j and the reduction of shift * theta_j modulo 2 pi in double precision, then a
 // float sine/cosine of the reduced angle; the rotation itself in float, rounded to the storage
-// type (round to nearest even).  One workgroup per 16-row destination tile; the tile's cos/sin
-// table (rows x rot_dims/2) is built in LDS once and shared by all heads.
+// type (round to nearest even).  One workgroup per 16-row tile; the tile's cos / sin table is
+// built in LDS once and shared by all heads.
 constexpr int kMaxHalfRot = 64;     // rot_dims <= head_dim <= 128
 constexpr double kTwoPi = 6.283185307179586476925286766559;
 
-// theta_j = base^(-2j / rot_dims) for j < rot_dims / 2, into LDS.
+// theta_j = base^(-2j / rot_dims) for j < rot_dims / 2, into LDS, by the workgroup's second wave
+// (the first one builds the unit plan meanwhile).
 __device__ inline void rope_thetas(double* theta, double rope_base, int rot_dims) {
-  if (static_cast<int>(threadIdx.x) < rot_dims / 2)
-    theta[threadIdx.x] = pow(rope_base, -2.0 * static_cast<int>(threadIdx.x) / rot_dims);
+  const int j = static_cast<int>(threadIdx.x) - kWave;
+  if (j >= 0 && j < rot_dims / 2) theta[j] = pow(rope_base, -2.0 * j / rot_dims);
 }
 
-// cos / sin of shift * theta_j for each of the tile's rows: the angle reduced modulo 2 pi in
-// double precision, then a float sine and cosine (rows with shift 0: exactly (1, 0)).
+// cos / sin of shift * theta_j, one table row per run of equal shifts among the tile's rows (the
+// rows of a unit share their shift, so a tile mostly needs one or two rows of angles);
+// tab_of[r] = the run of row r.  The angle is reduced modulo 2 pi in double precision, then a
+// float sine and cosine (shift 0: exactly (1, 0)).  Every thread finds the runs itself from
+// shift_row, so filling the table needs no barrier of its own.
 __device__ inline void rope_table(int nrows, int half, const int32_t* shift_row,
-                                  const double* theta, float2 (*cs)[kMaxHalfRot]) {
-  for (int idx = threadIdx.x; idx < nrows * half; idx += kCopyThreads) {
-    const int row = idx / half, j = idx % half;
-    const int sh = shift_row[row];
+                                  const double* theta, float2 (*cs)[kMaxHalfRot],
+                                  int32_t* tab_of) {
+  uint32_t starts = 1u;
+#pragma unroll
+  for (int r = 1; r < kTile; ++r)
+    starts |= (r < nrows && shift_row[r] != shift_row[r - 1]) ? (1u << r) : 0u;
+  const int tid = threadIdx.x;
+  if (tid < nrows) tab_of[tid] = __popc(starts & ((2u << tid) - 1u)) - 1;
+  const int runs = __popc(starts);
+  for (int idx = tid; idx < runs * half; idx += kCopyThreads) {
+    const int k = idx / half, j = idx - k * half;
+    const int sh = shift_row[nth_set_bit(starts, k)];
     float c = 1.f, sn = 0.f;
     if (sh != 0) {
       const double phi = static_cast<double>(sh) * theta[j];
       const double red = fma(-rint(phi * (1.0 / kTwoPi)), kTwoPi, phi);
       sincosf(static_cast<float>(red), &sn, &c);
     }
-    cs[row][j] = make_float2(c, sn);
+    cs[k][j] = make_float2(c, sn);
   }
 }
 
-// K rows of a tile: row r is read through src(r) and written through dst(r) (byte pointers to
-// the row); each pair (x, y) of its first rot_dims dimensions per head turns by the row's
-// angle, (x cos - y sin, x sin + y cos) in float, rounded to the storage type.  IN_PLACE
-// (src == dst): rows with shift 0 and dimensions past rot_dims are left alone; otherwise they
-// are copied bit for bit.  HALF: work item i < rot_dims/(2 EPC) of a head is the chunk pair
-// (i, i + rot_dims/(2 EPC)), the remaining items the chunks past rot_dims; else every chunk is
-// one item whose dimension pairs below rot_dims turn.
-template <int EB, bool HALF, bool IN_PLACE, class SrcF, class DstF>
-__device__ inline void rope_rows(int nrows, int n_kv_heads, int head_dim, int rot_dims,
-                                 const int32_t* shift_row, const float2 (*cs)[kMaxHalfRot],
-                                 SrcF src_of, DstF dst_of) {
-  constexpr int EPC = 16 / EB;                    // elements per 16-byte chunk
-  const int half = rot_dims / 2;
-  const int chunks = head_dim / EPC;
-  const int pair_items = HALF ? half / EPC : 0;
-  const int items = HALF ? pair_items + (head_dim - rot_dims) / EPC : chunks;
-  auto unpack = [](const u32x4& v, float* f) {
+// A tile's K work items in (row, head, item) order.  HALF: item it < pair_items of a head is the
+// chunk pair (it, it + pair_items), which hold the two members of the same dimension pairs; the
+// remaining items are the single chunks past rot_dims.  Otherwise every chunk is one item and
+// turns its own dimension pairs below rot_dims.  Thread tid visits items tid, tid +
+// kCopyThreads, ...; the cursor (row, head, item) steps by kCopyThreads items without a division.
+template <int EB, bool HALF>
+struct RopeItems {
+  static constexpr int EPC = 16 / EB;             // elements per 16-byte chunk
+  int n_kv_heads, rot_dims, chunks, pair_items, per_head;
+  int s_it, s_hd, s_row;                          // one step of kCopyThreads items
+  __device__ RopeItems(int n_kv_heads_, int head_dim, int rot_dims_)
+      : n_kv_heads(n_kv_heads_), rot_dims(rot_dims_), chunks(head_dim / EPC),
+        pair_items(HALF ? rot_dims_ / 2 / EPC : 0),
+        per_head(HALF ? rot_dims_ / 2 / EPC + (head_dim - rot_dims_) / EPC : head_dim / EPC) {
+    const int h = kCopyThreads / per_head;
+    s_it = kCopyThreads - h * per_head;
+    s_hd = h % n_kv_heads;
+    s_row = h / n_kv_heads;
+  }
+  __device__ int count(int nrows) const { return nrows * n_kv_heads * per_head; }
+  __device__ void start(int w, int& row, int& hd, int& it) const {
+    row = w / (n_kv_heads * per_head);
+    const int rem = w - row * n_kv_heads * per_head;
+    hd = rem / per_head;
+    it = rem - hd * per_head;
+  }
+  __device__ void step(int& row, int& hd, int& it) const {
+    it += s_it;                                   // it, s_it < per_head: one carry at most
+    const int c1 = it >= per_head ? 1 : 0;
+    it -= c1 ? per_head : 0;
+    hd += s_hd + c1;                              // hd, s_hd < n_kv_heads: likewise
+    const int c2 = hd >= n_kv_heads ? 1 : 0;
+    hd -= c2 ? n_kv_heads : 0;
+    row += s_row + c2;
+  }
+  __device__ bool pair(int it) const { return HALF && it < pair_items; }
+  // the item's (first) chunk, counted over its row
+  __device__ int chunk(int hd, int it) const {
+    return hd * chunks + (HALF && it >= pair_items ? it + pair_items : it);
+  }
+  // whether the item holds a dimension pair below rot_dims
+  __device__ bool turns(int it) const { return HALF ? it < pair_items : it * EPC < rot_dims; }
+};
+
+template <int EB>
+__device__ inline void unpack_chunk(const u32x4& v, float (&f)[16 / EB]) {
+#pragma unroll
+  for (int e = 0; e < 16 / EB; ++e) {
+    const uint32_t w = v[e * EB / 4];
+    if constexpr (EB == 2) f[e] = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    else f[e] = __uint_as_float(w);
+  }
+}
+
+template <int EB>
+__device__ inline u32x4 pack_chunk(const float (&f)[16 / EB]) {
+  u32x4 v;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if constexpr (EB == 2) {
+      const __bf16 lo = static_cast<__bf16>(f[2 * q]), hi = static_cast<__bf16>(f[2 * q + 1]);
+      v[q] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, lo)) |
+             (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, hi)) << 16);
+    } else {
+      v[q] = __float_as_uint(f[q]);
+    }
+  }
+  return v;
+}
+
+// Turns the dimension pairs of item `it` by the table row tab: (x, y) -> (x cos - y sin,
+// x sin + y cos) in float, rounded to the storage type.  A pair item's members are a and b.
+template <int EB, bool HALF>
+__device__ inline void turn_item(const RopeItems<EB, HALF>& g, int it, const float2* tab,
+                                 u32x4& a, u32x4& b) {
+  constexpr int EPC = 16 / EB;
+  if constexpr (HALF) {
+    float x[EPC], y[EPC];
+    unpack_chunk<EB>(a, x);
+    unpack_chunk<EB>(b, y);
 #pragma unroll
     for (int e = 0; e < EPC; ++e) {
-      const uint32_t w = v[e * EB / 4];
-      if constexpr (EB == 2) f[e] = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
-      else f[e] = __uint_as_float(w);
+      const float2 r = tab[it * EPC + e];
+      const float xe = x[e], ye = y[e];
+      x[e] = fmaf(xe, r.x, -ye * r.y);
+      y[e] = fmaf(xe, r.y, ye * r.x);
     }
-  };
-  auto pack = [](const float* f) {
-    u32x4 v;
+    a = pack_chunk<EB>(x);
+    b = pack_chunk<EB>(y);
+  } else {
+    float f[EPC];
+    unpack_chunk<EB>(a, f);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if constexpr (EB == 2) {
-        const __bf16 lo = static_cast<__bf16>(f[2 * q]), hi = static_cast<__bf16>(f[2 * q + 1]);
-        v[q] = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, lo)) |
-               (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, hi)) << 16);
-      } else {
-        v[q] = __float_as_uint(f[q]);
+    for (int m = 0; m < EPC / 2; ++m) {
+      const int d0 = it * EPC + 2 * m;
+      if (d0 < g.rot_dims) {
+        const float2 r = tab[d0 / 2];
+        const float x = f[2 * m], y = f[2 * m + 1];
+        f[2 * m] = fmaf(x, r.x, -y * r.y);
+        f[2 * m + 1] = fmaf(x, r.y, y * r.x);
       }
     }
-    return v;
-  };
-  for (int w = threadIdx.x; w < nrows * n_kv_heads * items; w += kCopyThreads) {
-    const int row = w / (n_kv_heads * items);
-    const int rem = w % (n_kv_heads * items);
-    const int hd = rem / items, it = rem % items;
-    const bool moved = shift_row[row] != 0;        // unmoved rows keep their bits
-    if (IN_PLACE && !moved) continue;
-    const u32x4* src = reinterpret_cast<const u32x4*>(src_of(row)) + hd * chunks;
-    u32x4* dst = reinterpret_cast<u32x4*>(dst_of(row)) + hd * chunks;
-    const float2* tab = cs[row];
-    if (HALF && it < pair_items) {
-      const int ca = it, cb = it + pair_items;
-      u32x4 va = __builtin_nontemporal_load(src + ca), vb = __builtin_nontemporal_load(src + cb);
-      if (moved) {
-        float a[EPC], bv[EPC];
-        unpack(va, a);
-        unpack(vb, bv);
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) {
-          const float2 r = tab[ca * EPC + e];
-          const float x = a[e], y = bv[e];
-          a[e] = fmaf(x, r.x, -y * r.y);
-          bv[e] = fmaf(x, r.y, y * r.x);
-        }
-        va = pack(a);
-        vb = pack(bv);
-      }
-      __builtin_nontemporal_store(va, dst + ca);
-      __builtin_nontemporal_store(vb, dst + cb);
-    } else {
-      const int c = HALF ? 2 * pair_items + (it - pair_items) : it;
-      const bool turns = !HALF && moved && c * EPC < rot_dims;
-      if (IN_PLACE && !turns) continue;            // nothing in this chunk changes
-      u32x4 v = __builtin_nontemporal_load(src + c);
-      if (turns) {
-        float f[EPC];
-        unpack(v, f);
-#pragma unroll
-        for (int m = 0; m < EPC / 2; ++m) {
-          const int d0 = c * EPC + 2 * m;
-          if (d0 < rot_dims) {
-            const float2 r = tab[d0 / 2];
-            const float x = f[2 * m], y = f[2 * m + 1];
-            f[2 * m] = fmaf(x, r.x, -y * r.y);
-            f[2 * m + 1] = fmaf(x, r.y, y * r.x);
-          }
-        }
-        v = pack(f);
-      }
-      __builtin_nontemporal_store(v, dst + c);
-    }
+    a = pack_chunk<EB>(f);
   }
 }
 
-// Copy with rotary re-encoding of the moved keys (paper: Applying the retention plan -- the
-// position of each retained token drops by the deleted tokens before it, and the cached keys
-// are re-rotated by that shift).  V rows, chunk rows and unshifted rows are copied unchanged.
-// One workgroup per 16-row destination tile; the tile's cos/sin table (rows x rot_dims/2) is
-// built in LDS once and shared by all heads.
+constexpr int kRopeKB = 4;     // K items per thread per batch (a pair item is two vectors)
+constexpr int kRopeVB = 8;     // V vectors per thread per batch
+// s_waitcnt operand for vmcnt(0) alone (gfx9 layout: vmcnt bits 3:0 and 15:14, expcnt 6:4 and
+// lgkmcnt 11:8 at their maxima)
+constexpr int kVmcntZero = 0x0f70;
+
+// A K item's row, head and item index in one register (row < 2^15, head < 2^8, item < 2^8);
+// -1: nothing to do.
+__device__ inline int pack_item(int row, int hd, int it) { return (row << 16) | (hd << 8) | it; }
+
+// Copy with rotary re-encoding of the moved keys (paper: section 5.2, Applying the retention
+// plan): V rows, chunk rows and unshifted rows are copied unchanged.  One workgroup per 16-row
+// destination tile.  Each thread issues the loads of a batch of its V vectors and K items
+// together; the first batch's loads are in flight while the tile's tags are written and its
+// cos / sin table is built in LDS (one row per run of equal shifts, shared by all heads).
 template <int EB, bool HALF, bool FUSED>
 __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     const uint8_t* __restrict__ k_src, const uint8_t* __restrict__ v_src, int n_slots,
@@ -709,9 +746,7 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
     uint8_t* __restrict__ mod_dst, int32_t* __restrict__ pos_dst,
     int32_t* __restrict__ src_of_dst, const int32_t* __restrict__ n_ctx_g,
     const uint8_t* __restrict__ ws, double rope_base, int rot_dims, FusedPlanArgs fp) {
-  __shared__ int32_t src_row[kTile];
-  __shared__ int32_t shift_row[kTile];
-  __shared__ int32_t rank_row[kTile];
+  __shared__ int32_t src_row[kTile], shift_row[kTile], rank_row[kTile], tab_of[kTile];
   __shared__ double theta[kMaxHalfRot];
   __shared__ float2 cs[kTile][kMaxHalfRot];
   __shared__ TilePlan<FUSED> plan;
@@ -734,44 +769,91 @@ __global__ __launch_bounds__(kCopyThreads) void compact_copy_rope_kernel(
                                  src_of_dst, ws, src_row, shift_row, pp, fp.mapped, rank_row);
   if (nrows == 0) return;
   const int r0 = t * kTile;
-  rope_table(nrows, rot_dims / 2, shift_row, theta, cs);
-  __syncthreads();
 
   const int row_bytes = n_kv_heads * head_dim * EB;
   const int row_vecs = row_bytes / 16;
+  const int nv = nrows * row_vecs;
   const size_t src_base = static_cast<size_t>(seg) * n_slots;
   const size_t chunk_base = static_cast<size_t>(seg) * chunk_len;
-  const size_t dst_base = static_cast<size_t>(seg) * cap_dst;
+  // the tile's destination rows are contiguous: vector f of the tile is vector f of these
+  u32x4* const kd = reinterpret_cast<u32x4*>(k_dst + (static_cast<size_t>(seg) * cap_dst + r0) *
+                                                         row_bytes);
+  u32x4* const vd = reinterpret_cast<u32x4*>(v_dst + (static_cast<size_t>(seg) * cap_dst + r0) *
+                                                         row_bytes);
   auto row_src = [&](const uint8_t* pool, const uint8_t* chunk, int row) {
     const int s = src_row[row];
-    return s >= 0 ? pool + (src_base + s) * row_bytes
-                  : chunk + (chunk_base + (-1 - s)) * row_bytes;
+    return reinterpret_cast<const u32x4*>(s >= 0 ? pool + (src_base + s) * row_bytes
+                                                 : chunk + (chunk_base + (-1 - s)) * row_bytes);
   };
-  // V rows: verbatim.
-  for (int f = tid; f < nrows * row_vecs; f += kCopyThreads) {
-    const int row = f / row_vecs, vec = f % row_vecs;
-    const u32x4 x = __builtin_nontemporal_load(
-        reinterpret_cast<const u32x4*>(row_src(v_src, v_chunk, row)) + vec);
-    __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(v_dst + (dst_base + r0 + row) *
-                                                            row_bytes) + vec);
-  }
-  tile_tags(seg, r0, nrows, nctx, n_slots, chunk_len, cap_dst, mod_src, pos_src, chunk_mod,
-            chunk_unit, uid_dst, mod_dst, pos_dst, src_of_dst, src_row, shift_row, rank_row,
-            fp.mapped);
-  rope_rows<EB, HALF, false>(
-      nrows, n_kv_heads, head_dim, rot_dims, shift_row, cs,
-      [&](int row) { return row_src(k_src, k_chunk, row); },
-      [&](int row) { return k_dst + (dst_base + r0 + row) * row_bytes; });
+  const RopeItems<EB, HALF> g(n_kv_heads, head_dim, rot_dims);
+  int kr, kh, ki;
+  g.start(tid, kr, kh, ki);
+  const int s_vr = kCopyThreads / row_vecs, s_vv = kCopyThreads - s_vr * row_vecs;
+  int vr = tid / row_vecs, vv = tid - vr * row_vecs;
+  constexpr int kItemsPerBatch = kCopyThreads * kRopeKB, kVecsPerBatch = kCopyThreads * kRopeVB;
+  const int n_batches = max((g.count(nrows) + kItemsPerBatch - 1) / kItemsPerBatch,
+                            (nv + kVecsPerBatch - 1) / kVecsPerBatch);
+  // one batch: the loads, then (first batch) the tags and the table, then the stores
+  auto batch = [&](int b) {
+    u32x4 va[kRopeVB], ka[kRopeKB], kb[kRopeKB];
+    int kp[kRopeKB];
+#pragma unroll
+    for (int i = 0; i < kRopeVB; ++i) {
+      if (vr < nrows) va[i] = __builtin_nontemporal_load(row_src(v_src, v_chunk, vr) + vv);
+      vv += s_vv;
+      const int c = vv >= row_vecs ? 1 : 0;
+      vv -= c ? row_vecs : 0;
+      vr += s_vr + c;
+    }
+#pragma unroll
+    for (int i = 0; i < kRopeKB; ++i) {
+      kp[i] = kr < nrows ? pack_item(kr, kh, ki) : -1;
+      if (kr < nrows) {
+        const u32x4* src = row_src(k_src, k_chunk, kr) + g.chunk(kh, ki);
+        ka[i] = __builtin_nontemporal_load(src);
+        if (g.pair(ki)) kb[i] = __builtin_nontemporal_load(src + g.pair_items);
+      }
+      g.step(kr, kh, ki);
+    }
+    if (b == 0) {
+      tile_tags(seg, r0, nrows, nctx, n_slots, chunk_len, cap_dst, mod_src, pos_src, chunk_mod,
+                chunk_unit, uid_dst, mod_dst, pos_dst, src_of_dst, src_row, shift_row, rank_row,
+                fp.mapped);
+      rope_table(nrows, rot_dims / 2, shift_row, theta, cs, tab_of);
+      __syncthreads();
+    }
+    // every load of the batch has landed before the first store: the stores, each under its
+    // own condition, then need no wait between them
+    __builtin_amdgcn_s_waitcnt(kVmcntZero);
+#pragma unroll
+    for (int i = 0; i < kRopeVB; ++i) {
+      const int f = tid + kCopyThreads * (b * kRopeVB + i);
+      if (f < nv) __builtin_nontemporal_store(va[i], vd + f);
+    }
+#pragma unroll
+    for (int i = 0; i < kRopeKB; ++i) {
+      if (kp[i] < 0) continue;
+      const int row = kp[i] >> 16, hd = (kp[i] >> 8) & 0xff, it = kp[i] & 0xff;
+      if (shift_row[row] != 0 && g.turns(it))
+        turn_item<EB, HALF>(g, it, cs[tab_of[row]], ka[i], kb[i]);
+      u32x4* dst = kd + row * row_vecs + g.chunk(hd, it);
+      __builtin_nontemporal_store(ka[i], dst);
+      if (g.pair(it)) __builtin_nontemporal_store(kb[i], dst + g.pair_items);
+    }
+  };
+  batch(0);                                      // the first batch on its own, so that no
+  for (int b = 1; b < n_batches; ++b) batch(b);  // wait is placed for a later one's registers
 }
 
 // In-place rotary adjustment of the keys that stay in their slots while their position shifts
 // (native eviction): one workgroup per 16-slot tile of the pool; shift_g holds each slot's
-// position change (0: empty, evicted or unmoved; such rows are not touched).
+// position change (0: empty, evicted or unmoved; such rows are not touched, nor are the chunks
+// past rot_dims).  Batches of a thread's K items as in the rotary copy.
 template <int EB, bool HALF>
 __global__ __launch_bounds__(kCopyThreads) void rope_in_place_kernel(
     uint8_t* __restrict__ k, int cap, int n_kv_heads, int head_dim,
     const int32_t* __restrict__ shift_g, double rope_base, int rot_dims) {
-  __shared__ int32_t shift_row[kTile];
+  __shared__ int32_t shift_row[kTile], tab_of[kTile];
   __shared__ double theta[kMaxHalfRot];
   __shared__ float2 cs[kTile][kMaxHalfRot];
   const int seg = blockIdx.y;
@@ -782,13 +864,45 @@ __global__ __launch_bounds__(kCopyThreads) void rope_in_place_kernel(
   if (tid < kTile) shift_row[tid] = sh;
   rope_thetas(theta, rope_base, rot_dims);
   if (__syncthreads_or(sh != 0) == 0) return;     // nothing in this tile moves
-  rope_table(nrows, rot_dims / 2, shift_row, theta, cs);
-  __syncthreads();
-  const size_t row_bytes = static_cast<size_t>(n_kv_heads) * head_dim * EB;
-  uint8_t* base = k + (static_cast<size_t>(seg) * cap + r0) * row_bytes;
-  auto row_at = [&](int row) { return base + row * row_bytes; };
-  rope_rows<EB, HALF, true>(nrows, n_kv_heads, head_dim, rot_dims, shift_row, cs, row_at,
-                            row_at);
+  const int row_vecs = n_kv_heads * head_dim * EB / 16;
+  u32x4* const base = reinterpret_cast<u32x4*>(
+      k + (static_cast<size_t>(seg) * cap + r0) * n_kv_heads * head_dim * EB);
+  const RopeItems<EB, HALF> g(n_kv_heads, head_dim, rot_dims);
+  int kr, kh, ki;
+  g.start(tid, kr, kh, ki);
+  constexpr int kItemsPerBatch = kCopyThreads * kRopeKB;
+  const int n_batches = (g.count(nrows) + kItemsPerBatch - 1) / kItemsPerBatch;
+  auto batch = [&](int b) {
+    u32x4 ka[kRopeKB], kb[kRopeKB];
+    int kp[kRopeKB];
+#pragma unroll
+    for (int i = 0; i < kRopeKB; ++i) {
+      const bool live = kr < nrows && shift_row[min(kr, kTile - 1)] != 0 && g.turns(ki);
+      kp[i] = live ? pack_item(kr, kh, ki) : -1;
+      if (live) {
+        const u32x4* src = base + kr * row_vecs + g.chunk(kh, ki);
+        ka[i] = __builtin_nontemporal_load(src);
+        if (g.pair(ki)) kb[i] = __builtin_nontemporal_load(src + g.pair_items);
+      }
+      g.step(kr, kh, ki);
+    }
+    if (b == 0) {
+      rope_table(nrows, rot_dims / 2, shift_row, theta, cs, tab_of);
+      __syncthreads();
+    }
+    __builtin_amdgcn_s_waitcnt(kVmcntZero);
+#pragma unroll
+    for (int i = 0; i < kRopeKB; ++i) {
+      if (kp[i] < 0) continue;
+      const int row = kp[i] >> 16, hd = (kp[i] >> 8) & 0xff, it = kp[i] & 0xff;
+      turn_item<EB, HALF>(g, it, cs[tab_of[row]], ka[i], kb[i]);
+      u32x4* dst = base + row * row_vecs + g.chunk(hd, it);
+      __builtin_nontemporal_store(ka[i], dst);
+      if (g.pair(it)) __builtin_nontemporal_store(kb[i], dst + g.pair_items);
+    }
+  };
+  batch(0);
+  for (int b = 1; b < n_batches; ++b) batch(b);
 }
 
 template <int EB, bool HALF, bool FUSED>

@@ -166,20 +166,6 @@ __global__ __launch_bounds__(kCopyThreads) void evict_apply_kernel(
   if ((threadIdx.x & (kWave - 1)) == 0 && end > 0) atomicMax(span_g + seg, end);
 }
 
-// Position of set bit number n (0-based) of x; x has more than n set bits.
-__device__ inline int nth_set_bit(uint32_t x, int n) {
-  int pos = 0;
-#pragma unroll
-  for (int width = 16; width >= 1; width >>= 1) {
-    const int c = __popc((x >> pos) & ((1u << width) - 1u));
-    if (n >= c) {
-      n -= c;
-      pos += width;
-    }
-  }
-  return pos;
-}
-
 __global__ __launch_bounds__(kNatThreads) void suffix_plan_kernel(
     const uint32_t* __restrict__ bits_g, int cap, int page_size, int min_pages,
     int32_t* __restrict__ list, int32_t* __restrict__ meta, int32_t* __restrict__ span_g,
