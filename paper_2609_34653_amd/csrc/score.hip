@@ -8,8 +8,10 @@
 //
 // Work split: each wave owns RPW consecutive slots.  Tags are wave-uniform per row, so the
 // segmentation by unit is scalar control flow: a lane keeps a 64-bit running sum of its share of
-// the current unit and the wave reduces and publishes it (global atomics) only when the unit id
-// changes or its slot range ends.  Rows of empty slots (unit id -1) are never read.
+// the current unit and the wave reduces it when the unit id changes or its slot range ends.  A
+// wave's first and last runs are merged over the workgroup's four waves (64 consecutive slots,
+// mostly one unit) before they are published with global atomics.  Rows of empty slots (unit
+// id -1) are never read.
 #include "common.h"
 #include "kernels.h"
 
@@ -62,6 +64,27 @@ __global__ void score_init_kernel(int total, int n_slots, uint64_t* __restrict__
 }
 
 constexpr int kScoreWaves = 4;
+constexpr int kBufFlags = 0x00020000;     // buffer descriptor word 3 for raw 32-bit accesses
+constexpr int kOutOfBuf = 0x7ffffff0;     // an offset past every buffer view used here
+constexpr int kNontemporal = 2;           // cache policy of a buffer access: nontemporal
+
+// The rows of one unit summed by one wave (or merged over a workgroup's waves).
+struct UnitRun {
+  uint64_t wsum;
+  int unit, cnt, first, last;
+  uint32_t sys;
+};
+
+// Adds a run into the unit's accumulators (order-independent integer atomics).
+__device__ inline void publish_run(const UnitRun& r, uint64_t* wsum, int32_t* len,
+                                   int32_t* first, int32_t* last, uint32_t* flags) {
+  atomicAdd(reinterpret_cast<unsigned long long*>(wsum + r.unit),
+            static_cast<unsigned long long>(r.wsum));
+  atomicAdd(len + r.unit, r.cnt);
+  atomicMin(first + r.unit, r.first);
+  atomicMax(last + r.unit, r.last);
+  if (r.sys) atomicOr(flags + r.unit, 1u);
+}
 
 template <int VPL>
 struct ScoreShape {
@@ -80,10 +103,16 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
   constexpr int RPW = ScoreShape<VPL>::RPW;
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
+  // wave-uniform by construction; the compiler is told, so the buffer view below is scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const long s0 = (static_cast<long>(blockIdx.x) * kScoreWaves + wave) * RPW;
-  if (s0 >= n_slots) return;
-  const int nrows = static_cast<int>(min(static_cast<long>(RPW), n_slots - s0));
+  // a wave past the pool has no rows but still takes part in the workgroup merge
+  const int nrows = static_cast<int>(max(0L, min(static_cast<long>(RPW), n_slots - s0)));
+  __shared__ UnitRun runs[kScoreWaves][2];
+  if (lane == 0) {
+    runs[wave][0].unit = -1;
+    runs[wave][1].unit = -1;
+  }
 
   const size_t tag0 = static_cast<size_t>(seg) * n_slots + s0;
   int uid = -1, mod = 0;
@@ -97,25 +126,33 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
     uid = -1;
   }
   const uint32_t w = mod == 0 ? w0 : mod == 1 ? w1 : mod == 2 ? w2 : w3;
-  const u32x4* rows = k + (static_cast<size_t>(seg) * n_slots + s0) * row_vecs;
+  const u32x4* rows = k + (static_cast<size_t>(seg) * n_slots + min(s0, static_cast<long>(n_slots))) *
+                              row_vecs;
   const size_t uo = static_cast<size_t>(seg) * n_units;
 
   uint64_t acc = 0;       // this lane's share of the current unit's weighted sum
-  int cur = -1, cnt = 0, f = 0, l = 0;
+  int cur = -1, cnt = 0, f = 0, l = 0, n_runs = 0;
   uint32_t sysf = 0;
-  auto flush = [&]() {
+  // A finished run of rows of one unit: the wave's first and last runs go to LDS for the
+  // workgroup merge (neighbouring waves mostly share them); a run between them belongs to this
+  // wave alone and is published at once.
+  auto flush = [&](bool last_run) {
     if (cur < 0) return;
     const uint64_t tot = wave_sum_u64(acc);
-    if (lane == 0) {
-      atomicAdd(reinterpret_cast<unsigned long long*>(wsum + uo + cur),
-                static_cast<unsigned long long>(tot));
-      atomicAdd(len + uo + cur, cnt);
-      atomicMin(first + uo + cur, f);
-      atomicMax(last + uo + cur, l);
-      if (sysf) atomicOr(flags + uo + cur, 1u);
+    if (n_runs == 0 || last_run) {
+      if (lane == 0) runs[wave][n_runs == 0 ? 0 : 1] = UnitRun{tot, cur, cnt, f, l, sysf};
+    } else if (lane == 0) {
+      publish_run(UnitRun{tot, cur, cnt, f, l, sysf}, wsum + uo, len + uo, first + uo, last + uo,
+                  flags + uo);
     }
+    ++n_runs;
   };
 
+  // A buffer view of the wave's rows: the load of an empty slot's row (or of a vector past the
+  // row) gets an offset out of range and returns zeros without a memory access, so every load is
+  // issued whatever the tags say.
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<u32x4*>(rows), 0, 16 * nrows * row_vecs, kBufFlags);
   for (int r0 = 0; r0 < nrows; r0 += RB) {
     u32x4 buf[RB][VPL];
 #pragma unroll
@@ -125,9 +162,9 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
 #pragma unroll
       for (int v = 0; v < VPL; ++v) {
         const int idx = lane + kWave * v;
-        buf[r][v] = u32x4{0, 0, 0, 0};
-        if (u >= 0 && idx < row_vecs)
-          buf[r][v] = __builtin_nontemporal_load(rows + static_cast<size_t>(row) * row_vecs + idx);
+        const int off = (u >= 0 && idx < row_vecs) ? 16 * (row * row_vecs + idx) : kOutOfBuf;
+        buf[r][v] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kNontemporal));
       }
     }
 #pragma unroll
@@ -137,7 +174,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
       const int u = readlane(uid, row);
       if (u < 0) continue;
       if (u != cur) {
-        flush();
+        flush(false);
         cur = u;
         acc = 0;
         cnt = 0;
@@ -153,7 +190,30 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
       sysf |= readlane(mod, row) == 0 ? 1u : 0u;
     }
   }
-  flush();
+  flush(true);
+
+  // Workgroup merge, in slot order: runs of one unit from consecutive waves add up to a single
+  // publication.
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    UnitRun m = runs[0][0];
+#pragma unroll
+    for (int i = 1; i < 2 * kScoreWaves; ++i) {
+      const UnitRun r = runs[i / 2][i % 2];
+      if (r.unit < 0) continue;
+      if (r.unit == m.unit) {
+        m.wsum += r.wsum;
+        m.cnt += r.cnt;
+        m.first = min(m.first, r.first);
+        m.last = max(m.last, r.last);
+        m.sys |= r.sys;
+      } else {
+        if (m.unit >= 0) publish_run(m, wsum + uo, len + uo, first + uo, last + uo, flags + uo);
+        m = r;
+      }
+    }
+    if (m.unit >= 0) publish_run(m, wsum + uo, len + uo, first + uo, last + uo, flags + uo);
+  }
 }
 
 template <bool BF16, int VPL>
