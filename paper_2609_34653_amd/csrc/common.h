@@ -13,6 +13,10 @@ constexpr int kWave = 64;
 // Native 16-byte vector (usable with the nontemporal load/store builtins).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// s_waitcnt operand for vmcnt(0) alone (gfx9 layout: vmcnt bits 3:0 and 15:14, expcnt 6:4 and
+// lgkmcnt 11:8 at their maxima)
+constexpr int kVmcntZero = 0x0f70;
+
 // First error wins: only a zero status word is overwritten.
 __device__ inline void set_status(int32_t* status, int32_t code) {
   if (status != nullptr) atomicCAS(status, 0, code);

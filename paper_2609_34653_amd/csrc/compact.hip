@@ -722,9 +722,6 @@ __device__ inline void turn_item(const RopeItems<EB, HALF>& g, int it, const flo
 
 constexpr int kRopeKB = 4;     // K items per thread per batch (a pair item is two vectors)
 constexpr int kRopeVB = 8;     // V vectors per thread per batch
-// s_waitcnt operand for vmcnt(0) alone (gfx9 layout: vmcnt bits 3:0 and 15:14, expcnt 6:4 and
-// lgkmcnt 11:8 at their maxima)
-constexpr int kVmcntZero = 0x0f70;
 
 // A K item's row, head and item index in one register (row < 2^15, head < 2^8, item < 2^8);
 // -1: nothing to do.

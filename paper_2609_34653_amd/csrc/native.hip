@@ -30,6 +30,7 @@ namespace {
 constexpr int kNatThreads = 1024;
 constexpr int kNatPer = OMNITIDE_MAX_UNITS / kNatThreads;
 constexpr int kRowsPerBlock = 16;
+constexpr int kNatBatch = 8;       // 16-byte vectors of K (and of V) per thread per copy batch
 constexpr int kCopyThreads = 256;
 
 struct UnitRec {
@@ -305,23 +306,43 @@ __global__ __launch_bounds__(kCopyThreads) void suffix_copy_kernel(
   }
   __syncthreads();
   const int vecs = row_bytes / 16;
-  for (int f = tid; f < nr * vecs; f += kCopyThreads) {
-    const int i = f / vecs, e = f % vecs;
-    const int s = src_row[i];
-    if (s < 0) continue;
-    const int r = r0 + i;
-    const size_t scr_off = ((sb + r) * 2) * static_cast<size_t>(row_bytes);
-    const u32x4* ks = reinterpret_cast<const u32x4*>(
-        SCATTER ? scr_rows + scr_off : k + (sb + s) * static_cast<size_t>(row_bytes));
-    const u32x4* vs = reinterpret_cast<const u32x4*>(
-        SCATTER ? scr_rows + scr_off + row_bytes : v + (sb + s) * static_cast<size_t>(row_bytes));
-    u32x4* kd = reinterpret_cast<u32x4*>(
-        SCATTER ? k + (sb + c + r) * static_cast<size_t>(row_bytes) : scr_rows + scr_off);
-    u32x4* vd = reinterpret_cast<u32x4*>(
-        SCATTER ? v + (sb + c + r) * static_cast<size_t>(row_bytes)
-                : scr_rows + scr_off + row_bytes);
-    kd[e] = __builtin_nontemporal_load(ks + e);
-    vd[e] = __builtin_nontemporal_load(vs + e);
+  const int total = nr * vecs;
+  // kNatBatch vectors of K and of V per thread in flight together, then the stores back to back
+  for (int f0 = 0; f0 < total; f0 += kCopyThreads * kNatBatch) {
+    u32x4 kb[kNatBatch], vb[kNatBatch];
+#pragma unroll
+    for (int j = 0; j < kNatBatch; ++j) {
+      const int f = f0 + tid + kCopyThreads * j;
+      const int i = f / vecs, e = f - i * vecs;
+      const int s = f < total ? src_row[i] : -1;
+      if (s < 0) continue;
+      const int r = r0 + i;
+      const size_t scr_off = ((sb + r) * 2) * static_cast<size_t>(row_bytes);
+      const u32x4* ks = reinterpret_cast<const u32x4*>(
+          SCATTER ? scr_rows + scr_off : k + (sb + s) * static_cast<size_t>(row_bytes));
+      const u32x4* vs = reinterpret_cast<const u32x4*>(
+          SCATTER ? scr_rows + scr_off + row_bytes
+                  : v + (sb + s) * static_cast<size_t>(row_bytes));
+      kb[j] = __builtin_nontemporal_load(ks + e);
+      vb[j] = __builtin_nontemporal_load(vs + e);
+    }
+    __builtin_amdgcn_s_waitcnt(kVmcntZero);
+#pragma unroll
+    for (int j = 0; j < kNatBatch; ++j) {
+      const int f = f0 + tid + kCopyThreads * j;
+      const int i = f / vecs, e = f - i * vecs;
+      const int s = f < total ? src_row[i] : -1;
+      if (s < 0) continue;
+      const int r = r0 + i;
+      const size_t scr_off = ((sb + r) * 2) * static_cast<size_t>(row_bytes);
+      u32x4* kd = reinterpret_cast<u32x4*>(
+          SCATTER ? k + (sb + c + r) * static_cast<size_t>(row_bytes) : scr_rows + scr_off);
+      u32x4* vd = reinterpret_cast<u32x4*>(
+          SCATTER ? v + (sb + c + r) * static_cast<size_t>(row_bytes)
+                  : scr_rows + scr_off + row_bytes);
+      kd[e] = kb[j];
+      vd[e] = vb[j];
+    }
   }
 }
 
@@ -409,12 +430,27 @@ __global__ __launch_bounds__(kCopyThreads) void chunk_write_kernel(
     pos_g[sb + s + i] = kept_g[seg] + i;
   }
   const int vecs = row_bytes / 16;
-  for (int f = tid; f < nr * vecs; f += kCopyThreads) {
-    const int i = r0 + f / vecs, e = f % vecs;
-    const u32x4* ks = reinterpret_cast<const u32x4*>(k_chunk + (cb + i) * row_bytes);
-    const u32x4* vs = reinterpret_cast<const u32x4*>(v_chunk + (cb + i) * row_bytes);
-    reinterpret_cast<u32x4*>(k + (sb + s + i) * static_cast<size_t>(row_bytes))[e] = ks[e];
-    reinterpret_cast<u32x4*>(v + (sb + s + i) * static_cast<size_t>(row_bytes))[e] = vs[e];
+  const int total = nr * vecs;
+  // kNatBatch vectors of K and of V per thread in flight together, then the stores back to back
+  for (int f0 = 0; f0 < total; f0 += kCopyThreads * kNatBatch) {
+    u32x4 kb[kNatBatch], vb[kNatBatch];
+#pragma unroll
+    for (int j = 0; j < kNatBatch; ++j) {
+      const int f = f0 + tid + kCopyThreads * j;
+      if (f >= total) continue;
+      const int i = r0 + f / vecs, e = f % vecs;
+      kb[j] = reinterpret_cast<const u32x4*>(k_chunk + (cb + i) * row_bytes)[e];
+      vb[j] = reinterpret_cast<const u32x4*>(v_chunk + (cb + i) * row_bytes)[e];
+    }
+    __builtin_amdgcn_s_waitcnt(kVmcntZero);
+#pragma unroll
+    for (int j = 0; j < kNatBatch; ++j) {
+      const int f = f0 + tid + kCopyThreads * j;
+      if (f >= total) continue;
+      const int i = r0 + f / vecs, e = f % vecs;
+      reinterpret_cast<u32x4*>(k + (sb + s + i) * static_cast<size_t>(row_bytes))[e] = kb[j];
+      reinterpret_cast<u32x4*>(v + (sb + s + i) * static_cast<size_t>(row_bytes))[e] = vb[j];
+    }
   }
 }
 
