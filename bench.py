@@ -35,17 +35,17 @@ CSRC = os.path.join(ROOT, "paper_2609_34653_amd", "csrc")
 # --no-other-configs --copy-calibration-mb 1024` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch,
 # summed over the stage's kernels).  Scaled by what the same
 # counters read for the calibration copy (1 GiB read + 1 GiB written by one elementwise kernel):
-# FETCH_SIZE reads 524,302 KiB for 1,048,576 KiB fetched (x2.000), WRITE_SIZE reads 1,048,576 KiB
+# FETCH_SIZE reads 524,297 KiB for 1,048,576 KiB fetched (x2.000), WRITE_SIZE reads 1,048,576 KiB
 # (x1.000).  Each entry carries a hash of the sources of its kernels and is reported only while
 # they are unchanged (otherwise null: the counters describe other code).
 FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 COUNTER_TRAFFIC = {
-    "score": (("score.hip", "common.h"), "46a9a171dafd4b1d", 57068.4, 490.7),
-    "select": (("select.hip", "common.h"), "61b3be946f7bfd15", 20.6, 3.0),
-    "compact": (("compact.hip", "common.h"), "2a97c3e8c4cc769a", 34169.7, 68126.8),
-    "attend": (("attention.hip", "combine.h", "common.h"), "f4c038b004d2a541", 54334.1, 43058.8),
-    "compact_rope": (("compact.hip", "common.h"), "2a97c3e8c4cc769a", 34173.0, 68026.7),
-    "decode": (("decode.hip", "combine.h", "common.h"), "39dd25c90d8abd01", 34358.5, 536.0),
+    "score": (("score.hip", "common.h"), "de1fdff5d2812b39", 57104.7, 161.3),
+    "select": (("select.hip", "common.h"), "3b421e2e735569a4", 20.6, 3.0),
+    "compact": (("compact.hip", "common.h"), "24dbee1220980cfc", 34169.7, 68112.2),
+    "attend": (("attention.hip", "combine.h", "common.h"), "d63ac68aa9ca9311", 54333.9, 43058.8),
+    "compact_rope": (("compact.hip", "common.h"), "24dbee1220980cfc", 34232.0, 68038.0),
+    "decode": (("decode.hip", "combine.h", "common.h"), "fa19aaa661646b8a", 34358.5, 536.0),
 }
 
 
@@ -53,7 +53,7 @@ COUNTER_TRAFFIC = {
 # `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0 --no-other-configs`:
 # SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1,024 SIMDs) per dispatch (the MFMA-only
 # probe reads 0.97 with this normalisation); keyed by the kernel's sources like COUNTER_TRAFFIC.
-MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "f4c038b004d2a541", 0.541)
+MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "d63ac68aa9ca9311", 0.527)
 
 
 def mfma_busy(config):
