@@ -12,7 +12,8 @@
 // Mask: a count kernel (one wave per unit) gives each unit its kept count, the plan kernel
 // scans those, and a map kernel (one wave per unit, one aligned 16-byte block of the mask per
 // lane, an in-lane count plus one wave scan per 1,024 slots) writes each kept slot's
-// destination row, its tags and its position shift.
+// destination row, its tags and its position shift.  Up to 512 units the map kernel builds the
+// unit plan in LDS itself (as the copy workgroups do), so no plan kernel runs.
 // Copy: one workgroup per destination tile of kTile rows.  The tile's rows are resolved to
 // source slots (binary search over the LDS table, or a short forward walk from the workspace
 // hint), then every thread moves 16-byte vectors of the K and V rows, and the rows' tags are

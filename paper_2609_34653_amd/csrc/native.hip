@@ -19,7 +19,8 @@
 //   suffix_scatter workspace -> slots c + rank, vacated slots marked empty.  A destination can
 //                  be the source of an earlier entry, hence the round trip through scratch.
 //   place_plan     one workgroup per segment: the lowest slot s with [s, s + L) empty, from a
-//                  running "last occupied slot" carried across threads.
+//                  running "last occupied slot" carried across threads (for L >= 32 decided
+//                  per bitmap word, since such a run must contain a whole empty word).
 //   chunk_write    the chunk's K/V rows and tags into [s, s + L).
 #include "common.h"
 #include "kernels.h"
