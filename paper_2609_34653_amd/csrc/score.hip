@@ -88,23 +88,26 @@ __device__ inline void publish_run(const UnitRun& r, uint64_t* wsum, int32_t* le
 
 // Rows per wave, and rows whose loads a wave issues as one batch before their arithmetic.  With
 // the unconditional buffer loads the waits are graded (the compiler moves later rows' loads up
-// past earlier rows' arithmetic), and small batches measured fastest: at 2 KB rows, one row per
-// batch 25.0 us per call on the 80K history, two 25.1, four 25.4, eight 26.2.
-template <int VPL>
+// past earlier rows' arithmetic).  When the grid holds enough waves to keep the memory system
+// busy, small batches measured fastest (2 KB rows, 80K-slot pool, 5,120 waves: one row per batch
+// 25.0 us per call, two 25.1, four 25.4, eight 26.2); a small pool needs the deep batches for
+// enough loads in flight (8K-slot pool, 512 waves: 10.3 us with eight rows, 15.0 us with one).
+template <int VPL, bool DEEP>
 struct ScoreShape {
-  static constexpr int RB = VPL >= 2 ? 1 : 2;
+  static constexpr int RB = DEEP ? (VPL >= 16 ? 1 : 16 / VPL) : (VPL >= 2 ? 1 : 2);
   static constexpr int RPW = 16;
 };
+constexpr long kShallowMinWaves = 4096;   // four waves per SIMD of the whole chip
 
-template <bool BF16, int VPL>
+template <bool BF16, int VPL, bool DEEP>
 __global__ __launch_bounds__(kScoreWaves * kWave) void score_kernel(
     const u32x4* __restrict__ k, int n_slots, int row_vecs, const int32_t* __restrict__ unit_id,
     const uint8_t* __restrict__ modality, uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
     int n_units, uint64_t* __restrict__ wsum, int32_t* __restrict__ len,
     int32_t* __restrict__ first, int32_t* __restrict__ last, uint32_t* __restrict__ flags,
     int32_t* __restrict__ status) {
-  constexpr int RB = ScoreShape<VPL>::RB;
-  constexpr int RPW = ScoreShape<VPL>::RPW;
+  constexpr int RB = ScoreShape<VPL, DEEP>::RB;
+  constexpr int RPW = ScoreShape<VPL, DEEP>::RPW;
   const int seg = blockIdx.y;
   const int lane = threadIdx.x & (kWave - 1);
   // wave-uniform by construction; the compiler is told, so the buffer view below is scalar
@@ -225,13 +228,21 @@ hipError_t launch_score_t(const void* k, int n_seg, int n_slots, int row_vecs,
                           const int32_t* unit_id, const uint8_t* modality, const uint32_t wq[4],
                           int n_units, uint64_t* wsum, int32_t* len, int32_t* first,
                           int32_t* last, uint32_t* flags, int32_t* status, hipStream_t stream) {
-  constexpr int RPW = ScoreShape<VPL>::RPW;
+  constexpr int RPW = ScoreShape<VPL, false>::RPW;
+  static_assert(ScoreShape<VPL, true>::RPW == RPW, "one grid for both shapes");
   const long waves = (static_cast<long>(n_slots) + RPW - 1) / RPW;
   const dim3 grid(static_cast<unsigned>((waves + kScoreWaves - 1) / kScoreWaves),
                   static_cast<unsigned>(n_seg));
-  hipLaunchKernelGGL((score_kernel<BF16, VPL>), grid, dim3(kScoreWaves * kWave), 0, stream,
-                     static_cast<const u32x4*>(k), n_slots, row_vecs, unit_id, modality, wq[0],
-                     wq[1], wq[2], wq[3], n_units, wsum, len, first, last, flags, status);
+  if (waves * n_seg >= kShallowMinWaves)
+    hipLaunchKernelGGL((score_kernel<BF16, VPL, false>), grid, dim3(kScoreWaves * kWave), 0,
+                       stream, static_cast<const u32x4*>(k), n_slots, row_vecs, unit_id,
+                       modality, wq[0], wq[1], wq[2], wq[3], n_units, wsum, len, first, last,
+                       flags, status);
+  else
+    hipLaunchKernelGGL((score_kernel<BF16, VPL, true>), grid, dim3(kScoreWaves * kWave), 0,
+                       stream, static_cast<const u32x4*>(k), n_slots, row_vecs, unit_id,
+                       modality, wq[0], wq[1], wq[2], wq[3], n_units, wsum, len, first, last,
+                       flags, status);
   return hipGetLastError();
 }
 
