@@ -1,8 +1,8 @@
 """HIP unit scoring (omnitide_score_units) vs the oracle, bit for bit, called directly through the
 C ABI: every row width the kernel specialises (16-byte vectors per lane 1, 2, 4, 8 and 16,
 full and partial), bf16 and float32 pools, two segments, units as runs with holes and units
-scattered over the pool, and special key values (NaN, infinities, subnormals, zeros, values past
-the clamp).
+scattered over the pool, special key values (NaN, infinities, subnormals, zeros, values past
+the clamp), and both load-batch depths (small grids, and grids of at least 4,096 waves).
 """
 import numpy as np
 import pytest
@@ -57,6 +57,9 @@ def random_keys(rng, shape, dtype):
     (1, 900, 32, 128, "bf16", 20, False),   # 512 vectors: eight per lane
     (1, 700, 12, 128, "f32", 9, False),     # 384 vectors: eight per lane, partial
     (1, 600, 32, 128, "f32", 12, True),     # 1,024 vectors: sixteen per lane
+    # grids of at least 4,096 waves take the one-row batches (the 80K and 36-layer workloads)
+    (4, 16384, 3, 64, "f32", 200, False),   # 48 vectors per row, partial, shallow batches
+    (2, 32768, 8, 128, "f32", 300, True),   # 256 vectors: four per lane, shallow batches
 ])
 def test_score_units_bit_exact(n_seg, n_slots, H, d, dtype, n_units, scattered):
     from paper_2609_34653_amd import omnitide as ot
