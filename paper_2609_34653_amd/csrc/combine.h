@@ -86,6 +86,95 @@ __global__ __launch_bounds__(BLOCK) void attn_combine_kernel(const float* __rest
              num.w * inv);
 }
 
+// Quad reductions (lanes 4i .. 4i+3) by DPP moves; every lane of the quad must be active.
+constexpr int kDppQuadSwap1 = 0xb1;   // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadSwap2 = 0x4e;   // quad_perm [2, 3, 0, 1]
+template <int CTRL>
+__device__ inline float quad_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+__device__ inline float quad_max(float v) {
+  v = fmaxf(v, quad_move<kDppQuadSwap1>(v));
+  return fmaxf(v, quad_move<kDppQuadSwap2>(v));
+}
+__device__ inline float quad_sum(float v) {
+  v += quad_move<kDppQuadSwap1>(v);
+  return v + quad_move<kDppQuadSwap2>(v);
+}
+
+// Many splits and few rows (decode): the four lanes of a quad share one row's four output values
+// and take every fourth split each (all of a lane's loads in flight together); each lane keeps a
+// running (M, num, den) as above, and the quad then merges its four by DPP moves: rescaled to
+// the quad's maximum and summed (a fixed order, so the result is deterministic).  A row is
+// D/4 quads, 2 rows per 256-thread workgroup at D = 128; a wave never straddles two rows.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_quad_kernel(const float* __restrict__ part_o,
+                                                              const float* __restrict__ part_ml,
+                                                              int n_split, size_t n_rows,
+                                                              const int32_t* __restrict__ n_ctx_g,
+                                                              int L, int Hq, int cap,
+                                                              void* __restrict__ out,
+                                                              bool out_bf16) {
+  constexpr int kTPS = 4;                          // lanes per (row, four values)
+  constexpr int TPR = D / 4 * kTPS;                // threads per row
+  static_assert(TPR % kWave == 0 && 256 % TPR == 0, "whole waves per row");
+  constexpr int kPer = 8;                          // splits per lane per load batch
+  const size_t row = static_cast<size_t>(blockIdx.x) * (256 / TPR) + threadIdx.x / TPR;
+  if (row >= n_rows) return;                       // whole waves
+  const int seg = static_cast<int>(row / (static_cast<size_t>(L) * Hq));
+  const int nctx = n_ctx_g[seg];
+  const int within = threadIdx.x % TPR;
+  const int d4 = within / kTPS, ts = within % kTPS;
+  float M = -INFINITY, den = 0.f;
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = ts; s0 < n_split; s0 += kTPS * kPer) {
+    float2 ml[kPer];
+    float4 ov[kPer];
+#pragma unroll
+    for (int c = 0; c < kPer; ++c) {
+      const int sp = s0 + kTPS * c;
+      const size_t pr = static_cast<size_t>(sp) * n_rows + row;
+      const bool in = sp < n_split;
+      ml[c] = in ? *reinterpret_cast<const float2*>(part_ml + 2 * pr) : make_float2(-INFINITY, 0.f);
+      ov[c] = in ? *reinterpret_cast<const float4*>(part_o + pr * D + 4 * d4)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    float cm = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < kPer; ++c) cm = fmaxf(cm, ml[c].x);
+    const float Mn = fmaxf(M, cm);
+    if (Mn == -INFINITY) continue;
+    const float a = M == -INFINITY ? 0.f : exp2f(M - Mn);
+    den *= a;
+    num.x *= a;
+    num.y *= a;
+    num.z *= a;
+    num.w *= a;
+#pragma unroll
+    for (int c = 0; c < kPer; ++c) {
+      const float w = ml[c].x == -INFINITY ? 0.f : exp2f(ml[c].x - Mn);
+      den = fmaf(w, ml[c].y, den);
+      num.x = fmaf(w, ov[c].x, num.x);
+      num.y = fmaf(w, ov[c].y, num.y);
+      num.z = fmaf(w, ov[c].z, num.z);
+      num.w = fmaf(w, ov[c].w, num.w);
+    }
+    M = Mn;
+  }
+  const float Mq = quad_max(M);
+  // a lane without a visible key adds nothing (if no lane has one, every output is zero)
+  const float a = (M == -INFINITY) ? 0.f : exp2f(M - Mq);
+  den = quad_sum(den * a);
+  num.x = quad_sum(num.x * a);
+  num.y = quad_sum(num.y * a);
+  num.z = quad_sum(num.z * a);
+  num.w = quad_sum(num.w * a);
+  if (ts != 0 || nctx < L || nctx > cap) return;
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  store_out4(out, row * D + 4 * d4, out_bf16, num.x * inv, num.y * inv, num.z * inv,
+             num.w * inv);
+}
+
 // Launch the combine for n_rows rows.
 template <int D>
 hipError_t launch_combine(const float* part_o, const float* part_ml, int n_split, size_t n_rows,
@@ -100,12 +189,11 @@ hipError_t launch_combine(const float* part_o, const float* part_ml, int n_split
     hipLaunchKernelGGL((attn_combine_kernel<D, 16>), dim3(blocks), dim3(256), 0, stream, part_o,
                        part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out, out_bf16);
   else
-    // many splits and few rows (decode): two rows per 64-thread block, so that the loads of the
-    // partials spread over more CUs
-    hipLaunchKernelGGL((attn_combine_kernel<D, 32, 64>),
-                       dim3(static_cast<unsigned>((n_rows + 64 / (D / 4) - 1) / (64 / (D / 4)))),
-                       dim3(64), 0, stream, part_o, part_ml, n_split, n_rows, n_ctx, L, Hq, cap,
-                       out, out_bf16);
+    // many splits and few rows (decode): four lanes per output quad share the splits
+    hipLaunchKernelGGL((attn_combine_quad_kernel<D>),
+                       dim3(static_cast<unsigned>((n_rows + 256 / D - 1) / (256 / D))), dim3(256),
+                       0, stream, part_o, part_ml, n_split, n_rows, n_ctx, L, Hq, cap, out,
+                       out_bf16);
   return hipGetLastError();
 }
 
