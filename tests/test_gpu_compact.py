@@ -1,8 +1,9 @@
 """HIP compaction (omnitide_compact_kv) vs the oracle, bit for bit, called directly through the C
 ABI on layouts built here: every row size the copy kernel specialises (1, 2, 4 and 8 vectors
 per thread, a partial row), bf16 and float32, two segments, more than 512 units (the separate
-plan kernel), and a random keep set with holes between the units.  K/V rows of the destination
-must equal the oracle's bytes, and every tag row (the tail included) its value.
+plan kernel, also feeding the rotary copy), and a random keep set with holes between the units.
+K/V rows of the destination must equal the oracle's bytes (rotated keys: the rotary bar), and
+every tag row (the tail included) its value.
 """
 import numpy as np
 import pytest
@@ -56,6 +57,21 @@ def pool(rng, shape, dtype):
     (1, 6000, 8, 128, "bf16", 600, 100, 64),  # 600 units: the plan kernel, then the copy
 ])
 def test_compact_kv_bit_exact(n_seg, n_slots, H, d, dtype, n_units, L, page):
+    run_and_check(n_seg, n_slots, H, d, dtype, n_units, L, page)
+
+
+@pytest.mark.parametrize("n_seg,n_slots,H,d,dtype,n_units,L,page,rope", [
+    (1, 6000, 8, 128, "bf16", 600, 100, 64, (1.0e6, 128, 0)),    # plan kernel, split halves
+    (2, 3000, 4, 64, "f32", 700, 40, 32, (10000.0, 48, 1)),     # float32, interleaved, R < d
+])
+def test_compact_kv_rope_plan_kernel(n_seg, n_slots, H, d, dtype, n_units, L, page, rope):
+    """Rotary compaction with more than 512 units (the separate plan kernel feeds the rotary
+    copy): tags, V rows, chunk rows, unshifted rows and dimensions past the rotary width
+    bit-exact; rotated elements at the rotary parity bar."""
+    run_and_check(n_seg, n_slots, H, d, dtype, n_units, L, page, rope)
+
+
+def run_and_check(n_seg, n_slots, H, d, dtype, n_units, L, page, rope=None):
     from paper_2609_34653_amd import omnitide as ot
     rng = np.random.default_rng(n_slots + n_units + H)
     lays = [random_layout(rng, n_slots, n_units) for _ in range(n_seg)]
@@ -90,12 +106,15 @@ def test_compact_kv_bit_exact(n_seg, n_slots, H, d, dtype, n_units, L, page):
     ws = torch.full((max(1, ot.omnitide_compact_workspace_bytes(n_seg, n_units, cap)),), 0xFF,
                     dtype=torch.uint8, device="cuda")
     st = torch.zeros(1, **i32)
-    ot.omnitide_compact_kv(
-        k_src.cuda(), v_src.cuda(), page, dev(np.concatenate([x[0] for x in lays])),
-        dev(np.concatenate([x[1] for x in lays])), dev(np.concatenate([x[2] for x in lays])),
-        dev(np.concatenate(keeps)), dev(unit_len.ravel()), dev(unit_first.ravel()), n_units,
-        k_chunk.cuda(), v_chunk.cuda(), dev(chunk_mod), dev(chunk_unit), k_dst, v_dst, uid_dst,
-        mod_dst, pos_dst, src_dst, remap, n_ctx, n_pages, ws, st)
+    args = (k_src.cuda(), v_src.cuda(), page, dev(np.concatenate([x[0] for x in lays])),
+            dev(np.concatenate([x[1] for x in lays])), dev(np.concatenate([x[2] for x in lays])),
+            dev(np.concatenate(keeps)), dev(unit_len.ravel()), dev(unit_first.ravel()), n_units,
+            k_chunk.cuda(), v_chunk.cuda(), dev(chunk_mod), dev(chunk_unit), k_dst, v_dst,
+            uid_dst, mod_dst, pos_dst, src_dst, remap, n_ctx, n_pages, ws)
+    if rope is None:
+        ot.omnitide_compact_kv(*args, st)
+    else:
+        ot.omnitide_compact_kv_rope(*args, rope[0], rope[1], rope[2], d_status=st)
     torch.cuda.synchronize()
     assert int(st.item()) == 0
     kd, vd = storage_np(k_dst), storage_np(v_dst)
@@ -104,15 +123,42 @@ def test_compact_kv_bit_exact(n_seg, n_slots, H, d, dtype, n_units, L, page):
                           ("src_of_dst", src_dst), ("unit_remap", remap))}
     for s in range(n_seg):
         uid, mod, pos = lays[s]
+        style = None if rope is None else ("half", "interleaved")[rope[2]]
         cp = oracle.compact_kv(storage_np(k_src[s]), storage_np(v_src[s]), uid, mod, pos,
                                keeps[s], n_units, storage_np(k_chunk[s]), storage_np(v_chunk[s]),
-                               chunk_mod, chunk_unit, cap, page)
+                               chunk_mod, chunk_unit, cap, page,
+                               rope=None if rope is None else
+                               dict(base=rope[0], dims=rope[1], style=style, dtype=dtype))
         n = cp["n_ctx"]
         assert n == kept[s] + L
         assert int(n_ctx[s]) == n and int(n_pages[s]) == cp["n_pages"]
-        assert np.array_equal(kd[s][:n], cp["k"]) and np.array_equal(vd[s][:n], cp["v"])
+        assert np.array_equal(vd[s][:n], cp["v"])
+        if rope is None:
+            assert np.array_equal(kd[s][:n], cp["k"])
+        else:
+            check_rotated(kd[s][:n], cp, pos, dtype, rope[1], style)
         for nm in ("unit_id", "modality", "pos", "src_of_dst"):
             assert np.array_equal(tags[nm][s][:n].astype(np.int64), cp[nm].astype(np.int64)), nm
         assert np.all(tags["unit_id"][s][n:] == -1) and np.all(tags["modality"][s][n:] == 0)
         assert np.all(tags["pos"][s][n:] == -1) and np.all(tags["src_of_dst"][s][n:] == -1)
         assert np.array_equal(tags["unit_remap"][s].astype(np.int64), cp["unit_remap"])
+
+
+def check_rotated(got_bits, cp, pos_src, dtype, rot_dims, style):
+    """Rotary compaction bar (as in test_gpu_rope): rows whose position does not change and
+    dimensions past the rotary width bit-exact; rotated elements within half an ulp of the exact
+    rotation plus 2^-21 of their pair's length."""
+    from tests.test_gpu_rope import pair_norm, ulp
+    n = got_bits.shape[0]
+    shift = np.zeros(n, np.int64)
+    kept = cp["kept"]
+    shift[:kept] = cp["pos"][:kept] - np.asarray(pos_src)[cp["src_of_dst"][:kept]]
+    assert np.any(shift != 0), "the layout must move some rows"
+    same = shift == 0
+    assert np.array_equal(got_bits[same], cp["k"][same])
+    assert np.array_equal(got_bits[..., rot_dims:], cp["k"][..., rot_dims:])
+    got = oracle.to_f64(got_bits, dtype)[~same][..., :rot_dims]
+    want = cp["k_f64"][~same][..., :rot_dims]
+    src = oracle.to_f64(cp["k"], dtype)[~same]
+    bound = 0.5 * ulp(want, dtype) + 2.0 ** -21 * pair_norm(src, rot_dims, style)[..., :rot_dims]
+    assert np.all(np.abs(got - want) <= bound)
