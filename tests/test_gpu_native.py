@@ -508,3 +508,135 @@ def test_evict_native_rope_then_span_attention_equals_compaction():
     torch.cuda.synchronize()
     assert int(host(g["st"])[0]) == 0 and int(host(st.d_status)[0]) == 0
     assert np.abs(host(out_n) - host(st.out)).max() <= 2e-3
+
+
+def test_stream_loop_native_layouts_chained():
+    """The stream loop's native and ordered-suffix (11 pages of 64 slots) layouts chained on the
+    device for 24 steps, each step applying the whole-unit selection of the eager step (the
+    unit ids of all layouts coincide).  Against the oracle chained on its own outputs (its own
+    score and select of its own eager chain): eviction, suffix packing and chunk placement
+    bit-exact at every step (every tag row, the chunk slot, the span, the kept count), the K/V
+    bytes of every occupied slot and span attention on every query row after steps 12 and 24."""
+    from paper_2609_34653_amd import omnitide as ot
+    from paper_2609_34653_amd.step import StreamStep
+    cfg = sg.CONFIG_BY_NAME["stream_loop_64x665"]
+    stream = sg.make_stream(cfg)
+    lay, seg0 = stream.layout, stream.segment(0)
+    U, L, page, steps = 512, lay.chunk_len, 64, 24
+    H, d, Hq = cfg.n_kv_heads, cfg.head_dim, cfg.n_q_heads
+    cap_e, cap_n = cfg.budget + L, 65536
+    i32 = dict(dtype=torch.int32, device="cuda")
+    pad = cap_n - lay.n_slots
+    # eager chains: the device's drives the device layouts, the oracle's the oracle layouts
+    src = dict(k=seg0.k_hist.cuda()[None], v=seg0.v_hist.cuda()[None], uid=dev(lay.unit_id),
+               mod=dev(lay.modality), pos=dev(lay.pos))
+    e_k, e_v = storage_np(seg0.k_hist), storage_np(seg0.v_hist)
+    e_uid, e_mod, e_pos = lay.unit_id.astype(np.int64), lay.modality, lay.pos
+    k0 = np.zeros((cap_n,) + e_k.shape[1:], e_k.dtype)
+    k0[:lay.n_slots] = e_k
+    v0 = np.zeros_like(k0)
+    v0[:lay.n_slots] = e_v
+    tags0 = (np.concatenate([lay.unit_id, np.full(pad, -1)]).astype(np.int64),
+             np.concatenate([lay.modality, np.full(pad, 1)]).astype(np.uint8),
+             np.concatenate([lay.pos, np.full(pad, -1)]).astype(np.int64))
+    layouts = {}
+    for name, T in (("native", 0), ("ordered_suffix", 11)):
+        kd = torch.from_numpy(k0.view(np.int16)).view(torch.bfloat16).cuda()[None].contiguous()
+        vd = torch.from_numpy(v0.view(np.int16)).view(torch.bfloat16).cuda()[None].contiguous()
+        layouts[name] = dict(
+            T=T, k=kd, v=vd, uid=dev(tags0[0].astype(np.int32)), mod=dev(tags0[1]),
+            pos=dev(tags0[2].astype(np.int32)), remap=torch.zeros(U, **i32),
+            kept=torch.zeros(1, **i32), nku=torch.zeros(1, **i32), span=torch.zeros(1, **i32),
+            slot=torch.zeros(1, **i32), cut=torch.zeros(1, **i32), moved=torch.zeros(1, **i32),
+            out=torch.zeros(1, L, Hq, d, device="cuda"),
+            o=dict(k=k0.copy(), v=v0.copy(), uid=tags0[0].copy(), mod=tags0[1].copy(),
+                   pos=tags0[2].copy()))
+    ws_e = torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, U), dtype=torch.uint8,
+                       device="cuda")
+    ws_p = torch.zeros(ot.omnitide_pack_suffix_workspace_bytes(0, 1, cap_n, H, d),
+                       dtype=torch.uint8, device="cuda")
+    ws_c = torch.zeros(ot.omnitide_place_chunk_workspace_bytes(1, cap_n), dtype=torch.uint8,
+                       device="cuda")
+    ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap_n, L, Hq, H, d),
+                       dtype=torch.uint8, device="cuda")
+    for t in range(steps):
+        clay, cseg = sg.loop_chunk(cfg, t)
+        ck, cv = storage_np(cseg.k_chunk), storage_np(cseg.v_chunk)
+        st = StreamStep(n_seg=1, n_slots=src["k"].shape[1], n_units=U, n_q_heads=Hq,
+                        n_kv_heads=H, head_dim=d, chunk_len=L, budget=cfg.budget,
+                        recent=cfg.recent, page_size=cfg.page_size, weights=cfg.weights,
+                        cap_dst=cap_e)
+        st.score(src["k"], src["uid"], src["mod"])
+        st.select()
+        kc, vc = cseg.k_chunk.cuda()[None], cseg.v_chunk.cuda()[None]
+        cm, cu = dev(clay.chunk_modality), dev(clay.chunk_unit)
+        st.compact(src["k"], src["v"], src["uid"], src["mod"], src["pos"], kc, vc, cm, cu)
+        check_now = t in (11, 23)
+        for pl in layouts.values():
+            ot.omnitide_evict_native(pl["uid"], pl["pos"], 1, U, st.unit_len, pl["remap"],
+                                     pl["kept"], pl["nku"], pl["span"], ws_e, keep=st.keep,
+                                     d_status=st.d_status)
+            if pl["T"] > 0:
+                ot.omnitide_pack_suffix(pl["k"], pl["v"], page, pl["T"], pl["uid"], pl["mod"],
+                                        pl["pos"], pl["span"], pl["cut"], pl["moved"], ws_p)
+            ot.omnitide_place_chunk(pl["k"], pl["v"], pl["uid"], pl["mod"], pl["pos"], kc, vc,
+                                    cm, cu, pl["kept"], pl["nku"], pl["slot"], pl["span"], ws_c,
+                                    d_status=st.d_status)
+            if check_now:
+                ot.omnitide_span_attn(cseg.q.cuda()[None], pl["k"], pl["v"], pl["pos"],
+                                      pl["span"], pl["kept"], cfg.scale, pl["out"], ws_a,
+                                      st.d_status, skip_empty_tiles=True)
+        torch.cuda.synchronize()
+        assert int(host(st.d_status)[0]) == 0, t
+        # the oracle: its eager step gives the plan
+        sc = oracle.score_units(e_k, "bf16", e_uid, e_mod, cfg.weights, U)
+        _, keep, _ = oracle.select_units(sc["wsum"], sc["len"], sc["first"], sc["last"],
+                                         sc["flags"], cfg.budget, cfg.recent)
+        keep_len = np.where(keep != 0, sc["len"], 0)
+        for name, pl in layouts.items():
+            o = pl["o"]
+            ev = oracle.evict_logical(o["uid"], o["pos"], keep_len, U)
+            o["uid"], o["pos"] = ev["unit_id"], ev["pos"]
+            if pl["T"] > 0:
+                c, _ = oracle.plan_suffix(o["uid"] >= 0, page, pl["T"])
+                assert int(host(pl["cut"])[0]) == c, (name, t)
+                if c >= 0:
+                    pk = oracle.pack_suffix(o["k"], o["v"], o["uid"], o["mod"], o["pos"], c)
+                    o.update(k=pk["k"], v=pk["v"], uid=pk["unit_id"], mod=pk["modality"],
+                             pos=pk["pos"])
+            s0 = oracle.place_chunk(o["uid"], L, cap_n)
+            o["k"][s0:s0 + L], o["v"][s0:s0 + L] = ck, cv
+            o["uid"][s0:s0 + L] = ev["n_kept_units"] + clay.chunk_unit
+            o["mod"][s0:s0 + L] = clay.chunk_modality
+            o["pos"][s0:s0 + L] = ev["kept"] + np.arange(L)
+            assert int(host(pl["slot"])[0]) == s0, (name, t)
+            assert int(host(pl["kept"])[0]) == ev["kept"], (name, t)
+            assert int(host(pl["span"])[0]) == oracle.span_of(o["uid"]), (name, t)
+            uid_d, pos_d = host(pl["uid"]).astype(np.int64), host(pl["pos"]).astype(np.int64)
+            assert np.array_equal(uid_d, o["uid"]), (name, t)
+            assert np.array_equal(pos_d, o["pos"]), (name, t)
+            occ = o["uid"] >= 0
+            assert np.array_equal(host(pl["mod"])[occ], o["mod"][occ]), (name, t)
+            if check_now:
+                assert np.array_equal(storage_np(pl["k"][0])[occ], o["k"][occ]), (name, t)
+                assert np.array_equal(storage_np(pl["v"][0])[occ], o["v"][occ]), (name, t)
+                span = oracle.span_of(o["uid"])
+                check(host(pl["out"])[0], cseg.q, bf16_view(o["k"]), bf16_view(o["v"]),
+                      o["pos"], span, ev["kept"], cfg.scale)
+        # next eager state, on both sides
+        cp = oracle.compact_kv(e_k, e_v, e_uid, e_mod, e_pos, keep, U, ck, cv,
+                               clay.chunk_modality, clay.chunk_unit, cap_e, cfg.page_size)
+        n = cp["n_ctx"]
+        tail = cap_e - n
+        e_k = np.concatenate([cp["k"], np.zeros((tail,) + cp["k"].shape[1:], cp["k"].dtype)])
+        e_v = np.concatenate([cp["v"], np.zeros((tail,) + cp["v"].shape[1:], cp["v"].dtype)])
+        e_uid = np.concatenate([cp["unit_id"], np.full(tail, -1)])
+        e_mod = np.concatenate([cp["modality"], np.zeros(tail, np.int64)]).astype(np.uint8)
+        e_pos = np.concatenate([cp["pos"], np.full(tail, -1)])
+        src = dict(k=st.k_dst, v=st.v_dst, uid=st.unit_id_dst, mod=st.modality_dst,
+                   pos=st.pos_dst)
+
+
+def bf16_view(a):
+    """Storage values (uint16 bf16 bit patterns) as a CPU bf16 tensor."""
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
