@@ -72,6 +72,10 @@ enum { OMNITIDE_ROPE_HALF = 0,          /* pairs (j, j + rope_dims/2) */
        OMNITIDE_ROPE_INTERLEAVED = 1 }; /* pairs (2j, 2j + 1) */
 enum { OMNITIDE_MOD_SYS = 0, OMNITIDE_MOD_VIDEO = 1, OMNITIDE_MOD_AUDIO = 2, OMNITIDE_MOD_TEXT = 3,
        OMNITIDE_MOD_MARK = 4 };
+/* key traversal of omnitide_span_attn */
+enum { OMNITIDE_SPAN_FULL = 0,            /* every 64-slot tile of the span, masked */
+       OMNITIDE_SPAN_SKIP_EMPTY = 1,      /* tiles without an entry skipped */
+       OMNITIDE_SPAN_POSITION_ORDER = 2 };/* entries gathered in position order */
 
 /* Limits checked on the host. */
 #define OMNITIDE_MAX_UNITS 8192       /* units per segment */
@@ -451,9 +455,23 @@ size_t omnitide_place_chunk_workspace_bytes(int n_seg, int cap);
  *   (they may hold anything, NaN included).
  *   q, k, v are bf16 and out float32 (OMNITIDE_E_DTYPE is not used here).
  *   workspace  device scratch of omnitide_span_attn_workspace_bytes() bytes (always > 0).
- * skip_empty_tiles != 0: 64-slot tiles without an entry are skipped (kernels with tile
- * skipping); 0: every tile of the span is traversed, masked (kernels that traverse the physical
- * span).  Tiles whose entries are all visible to every query of a workgroup run unmasked.
+ * traversal -- which slots the kernel visits (the result is the same up to summation order):
+ *   OMNITIDE_SPAN_FULL        every 64-slot tile of the span, masked (a kernel presented the
+ *                             physical span);
+ *   OMNITIDE_SPAN_SKIP_EMPTY  64-slot tiles without an entry are skipped (tile skipping).  In
+ *                             both, tiles whose entries are all visible to every query of a
+ *                             workgroup run unmasked;
+ *   OMNITIDE_SPAN_POSITION_ORDER  the entries are gathered in position order through a
+ *                             position -> slot index built in the workspace, so the attention
+ *                             visits n = q_pos0 + chunk_len keys in dense 64-key tiles, as
+ *                             omnitide_chunk_attn over a compacted pool.  Requires the entries of
+ *                             [0, span) to hold the positions 0 .. n - 1 once each (the layout
+ *                             omnitide_evict_native and omnitide_place_chunk maintain); a position
+ *                             >= n, one held twice, one missing, or q_pos0 outside
+ *                             [0, span - chunk_len] is reported as OMNITIDE_E_TAGS on the device
+ *                             (the output is then unspecified).  Host limit: cap * n_kv_heads *
+ *                             head_dim * 2 < 2^32 (OMNITIDE_E_SHAPE).
+ *   other values: OMNITIDE_E_SHAPE.
  * With key_pos[j] = j for j < span and q_pos0 = span - chunk_len this computes
  * omnitide_chunk_attn with n_ctx = span (up to summation order).
  * Limits: as omnitide_chunk_attn, and cap <= 2,097,152.
@@ -461,8 +479,8 @@ size_t omnitide_place_chunk_workspace_bytes(int n_seg, int cap);
 int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_t* key_pos,
                        const int32_t* span, const int32_t* q_pos0, int n_seg, int cap,
                        int chunk_len, int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                       int skip_empty_tiles, float* out, void* workspace,
-                       size_t workspace_bytes, int32_t* d_status, void* stream);
+                       int traversal, float* out, void* workspace, size_t workspace_bytes,
+                       int32_t* d_status, void* stream);
 
 size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                           int n_kv_heads, int head_dim);

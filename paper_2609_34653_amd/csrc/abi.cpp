@@ -366,7 +366,8 @@ int attn_impl(const void* q, const void* k, const void* v, int dtype, const int3
               const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int chunk_len,
               int n_q_heads, int n_kv_heads, int head_dim, float scale, void* out,
               int out_dtype, void* workspace, size_t workspace_bytes, int32_t* d_status,
-              void* stream, bool skip_empty = true, bool noalloc = false) {
+              void* stream, bool skip_empty = true, bool noalloc = false,
+              bool pos_order = false) {
   const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
   if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
@@ -381,6 +382,9 @@ int attn_impl(const void* q, const void* k, const void* v, int dtype, const int3
     return OMNITIDE_E_SHAPE;
   if (cap < chunk_len || (span && cap > omnitide::span_attn_max_cap()))
     return OMNITIDE_E_CAPACITY;
+  // position order gathers rows by 32-bit byte offsets from the segment's base
+  if (pos_order && static_cast<size_t>(cap) * n_kv_heads * head_dim * 2 > 0xffffffffull)
+    return OMNITIDE_E_SHAPE;
   size_t need =
       span ? omnitide::span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads,
                                                  head_dim)
@@ -421,6 +425,7 @@ int attn_impl(const void* q, const void* k, const void* v, int dtype, const int3
   a.key_pos = key_pos;
   a.q_pos0 = q_pos0;
   a.skip_empty = skip_empty;
+  a.pos_order = pos_order;
   if (noalloc) return hip_status(omnitide::launch_attn_noalloc(a, static_cast<hipStream_t>(stream)));
   return hip_status(omnitide::launch_attn(a, static_cast<hipStream_t>(stream)));
 }
@@ -458,12 +463,16 @@ size_t omnitide_span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int
 int omnitide_span_attn(const void* q, const void* k, const void* v, const int32_t* key_pos,
                        const int32_t* span, const int32_t* q_pos0, int n_seg, int cap,
                        int chunk_len, int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                       int skip_empty_tiles, float* out, void* workspace,
+                       int traversal, float* out, void* workspace,
                        size_t workspace_bytes, int32_t* d_status, void* stream) {
   if (key_pos == nullptr || q_pos0 == nullptr) return OMNITIDE_E_NULL;
+  if (traversal != OMNITIDE_SPAN_FULL && traversal != OMNITIDE_SPAN_SKIP_EMPTY &&
+      traversal != OMNITIDE_SPAN_POSITION_ORDER)
+    return OMNITIDE_E_SHAPE;
   return attn_impl(q, k, v, OMNITIDE_BF16, span, key_pos, q_pos0, n_seg, cap, chunk_len,
                    n_q_heads, n_kv_heads, head_dim, scale, out, OMNITIDE_F32, workspace,
-                   workspace_bytes, d_status, stream, skip_empty_tiles != 0);
+                   workspace_bytes, d_status, stream, traversal != OMNITIDE_SPAN_FULL, false,
+                   traversal == OMNITIDE_SPAN_POSITION_ORDER);
 }
 
 size_t omnitide_evict_native_workspace_bytes(int n_seg, int n_units) {

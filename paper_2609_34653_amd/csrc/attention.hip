@@ -61,6 +61,8 @@ struct Smem {
   static constexpr int TILE_ELEMS = kKT * D;
   static constexpr int CHUNKS = D / 8;                         // 16-byte chunks per row
   static constexpr int CALLS = TILE_ELEMS / 8 / kWave / kAttnWaves;  // 1 KB loads per wave
+  // a lane's pieces cover keys k0 + (64 / CALLS) * cq with k0 < 64 / CALLS
+  static_assert(kAttnWaves * kWave / CHUNKS == kKT / CALLS, "key step of a lane's pieces");
 };
 
 __device__ inline int kswz(int key) {
@@ -106,6 +108,13 @@ __device__ inline void dma16(const void* base, uint32_t voff, uint32_t lds_base)
                : "v"(voff), "s"(base), "s"(lds_base)
                : "memory");
 }
+// The same for 4 bytes per lane (lane i writes LDS byte address lds_base + 4 i).
+__device__ inline void dma4(const void* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_base)
+               : "memory");
+}
 
 // max(x over both 32-lane halves): v_permlane32_swap exchanges the halves without LDS.
 // This lane's index in its wave, recomputed (two instructions) at the point of use.  The span
@@ -133,12 +142,19 @@ __device__ inline T& pick(T& a, T& b) {
   if constexpr (B == 0) return a; else return b;
 }
 
-// SPAN = false: keys are the contiguous rows [0, n_ctx) of the compacted pool, the chunk last.
-// SPAN = true: keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span);
-// slot j is visible to query i iff 0 <= key_pos[j] <= q_pos0 + i; only the active tiles listed
-// by span_list_kernel are visited, and a tile is masked only if it holds an empty slot or a
-// position past the workgroup's first row.
-template <int D, bool SPAN>
+// Key traversals of attn_kernel:
+//   kContig    keys are the contiguous rows [0, n_ctx) of the compacted pool, the chunk last.
+//   kSpanTiles keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span); slot j
+//              is visible to query i iff 0 <= key_pos[j] <= q_pos0 + i; only the active tiles
+//              listed by span_list_kernel are visited, and a tile is masked only if it holds an
+//              empty slot or a position past the workgroup's first row.
+//   kPosOrder  a pool with holes whose entries hold the positions 0 .. n-1 once each (n = q_pos0
+//              + L; n_ctx_g holds the span): keys are taken in position order, position p from
+//              the slot list[p] names (pos_index_kernel), so the tiles, bounds and causal masks
+//              are those of kContig with n_ctx = n; only the tile loads are gathers.
+constexpr int kContig = 0, kSpanTiles = 1, kPosOrder = 2;
+
+template <int D, int MODE>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int L, int Hq,
@@ -146,19 +162,33 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     float* __restrict__ part_o, float* __restrict__ part_ml, int n_mt, int n_split,
     int32_t* __restrict__ status,
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ qpos0_g,
-    const int4* __restrict__ tile_info, const int32_t* __restrict__ tile_list,
-    const int32_t* __restrict__ n_active_g, int max_tiles) {
+    const int4* __restrict__ tile_info, const int32_t* __restrict__ list,
+    const int32_t* __restrict__ list_n, int max_tiles) {
+  // list, list_n -- kSpanTiles: the visited tiles and their number; kPosOrder: the slot of each
+  // position and the number of entries the index counted.
+  constexpr bool SPAN = MODE == kSpanTiles;
+  constexpr bool POS = MODE == kPosOrder;
   using S = Smem<D>;
   // Tile buffers K0, K1, V0, V1 at fixed offsets (every access below names its buffer at
   // compile time, so LDS addresses are immediates).
   __shared__ __attribute__((aligned(1024))) uint16_t lds[4 * S::TILE_ELEMS];
   __shared__ int32_t kpos_lds[SPAN ? kKT : 1];     // positions of the current tile's keys
+  __shared__ __attribute__((aligned(16))) int32_t slot_ring[POS ? 4 * kKT : 1];  // tiles t..t+3
 
   const int seg = blockIdx.y;
-  const int nctx = n_ctx_g[seg];                   // SPAN: the span
+  int nctx = n_ctx_g[seg];                         // SPAN, POS: the span
   if (nctx < L || nctx > cap) {
     if (threadIdx.x == 0) set_status(status, OMNITIDE_E_CAPACITY);
     return;
+  }
+  if constexpr (POS) {
+    // the entries must be exactly the positions 0 .. q_pos0 + L - 1
+    const int qp0 = qpos0_g[seg];
+    if (qp0 < 0 || qp0 > nctx - L || list_n[seg] != qp0 + L) {
+      if (threadIdx.x == 0) set_status(status, OMNITIDE_E_TAGS);
+      return;
+    }
+    nctx = qp0 + L;
   }
   // XCD-aware order: blocks b with equal b % 8 run on one XCD; give them consecutive work ids.
   const int nb = gridDim.x, b = blockIdx.x;
@@ -175,7 +205,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   const int p_lo = m0 / G;
   const int p_hi = min(L - 1, (m0 + kRowsWG - 1) / G);
   const int kmax = kept + p_hi + 1;               // keys [0, kmax) are needed by this workgroup
-  const int n_tiles = SPAN ? n_active_g[seg] : (kmax + kKT - 1) / kKT;
+  const int n_tiles = SPAN ? list_n[seg] : (kmax + kKT - 1) / kKT;
   const int t_begin = static_cast<int>(static_cast<long>(n_tiles) * split / n_split);
   const int t_end = static_cast<int>(static_cast<long>(n_tiles) * (split + 1) / n_split);
   const int full_lim = kept + p_lo;               // keys <= full_lim are visible to every row
@@ -212,9 +242,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   for (int cq = 0; cq < S::CALLS; ++cq) {
     const int lc = (wave + kAttnWaves * cq) * kWave + lane;
     const int key = lc / S::CHUNKS, pc = lc % S::CHUNKS;
+    const int row = POS ? 0 : key * row_stride;   // POS: the row comes from the slot index
     krowl[cq] = key;
-    koff[cq] = 2u * (key * row_stride + 8 * (pc ^ (kswz(key) & (S::CHUNKS - 1))));
-    voff[cq] = 2u * (key * row_stride + 8 * (2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1)));
+    koff[cq] = 2u * (row + 8 * (pc ^ (kswz(key) & (S::CHUNKS - 1))));
+    voff[cq] = 2u * (row + 8 * (2 * ((pc >> 1) ^ vswz<D>(key)) + (pc & 1)));
   }
   const uint16_t* k_head = k + (kv_seg * Hkv + g) * D;
   const uint16_t* v_head = v + (kv_seg * Hkv + g) * D;
@@ -225,6 +256,21 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const int j0 = t * kKT;
     const uint16_t* tile = head_base + static_cast<size_t>(j0) * row_stride;
     const uint32_t dst = lds_wave + static_cast<uint32_t>(buf * S::TILE_ELEMS * 2);
+    if constexpr (POS) {
+      // key r of tile t is the entry at position 64t + r (positions past n_ctx were clamped to
+      // n_ctx - 1 when the ring was filled); this lane's keys krowl[0] + KS * cq have adjacent
+      // ring words, read at once.  The host keeps cap * Hkv * D * 2 below 2^32.
+      typedef int32_t SlotVec __attribute__((ext_vector_type(S::CALLS)));
+      const SlotVec sl = *reinterpret_cast<const SlotVec*>(slot_ring + (t & 3) * kKT +
+                                                           krowl[0] * S::CALLS);
+#pragma unroll
+      for (int cq = 0; cq < S::CALLS; ++cq) {
+        const uint32_t slot = min(static_cast<uint32_t>(sl[cq]), static_cast<uint32_t>(cap - 1));
+        dma16(head_base, offs[cq] + 2u * slot * static_cast<uint32_t>(row_stride),
+              dst + static_cast<uint32_t>(cq * kAttnWaves * kWave * 16));
+      }
+      return;
+    }
     if (j0 + kKT <= nctx) {
 #pragma unroll
       for (int cq = 0; cq < S::CALLS; ++cq)
@@ -250,11 +296,21 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         *reinterpret_cast<u32x4*>(base + 8 * idx) = u32x4{0, 0, 0, 0};
   };
 
-  // SPAN: the a-th visited tile is tile_list[a]; tile_info holds its (largest position, has an
+  // SPAN: the a-th visited tile is list[a]; tile_info holds its (largest position, has an
   // empty slot, occupancy bits 0-31, occupancy bits 32-63).
   const size_t tl_base = static_cast<size_t>(seg) * max_tiles;
   auto tile_of = [&](int a) -> int {
-    if constexpr (SPAN) return tile_list[tl_base + a]; else return a;
+    if constexpr (SPAN) return list[tl_base + a]; else return a;
+  };
+  // POS: wave 0 copies the slots of positions 64t .. 64t+63 (clamped to n_ctx - 1) into ring
+  // entry t & 3 (a direct load, waited for with the tile loads before the loop barrier).  Word i
+  // of an entry holds key (i % CALLS) * KS + i / CALLS, KS = 64 / CALLS: the CALLS keys a lane
+  // loads rows for (krowl[0] + KS * cq) are adjacent.
+  auto load_ring = [&](int t) {
+    constexpr int KS = kKT / S::CALLS;
+    const int p = min(t * kKT + (lane % S::CALLS) * KS + lane / S::CALLS, nctx - 1);
+    dma4(list + static_cast<size_t>(seg) * cap, 4u * static_cast<uint32_t>(p),
+         lds_addr(slot_ring) + static_cast<uint32_t>((t & 3) * kKT * 4));
   };
   // SPAN: wave 0 holds the positions of the next V tile's keys (one per lane, -1 past the span)
   int kp_next = -1;
@@ -290,6 +346,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
   };
 
   if (t_begin < t_end) {
+    if constexpr (POS) {
+      if (wave == 0) {
+        for (int a = 0; a < 3 && t_begin + a < t_end; ++a) load_ring(t_begin + a);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
     issue(k_head, koff, tile_of(t_begin), 0);
     issue(v_head, voff, tile_of(t_begin), 2);
     if constexpr (SPAN) {
@@ -360,6 +423,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
         }
         if (t + 2 < t_end) issue(k_head, koff, t + 2, B);
         if (has_next) issue(v_head, voff, t + 1, 3 - B);
+        if constexpr (POS) {
+          // ring entry (t + 3) & 3 held tile t - 1's slots, last read two iterations ago
+          if (wave == 0 && t + 3 < t_end) load_ring(t + 3);
+        }
         masked = j0 + kKT - 1 > full_lim;  // causal mask: only tiles past the first row's limit
       }
 
@@ -588,6 +655,49 @@ __global__ __launch_bounds__(kSpanThreads) void span_list_kernel(
   if (tid == 0) n_active_g[seg] = running;
 }
 
+// Position index of a span whose entries should hold the positions 0 .. n-1 once each (n =
+// q_pos0 + chunk_len): slot_of[p] = the slot holding position p.  pos_clear_kernel empties
+// slot_of[0, n) and zeroes the segment's entry count; pos_index_kernel (one thread per slot of
+// the span) claims slot_of[key_pos[j]] for its slot j by compare-and-swap and counts the claims
+// (one atomic add per wave).  A position >= n, or one held by two slots, is reported as
+// OMNITIDE_E_TAGS here; an absent one leaves the count below n, which the attention kernel
+// reports.  Segments with an invalid span or q_pos0 are left to the attention kernel.
+__global__ __launch_bounds__(kInfoThreads) void pos_clear_kernel(
+    const int32_t* __restrict__ span_g, const int32_t* __restrict__ qpos0_g, int cap, int L,
+    int32_t* __restrict__ slot_of, int32_t* __restrict__ count) {
+  const int seg = blockIdx.y;
+  const long n = min(static_cast<long>(qpos0_g[seg]) + L, static_cast<long>(span_g[seg]));
+  const int n_clear = static_cast<int>(max(0L, min(n, static_cast<long>(cap))));
+  int32_t* so = slot_of + static_cast<size_t>(seg) * cap;
+  for (int p = blockIdx.x * kInfoThreads + threadIdx.x; p < n_clear;
+       p += gridDim.x * kInfoThreads)
+    so[p] = -1;
+  if (blockIdx.x == 0 && threadIdx.x == 0) count[seg] = 0;
+}
+
+__global__ __launch_bounds__(kInfoThreads) void pos_index_kernel(
+    const int32_t* __restrict__ key_pos, const int32_t* __restrict__ span_g,
+    const int32_t* __restrict__ qpos0_g, int cap, int L, int32_t* __restrict__ slot_of,
+    int32_t* __restrict__ count, int32_t* __restrict__ status) {
+  const int seg = blockIdx.y;
+  const int span = span_g[seg];
+  const int qp0 = qpos0_g[seg];
+  if (span < L || span > cap || qp0 < 0 || qp0 > span - L) return;
+  const int j0 = blockIdx.x * kInfoThreads;
+  if (j0 >= span) return;
+  const int n = qp0 + L;
+  const int j = j0 + static_cast<int>(threadIdx.x);
+  const size_t sb = static_cast<size_t>(seg) * cap;
+  const int p = j < span ? key_pos[sb + j] : -1;
+  bool claimed = false;
+  if (p >= 0) {
+    if (p < n) claimed = atomicCAS(&slot_of[sb + p], -1, j) == -1;
+    if (!claimed) set_status(status, OMNITIDE_E_TAGS);
+  }
+  const uint64_t c = __ballot(claimed);
+  if ((threadIdx.x & (kWave - 1)) == 0 && c != 0) atomicAdd(&count[seg], __popcll(c));
+}
+
 }  // namespace
 
 // Tables of n_seg segments: int4 info, int32 list, int32 counts, then the byte flags (the
@@ -607,6 +717,29 @@ size_t span_tiles_bytes(int n_seg, int cap) {
   const size_t nt = static_cast<size_t>(n_seg) * ((cap + kKT - 1) / kKT);
   return nt * (sizeof(int4) + sizeof(int32_t) + 1) + static_cast<size_t>(n_seg) * sizeof(int32_t);
 }
+
+namespace {
+
+// Position index of n_seg segments (kPosOrder): int32 slot_of[n_seg][cap], then the counts.
+size_t pos_index_bytes(int n_seg, int cap) {
+  return (static_cast<size_t>(n_seg) * cap + n_seg) * sizeof(int32_t);
+}
+
+hipError_t launch_pos_index(const int32_t* key_pos, const int32_t* span, const int32_t* q_pos0,
+                            int n_seg, int cap, int L, int32_t* slot_of, hipStream_t stream,
+                            int32_t* d_status) {
+  int32_t* count = slot_of + static_cast<size_t>(n_seg) * cap;
+  const int blocks = (cap + kInfoThreads - 1) / kInfoThreads;
+  hipLaunchKernelGGL(pos_clear_kernel, dim3(std::min(blocks, 1024), n_seg), dim3(kInfoThreads),
+                     0, stream, span, q_pos0, cap, L, slot_of, count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(pos_index_kernel, dim3(blocks, n_seg), dim3(kInfoThreads), 0, stream,
+                     key_pos, span, q_pos0, cap, L, slot_of, count, d_status);
+  return hipGetLastError();
+}
+
+}  // namespace
 
 hipError_t launch_span_tiles(const int32_t* key_pos, const int32_t* span, int n_seg, int cap,
                              int min_span, bool skip_empty, void* buf, hipStream_t stream) {
@@ -634,7 +767,21 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
   float* part_o = n_split > 1 ? static_cast<float*>(a.workspace) : nullptr;
   float* part_ml = part_o ? part_o + static_cast<size_t>(n_split) * n_rows * D : nullptr;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  if (a.key_pos != nullptr) {
+  if (a.key_pos != nullptr && a.pos_order) {
+    // position order: the position index after the partials
+    int32_t* slot_of = reinterpret_cast<int32_t*>(
+        static_cast<uint8_t*>(a.workspace) +
+        align256(n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0));
+    hipError_t e = launch_pos_index(a.key_pos, a.n_ctx, a.q_pos0, a.n_seg, a.cap, a.chunk_len,
+                                    slot_of, stream, a.d_status);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_kernel<D, kPosOrder>), grid, dim3(kAttnThreads), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                       static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
+                       a.n_q_heads, a.n_kv_heads, scale_log2, a.out, a.out_bf16, part_o, part_ml,
+                       n_mt, n_split, a.d_status, a.key_pos, a.q_pos0, nullptr, slot_of,
+                       slot_of + static_cast<size_t>(a.n_seg) * a.cap, 0);
+  } else if (a.key_pos != nullptr) {
     // span mode: tile table after the partials
     const int max_tiles = (a.cap + kKT - 1) / kKT;
     uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
@@ -646,14 +793,14 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
     hipError_t e = launch_span_tiles(a.key_pos, a.n_ctx, a.n_seg, a.cap, a.chunk_len,
                                      a.skip_empty, tbl, stream);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_kernel<D, true>), grid, dim3(kAttnThreads), 0, stream,
+    hipLaunchKernelGGL((attn_kernel<D, kSpanTiles>), grid, dim3(kAttnThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
                        a.n_q_heads, a.n_kv_heads, scale_log2, a.out, a.out_bf16, part_o, part_ml,
                        n_mt, n_split, a.d_status, a.key_pos, a.q_pos0, tile_info, tile_list,
                        n_active, max_tiles);
   } else {
-    hipLaunchKernelGGL((attn_kernel<D, false>), grid, dim3(kAttnThreads), 0, stream,
+    hipLaunchKernelGGL((attn_kernel<D, kContig>), grid, dim3(kAttnThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
                        a.n_q_heads, a.n_kv_heads, scale_log2, a.out, a.out_bf16, part_o, part_ml,
@@ -689,8 +836,9 @@ size_t attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads, in
 
 size_t span_attn_workspace_bytes(int n_seg, int cap, int chunk_len, int n_q_heads,
                                  int n_kv_heads, int head_dim) {
+  // the tile table (tile traversals) or the position index (position order) after the partials
   return align256(attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_heads, head_dim)) +
-         span_tiles_bytes(n_seg, cap);
+         std::max(span_tiles_bytes(n_seg, cap), pos_index_bytes(n_seg, cap));
 }
 
 int span_attn_max_cap() { return 32768 * kKT; }

@@ -169,6 +169,8 @@ struct AttnArgs {
   const int32_t* key_pos = nullptr;   // [n_seg][cap] logical position, -1 = empty slot
   const int32_t* q_pos0 = nullptr;    // [n_seg] logical position of chunk query 0
   bool skip_empty = true;             // skip 64-slot tiles without an entry
+  bool pos_order = false;             // keys in position order through a position index (the
+                                      // entries hold positions 0 .. q_pos0 + chunk_len - 1)
 };
 
 int attn_num_splits(int n_seg, int cap, int chunk_len, int n_q_heads, int n_kv_heads,

@@ -410,9 +410,12 @@ def omnitide_span_attn_workspace_bytes(n_seg, cap, chunk_len, n_q_heads, n_kv_he
 
 
 def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_status=None,
-                       stream=None, skip_empty_tiles=True):
+                       stream=None, skip_empty_tiles=True, position_order=False):
     """q [n_seg, L, Hq, d] bf16; k/v [n_seg, cap, Hkv, d] bf16; key_pos int32 [n_seg * cap]
-    (-1 = empty slot); span, q_pos0 int32 [n_seg] (device); out float32 like q."""
+    (-1 = empty slot); span, q_pos0 int32 [n_seg] (device); out float32 like q.
+    Traversal: position_order (the entries gathered in position order; they must hold the
+    positions 0 .. q_pos0 + L - 1 once each), else tile skipping if skip_empty_tiles, else the
+    full span."""
     if q.dim() == 3:
         n_seg, (L, Hq, d) = 1, q.shape
     else:
@@ -432,7 +435,8 @@ def omnitide_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace, d_
         _need(d_status, "d_status", I32, 1)
     _check(lib().omnitide_span_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(key_pos), _ptr(span),
                                     _ptr(q_pos0), n_seg, cap, L, Hq, Hkv, d, float(scale),
-                                    1 if skip_empty_tiles else 0, _ptr(out), _ptr(workspace),
+                                    2 if position_order else 1 if skip_empty_tiles else 0,
+                                    _ptr(out), _ptr(workspace),
                                     workspace.numel(),
                                     _ptr(d_status), _stream(stream)), "omnitide_span_attn")
 

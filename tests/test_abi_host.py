@@ -300,11 +300,11 @@ def test_noalloc_scratch_covers_every_shape():
 def span_attn(L, **kw):
     a = dict(q=fake(0), k=fake(1), v=fake(2), kp=fake(3), span=fake(4), qp=fake(5), n_seg=1,
              cap=81920, Lc=665, Hq=32, Hkv=8, d=128, scale=0.0884, out=fake(6), ws=fake(7),
-             wsb=1 << 30, st=fake(8))
+             wsb=1 << 30, st=fake(8), trav=1)
     a.update(kw)
     return L.omnitide_span_attn(a["q"], a["k"], a["v"], a["kp"], a["span"], a["qp"], a["n_seg"],
-                                a["cap"], a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"], 1,
-                                a["out"], a["ws"], a["wsb"], a["st"], None)
+                                a["cap"], a["Lc"], a["Hq"], a["Hkv"], a["d"], a["scale"],
+                                a["trav"], a["out"], a["ws"], a["wsb"], a["st"], None)
 
 
 def test_span_attention_validation(L):
@@ -320,6 +320,14 @@ def test_span_attention_validation(L):
     assert span_attn(L, out=P(fake(3).value + 256)) == ot.E_ALIAS   # output over key_pos
     # chunk_attn keeps its own (smaller) workspace and needs no positions
     assert ot.omnitide_span_attn_workspace_bytes(1, 81920, 665, 30, 8, 128) == 0
+    # traversals: 0 full span, 1 tile skipping, 2 position order; nothing else
+    for trav in (-1, 3, 7):
+        assert span_attn(L, trav=trav) == ot.E_SHAPE, trav
+    # position order: 32-bit row offsets within a segment's pool, and room for the index
+    assert span_attn(L, trav=2, cap=1 << 21) == ot.E_SHAPE        # 2^21 rows of 2 KB = 4 GiB
+    assert span_attn(L, trav=2, cap=1 << 21, Hkv=4, ws=None) == ot.E_WORKSPACE
+    part = ot.omnitide_attn_workspace_bytes(1, 81920, 665, 32, 8, 128)
+    assert need >= -(-part // 256) * 256 + (81920 + 1) * 4
 
 
 def evict(L, **kw):

@@ -33,7 +33,8 @@ def bf16(a):
 
 
 def run_span_attn(q, k, v, key_pos, span, q_pos0, scale, expect_status=0, skip=True):
-    """q [n_seg, L, Hq, d], k/v [n_seg, cap, Hkv, d] bf16 (CPU); key_pos [n_seg, cap]."""
+    """q [n_seg, L, Hq, d], k/v [n_seg, cap, Hkv, d] bf16 (CPU); key_pos [n_seg, cap].
+    skip: True (tile skipping), False (the full span) or "pos" (position order)."""
     from paper_2609_34653_amd import omnitide as ot
     n_seg, L, Hq, d = q.shape
     cap, Hkv = k.shape[1], k.shape[2]
@@ -44,25 +45,28 @@ def run_span_attn(q, k, v, key_pos, span, q_pos0, scale, expect_status=0, skip=T
     ot.omnitide_span_attn(q.cuda(), k.cuda(), v.cuda(),
                           dev(np.asarray(key_pos, np.int32).reshape(-1)),
                           dev(np.asarray(span, np.int32)), dev(np.asarray(q_pos0, np.int32)),
-                          scale, out, ws, st, skip_empty_tiles=skip)
+                          scale, out, ws, st, skip_empty_tiles=skip is True,
+                          position_order=skip == "pos")
     torch.cuda.synchronize()
     assert int(host(st)[0]) == expect_status
     return host(out)
 
 
 def check(out, q, k, v, key_pos, span, q_pos0, scale):
-    """Every query row against the oracle; mean absolute error over the whole output."""
+    """Every query row against the oracle; mean absolute error over the whole output.  out: one
+    output or a list of outputs of the same call (one oracle evaluation for all)."""
     f = lambda t: oracle.to_f64(storage_np(t), "bf16")  # noqa: E731
     L = q.shape[0]
     # only occupied slots can be visible: hand the oracle those (in slot order)
     occ = np.nonzero(np.asarray(key_pos)[:span] >= 0)[0]
     k, v, key_pos, span = k[occ], v[occ], np.asarray(key_pos)[occ], len(occ)
     ref = oracle.span_attention(f(q), f(k), f(v), key_pos, span, q_pos0, scale)
-    assert out.shape[0] == L
-    err = np.abs(out.astype(np.float64) - ref)
-    assert np.isfinite(out).all()
-    assert err.max() <= MAX_ABS, err.max()
-    assert err.mean() <= MEAN_ABS, err.mean()
+    for o in (out if isinstance(out, (list, tuple)) else [out]):
+        assert o.shape[0] == L
+        err = np.abs(o.astype(np.float64) - ref)
+        assert np.isfinite(o).all()
+        assert err.max() <= MAX_ABS, err.max()
+        assert err.mean() <= MEAN_ABS, err.mean()
 
 
 def random_span_pool(rng, cap, L, Hkv, d, fill, empty_tiles=True, nan_holes=True):
@@ -96,6 +100,12 @@ def random_span_pool(rng, cap, L, Hkv, d, fill, empty_tiles=True, nan_holes=True
     (5000, 64, 8, 1, 128, 0.1, 3, True),      # sparse: many empty tiles
     (5000, 64, 8, 1, 128, 0.1, 3, False),     # the same, every tile traversed
     (2000, 100, 4, 4, 64, 0.3, 1, False),
+    (700, 37, 8, 2, 128, 0.5, 0, "pos"),      # position order: the same pools
+    (2000, 100, 4, 4, 64, 0.3, 1, "pos"),
+    (1500, 200, 32, 8, 128, 0.9, 2, "pos"),
+    (5000, 64, 8, 1, 128, 0.1, 3, "pos"),
+    (9000, 1, 8, 8, 64, 0.02, 4, "pos"),      # one query over a sparse pool
+    (3000, 150, 16, 2, 128, 0.7, 5, "pos"),   # 8 query heads per KV head
 ])
 def test_span_attention_random_pools(cap, L, Hq, Hkv, d, fill, seed, skip):
     rng = np.random.default_rng(seed)
@@ -112,11 +122,12 @@ def test_span_attention_several_segments():
     cap, L, Hq, Hkv, d = 1200, 50, 8, 2, 128
     pools = [random_span_pool(rng, cap, L, Hkv, d, f) for f in (0.2, 0.6, 0.95)]
     q = bf16(rng.standard_normal((3, L, Hq, d)))
-    out = run_span_attn(q, torch.stack([p[0] for p in pools]), torch.stack([p[1] for p in pools]),
-                        np.stack([p[2] for p in pools]), [p[3] for p in pools],
-                        [p[4] for p in pools], 0.1)
+    args = (q, torch.stack([p[0] for p in pools]), torch.stack([p[1] for p in pools]),
+            np.stack([p[2] for p in pools]), [p[3] for p in pools], [p[4] for p in pools], 0.1)
+    out = run_span_attn(*args)
+    out_p = run_span_attn(*args, skip="pos")
     for i, (k, v, kp, span, qp) in enumerate(pools):
-        check(out[i], q[i], k, v, kp, span, qp, 0.1)
+        check([out[i], out_p[i]], q[i], k, v, kp, span, qp, 0.1)
 
 
 def test_dense_positions_match_chunk_attention():
@@ -137,6 +148,73 @@ def test_dense_positions_match_chunk_attention():
     torch.cuda.synchronize()
     assert np.abs(out - host(ref)).max() <= 2e-3
     check(out[0], q[0], k[0], v[0], kp, n, n - L, 0.09)
+
+
+def chunk_attn_compacted(q, k, v, key_pos, n, scale):
+    """omnitide_chunk_attn over the entries of a holey pool moved to slots 0 .. n-1 in position
+    order (the same capacity, so the same split count)."""
+    from paper_2609_34653_amd import omnitide as ot
+    n_seg, cap, Hkv, d = k.shape
+    L, Hq = q.shape[1], q.shape[2]
+    kc, vc = torch.zeros_like(k), torch.zeros_like(v)
+    for i in range(n_seg):
+        slots = np.argsort(np.where(key_pos[i] >= 0, key_pos[i], np.iinfo(np.int64).max),
+                           kind="stable")[:n[i]]
+        assert np.array_equal(key_pos[i][slots], np.arange(n[i]))
+        kc[i, :n[i]] = k[i, torch.from_numpy(slots)]
+        vc[i, :n[i]] = v[i, torch.from_numpy(slots)]
+    out = torch.zeros(n_seg, L, Hq, d, device="cuda")
+    nb = ot.omnitide_attn_workspace_bytes(n_seg, cap, L, Hq, Hkv, d)
+    ws = torch.zeros(max(nb, 1), dtype=torch.uint8, device="cuda")
+    ot.omnitide_chunk_attn(q.cuda(), kc.cuda(), vc.cuda(), dev(np.asarray(n, np.int32)), scale,
+                           out, ws)
+    torch.cuda.synchronize()
+    return host(out)
+
+
+@pytest.mark.parametrize("cap,L,Hq,Hkv,d,fills,seed", [
+    (3000, 300, 16, 4, 128, (0.4,), 7),
+    (2500, 77, 8, 2, 64, (0.15, 0.8), 8),     # two segments, d = 64, ragged last tile
+])
+def test_position_order_bitwise_equals_compacted(cap, L, Hq, Hkv, d, fills, seed):
+    """Position order visits the same tiles, in the same order, with the same masks as the chunk
+    attention over the compacted pool: the outputs agree bit for bit."""
+    rng = np.random.default_rng(seed)
+    pools = [random_span_pool(rng, cap, L, Hkv, d, f, nan_holes=False) for f in fills]
+    q = bf16(rng.standard_normal((len(fills), L, Hq, d)))
+    k, v = torch.stack([p[0] for p in pools]), torch.stack([p[1] for p in pools])
+    kp = np.stack([p[2] for p in pools])
+    n = [p[4] + L for p in pools]
+    out = run_span_attn(q, k, v, kp, [p[3] for p in pools], [p[4] for p in pools], 0.08,
+                        skip="pos")
+    ref = chunk_attn_compacted(q, k, v, kp, n, 0.08)
+    assert np.array_equal(out, ref)
+
+
+def test_position_order_errors_reported():
+    """Entries that are not the positions 0 .. q_pos0 + L - 1 once each: OMNITIDE_E_TAGS on the
+    device (a repeated, a missing or a too-large position, q_pos0 out of range); an invalid
+    span: OMNITIDE_E_CAPACITY."""
+    rng = np.random.default_rng(10)
+    k, v, kp, span, qp = random_span_pool(rng, 1500, 60, 2, 128, 0.5, nan_holes=False)
+    q = bf16(rng.standard_normal((1, 60, 8, 128)))
+    hist = np.nonzero((kp >= 0) & (kp < qp))[0]
+    run = lambda kp2, span2=span, qp2=qp, st=-17: run_span_attn(  # noqa: E731
+        q, k[None], v[None], kp2[None], [span2], [qp2], 0.1, expect_status=st, skip="pos")
+    run(kp, st=0)
+    dup = kp.copy()
+    dup[hist[3]] = kp[hist[10]]                 # position held twice (and one missing)
+    run(dup)
+    big = kp.copy()
+    big[hist[5]] = qp + 60                      # position n
+    run(big)
+    gone = kp.copy()
+    gone[hist[7]] = -1                          # one position missing
+    run(gone)
+    run(kp, qp2=-1)
+    run(kp, qp2=span - 59)                      # q_pos0 + L > span
+    run(kp, qp2=qp - 1)                         # the chunk's last position >= n
+    run(kp, span2=1501, st=-5)
 
 
 def native_80k(keep_whole=True):
@@ -168,10 +246,13 @@ def native_80k(keep_whole=True):
 def test_span_attention_native_80k():
     cfg, q, k, v, key_pos, span, q_pos0, s0 = native_80k()
     assert s0 < span - 665 and span > 60000, "the chunk fills a hole, the span stays long"
-    for skip in (True, False):
-        out = run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0],
-                            cfg.scale, skip=skip)
-        check(out[0], q, k, v, key_pos, span, q_pos0, cfg.scale)
+    outs = [run_span_attn(q[None], k[None], v[None], key_pos[None], [span], [q_pos0], cfg.scale,
+                          skip=skip)[0] for skip in (True, False, "pos")]
+    check(outs, q, k, v, key_pos, span, q_pos0, cfg.scale)
+    # position order over the native pool = the chunk attention over the compacted pool
+    ref = chunk_attn_compacted(q[None], k[None], v[None], key_pos[None], [q_pos0 + 665],
+                               cfg.scale)
+    assert np.array_equal(outs[2], ref[0])
 
 
 def test_span_attention_capacity_error():
@@ -516,7 +597,8 @@ def test_stream_loop_native_layouts_chained():
     unit ids of all layouts coincide).  Against the oracle chained on its own outputs (its own
     score and select of its own eager chain): eviction, suffix packing and chunk placement
     bit-exact at every step (every tag row, the chunk slot, the span, the kept count), the K/V
-    bytes of every occupied slot and span attention on every query row after steps 12 and 24."""
+    bytes of every occupied slot and span attention (tile skipping and position order) on every
+    query row after steps 12 and 24."""
     from paper_2609_34653_amd import omnitide as ot
     from paper_2609_34653_amd.step import StreamStep
     cfg = sg.CONFIG_BY_NAME["stream_loop_64x665"]
@@ -549,6 +631,7 @@ def test_stream_loop_native_layouts_chained():
             kept=torch.zeros(1, **i32), nku=torch.zeros(1, **i32), span=torch.zeros(1, **i32),
             slot=torch.zeros(1, **i32), cut=torch.zeros(1, **i32), moved=torch.zeros(1, **i32),
             out=torch.zeros(1, L, Hq, d, device="cuda"),
+            out_p=torch.zeros(1, L, Hq, d, device="cuda"),
             o=dict(k=k0.copy(), v=v0.copy(), uid=tags0[0].copy(), mod=tags0[1].copy(),
                    pos=tags0[2].copy()))
     ws_e = torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, U), dtype=torch.uint8,
@@ -583,9 +666,11 @@ def test_stream_loop_native_layouts_chained():
                                     cm, cu, pl["kept"], pl["nku"], pl["slot"], pl["span"], ws_c,
                                     d_status=st.d_status)
             if check_now:
-                ot.omnitide_span_attn(cseg.q.cuda()[None], pl["k"], pl["v"], pl["pos"],
-                                      pl["span"], pl["kept"], cfg.scale, pl["out"], ws_a,
-                                      st.d_status, skip_empty_tiles=True)
+                for key, po in (("out", False), ("out_p", True)):
+                    ot.omnitide_span_attn(cseg.q.cuda()[None], pl["k"], pl["v"], pl["pos"],
+                                          pl["span"], pl["kept"], cfg.scale, pl[key], ws_a,
+                                          st.d_status, skip_empty_tiles=True,
+                                          position_order=po)
         torch.cuda.synchronize()
         assert int(host(st.d_status)[0]) == 0, t
         # the oracle: its eager step gives the plan
@@ -621,8 +706,8 @@ def test_stream_loop_native_layouts_chained():
                 assert np.array_equal(storage_np(pl["k"][0])[occ], o["k"][occ]), (name, t)
                 assert np.array_equal(storage_np(pl["v"][0])[occ], o["v"][occ]), (name, t)
                 span = oracle.span_of(o["uid"])
-                check(host(pl["out"])[0], cseg.q, bf16_view(o["k"]), bf16_view(o["v"]),
-                      o["pos"], span, ev["kept"], cfg.scale)
+                check([host(pl["out"])[0], host(pl["out_p"])[0]], cseg.q, bf16_view(o["k"]),
+                      bf16_view(o["v"]), o["pos"], span, ev["kept"], cfg.scale)
         # next eager state, on both sides
         cp = oracle.compact_kv(e_k, e_v, e_uid, e_mod, e_pos, keep, U, ck, cv,
                                clay.chunk_modality, clay.chunk_unit, cap_e, cfg.page_size)
