@@ -632,8 +632,9 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
         ot.omnitide_place_chunk(k, v, uid, mod, pos, c["kc"], c["vc"], c["cm"], c["cu"], kept,
                                 nku, slot, span, ws_c, d_status=st.d_status)
 
-    def attend():
-        ot.omnitide_span_attn(c["q"], k, v, pos, span, kept, cfg.scale, out, ws_a, st.d_status)
+    def attend(position_order=False):
+        ot.omnitide_span_attn(c["q"], k, v, pos, span, kept, cfg.scale, out, ws_a, st.d_status,
+                              position_order=position_order)
 
     def staged(snap, call):
         """(us per call, method): graph of [restore, call] minus graph of [restore]."""
@@ -674,6 +675,8 @@ def layout_ablation(ot, st, c, lay, cfg, L, H, Hq, d, dev, reps, n_ctx, use_grap
         if packed:
             r.update(cut=int(cut.item()), moved_rows=int(moved.item()))
         attn_us, how = graph_time_us(lambda i: attend(), reps, dev, use_graph)
+        r["attend_position_order_us"], _ = graph_time_us(lambda i: attend(True), reps, dev,
+                                                         use_graph)
         final = tuple(x.clone() for x in (uid, pos, mod))
         span_final = span.clone()
         span.copy_(torch.zeros_like(span))
@@ -708,7 +711,9 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     native pool runs twice per step: skipping empty 64-slot tiles, and traversing the whole
     span (as kernels without tile skipping do).  Each step then decodes the chunk's last token
     over each layout (the eager pool's rows [0, n_ctx); a native pool's span, with and without
-    tile skipping), as the decode half of the paper's layout ablation.  Attention, decode and
+    tile skipping), as the decode half of the paper's layout ablation.  A third attention over
+    each native pool takes its entries in position order through a position -> slot index (the
+    compacted pool's tiles, gathered).  Attention, decode and
     maintenance are timed with events around their launches (the per-step latency percentiles
     come from the same events); spans and active pages are recorded per step."""
     from paper_2609_34653_amd.step import StreamStep
@@ -770,12 +775,13 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         pl["dec"] = torch.zeros(1, 1, Hq, d, device=dev)
         pl["qpos"] = torch.zeros(1, **i32)
     names = ["eager"] + list(pools)
-    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(steps)]
+    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(steps)]
           for n in names}
     spans = {n: torch.zeros(steps, **i32) for n in names}
     active = {n: torch.zeros(steps, **i32) for n in names}
     diff = torch.zeros(len(pools), device=dev)
     diff_dec = torch.zeros(len(pools), device=dev)
+    diff_pos = torch.zeros(len(pools), device=dev)
     s = torch.cuda.current_stream()
     d_status = st_first.d_status
     for i in range(steps):
@@ -831,10 +837,15 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
                                          skip_empty_tiles=False)
             e[7].record(s)
             diff_dec[j] = torch.maximum(diff_dec[j], (pl["dec"] - dec_e).abs().max())
+            diff[j] = torch.maximum(diff[j], (pl["out"] - st.out).abs().max())
+            e[8].record(s)
+            ot.omnitide_span_attn(c["q"], pl["k"], pl["v"], pl["pos"], pl["span"], pl["kept"],
+                                  cfg.scale, pl["out"], ws_a, d_status, position_order=True)
+            e[9].record(s)
+            diff_pos[j] = torch.maximum(diff_pos[j], (pl["out"] - st.out).abs().max())
             spans[n][i:i + 1].copy_(pl["span"])
             occ = (pl["uid"] >= 0).view(-1, page).any(dim=1)
             active[n][i:i + 1].copy_(occ.sum().view(1).to(torch.int32))
-            diff[j] = torch.maximum(diff[j], (pl["out"] - st.out).abs().max())
         src = dict(k=st.k_dst, v=st.v_dst, uid=st.unit_id_dst, mod=st.modality_dst,
                    pos=st.pos_dst)
     torch.cuda.synchronize()
@@ -843,6 +854,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         raise RuntimeError(f"device status {status}: {ot.status_string(status)}")
     res = {"steps": steps, "page_size": page,
            "max_abs_diff_vs_eager": round(float(diff.max().item()), 6),
+           "position_order_max_abs_diff_vs_eager": round(float(diff_pos.max().item()), 6),
            "decode_max_abs_diff_vs_eager": round(float(diff_dec.max().item()), 8)}
     for n in names:
         ms = lambda a, b: sum(ev[n][i][a].elapsed_time(ev[n][i][b]) for i in range(steps))  # noqa
@@ -862,6 +874,11 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         r["step_ms_p50"] = round(float(np.percentile(lat, 50)), 4)
         r["step_ms_p99"] = round(float(np.percentile(lat, 99)), 4)
         r["step_ms_max"] = round(float(lat.max()), 4)
+        if n != "eager":
+            # maintenance + attention in position order
+            lat_p = per_step(0, 1) + per_step(8, 9)
+            r["step_position_order_ms_p50"] = round(float(np.percentile(lat_p, 50)), 4)
+            r["step_position_order_ms_p99"] = round(float(np.percentile(lat_p, 99)), 4)
         # the same per call: eager score + select, compaction, attention; native maintenance
         # (eviction, packing, placement), attention with and without tile skipping
         if n == "eager":
@@ -872,6 +889,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
             r["per_call_ms"] = {"maintenance": pct(per_step(0, 1)),
                                 "attend_skip": pct(per_step(1, 2)),
                                 "attend_full_span": pct(per_step(2, 3)),
+                                "attend_position_order": pct(per_step(8, 9)),
                                 "decode_skip": pct(per_step(5, 6)),
                                 "decode_full_span": pct(per_step(6, 7))}
         if n == "eager":
@@ -880,6 +898,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         else:
             r["attend_skip_ms_total"] = round(ms(1, 2), 3)
             r["attend_full_span_ms_total"] = round(ms(2, 3), 3)
+            r["attend_position_order_ms_total"] = round(ms(8, 9), 3)
             r["decode_skip_ms_total"] = round(ms(5, 6), 3)
             r["decode_full_span_ms_total"] = round(ms(6, 7), 3)
             if pools[n]["min_pages"] > 0:
@@ -894,6 +913,9 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
                 1 - res[n][f"attend_{mode}_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
             res[n][f"decode_{mode}_reduction_vs_native"] = round(
                 1 - res[n][f"decode_{mode}_ms_total"] / nat[f"decode_{mode}_ms_total"], 4)
+    for n in names[1:]:
+        res[n]["attend_position_order_vs_eager"] = round(
+            res[n]["attend_position_order_ms_total"] / res["eager"]["attend_ms_total"], 4)
     for mode in ("skip", "full_span"):
         res["eager"][f"attend_reduction_vs_native_{mode}"] = round(
             1 - res["eager"]["attend_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
