@@ -523,8 +523,13 @@ size_t omnitide_decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_head
  *            positions q_pos0 + i); n_q <= span <= cap, else OMNITIDE_E_CAPACITY on the device
  *            and that segment's output is not written.  The K/V bytes of empty slots are never
  *            used (they may hold anything, NaN included).
- *   skip_empty_tiles != 0: 64-slot tiles without an entry are not read; 0: every tile of the
- *            span is read and masked (a kernel presented the physical span).
+ *   traversal  as omnitide_span_attn: OMNITIDE_SPAN_FULL (every tile of the span is read and
+ *            masked, a kernel presented the physical span), OMNITIDE_SPAN_SKIP_EMPTY (64-slot
+ *            tiles without an entry are not read) or OMNITIDE_SPAN_POSITION_ORDER (the entries
+ *            read in position order through a position -> slot index; they must hold the
+ *            positions 0 .. q_pos0 + n_q - 1 once each, else OMNITIDE_E_TAGS on the device and
+ *            the output is unspecified; host limit cap * n_kv_heads * head_dim * 2 < 2^32);
+ *            other values: OMNITIDE_E_SHAPE.
  *   q, k, v, out, scale, arithmetic and limits: as omnitide_decode_attn; cap <= 2,097,152.
  *   workspace  device scratch of omnitide_decode_span_workspace_bytes() bytes (always > 0).
  * With key_pos[j] = j for j < span and q_pos0 = span - n_q this computes omnitide_decode_attn
@@ -534,7 +539,7 @@ int omnitide_decode_span_attn(const void* q, const void* k, const void* v,
                               const int32_t* key_pos, const int32_t* span,
                               const int32_t* q_pos0, int n_seg, int cap, int n_q,
                               int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                              int skip_empty_tiles, float* out, void* workspace,
+                              int traversal, float* out, void* workspace,
                               size_t workspace_bytes, int32_t* d_status, void* stream);
 
 size_t omnitide_decode_span_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads,

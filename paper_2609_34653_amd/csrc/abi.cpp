@@ -688,7 +688,7 @@ int decode_impl(const void* q, const void* k, const void* v, const int32_t* n_ct
                 const int32_t* key_pos, const int32_t* q_pos0, int n_seg, int cap, int n_q,
                 int n_q_heads, int n_kv_heads, int head_dim, float scale, bool skip_empty,
                 float* out, void* workspace, size_t workspace_bytes, int32_t* d_status,
-                void* stream) {
+                void* stream, bool pos_order = false) {
   const bool span = key_pos != nullptr || q_pos0 != nullptr;
   if (!all_set({q, k, v, n_ctx, out})) return OMNITIDE_E_NULL;
   if (span && !all_set({key_pos, q_pos0})) return OMNITIDE_E_NULL;
@@ -698,6 +698,9 @@ int decode_impl(const void* q, const void* k, const void* v, const int32_t* n_ct
       static_cast<long>(n_q) * (n_q_heads / n_kv_heads) > omnitide::decode_max_query_vectors())
     return OMNITIDE_E_SHAPE;
   if (cap < n_q || (span && cap > omnitide::span_attn_max_cap())) return OMNITIDE_E_CAPACITY;
+  // position order gathers V rows by 32-bit byte offsets from the segment's base
+  if (pos_order && static_cast<size_t>(cap) * n_kv_heads * head_dim * 2 > 0xffffffffull)
+    return OMNITIDE_E_SHAPE;
   const size_t need =
       span ? omnitide::decode_span_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
                                                    head_dim)
@@ -727,6 +730,7 @@ int decode_impl(const void* q, const void* k, const void* v, const int32_t* n_ct
   a.key_pos = key_pos;
   a.q_pos0 = q_pos0;
   a.skip_empty = skip_empty;
+  a.pos_order = pos_order;
   return hip_status(omnitide::launch_decode(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -753,12 +757,16 @@ int omnitide_decode_span_attn(const void* q, const void* k, const void* v,
                               const int32_t* key_pos, const int32_t* span,
                               const int32_t* q_pos0, int n_seg, int cap, int n_q,
                               int n_q_heads, int n_kv_heads, int head_dim, float scale,
-                              int skip_empty_tiles, float* out, void* workspace,
+                              int traversal, float* out, void* workspace,
                               size_t workspace_bytes, int32_t* d_status, void* stream) {
   if (key_pos == nullptr || q_pos0 == nullptr) return OMNITIDE_E_NULL;
+  if (traversal != OMNITIDE_SPAN_FULL && traversal != OMNITIDE_SPAN_SKIP_EMPTY &&
+      traversal != OMNITIDE_SPAN_POSITION_ORDER)
+    return OMNITIDE_E_SHAPE;
   return decode_impl(q, k, v, span, key_pos, q_pos0, n_seg, cap, n_q, n_q_heads, n_kv_heads,
-                     head_dim, scale, skip_empty_tiles != 0, out, workspace, workspace_bytes,
-                     d_status, stream);
+                     head_dim, scale, traversal != OMNITIDE_SPAN_FULL, out, workspace,
+                     workspace_bytes, d_status, stream,
+                     traversal == OMNITIDE_SPAN_POSITION_ORDER);
 }
 
 const char* omnitide_status_string(int code) {

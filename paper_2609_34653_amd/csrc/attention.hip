@@ -152,8 +152,6 @@ __device__ inline T& pick(T& a, T& b) {
 //              + L; n_ctx_g holds the span): keys are taken in position order, position p from
 //              the slot list[p] names (pos_index_kernel), so the tiles, bounds and causal masks
 //              are those of kContig with n_ctx = n; only the tile loads are gathers.
-constexpr int kContig = 0, kSpanTiles = 1, kPosOrder = 2;
-
 template <int D, int MODE>
 __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -718,8 +716,6 @@ size_t span_tiles_bytes(int n_seg, int cap) {
   return nt * (sizeof(int4) + sizeof(int32_t) + 1) + static_cast<size_t>(n_seg) * sizeof(int32_t);
 }
 
-namespace {
-
 // Position index of n_seg segments (kPosOrder): int32 slot_of[n_seg][cap], then the counts.
 size_t pos_index_bytes(int n_seg, int cap) {
   return (static_cast<size_t>(n_seg) * cap + n_seg) * sizeof(int32_t);
@@ -738,8 +734,6 @@ hipError_t launch_pos_index(const int32_t* key_pos, const int32_t* span, const i
                      key_pos, span, q_pos0, cap, L, slot_of, count, d_status);
   return hipGetLastError();
 }
-
-}  // namespace
 
 hipError_t launch_span_tiles(const int32_t* key_pos, const int32_t* span, int n_seg, int cap,
                              int min_span, bool skip_empty, void* buf, hipStream_t stream) {

@@ -89,12 +89,17 @@ __device__ inline int vsw(int key) { return D == 128 ? (key & 7) : (key & 3); }
 // Each wave owns 16 keys of every 128-key workgroup step, prefetched one step ahead (K
 // operands in registers, V in a private double buffer), so no workgroup barrier is needed
 // until the waves merge.  Softmax reference per column: optimistic, as in the chunk attention.
-// SPAN = false: keys are the contiguous rows [0, n_ctx) of the compacted pool.
-// SPAN = true: keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span); a
-// step covers two 64-slot tiles of the span's tile list (four waves each), slot j is visible
+// MODE kContig: keys are the contiguous rows [0, n_ctx) of the compacted pool.
+// MODE kSpanTiles: keys are the slots [0, span) of a pool with holes (n_ctx_g holds the span);
+// a step covers two 64-slot tiles of the span's tile list (four waves each), slot j is visible
 // to query token i iff 0 <= key_pos[j] <= q_pos0 + i, and the V rows of empty slots are zeroed
 // in the wave's LDS block before use (their bytes may be anything, NaN included).
-template <int D, bool SPAN>
+// MODE kPosOrder: a pool with holes whose entries hold the positions 0 .. n-1 once each (n =
+// q_pos0 + n_q; n_ctx_g holds the span): keys are taken in position order, position p from
+// the slot list[p] names, so blocks, bounds and masks are those of kContig with n_ctx = n.  A
+// wave loads the slot of its next block's key c16 one iteration ahead (a register), and its
+// V keys' slots come from the lanes holding them.
+template <int D, int MODE>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const int32_t* __restrict__ n_ctx_g, int cap, int nq,
@@ -103,6 +108,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ qpos0_g,
     const int32_t* __restrict__ tile_list, const int32_t* __restrict__ n_active_g,
     int max_tiles) {
+  // tile_list, n_active_g -- kSpanTiles: the visited tiles and their number; kPosOrder: the
+  // slot of each position and the number of entries the index counted.
+  constexpr bool SPAN = MODE == kSpanTiles;
+  constexpr bool POS = MODE == kPosOrder;
   constexpr int KC = D / 32;               // 32-dim slices (QK k-steps)
   constexpr int DB = D / 16;               // 16-dim blocks of the output
   constexpr int CHK = D / 8;               // 16-byte chunks per key row
@@ -113,10 +122,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   __shared__ float sm[kDecWaves][16], sl[kDecWaves][16];
 
   const int split = blockIdx.x, g = blockIdx.y, seg = blockIdx.z;
-  const int nctx = n_ctx_g[seg];
+  int nctx = n_ctx_g[seg];                          // SPAN, POS: the span
   if (nctx < nq || nctx > cap) {
     if (threadIdx.x == 0) set_status(status, OMNITIDE_E_CAPACITY);
     return;
+  }
+  if constexpr (POS) {
+    // the entries must be exactly the positions 0 .. q_pos0 + n_q - 1
+    const int qp0 = qpos0_g[seg];
+    if (qp0 < 0 || qp0 > nctx - nq || n_active_g[seg] != qp0 + nq) {
+      if (threadIdx.x == 0) set_status(status, OMNITIDE_E_TAGS);
+      return;
+    }
+    nctx = qp0 + nq;
   }
   const int G = Hq / Hkv;
   const int nqg = nq * G;
@@ -181,10 +199,21 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     }
   };
   const int row_end = SPAN ? nctx : j1;      // rows >= row_end are clamped
+  const int n_it = SPAN ? j1 - j0 : (j1 - j0 + kStep - 1) / kStep;
+  // POS: slot of this lane's key c16 in the next block to issue (positions past row_end - 1
+  // clamped), loaded one iteration ahead
+  const int32_t* slot_of = POS ? tile_list + static_cast<size_t>(seg) * cap : nullptr;
+  auto load_slot = [&](int it) {
+    bool blk_ok;
+    return slot_of[min(block_base(it, blk_ok) + c16, row_end - 1)];
+  };
+  int slot_next = 0;
   auto issue = [&](int it, int buf, bf16x8 (&ka)[KC], int (&kp)[5]) {
     bool blk_ok;
     const int kb0 = block_base(it, blk_ok);
-    const int kr = min(kb0 + c16, row_end - 1);
+    uint32_t kslot = 0;
+    if constexpr (POS) kslot = min(static_cast<uint32_t>(slot_next), static_cast<uint32_t>(cap - 1));
+    const int kr = POS ? static_cast<int>(kslot) : min(kb0 + c16, row_end - 1);
     const uint16_t* kp_ = kh + static_cast<size_t>(kr) * row_stride + 8 * g4;
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc)
@@ -194,6 +223,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) kp[i] = kpos[min(kb0 + 4 * g4 + i, row_end - 1)];
       kp[4] = kpos[kr];
+    }
+    if constexpr (POS) {
+      // V rows of keys vkey[cq] (< 16): their slots are held by lanes vkey[cq]; the host keeps
+      // cap * Hkv * D * 2 below 2^32
+#pragma unroll
+      for (int cq = 0; cq < CALLS; ++cq) {
+        const uint32_t vs = static_cast<uint32_t>(__shfl(static_cast<int>(kslot), vkey[cq], kWave));
+        dma16(vh, voff[cq] + 2u * vs * static_cast<uint32_t>(row_stride),
+              vlds + static_cast<uint32_t>((buf * BLK + cq * kWave * 8) * 2));
+      }
+      // the block after this one (the last iteration re-reads its own block's slot)
+      slot_next = load_slot(min(it + 1, n_it - 1));
+      return;
     }
     const int r0 = min(kb0, row_end - 1);
 #pragma unroll
@@ -209,7 +251,6 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
 #pragma unroll
   for (int db = 0; db < DB; ++db) o[db] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  const int n_it = SPAN ? j1 - j0 : (j1 - j0 + kStep - 1) / kStep;
   bf16x8 kA[KC], kB[KC];
   int pA[5] = {-1, -1, -1, -1, -1}, pB[5] = {-1, -1, -1, -1, -1};
   // V^T operand read: lane (g4, i) takes dims 16db + i of keys 4g4 .. 4g4+3; the lanes of its
@@ -276,11 +317,15 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     l_run += lsum;
     // this iteration's V block has landed (the next one's loads may still be in flight: KC K
     // loads, in SPAN mode 5 position loads, CALLS direct loads)
-    constexpr int NEXT = CALLS + KC + (SPAN ? 5 : 0);
-    static_assert(NEXT == 8 || NEXT == 4 || NEXT == 13 || NEXT == 9, "vmcnt immediates below");
+    // (POS: the next block's slot load before them and the one after next's after them)
+    constexpr int NEXT = CALLS + KC + (SPAN ? 5 : 0) + (POS ? 2 : 0);
+    static_assert(NEXT == 8 || NEXT == 4 || NEXT == 13 || NEXT == 9 || NEXT == 10 || NEXT == 6,
+                  "vmcnt immediates below");
     if (more) {
       if constexpr (NEXT == 13) asm volatile("s_waitcnt vmcnt(13)" ::: "memory");
+      else if constexpr (NEXT == 10) asm volatile("s_waitcnt vmcnt(10)" ::: "memory");
       else if constexpr (NEXT == 9) asm volatile("s_waitcnt vmcnt(9)" ::: "memory");
+      else if constexpr (NEXT == 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
       else if constexpr (NEXT == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
       else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
     } else {
@@ -304,6 +349,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
       o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, pl, o[db], 0, 0, 0);
     }
   };
+  if constexpr (POS) {
+    if (n_it > 0) slot_next = load_slot(0);
+  }
   if (n_it > 0) issue(0, 0, kA, pA);
   int it = 0;
   for (; it + 1 < n_it; it += 2) {
@@ -366,7 +414,21 @@ hipError_t launch_decode_t(const DecodeArgs& a, int n_split, hipStream_t stream)
   float* part_o = n_split > 1 ? static_cast<float*>(a.workspace) : nullptr;
   float* part_ml = part_o ? part_o + static_cast<size_t>(n_split) * n_rows * D : nullptr;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  if (a.key_pos != nullptr) {
+  if (a.key_pos != nullptr && a.pos_order) {
+    // position order: the position index after the partials
+    int32_t* slot_of = reinterpret_cast<int32_t*>(
+        static_cast<uint8_t*>(a.workspace) +
+        align256(n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0));
+    hipError_t e = launch_pos_index(a.key_pos, a.n_ctx, a.q_pos0, a.n_seg, a.cap, a.n_q,
+                                    slot_of, stream, a.d_status);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((decode_kernel<D, kPosOrder>), grid, dim3(kDecThreads), 0, stream,
+                       static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
+                       static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
+                       a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status,
+                       a.key_pos, a.q_pos0, slot_of,
+                       slot_of + static_cast<size_t>(a.n_seg) * a.cap, 0);
+  } else if (a.key_pos != nullptr) {
     // span mode: the tile tables after the partials
     uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +
                    align256(n_split > 1 ? static_cast<size_t>(n_split) * n_rows * (D + 2) * 4 : 0);
@@ -374,13 +436,13 @@ hipError_t launch_decode_t(const DecodeArgs& a, int n_split, hipStream_t stream)
                                      tbl, stream);
     if (e != hipSuccess) return e;
     const SpanTiles T = span_tiles_at(tbl, a.n_seg, a.cap);
-    hipLaunchKernelGGL((decode_kernel<D, true>), grid, dim3(kDecThreads), 0, stream,
+    hipLaunchKernelGGL((decode_kernel<D, kSpanTiles>), grid, dim3(kDecThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
                        a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status,
                        a.key_pos, a.q_pos0, T.list, T.n_active, (a.cap + kKT - 1) / kKT);
   } else {
-    hipLaunchKernelGGL((decode_kernel<D, false>), grid, dim3(kDecThreads), 0, stream,
+    hipLaunchKernelGGL((decode_kernel<D, kContig>), grid, dim3(kDecThreads), 0, stream,
                        static_cast<const uint16_t*>(a.q), static_cast<const uint16_t*>(a.k),
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
                        a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status,
@@ -411,8 +473,9 @@ size_t decode_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_
 
 size_t decode_span_workspace_bytes(int n_seg, int cap, int n_q, int n_q_heads, int n_kv_heads,
                                    int head_dim) {
+  // the tile tables (tile traversals) or the position index (position order)
   return align256(decode_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads, head_dim)) +
-         span_tiles_bytes(n_seg, cap);
+         std::max(span_tiles_bytes(n_seg, cap), pos_index_bytes(n_seg, cap));
 }
 
 int decode_max_query_vectors() { return kMaxQG; }

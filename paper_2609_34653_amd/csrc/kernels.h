@@ -187,6 +187,16 @@ struct SpanTiles {
   uint8_t* act;        // [n_seg][max_tiles]
 };
 SpanTiles span_tiles_at(void* buf, int n_seg, int cap);
+// Key traversals of the chunk and decode attention kernels: the compacted pool's rows, a span's
+// 64-slot tiles, or a span's entries in position order through a position -> slot index.
+constexpr int kContig = 0, kSpanTiles = 1, kPosOrder = 2;
+// Position -> slot index of n_seg spans whose entries hold the positions 0 .. q_pos0 + L - 1
+// once each: int32 slot_of[n_seg][cap], then the per-segment entry counts.  The build reports a
+// repeated or too-large position as OMNITIDE_E_TAGS; the attention kernels check the counts.
+size_t pos_index_bytes(int n_seg, int cap);
+hipError_t launch_pos_index(const int32_t* key_pos, const int32_t* span, const int32_t* q_pos0,
+                            int n_seg, int cap, int L, int32_t* slot_of, hipStream_t stream,
+                            int32_t* d_status);
 size_t span_tiles_bytes(int n_seg, int cap);
 hipError_t launch_span_tiles(const int32_t* key_pos, const int32_t* span, int n_seg, int cap,
                              int min_span, bool skip_empty, void* buf, hipStream_t stream);
@@ -217,6 +227,7 @@ struct DecodeArgs {
   const int32_t* key_pos = nullptr;   // [n_seg][cap] logical position, -1 = empty slot
   const int32_t* q_pos0 = nullptr;    // [n_seg] logical position of query token 0
   bool skip_empty = true;             // visit only 64-slot tiles holding an entry
+  bool pos_order = false;             // keys in position order through a position index
 };
 
 int decode_num_splits(int n_seg, int cap, int n_kv_heads);

@@ -448,10 +448,11 @@ def omnitide_decode_span_workspace_bytes(n_seg, cap, n_q, n_q_heads, n_kv_heads,
 
 
 def omnitide_decode_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, workspace,
-                              d_status=None, stream=None, skip_empty_tiles=True):
+                              d_status=None, stream=None, skip_empty_tiles=True,
+                              position_order=False):
     """Decode attention of n_q tokens over a pool with holes: q [n_seg, n_q, Hq, d] bf16;
     k/v [n_seg, cap, Hkv, d] bf16; key_pos int32 [n_seg * cap] (-1 = empty slot); span, q_pos0
-    int32 [n_seg] (device); out float32 like q."""
+    int32 [n_seg] (device); out float32 like q.  Traversal as omnitide_span_attn."""
     if q.dim() == 3:
         n_seg, (nq, Hq, d) = 1, q.shape
     else:
@@ -471,7 +472,9 @@ def omnitide_decode_span_attn(q, k, v, key_pos, span, q_pos0, scale, out, worksp
         _need(d_status, "d_status", I32, 1)
     _check(lib().omnitide_decode_span_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(key_pos), _ptr(span),
                                            _ptr(q_pos0), n_seg, cap, nq, Hq, Hkv, d,
-                                           float(scale), 1 if skip_empty_tiles else 0, _ptr(out),
+                                           float(scale),
+                                           2 if position_order else 1 if skip_empty_tiles else 0,
+                                           _ptr(out),
                                            _ptr(workspace), workspace.numel(), _ptr(d_status),
                                            _stream(stream)), "omnitide_decode_span_attn")
 

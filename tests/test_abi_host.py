@@ -418,3 +418,30 @@ def test_decode_validation(L):
     assert ot.omnitide_decode_workspace_bytes(1, 1000, 1, 32, 8, 128) > 0
     assert ot.omnitide_decode_workspace_bytes(1, 1000, 1, 30, 8, 128) == 0
 
+
+
+def decode_span(L, **kw):
+    a = dict(q=fake(0), k=fake(1), v=fake(2), kp=fake(3), span=fake(4), qp=fake(5), n_seg=1,
+             cap=81920, nq=1, Hq=32, Hkv=8, d=128, scale=0.088, trav=1, out=fake(6), ws=fake(7),
+             wsb=1 << 30, st=fake(8))
+    a.update(kw)
+    return L.omnitide_decode_span_attn(a["q"], a["k"], a["v"], a["kp"], a["span"], a["qp"],
+                                       a["n_seg"], a["cap"], a["nq"], a["Hq"], a["Hkv"], a["d"],
+                                       a["scale"], a["trav"], a["out"], a["ws"], a["wsb"],
+                                       a["st"], None)
+
+
+def test_decode_span_validation(L):
+    for k in ("q", "kp", "span", "qp", "out"):
+        assert decode_span(L, **{k: None}) == ot.E_NULL, k
+    assert decode_span(L, nq=3) == ot.E_SHAPE
+    assert decode_span(L, cap=(1 << 21) + 1) == ot.E_CAPACITY
+    for trav in (-1, 3):
+        assert decode_span(L, trav=trav) == ot.E_SHAPE, trav
+    # position order: 32-bit row offsets within a segment's pool, and room for the index
+    assert decode_span(L, trav=2, cap=1 << 21) == ot.E_SHAPE
+    assert decode_span(L, trav=2, ws=None) == ot.E_WORKSPACE
+    need = ot.omnitide_decode_span_workspace_bytes(1, 81920, 1, 32, 8, 128)
+    part = ot.omnitide_decode_workspace_bytes(1, 81920, 1, 32, 8, 128)
+    assert need >= -(-part // 256) * 256 + (81920 + 1) * 4
+    assert decode_span(L, trav=2, wsb=need - 1) == ot.E_WORKSPACE
