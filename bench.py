@@ -713,7 +713,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     over each layout (the eager pool's rows [0, n_ctx); a native pool's span, with and without
     tile skipping), as the decode half of the paper's layout ablation.  A third attention over
     each native pool takes its entries in position order through a position -> slot index (the
-    compacted pool's tiles, gathered).  Attention, decode and
+    compacted pool's tiles, gathered), and so does a third decode.  Attention, decode and
     maintenance are timed with events around their launches (the per-step latency percentiles
     come from the same events); spans and active pages are recorded per step."""
     from paper_2609_34653_amd.step import StreamStep
@@ -775,13 +775,14 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
         pl["dec"] = torch.zeros(1, 1, Hq, d, device=dev)
         pl["qpos"] = torch.zeros(1, **i32)
     names = ["eager"] + list(pools)
-    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(steps)]
+    ev = {n: [[torch.cuda.Event(enable_timing=True) for _ in range(11)] for _ in range(steps)]
           for n in names}
     spans = {n: torch.zeros(steps, **i32) for n in names}
     active = {n: torch.zeros(steps, **i32) for n in names}
     diff = torch.zeros(len(pools), device=dev)
     diff_dec = torch.zeros(len(pools), device=dev)
     diff_pos = torch.zeros(len(pools), device=dev)
+    diff_dec_pos = torch.zeros(len(pools), device=dev)
     s = torch.cuda.current_stream()
     d_status = st_first.d_status
     for i in range(steps):
@@ -842,7 +843,12 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
             ot.omnitide_span_attn(c["q"], pl["k"], pl["v"], pl["pos"], pl["span"], pl["kept"],
                                   cfg.scale, pl["out"], ws_a, d_status, position_order=True)
             e[9].record(s)
+            ot.omnitide_decode_span_attn(qd, pl["k"], pl["v"], pl["pos"], pl["span"],
+                                         pl["qpos"], cfg.scale, pl["dec"], ws_ds, d_status,
+                                         position_order=True)
+            e[10].record(s)
             diff_pos[j] = torch.maximum(diff_pos[j], (pl["out"] - st.out).abs().max())
+            diff_dec_pos[j] = torch.maximum(diff_dec_pos[j], (pl["dec"] - dec_e).abs().max())
             spans[n][i:i + 1].copy_(pl["span"])
             occ = (pl["uid"] >= 0).view(-1, page).any(dim=1)
             active[n][i:i + 1].copy_(occ.sum().view(1).to(torch.int32))
@@ -855,7 +861,9 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     res = {"steps": steps, "page_size": page,
            "max_abs_diff_vs_eager": round(float(diff.max().item()), 6),
            "position_order_max_abs_diff_vs_eager": round(float(diff_pos.max().item()), 6),
-           "decode_max_abs_diff_vs_eager": round(float(diff_dec.max().item()), 8)}
+           "decode_max_abs_diff_vs_eager": round(float(diff_dec.max().item()), 8),
+           "decode_position_order_max_abs_diff_vs_eager": round(float(diff_dec_pos.max().item()),
+                                                                8)}
     for n in names:
         ms = lambda a, b: sum(ev[n][i][a].elapsed_time(ev[n][i][b]) for i in range(steps))  # noqa
         sp = spans[n].cpu().numpy()
@@ -891,7 +899,8 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
                                 "attend_full_span": pct(per_step(2, 3)),
                                 "attend_position_order": pct(per_step(8, 9)),
                                 "decode_skip": pct(per_step(5, 6)),
-                                "decode_full_span": pct(per_step(6, 7))}
+                                "decode_full_span": pct(per_step(6, 7)),
+                                "decode_position_order": pct(per_step(9, 10))}
         if n == "eager":
             r["attend_ms_total"] = round(ms(1, 2), 3)
             r["decode_ms_total"] = round(ms(2, 5), 3)
@@ -901,6 +910,7 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
             r["attend_position_order_ms_total"] = round(ms(8, 9), 3)
             r["decode_skip_ms_total"] = round(ms(5, 6), 3)
             r["decode_full_span_ms_total"] = round(ms(6, 7), 3)
+            r["decode_position_order_ms_total"] = round(ms(9, 10), 3)
             if pools[n]["min_pages"] > 0:
                 r["min_pages"] = pools[n]["min_pages"]
                 r["moved_rows_total"] = int(pools[n]["moved_sum"].item())
@@ -916,6 +926,8 @@ def stream_loop_ablation(ot, dev, steps, page=64, suffix_pages=(1, 11)):
     for n in names[1:]:
         res[n]["attend_position_order_vs_eager"] = round(
             res[n]["attend_position_order_ms_total"] / res["eager"]["attend_ms_total"], 4)
+        res[n]["decode_position_order_vs_eager"] = round(
+            res[n]["decode_position_order_ms_total"] / res["eager"]["decode_ms_total"], 4)
     for mode in ("skip", "full_span"):
         res["eager"][f"attend_reduction_vs_native_{mode}"] = round(
             1 - res["eager"]["attend_ms_total"] / nat[f"attend_{mode}_ms_total"], 4)
