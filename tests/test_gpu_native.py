@@ -597,8 +597,9 @@ def test_stream_loop_native_layouts_chained():
     unit ids of all layouts coincide).  Against the oracle chained on its own outputs (its own
     score and select of its own eager chain): eviction, suffix packing and chunk placement
     bit-exact at every step (every tag row, the chunk slot, the span, the kept count), the K/V
-    bytes of every occupied slot and span attention (tile skipping and position order) on every
-    query row after steps 12 and 24."""
+    bytes of every occupied slot, span attention (tile skipping and position order) on every
+    query row, and the decode of the chunk's last token (all three traversals) after steps 12
+    and 24."""
     from paper_2609_34653_amd import omnitide as ot
     from paper_2609_34653_amd.step import StreamStep
     cfg = sg.CONFIG_BY_NAME["stream_loop_64x665"]
@@ -632,6 +633,7 @@ def test_stream_loop_native_layouts_chained():
             slot=torch.zeros(1, **i32), cut=torch.zeros(1, **i32), moved=torch.zeros(1, **i32),
             out=torch.zeros(1, L, Hq, d, device="cuda"),
             out_p=torch.zeros(1, L, Hq, d, device="cuda"),
+            dec=torch.zeros(3, 1, Hq, d, device="cuda"), qpos=torch.zeros(1, **i32),
             o=dict(k=k0.copy(), v=v0.copy(), uid=tags0[0].copy(), mod=tags0[1].copy(),
                    pos=tags0[2].copy()))
     ws_e = torch.zeros(ot.omnitide_evict_native_workspace_bytes(1, U), dtype=torch.uint8,
@@ -641,6 +643,8 @@ def test_stream_loop_native_layouts_chained():
     ws_c = torch.zeros(ot.omnitide_place_chunk_workspace_bytes(1, cap_n), dtype=torch.uint8,
                        device="cuda")
     ws_a = torch.zeros(ot.omnitide_span_attn_workspace_bytes(1, cap_n, L, Hq, H, d),
+                       dtype=torch.uint8, device="cuda")
+    ws_d = torch.zeros(ot.omnitide_decode_span_workspace_bytes(1, cap_n, 1, Hq, H, d),
                        dtype=torch.uint8, device="cuda")
     for t in range(steps):
         clay, cseg = sg.loop_chunk(cfg, t)
@@ -671,6 +675,14 @@ def test_stream_loop_native_layouts_chained():
                                           pl["span"], pl["kept"], cfg.scale, pl[key], ws_a,
                                           st.d_status, skip_empty_tiles=True,
                                           position_order=po)
+                # the chunk's last token decodes: every tile, non-empty tiles, position order
+                torch.add(pl["kept"], L - 1, out=pl["qpos"])
+                qd = cseg.q.cuda()[None, L - 1:L].contiguous()
+                for i, (sk, po) in enumerate(((False, False), (True, False), (True, True))):
+                    ot.omnitide_decode_span_attn(qd, pl["k"], pl["v"], pl["pos"], pl["span"],
+                                                 pl["qpos"], cfg.scale, pl["dec"][i], ws_d,
+                                                 st.d_status, skip_empty_tiles=sk,
+                                                 position_order=po)
         torch.cuda.synchronize()
         assert int(host(st.d_status)[0]) == 0, t
         # the oracle: its eager step gives the plan
@@ -708,6 +720,8 @@ def test_stream_loop_native_layouts_chained():
                 span = oracle.span_of(o["uid"])
                 check([host(pl["out"])[0], host(pl["out_p"])[0]], cseg.q, bf16_view(o["k"]),
                       bf16_view(o["v"]), o["pos"], span, ev["kept"], cfg.scale)
+                dec = host(pl["dec"])
+                check_decode(dec, cseg.q[L - 1:L], o, span, ev["kept"] + L - 1, cfg.scale)
         # next eager state, on both sides
         cp = oracle.compact_kv(e_k, e_v, e_uid, e_mod, e_pos, keep, U, ck, cv,
                                clay.chunk_modality, clay.chunk_unit, cap_e, cfg.page_size)
@@ -720,6 +734,20 @@ def test_stream_loop_native_layouts_chained():
         e_pos = np.concatenate([cp["pos"], np.full(tail, -1)])
         src = dict(k=st.k_dst, v=st.v_dst, uid=st.unit_id_dst, mod=st.modality_dst,
                    pos=st.pos_dst)
+
+
+def check_decode(outs, qd, o, span, q_pos0, scale):
+    """Decode outputs [n, 1, Hq, d] of one token against the oracle over the occupied slots, to
+    the decode bar (max 2e-5, mean 2e-6)."""
+    f = lambda t: oracle.to_f64(storage_np(t), "bf16")  # noqa: E731
+    occ = np.nonzero(o["pos"][:span] >= 0)[0]
+    ref = oracle.span_attention(f(qd), f(bf16_view(o["k"][occ])), f(bf16_view(o["v"][occ])),
+                                o["pos"][occ], len(occ), q_pos0, scale)
+    for out in outs:
+        err = np.abs(out.astype(np.float64) - ref)
+        assert np.isfinite(out).all()
+        assert err.max() <= 2e-5, err.max()
+        assert err.mean() <= 2e-6, err.mean()
 
 
 def bf16_view(a):
