@@ -163,7 +163,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     const int4* __restrict__ tile_info, const int32_t* __restrict__ list,
     const int32_t* __restrict__ list_n, int max_tiles) {
   // list, list_n -- kSpanTiles: the visited tiles and their number; kPosOrder: the slot of each
-  // position and the number of entries the index counted.
+  // position and the index's per-workgroup entry counts (max_tiles of them per segment).
   constexpr bool SPAN = MODE == kSpanTiles;
   constexpr bool POS = MODE == kPosOrder;
   using S = Smem<D>;
@@ -180,9 +180,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     return;
   }
   if constexpr (POS) {
-    // the entries must be exactly the positions 0 .. q_pos0 + L - 1
+    // the entries must be exactly the positions 0 .. q_pos0 + L - 1 (their number is checked
+    // after the loop: the index clamps every slot it hands out, so the loop is safe either way)
     const int qp0 = qpos0_g[seg];
-    if (qp0 < 0 || qp0 > nctx - L || list_n[seg] != qp0 + L) {
+    if (qp0 < 0 || qp0 > nctx - L) {
       if (threadIdx.x == 0) set_status(status, OMNITIDE_E_TAGS);
       return;
     }
@@ -569,6 +570,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(
     if (t < t_end) step(std::integral_constant<int, 0>{}, t);
   }
 
+  if constexpr (POS) {
+    // one wave per segment: the index's workgroup counts must add up to n_ctx entries
+    if (blockIdx.x == 0 && wave == 0) {
+      int c = 0;
+      for (int b = lane; b < max_tiles; b += kWave)
+        c += list_n[static_cast<size_t>(seg) * max_tiles + b];
+      // the whole wave sums (a cross-lane scan), then one lane reports
+      const int total = static_cast<int>(wave_sum_u32(static_cast<uint32_t>(c)));
+      if (lane == 0 && total != nctx) set_status(status, OMNITIDE_E_TAGS);
+    }
+  }
   const float l_tot = sum_halves(l_run);
   if (!row_ok) return;
   const size_t orow = (static_cast<size_t>(seg) * L + p) * Hq + head;
@@ -654,46 +666,43 @@ __global__ __launch_bounds__(kSpanThreads) void span_list_kernel(
 }
 
 // Position index of a span whose entries should hold the positions 0 .. n-1 once each (n =
-// q_pos0 + chunk_len): slot_of[p] = the slot holding position p.  pos_clear_kernel empties
-// slot_of[0, n) and zeroes the segment's entry count; pos_index_kernel (one thread per slot of
-// the span) claims slot_of[key_pos[j]] for its slot j by compare-and-swap and counts the claims
-// (one atomic add per wave).  A position >= n, or one held by two slots, is reported as
-// OMNITIDE_E_TAGS here; an absent one leaves the count below n, which the attention kernel
-// reports.  Segments with an invalid span or q_pos0 are left to the attention kernel.
-__global__ __launch_bounds__(kInfoThreads) void pos_clear_kernel(
-    const int32_t* __restrict__ span_g, const int32_t* __restrict__ qpos0_g, int cap, int L,
-    int32_t* __restrict__ slot_of, int32_t* __restrict__ count) {
-  const int seg = blockIdx.y;
-  const long n = min(static_cast<long>(qpos0_g[seg]) + L, static_cast<long>(span_g[seg]));
-  const int n_clear = static_cast<int>(max(0L, min(n, static_cast<long>(cap))));
-  int32_t* so = slot_of + static_cast<size_t>(seg) * cap;
-  for (int p = blockIdx.x * kInfoThreads + threadIdx.x; p < n_clear;
-       p += gridDim.x * kInfoThreads)
-    so[p] = -1;
-  if (blockIdx.x == 0 && threadIdx.x == 0) count[seg] = 0;
-}
-
+// q_pos0 + chunk_len): slot_of[p] = the slot holding position p, built in one launch without
+// clearing.  One thread per slot j of the span exchanges j into slot_of[key_pos[j]] and gets
+// the previous content back: a slot written by an earlier call (anything, even garbage), or one
+// written by this call if the position is held twice.  It is the latter exactly when that slot
+// lies inside the span and holds the same position now, which is reported as OMNITIDE_E_TAGS,
+// as is a position >= n.  Each workgroup stores its count of entries (so no accumulator needs
+// clearing); the attention kernels compare their sum with n, which reports a missing position.
+// With no position repeated, none >= n and n entries, every slot_of[0, n) was written by this
+// call.  Segments with an invalid span or q_pos0 are left to the attention kernels.
 __global__ __launch_bounds__(kInfoThreads) void pos_index_kernel(
     const int32_t* __restrict__ key_pos, const int32_t* __restrict__ span_g,
     const int32_t* __restrict__ qpos0_g, int cap, int L, int32_t* __restrict__ slot_of,
-    int32_t* __restrict__ count, int32_t* __restrict__ status) {
+    int32_t* __restrict__ counts, int32_t* __restrict__ status) {
+  __shared__ int32_t wave_counts[kInfoThreads / kWave];
   const int seg = blockIdx.y;
   const int span = span_g[seg];
   const int qp0 = qpos0_g[seg];
-  if (span < L || span > cap || qp0 < 0 || qp0 > span - L) return;
-  const int j0 = blockIdx.x * kInfoThreads;
-  if (j0 >= span) return;
-  const int n = qp0 + L;
-  const int j = j0 + static_cast<int>(threadIdx.x);
+  const bool seg_ok = span >= L && span <= cap && qp0 >= 0 && qp0 <= span - L;
+  const int n = seg_ok ? qp0 + L : 0;
+  const int j = blockIdx.x * kInfoThreads + static_cast<int>(threadIdx.x);
   const size_t sb = static_cast<size_t>(seg) * cap;
-  const int p = j < span ? key_pos[sb + j] : -1;
-  bool claimed = false;
-  if (p >= 0) {
-    if (p < n) claimed = atomicCAS(&slot_of[sb + p], -1, j) == -1;
-    if (!claimed) set_status(status, OMNITIDE_E_TAGS);
+  const int p = seg_ok && j < span ? key_pos[sb + j] : -1;
+  if (p >= n) {
+    set_status(status, OMNITIDE_E_TAGS);
+  } else if (p >= 0) {
+    const int old = atomicExch(&slot_of[sb + p], j);
+    if (old != j && old >= 0 && old < span && key_pos[sb + old] == p)
+      set_status(status, OMNITIDE_E_TAGS);
   }
-  const uint64_t c = __ballot(claimed);
-  if ((threadIdx.x & (kWave - 1)) == 0 && c != 0) atomicAdd(&count[seg], __popcll(c));
+  const uint64_t c = __ballot(p >= 0);
+  if ((threadIdx.x & (kWave - 1)) == 0) wave_counts[threadIdx.x / kWave] = __popcll(c);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int total = 0;
+    for (int w = 0; w < kInfoThreads / kWave; ++w) total += wave_counts[w];
+    counts[static_cast<size_t>(seg) * gridDim.x + blockIdx.x] = total;
+  }
 }
 
 }  // namespace
@@ -716,22 +725,21 @@ size_t span_tiles_bytes(int n_seg, int cap) {
   return nt * (sizeof(int4) + sizeof(int32_t) + 1) + static_cast<size_t>(n_seg) * sizeof(int32_t);
 }
 
-// Position index of n_seg segments (kPosOrder): int32 slot_of[n_seg][cap], then the counts.
+// Position index of n_seg segments (kPosOrder): int32 slot_of[n_seg][cap], then the
+// per-workgroup entry counts [n_seg][pos_index_blocks(cap)].
+int pos_index_blocks(int cap) { return (cap + kInfoThreads - 1) / kInfoThreads; }
+
 size_t pos_index_bytes(int n_seg, int cap) {
-  return (static_cast<size_t>(n_seg) * cap + n_seg) * sizeof(int32_t);
+  return static_cast<size_t>(n_seg) * (static_cast<size_t>(cap) + pos_index_blocks(cap)) *
+         sizeof(int32_t);
 }
 
 hipError_t launch_pos_index(const int32_t* key_pos, const int32_t* span, const int32_t* q_pos0,
                             int n_seg, int cap, int L, int32_t* slot_of, hipStream_t stream,
                             int32_t* d_status) {
-  int32_t* count = slot_of + static_cast<size_t>(n_seg) * cap;
-  const int blocks = (cap + kInfoThreads - 1) / kInfoThreads;
-  hipLaunchKernelGGL(pos_clear_kernel, dim3(std::min(blocks, 1024), n_seg), dim3(kInfoThreads),
-                     0, stream, span, q_pos0, cap, L, slot_of, count);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(pos_index_kernel, dim3(blocks, n_seg), dim3(kInfoThreads), 0, stream,
-                     key_pos, span, q_pos0, cap, L, slot_of, count, d_status);
+  int32_t* counts = slot_of + static_cast<size_t>(n_seg) * cap;
+  hipLaunchKernelGGL(pos_index_kernel, dim3(pos_index_blocks(cap), n_seg), dim3(kInfoThreads), 0,
+                     stream, key_pos, span, q_pos0, cap, L, slot_of, counts, d_status);
   return hipGetLastError();
 }
 
@@ -774,7 +782,7 @@ hipError_t launch_attn_t(const AttnArgs& a, int n_split, hipStream_t stream) {
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.chunk_len,
                        a.n_q_heads, a.n_kv_heads, scale_log2, a.out, a.out_bf16, part_o, part_ml,
                        n_mt, n_split, a.d_status, a.key_pos, a.q_pos0, nullptr, slot_of,
-                       slot_of + static_cast<size_t>(a.n_seg) * a.cap, 0);
+                       slot_of + static_cast<size_t>(a.n_seg) * a.cap, pos_index_blocks(a.cap));
   } else if (a.key_pos != nullptr) {
     // span mode: tile table after the partials
     const int max_tiles = (a.cap + kKT - 1) / kKT;

@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     const int32_t* __restrict__ tile_list, const int32_t* __restrict__ n_active_g,
     int max_tiles) {
   // tile_list, n_active_g -- kSpanTiles: the visited tiles and their number; kPosOrder: the
-  // slot of each position and the number of entries the index counted.
+  // slot of each position and the index's per-workgroup entry counts (max_tiles per segment).
   constexpr bool SPAN = MODE == kSpanTiles;
   constexpr bool POS = MODE == kPosOrder;
   constexpr int KC = D / 32;               // 32-dim slices (QK k-steps)
@@ -128,9 +128,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
     return;
   }
   if constexpr (POS) {
-    // the entries must be exactly the positions 0 .. q_pos0 + n_q - 1
+    // the entries must be exactly the positions 0 .. q_pos0 + n_q - 1 (their number is checked
+    // after the loop: every slot taken from the index is clamped, so the loop is safe either way)
     const int qp0 = qpos0_g[seg];
-    if (qp0 < 0 || qp0 > nctx - nq || n_active_g[seg] != qp0 + nq) {
+    if (qp0 < 0 || qp0 > nctx - nq) {
       if (threadIdx.x == 0) set_status(status, OMNITIDE_E_TAGS);
       return;
     }
@@ -360,6 +361,17 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(
   }
   if (it < n_it) step(std::integral_constant<int, 0>{}, it);
 
+  if constexpr (POS) {
+    // one wave per segment: the index's workgroup counts must add up to n_ctx entries
+    if (split == 0 && g == 0 && wave == 0) {
+      int c = 0;
+      for (int b = lane; b < max_tiles; b += kWave)
+        c += n_active_g[static_cast<size_t>(seg) * max_tiles + b];
+      // the whole wave sums (a cross-lane scan), then one lane reports
+      const int total = static_cast<int>(wave_sum_u32(static_cast<uint32_t>(c)));
+      if (lane == 0 && total != nctx) set_status(status, OMNITIDE_E_TAGS);
+    }
+  }
   // merge the waves: per column the reference, the sum over the four lane groups, and O^T
   const float l_col = l_run + __shfl_xor(l_run, 16, kWave) + __shfl_xor(l_run, 32, kWave) +
                       __shfl_xor(l_run, 48, kWave);
@@ -427,7 +439,7 @@ hipError_t launch_decode_t(const DecodeArgs& a, int n_split, hipStream_t stream)
                        static_cast<const uint16_t*>(a.v), a.n_ctx, a.cap, a.n_q, a.n_q_heads,
                        a.n_kv_heads, scale_log2, a.out, part_o, part_ml, n_split, a.d_status,
                        a.key_pos, a.q_pos0, slot_of,
-                       slot_of + static_cast<size_t>(a.n_seg) * a.cap, 0);
+                       slot_of + static_cast<size_t>(a.n_seg) * a.cap, pos_index_blocks(a.cap));
   } else if (a.key_pos != nullptr) {
     // span mode: the tile tables after the partials
     uint8_t* tbl = static_cast<uint8_t*>(a.workspace) +

@@ -191,8 +191,10 @@ SpanTiles span_tiles_at(void* buf, int n_seg, int cap);
 // 64-slot tiles, or a span's entries in position order through a position -> slot index.
 constexpr int kContig = 0, kSpanTiles = 1, kPosOrder = 2;
 // Position -> slot index of n_seg spans whose entries hold the positions 0 .. q_pos0 + L - 1
-// once each: int32 slot_of[n_seg][cap], then the per-segment entry counts.  The build reports a
-// repeated or too-large position as OMNITIDE_E_TAGS; the attention kernels check the counts.
+// once each: int32 slot_of[n_seg][cap], then per segment pos_index_blocks(cap) entry counts
+// (one per workgroup of the build).  The build reports a repeated or too-large position as
+// OMNITIDE_E_TAGS; the attention kernels check that the counts add up to q_pos0 + L.
+int pos_index_blocks(int cap);
 size_t pos_index_bytes(int n_seg, int cap);
 hipError_t launch_pos_index(const int32_t* key_pos, const int32_t* span, const int32_t* q_pos0,
                             int n_seg, int cap, int L, int32_t* slot_of, hipStream_t stream,
