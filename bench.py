@@ -42,10 +42,10 @@ FETCH_SCALE, WRITE_SCALE = 2.000, 1.000
 COUNTER_TRAFFIC = {
     "score": (("score.hip", "common.h"), "8b69f17ec98290ac", 57031.8, 161.3),
     "select": (("select.hip", "common.h"), "3b421e2e735569a4", 20.6, 3.0),
-    "compact": (("compact.hip", "common.h"), "edffe68dcca4279a", 34169.7, 68121.8),
-    "attend": (("attention.hip", "combine.h", "common.h"), "67721ca770258f13", 54340.5, 43058.8),
+    "compact": (("compact.hip", "common.h"), "edffe68dcca4279a", 34169.7, 68113.6),
+    "attend": (("attention.hip", "combine.h", "common.h"), "6a3ec62fcf042dfe", 54348.0, 43058.8),
     "compact_rope": (("compact.hip", "common.h"), "edffe68dcca4279a", 34232.0, 68041.7),
-    "decode": (("decode.hip", "combine.h", "common.h"), "fa0f0a2f8bb2e48a", 34327.6, 536.0),
+    "decode": (("decode.hip", "combine.h", "common.h"), "2ec842b1862a6e13", 34325.6, 536.0),
 }
 
 
@@ -53,7 +53,7 @@ COUNTER_TRAFFIC = {
 # `bench.py --steps 5 --warmup 1 --no-cpu-baseline --no-graph --loop-steps 0 --no-other-configs`:
 # SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1,024 SIMDs) per dispatch (the MFMA-only
 # probe reads 0.97 with this normalisation); keyed by the kernel's sources like COUNTER_TRAFFIC.
-MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "67721ca770258f13", 0.552)
+MFMA_BUSY = (("attention.hip", "combine.h", "common.h"), "6a3ec62fcf042dfe", 0.549)
 
 
 def mfma_busy(config):
