@@ -217,6 +217,44 @@ def test_position_order_errors_reported():
     run(kp, span2=1501, st=-5)
 
 
+def test_position_order_workspace_reused_across_layouts():
+    """The position index is built without clearing: one workspace (NaN-filled at first) serves
+    calls over different layouts in turn, a malformed one among them, and each call sees only
+    its own entries (stale index entries of earlier calls neither leak into the output nor
+    raise a false OMNITIDE_E_TAGS)."""
+    from paper_2609_34653_amd import omnitide as ot
+    rng = np.random.default_rng(15)
+    cap, L, Hq, Hkv, d = 2400, 48, 8, 2, 128
+    pools = [random_span_pool(rng, cap, L, Hkv, d, f, nan_holes=False) for f in (0.3, 0.7, 0.5)]
+    q = bf16(rng.standard_normal((1, L, Hq, d)))
+    nb = ot.omnitide_span_attn_workspace_bytes(1, cap, L, Hq, Hkv, d)
+    ws = torch.full((nb // 4 + 1,), float("nan"), device="cuda").view(torch.uint8)[:nb]
+    st = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = torch.zeros(1, L, Hq, d, device="cuda")
+
+    def call(k, v, kp, span, qp, expect):
+        st.zero_()
+        ot.omnitide_span_attn(q.cuda(), k[None].cuda(), v[None].cuda(),
+                              dev(np.asarray(kp, np.int32)), dev(np.array([span], np.int32)),
+                              dev(np.array([qp], np.int32)), 0.1, out, ws, st,
+                              position_order=True)
+        torch.cuda.synchronize()
+        assert int(host(st)[0]) == expect
+        return host(out)[0]
+
+    for k, v, kp, span, qp in pools:
+        check(call(k, v, kp, span, qp, 0), q[0], k, v, kp, span, qp, 0.1)
+    k, v, kp, span, qp = pools[1]
+    gone = kp.copy()
+    gone[np.nonzero((kp >= 0) & (kp < qp))[0][17]] = -1   # its slot_of entry is stale now
+    call(k, v, gone, span, qp, -17)
+    dup = kp.copy()
+    a, b = np.nonzero((kp >= 0) & (kp < qp))[0][[5, 40]]
+    dup[a] = kp[b]
+    call(k, v, dup, span, qp, -17)
+    check(call(k, v, kp, span, qp, 0), q[0], k, v, kp, span, qp, 0.1)
+
+
 def native_80k(keep_whole=True):
     """The 80K history after the whole-unit plan, evicted in place, the chunk in the lowest run
     of empty slots."""
